@@ -1,0 +1,183 @@
+/*
+ * sa_sketch.h -- C ABI of the Sketch Attention (SA) sketching step on one
+ * AMD Instinct MI355X (gfx950).
+ *
+ * The operation (SequenceO1, section 3.1 "Sketch Attention", equations for the
+ * affinities S, the prototype-wise softmax A and the sketch; Appendix B steps
+ * 1-3; section 4.4 "FlashSA" for the fused, streaming evaluation with softmax
+ * statistics kept instead of the k x n scores):
+ *
+ *   for every user b, head h and token t of user b:
+ *     s[t,m]   = scale * <K[t,h,:], P[h,m,:]>                  m = 0..M-1
+ *     A[t,m]   = exp(s[t,m]) / sum_m' exp(s[t,m'])             normalised over the
+ *                                                              M prototypes, per token
+ *     sketch[b,h,m,:] = sum_{t in user b} A[t,m] * V[t,h,:]
+ *     lse[t,h] = log sum_m exp(s[t,m])
+ *
+ * K and P are the already projected keys (X W_K) and prototypes (P W_Q) of the
+ * paper; V is the tensor aggregated into the slots (the paper's X).  Heads are
+ * independent SA instances, each with its own P[h]; H = 1 is exactly the
+ * paper's single-head SA.  An empty user (no tokens) gets a zero sketch.
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ *  * Every pointer argument except the scalar ones is DEVICE memory owned by
+ *    the caller.  The library keeps no pointer after the call returns and
+ *    allocates no device memory of its own: scratch space is the caller's
+ *    `workspace` buffer, sized by the matching *_workspace_size() call.
+ *  * Work is enqueued on `stream` (a hipStream_t passed as void*; NULL = the
+ *    default stream) without any host synchronisation, except in the
+ *    validation mode described below.
+ *  * Layouts are row-major and token-major, packed without padding:
+ *        K, V     [T, H, d]        bf16 (SA_BF16) or fp32 (SA_FP32)
+ *        P        [H, M, d]        same dtype as K and V
+ *        offsets  [B + 1]          int64 CSR offsets: offsets[0] = 0,
+ *                                  non-decreasing, offsets[B] = T; user b owns
+ *                                  tokens offsets[b] .. offsets[b+1]-1
+ *        sketch   [B, H, M, d]     fp32
+ *        lse      [T, H]           fp32
+ *        dsketch  [B, R, H, M, d]  fp32
+ *        dK, dV   [T, H, d]        fp32
+ *        dP       [H, M, d]        fp32
+ *    Base addresses must be 16-byte aligned.
+ *  * Errors are returned as sa_status codes; nothing is thrown across the ABI.
+ *    Argument checks happen on the host before anything is enqueued.  Offsets
+ *    live on the device and are not read by the host: malformed offsets give
+ *    unspecified values but never an out-of-bounds access.  With the
+ *    environment variable SA_DEBUG_VALIDATE=1 the library copies the offsets to
+ *    the host (synchronising `stream`) and returns SA_ERR_BAD_OFFSETS for
+ *    malformed ones.
+ *  * Calls on different streams with disjoint outputs and workspaces may run
+ *    concurrently; the library holds no mutable global state besides
+ *    per-device constants (CU count) read once.
+ *  * Results are deterministic: the same inputs, shapes and device give
+ *    bit-identical outputs (fixed reduction orders, no floating-point atomics).
+ */
+#ifndef SA_SKETCH_H
+#define SA_SKETCH_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    SA_OK = 0,
+    SA_ERR_INVALID_ARG = 1, /* null pointer, negative size, misaligned pointer, bad scale */
+    SA_ERR_UNSUPPORTED = 2, /* a shape or dtype this build does not handle */
+    SA_ERR_WORKSPACE = 3,   /* workspace missing or smaller than *_workspace_size() */
+    SA_ERR_BAD_OFFSETS = 4, /* only with SA_DEBUG_VALIDATE=1 */
+    SA_ERR_HIP = 5          /* a HIP runtime or launch error */
+} sa_status;
+
+typedef enum {
+    SA_BF16 = 0, /* K, V, P in bfloat16; logits and accumulation in fp32 */
+    SA_FP32 = 1  /* K, V, P in fp32; no sub-fp32 rounding anywhere */
+} sa_dtype;
+
+/*
+ * Supported shapes (SA_ERR_UNSUPPORTED otherwise): 1 <= H, 1 <= M <= 4096,
+ * d in {64, 128}, T < 2^31, B >= 0.  bf16 with d = 64 and M a multiple of 128
+ * up to 1024, or d = 128 and M a multiple of 128 up to 512, runs the fused
+ * matrix-core kernels; other supported shapes and SA_FP32 run a plain fp32
+ * path with the same ABI and the same results up to rounding.
+ */
+
+/* Bytes of workspace that sa_sketch_fwd needs for this shape (0 is possible). */
+size_t sa_sketch_fwd_workspace_size(int64_t B, int64_t T, int32_t H, int32_t M,
+                                    int32_t d, sa_dtype dtype);
+
+/*
+ * Forward: sketch (and optionally lse) of every user.
+ *
+ * Section 3.1 (S, A, sketch) and section 4.4 (streaming evaluation that keeps
+ * the per-token softmax statistics instead of the scores).
+ *
+ *   K, V, P, offsets  inputs as above
+ *   B, T, H, M, d     sizes; B = 0 is a no-op returning SA_OK
+ *   scale             logit scale, normally 1/sqrt(d); finite and >= 0
+ *   dtype             SA_BF16 or SA_FP32 (K, V and P share it)
+ *   sketch            output [B,H,M,d] fp32, fully overwritten (zeros for an
+ *                     empty user)
+ *   lse               output [T,H] fp32 log-sum-exp of each token's scaled
+ *                     logits over the M prototypes, or NULL if not wanted
+ *                     (sa_sketch_bwd needs it)
+ *   workspace         device scratch of at least workspace_bytes; may be NULL
+ *                     when the size query returned 0
+ */
+sa_status sa_sketch_fwd(const void* K, const void* V, const void* P,
+                        const int64_t* offsets, int64_t B, int64_t T, int32_t H,
+                        int32_t M, int32_t d, float scale, sa_dtype dtype,
+                        float* sketch, float* lse, void* workspace,
+                        size_t workspace_bytes, void* stream);
+
+/* Bytes of workspace that sa_sketch_bwd needs for this shape. */
+size_t sa_sketch_bwd_workspace_size(int64_t B, int64_t T, int32_t H, int32_t M,
+                                    int32_t d, sa_dtype dtype, int32_t R);
+
+/*
+ * Backward of the forward above (the paper trains the sketch end to end,
+ * section 3.1; the gradients follow by the chain rule):
+ *
+ *   dY[b,h]  = sum_{r<R} dsketch[b,r,h]   one user's sketch reused by R target
+ *                                         instances receives the sum of their
+ *                                         gradients (section 4.2, MRLB)
+ *   dV[t,h]  = sum_m A[t,m] dY[b,h,m,:]
+ *   dS[t,m]  = A[t,m] (<V[t,h],dY[b,h,m]> - sum_m' A[t,m'] <V[t,h],dY[b,h,m']>)
+ *   dK[t,h]  = scale * sum_m dS[t,m] P[h,m,:]
+ *   dP[h,m]  = scale * sum over every user and token of dS[t,m] K[t,h,:]
+ *
+ *   lse       the lse written by sa_sketch_fwd for the same inputs (required)
+ *   dsketch   [B,R,H,M,d] fp32, R >= 1 target instances per user
+ *   dK, dV    outputs [T,H,d] fp32, overwritten (tokens outside every user get 0)
+ *   dP        output [H,M,d] fp32, overwritten (not accumulated into)
+ */
+sa_status sa_sketch_bwd(const void* K, const void* V, const void* P,
+                        const int64_t* offsets, int64_t B, int64_t T, int32_t H,
+                        int32_t M, int32_t d, float scale, sa_dtype dtype,
+                        const float* dsketch, int32_t R, const float* lse,
+                        float* dK, float* dV, float* dP, void* workspace,
+                        size_t workspace_bytes, void* stream);
+
+/*
+ * Work list used by the fused forward, exposed for exact testing.
+ *
+ * The (head, token) pairs are laid out head-major in one index space of
+ * length H*T, cut into n_ranges = ceil(H*T / chunk_tokens) equal ranges (one
+ * per workgroup).  Each (user, head) pair with at least one token is cut at
+ * the range boundaries into segments; segments are listed in (head, user,
+ * range) order.  Every token of every user is covered exactly once.
+ *
+ * Each item is 8 int32: {b, h, t0, t1, range, split, pair_first, 0}, where
+ * [t0, t1) are token indices, `range` is the workgroup range that processes
+ * the segment, split = 1 when the user's tokens span more than one range (its
+ * partial sketches are summed by the split-L merge), and pair_first is the
+ * index of the first segment of the same (user, head) pair.
+ *
+ *   offsets        device int64 [B+1]
+ *   chunk_tokens   range length, > 0
+ *   items          device int32 [max_items * 8]
+ *   max_items      capacity; at most ceil(H*T/chunk_tokens) + H*B items are produced
+ *   n_items        device int64 [1]: number of items written
+ */
+sa_status sa_build_worklist(const int64_t* offsets, int64_t B, int64_t T,
+                            int32_t H, int64_t chunk_tokens, int32_t* items,
+                            int64_t max_items, int64_t* n_items, void* stream);
+
+/* Tokens per workgroup range that sa_sketch_fwd uses for this shape. */
+int64_t sa_sketch_fwd_chunk_tokens(int64_t B, int64_t T, int32_t H, int32_t M,
+                                   int32_t d, sa_dtype dtype);
+
+/* Static text of a status code. */
+const char* sa_status_string(sa_status status);
+
+/* Detail of the last error returned on the calling thread ("" if none). */
+const char* sa_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SA_SKETCH_H */

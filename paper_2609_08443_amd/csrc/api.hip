@@ -1,0 +1,318 @@
+// Host side of the C ABI declared in include/sa_sketch.h: argument checks,
+// launch plans, workspace carving and kernel launches on the caller's stream.
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstdlib>
+#include <cstring>
+#include <mutex>
+#include <vector>
+
+#include "sa_internal.h"
+
+namespace {
+
+thread_local char g_last_error[512] = "";
+
+sa_status fail(sa_status st, const char* fmt, ...) {
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(g_last_error, sizeof(g_last_error), fmt, ap);
+    va_end(ap);
+    return st;
+}
+
+sa_status hip_fail(hipError_t e, const char* what) {
+    return fail(SA_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+inline size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+// per-device constant: number of compute units (read once per device)
+constexpr int kMaxDevices = 64;
+std::once_flag g_cu_once[kMaxDevices];
+int g_cu_count[kMaxDevices];
+
+int device_cus() {
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return 256;
+    std::call_once(g_cu_once[dev], [dev] {
+        int n = 0;
+        if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+            n <= 0)
+            n = 256;
+        g_cu_count[dev] = n;
+    });
+    return g_cu_count[dev];
+}
+
+bool debug_validate() {
+    const char* v = getenv("SA_DEBUG_VALIDATE");
+    return v && v[0] && strcmp(v, "0") != 0;
+}
+
+sa_status check_common(int64_t B, int64_t T, int32_t H, int32_t M, int32_t d, float scale,
+                       sa_dtype dtype) {
+    if (B < 0 || T < 0 || H < 1 || M < 1 || d < 1)
+        return fail(SA_ERR_INVALID_ARG, "bad sizes B=%lld T=%lld H=%d M=%d d=%d", (long long)B,
+                    (long long)T, H, M, d);
+    if (!(std::isfinite(scale) && scale >= 0.f))
+        return fail(SA_ERR_INVALID_ARG, "scale must be finite and >= 0 (got %g)", (double)scale);
+    if (dtype != SA_BF16 && dtype != SA_FP32)
+        return fail(SA_ERR_UNSUPPORTED, "unknown dtype %d", (int)dtype);
+    if (d != 64 && d != 128) return fail(SA_ERR_UNSUPPORTED, "d must be 64 or 128 (got %d)", d);
+    if (M > 4096) return fail(SA_ERR_UNSUPPORTED, "M must be <= 4096 (got %d)", M);
+    if (T >= (int64_t(1) << 31)) return fail(SA_ERR_UNSUPPORTED, "T must be < 2^31");
+    if ((int64_t)H * B >= (int64_t(1) << 31))
+        return fail(SA_ERR_UNSUPPORTED, "H*B must be < 2^31");
+    return SA_OK;
+}
+
+sa_status validate_offsets(const int64_t* offsets, int64_t B, int64_t T, hipStream_t stream) {
+    std::vector<int64_t> h((size_t)B + 1);
+    hipError_t e = hipMemcpyAsync(h.data(), offsets, sizeof(int64_t) * (B + 1),
+                                  hipMemcpyDeviceToHost, stream);
+    if (e == hipSuccess) e = hipStreamSynchronize(stream);
+    if (e != hipSuccess) return hip_fail(e, "copying offsets for validation");
+    if (h[0] != 0) return fail(SA_ERR_BAD_OFFSETS, "offsets[0] = %lld, expected 0", (long long)h[0]);
+    for (int64_t b = 0; b < B; ++b)
+        if (h[b + 1] < h[b])
+            return fail(SA_ERR_BAD_OFFSETS, "offsets decrease at user %lld", (long long)b);
+    if (h[B] != T)
+        return fail(SA_ERR_BAD_OFFSETS, "offsets[B] = %lld, expected T = %lld", (long long)h[B],
+                    (long long)T);
+    return SA_OK;
+}
+
+// ---------------------------------------------------------------- forward plan
+struct FwdPlan {
+    bool fused = false;
+    int64_t C = 0;         // tokens per workgroup range
+    int64_t n_ranges = 0;  // workgroups
+    int64_t max_items = 0;
+    // workspace offsets (bytes)
+    size_t off_nitems = 0, off_wgstart = 0, off_pairstart = 0, off_items = 0, off_partials = 0,
+           off_lse = 0, total = 0;
+};
+
+int64_t fused_chunk_tokens(int64_t T, int32_t H, int32_t M, int32_t d) {
+    int per_cu = 1;
+    if (sa::fused_fwd_occupancy(M, d, &per_cu) != hipSuccess || per_cu < 1) per_cu = 1;
+    const int64_t target = (int64_t)device_cus() * per_cu;
+    const int64_t HT = (int64_t)H * T;
+    int64_t C = (HT + target - 1) / target;
+    C = (C + sa::kTileTokens - 1) / sa::kTileTokens * sa::kTileTokens;
+    if (C < sa::kTileTokens) C = sa::kTileTokens;
+    return C;
+}
+
+FwdPlan plan_fwd(int64_t B, int64_t T, int32_t H, int32_t M, int32_t d, sa_dtype dtype,
+                 bool need_lse_scratch) {
+    FwdPlan p;
+    p.fused = dtype == SA_BF16 && sa::fused_fwd_supported(M, d);
+    size_t off = 0;
+    auto carve = [&](size_t bytes) {
+        const size_t o = off;
+        off = align_up(off + bytes, 256);
+        return o;
+    };
+    if (p.fused) {
+        const int64_t HT = (int64_t)H * T;
+        p.C = fused_chunk_tokens(T, H, M, d);
+        p.n_ranges = (HT + p.C - 1) / p.C;
+        p.max_items = p.n_ranges + (int64_t)H * B;
+        p.off_nitems = carve(sizeof(int64_t));
+        p.off_wgstart = carve(sizeof(int32_t) * (p.n_ranges + 1));
+        p.off_pairstart = carve(sizeof(int32_t) * ((int64_t)H * B + 1));
+        p.off_items = carve(sizeof(int32_t) * sa::IT_WORDS * p.max_items);
+        p.off_partials = carve(sizeof(float) * (size_t)p.max_items * M * d);
+    } else if (need_lse_scratch) {
+        p.off_lse = carve(sizeof(float) * (size_t)T * H);
+    }
+    p.total = off;
+    return p;
+}
+
+// ---------------------------------------------------------------- backward plan
+struct BwdPlan {
+    int32_t n_chunks = 1;
+    size_t off_dY = 0, off_D = 0, off_part = 0, total = 0;
+};
+
+BwdPlan plan_bwd(int64_t B, int64_t T, int32_t H, int32_t M, int32_t d) {
+    BwdPlan p;
+    p.n_chunks = sa::generic_dp_chunks(T, H, M);
+    size_t off = 0;
+    auto carve = [&](size_t bytes) {
+        const size_t o = off;
+        off = align_up(off + bytes, 256);
+        return o;
+    };
+    p.off_dY = carve(sizeof(float) * (size_t)B * H * M * d);
+    p.off_D = carve(sizeof(float) * (size_t)T * H);
+    p.off_part = carve(sizeof(float) * (size_t)p.n_chunks * H * M * d);
+    p.total = off;
+    return p;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* sa_status_string(sa_status s) {
+    switch (s) {
+        case SA_OK: return "SA_OK";
+        case SA_ERR_INVALID_ARG: return "SA_ERR_INVALID_ARG";
+        case SA_ERR_UNSUPPORTED: return "SA_ERR_UNSUPPORTED";
+        case SA_ERR_WORKSPACE: return "SA_ERR_WORKSPACE";
+        case SA_ERR_BAD_OFFSETS: return "SA_ERR_BAD_OFFSETS";
+        case SA_ERR_HIP: return "SA_ERR_HIP";
+    }
+    return "SA_ERR_UNKNOWN";
+}
+
+const char* sa_last_error(void) { return g_last_error; }
+
+size_t sa_sketch_fwd_workspace_size(int64_t B, int64_t T, int32_t H, int32_t M, int32_t d,
+                                    sa_dtype dtype) {
+    if (check_common(B, T, H, M, d, 1.0f, dtype) != SA_OK) return 0;
+    // the plain path needs lse scratch only when the caller passes lse = NULL;
+    // size for that case so one query serves both
+    return plan_fwd(B, T, H, M, d, dtype, true).total;
+}
+
+int64_t sa_sketch_fwd_chunk_tokens(int64_t B, int64_t T, int32_t H, int32_t M, int32_t d,
+                                   sa_dtype dtype) {
+    if (check_common(B, T, H, M, d, 1.0f, dtype) != SA_OK) return 0;
+    return plan_fwd(B, T, H, M, d, dtype, false).C;
+}
+
+sa_status sa_sketch_fwd(const void* K, const void* V, const void* P, const int64_t* offsets,
+                        int64_t B, int64_t T, int32_t H, int32_t M, int32_t d, float scale,
+                        sa_dtype dtype, float* sketch, float* lse, void* workspace,
+                        size_t workspace_bytes, void* stream_) {
+    g_last_error[0] = 0;
+    sa_status st = check_common(B, T, H, M, d, scale, dtype);
+    if (st != SA_OK) return st;
+    if (B == 0) return SA_OK;
+    if (!offsets || !sketch || !P || (T > 0 && (!K || !V)))
+        return fail(SA_ERR_INVALID_ARG, "null pointer argument");
+    if (!aligned16(K) || !aligned16(V) || !aligned16(P) || !aligned16(sketch) ||
+        !aligned16(lse))
+        return fail(SA_ERR_INVALID_ARG, "K, V, P, sketch and lse must be 16-byte aligned");
+    hipStream_t stream = reinterpret_cast<hipStream_t>(stream_);
+    const FwdPlan plan = plan_fwd(B, T, H, M, d, dtype, lse == nullptr);
+    if (plan.total > 0 && (!workspace || workspace_bytes < plan.total))
+        return fail(SA_ERR_WORKSPACE, "workspace of %zu bytes needed, %zu given", plan.total,
+                    workspace ? workspace_bytes : (size_t)0);
+    if (debug_validate()) {
+        st = validate_offsets(offsets, B, T, stream);
+        if (st != SA_OK) return st;
+    }
+    uint8_t* ws = reinterpret_cast<uint8_t*>(workspace);
+    hipError_t e;
+    if (plan.fused) {
+        int32_t* items = reinterpret_cast<int32_t*>(ws + plan.off_items);
+        int32_t* wg_start = reinterpret_cast<int32_t*>(ws + plan.off_wgstart);
+        int32_t* pair_start = reinterpret_cast<int32_t*>(ws + plan.off_pairstart);
+        int64_t* n_items = reinterpret_cast<int64_t*>(ws + plan.off_nitems);
+        float* partials = reinterpret_cast<float*>(ws + plan.off_partials);
+        e = sa::launch_worklist(offsets, B, T, H, plan.C, plan.n_ranges, items, plan.max_items,
+                                wg_start, pair_start, n_items, stream);
+        if (e != hipSuccess) return hip_fail(e, "work list launch");
+        sa::FusedFwdArgs a;
+        a.K = reinterpret_cast<const uint16_t*>(K);
+        a.V = reinterpret_cast<const uint16_t*>(V);
+        a.P = reinterpret_cast<const uint16_t*>(P);
+        a.items = items;
+        a.wg_start = wg_start;
+        a.n_ranges = plan.n_ranges;
+        a.max_items = plan.max_items;
+        a.T = T;
+        a.B = (int32_t)B;
+        a.H = H;
+        a.M = M;
+        a.d = d;
+        a.scale = scale;
+        a.sketch = sketch;
+        a.lse = lse;
+        a.partials = partials;
+        e = sa::launch_fused_fwd(a, stream);
+        if (e != hipSuccess) return hip_fail(e, "fused forward launch");
+        e = sa::launch_merge(pair_start, B, H, plan.max_items, partials, (int64_t)M * d, sketch,
+                             stream);
+        if (e != hipSuccess) return hip_fail(e, "split-L merge launch");
+        return SA_OK;
+    }
+    float* lse_out = lse ? lse : reinterpret_cast<float*>(ws + plan.off_lse);
+    e = sa::launch_generic_fwd(K, V, P, offsets, B, T, H, M, d, scale, dtype == SA_BF16, sketch,
+                               lse_out, stream);
+    if (e != hipSuccess) return hip_fail(e, "fp32 forward launch");
+    return SA_OK;
+}
+
+size_t sa_sketch_bwd_workspace_size(int64_t B, int64_t T, int32_t H, int32_t M, int32_t d,
+                                    sa_dtype dtype, int32_t R) {
+    if (check_common(B, T, H, M, d, 1.0f, dtype) != SA_OK || R < 1) return 0;
+    return plan_bwd(B, T, H, M, d).total;
+}
+
+sa_status sa_sketch_bwd(const void* K, const void* V, const void* P, const int64_t* offsets,
+                        int64_t B, int64_t T, int32_t H, int32_t M, int32_t d, float scale,
+                        sa_dtype dtype, const float* dsketch, int32_t R, const float* lse,
+                        float* dK, float* dV, float* dP, void* workspace,
+                        size_t workspace_bytes, void* stream_) {
+    g_last_error[0] = 0;
+    sa_status st = check_common(B, T, H, M, d, scale, dtype);
+    if (st != SA_OK) return st;
+    if (R < 1) return fail(SA_ERR_INVALID_ARG, "R must be >= 1 (got %d)", R);
+    if (!offsets || !P || !dP || (B > 0 && !dsketch) ||
+        (T > 0 && (!K || !V || !lse || !dK || !dV)))
+        return fail(SA_ERR_INVALID_ARG, "null pointer argument");
+    if (!aligned16(K) || !aligned16(V) || !aligned16(P) || !aligned16(dsketch) ||
+        !aligned16(lse) || !aligned16(dK) || !aligned16(dV) || !aligned16(dP))
+        return fail(SA_ERR_INVALID_ARG, "tensor arguments must be 16-byte aligned");
+    hipStream_t stream = reinterpret_cast<hipStream_t>(stream_);
+    const BwdPlan plan = plan_bwd(B, T, H, M, d);
+    if (plan.total > 0 && (!workspace || workspace_bytes < plan.total))
+        return fail(SA_ERR_WORKSPACE, "workspace of %zu bytes needed, %zu given", plan.total,
+                    workspace ? workspace_bytes : (size_t)0);
+    if (debug_validate() && B > 0) {
+        st = validate_offsets(offsets, B, T, stream);
+        if (st != SA_OK) return st;
+    }
+    uint8_t* ws = reinterpret_cast<uint8_t*>(workspace);
+    float* dY = reinterpret_cast<float*>(ws + plan.off_dY);
+    float* Dbuf = reinterpret_cast<float*>(ws + plan.off_D);
+    float* part = reinterpret_cast<float*>(ws + plan.off_part);
+    hipError_t e = sa::launch_dy_reduce(dsketch, B, R, H, (int64_t)M * d, dY, stream);
+    if (e != hipSuccess) return hip_fail(e, "dY reduce launch");
+    e = sa::launch_generic_bwd(K, V, P, offsets, B, T, H, M, d, scale, dtype == SA_BF16, dY, lse,
+                               Dbuf, dK, dV, dP, part, plan.n_chunks, stream);
+    if (e != hipSuccess) return hip_fail(e, "backward launch");
+    return SA_OK;
+}
+
+sa_status sa_build_worklist(const int64_t* offsets, int64_t B, int64_t T, int32_t H,
+                            int64_t chunk_tokens, int32_t* items, int64_t max_items,
+                            int64_t* n_items, void* stream_) {
+    g_last_error[0] = 0;
+    if (B < 0 || T < 0 || H < 1 || chunk_tokens < 1 || max_items < 0)
+        return fail(SA_ERR_INVALID_ARG, "bad sizes");
+    if (!offsets || !n_items || (max_items > 0 && !items))
+        return fail(SA_ERR_INVALID_ARG, "null pointer argument");
+    if (T >= (int64_t(1) << 31) || (int64_t)H * B >= (int64_t(1) << 31))
+        return fail(SA_ERR_UNSUPPORTED, "sizes beyond int32 indexing");
+    hipStream_t stream = reinterpret_cast<hipStream_t>(stream_);
+    const int64_t n_ranges = ((int64_t)H * T + chunk_tokens - 1) / chunk_tokens;
+    hipError_t e = sa::launch_worklist(offsets, B, T, H, chunk_tokens, n_ranges, items, max_items,
+                                       nullptr, nullptr, n_items, stream);
+    if (e != hipSuccess) return hip_fail(e, "work list launch");
+    return SA_OK;
+}
+
+}  // extern "C"

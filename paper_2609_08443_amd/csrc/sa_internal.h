@@ -1,0 +1,79 @@
+// Internal declarations shared by the host library and the kernel translation
+// units of the SA sketching library (gfx950).  Not part of the public ABI.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+#include <stddef.h>
+
+#include "../../include/sa_sketch.h"
+
+namespace sa {
+
+// ---------------------------------------------------------------------------
+// work list item: 8 x int32 (see sa_build_worklist in sa_sketch.h)
+// ---------------------------------------------------------------------------
+enum : int { IT_B = 0, IT_H = 1, IT_T0 = 2, IT_T1 = 3, IT_RANGE = 4, IT_SPLIT = 5,
+             IT_PAIR_FIRST = 6, IT_WORDS = 8 };
+
+constexpr int kTileTokens = 32;     // tokens per MFMA tile (rows of the 32x32 output)
+constexpr int kWorklistThreads = 1024;
+
+// ---------------------------------------------------------------------------
+// launchers (each returns hipSuccess or the launch error)
+// ---------------------------------------------------------------------------
+
+// Work list over the head-major (h, t) index space cut into ranges of C tokens.
+// wg_start[n_ranges + 1] and pair_start[H*B + 1] may be null.
+hipError_t launch_worklist(const int64_t* offsets, int64_t B, int64_t T, int32_t H,
+                           int64_t C, int64_t n_ranges, int32_t* items, int64_t max_items,
+                           int32_t* wg_start, int32_t* pair_start, int64_t* n_items,
+                           hipStream_t stream);
+
+// sketch[b,h] = sum of the partial sketches of a split (user, head) pair, in
+// segment order; zero for empty pairs; untouched for single-segment pairs.
+hipError_t launch_merge(const int32_t* pair_start, int64_t B, int32_t H, int64_t max_items,
+                        const float* partials, int64_t MD, float* sketch, hipStream_t stream);
+
+// Fused bf16 forward (matrix cores).  Returns hipErrorInvalidValue for a
+// (d, M) it has no instance for.
+struct FusedFwdArgs {
+    const uint16_t* K;
+    const uint16_t* V;
+    const uint16_t* P;
+    const int32_t* items;
+    const int32_t* wg_start;
+    int64_t n_ranges;
+    int64_t max_items;
+    int64_t T;
+    int32_t B, H, M, d;
+    float scale;
+    float* sketch;
+    float* lse;
+    float* partials;
+};
+bool fused_fwd_supported(int32_t M, int32_t d);
+size_t fused_fwd_lds_bytes(int32_t M, int32_t d);
+hipError_t fused_fwd_occupancy(int32_t M, int32_t d, int* blocks_per_cu);
+hipError_t launch_fused_fwd(const FusedFwdArgs& a, hipStream_t stream);
+
+// Plain fp32-arithmetic path (fp32 or bf16 inputs).
+hipError_t launch_generic_fwd(const void* K, const void* V, const void* P,
+                              const int64_t* offsets, int64_t B, int64_t T, int32_t H,
+                              int32_t M, int32_t d, float scale, bool bf16, float* sketch,
+                              float* lse_out, hipStream_t stream);
+
+// dY[b,h] = sum_r dsketch[b,r,h]  (fp32, [B,H,M,d])
+hipError_t launch_dy_reduce(const float* dsketch, int64_t B, int32_t R, int32_t H, int64_t MD,
+                            float* dY, hipStream_t stream);
+
+hipError_t launch_generic_bwd(const void* K, const void* V, const void* P,
+                              const int64_t* offsets, int64_t B, int64_t T, int32_t H,
+                              int32_t M, int32_t d, float scale, bool bf16, const float* dY,
+                              const float* lse, float* Dbuf, float* dK, float* dV, float* dP,
+                              float* dp_partials, int32_t n_chunks, hipStream_t stream);
+
+// number of token chunks the generic dP kernel uses (sizes its partial buffer)
+int32_t generic_dp_chunks(int64_t T, int32_t H, int32_t M);
+
+}  // namespace sa

@@ -1,0 +1,203 @@
+"""Python binding of the SA sketching library (include/sa_sketch.h).
+
+Argument marshalling only: every step of the computation runs in the HIP
+kernels of libsa_sketch.so.  torch provides device memory and the stream.
+There is no fallback: if the library is missing, or a call fails, an
+``SAError`` is raised.
+"""
+from __future__ import annotations
+
+import ctypes
+import math
+import os
+from typing import Optional, Tuple
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libsa_sketch.so")
+
+SA_BF16, SA_FP32 = 0, 1
+_STATUS = {0: "SA_OK", 1: "SA_ERR_INVALID_ARG", 2: "SA_ERR_UNSUPPORTED", 3: "SA_ERR_WORKSPACE",
+           4: "SA_ERR_BAD_OFFSETS", 5: "SA_ERR_HIP"}
+ITEM_WORDS = 8
+
+EXPORTS = ("sa_sketch_fwd_workspace_size", "sa_sketch_fwd", "sa_sketch_bwd_workspace_size",
+           "sa_sketch_bwd", "sa_build_worklist", "sa_sketch_fwd_chunk_tokens",
+           "sa_status_string", "sa_last_error")
+
+
+class SAError(RuntimeError):
+    def __init__(self, status: int, detail: str):
+        self.status = status
+        self.status_name = _STATUS.get(status, str(status))
+        super().__init__(f"{self.status_name}: {detail}")
+
+
+_lib = None
+
+
+def lib() -> ctypes.CDLL:
+    """Load the in-tree library (built by ``paper_2609_08443_amd.build``)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise SAError(-1, f"{LIB_PATH} is missing; run python -m paper_2609_08443_amd.build")
+    L = ctypes.CDLL(LIB_PATH)
+    c = ctypes
+    i64, i32, sz, vp, f32 = c.c_int64, c.c_int32, c.c_size_t, c.c_void_p, c.c_float
+    L.sa_sketch_fwd_workspace_size.argtypes = [i64, i64, i32, i32, i32, c.c_int]
+    L.sa_sketch_fwd_workspace_size.restype = sz
+    L.sa_sketch_bwd_workspace_size.argtypes = [i64, i64, i32, i32, i32, c.c_int, i32]
+    L.sa_sketch_bwd_workspace_size.restype = sz
+    L.sa_sketch_fwd_chunk_tokens.argtypes = [i64, i64, i32, i32, i32, c.c_int]
+    L.sa_sketch_fwd_chunk_tokens.restype = i64
+    L.sa_sketch_fwd.argtypes = [vp, vp, vp, vp, i64, i64, i32, i32, i32, f32, c.c_int, vp, vp,
+                                vp, sz, vp]
+    L.sa_sketch_fwd.restype = c.c_int
+    L.sa_sketch_bwd.argtypes = [vp, vp, vp, vp, i64, i64, i32, i32, i32, f32, c.c_int, vp, i32,
+                                vp, vp, vp, vp, vp, sz, vp]
+    L.sa_sketch_bwd.restype = c.c_int
+    L.sa_build_worklist.argtypes = [vp, i64, i64, i32, i64, vp, i64, vp, vp]
+    L.sa_build_worklist.restype = c.c_int
+    L.sa_status_string.argtypes = [c.c_int]
+    L.sa_status_string.restype = c.c_char_p
+    L.sa_last_error.argtypes = []
+    L.sa_last_error.restype = c.c_char_p
+    _lib = L
+    return L
+
+
+def _check(rc: int):
+    if rc != 0:
+        raise SAError(rc, lib().sa_last_error().decode())
+
+
+def _dtype_code(t) -> int:
+    import torch
+    if t.dtype == torch.bfloat16:
+        return SA_BF16
+    if t.dtype == torch.float32:
+        return SA_FP32
+    raise SAError(1, f"unsupported tensor dtype {t.dtype}")
+
+
+def _ptr(t) -> Optional[int]:
+    return None if t is None else t.data_ptr()
+
+
+def _stream_handle(stream) -> Optional[int]:
+    import torch
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return stream.cuda_stream or None
+
+
+def _require(t, name, shape, dtype, device):
+    if t.shape != tuple(shape):
+        raise SAError(1, f"{name} has shape {tuple(t.shape)}, expected {tuple(shape)}")
+    if t.dtype != dtype:
+        raise SAError(1, f"{name} has dtype {t.dtype}, expected {dtype}")
+    if not t.is_contiguous():
+        raise SAError(1, f"{name} must be contiguous")
+    if t.device != device:
+        raise SAError(1, f"{name} is on {t.device}, expected {device}")
+
+
+def fwd_workspace_size(B, T, H, M, d, dtype_code) -> int:
+    return int(lib().sa_sketch_fwd_workspace_size(B, T, H, M, d, dtype_code))
+
+
+def bwd_workspace_size(B, T, H, M, d, dtype_code, R) -> int:
+    return int(lib().sa_sketch_bwd_workspace_size(B, T, H, M, d, dtype_code, R))
+
+
+def fwd_chunk_tokens(B, T, H, M, d, dtype_code) -> int:
+    return int(lib().sa_sketch_fwd_chunk_tokens(B, T, H, M, d, dtype_code))
+
+
+def _workspace(nbytes, device, workspace):
+    import torch
+    if nbytes == 0:
+        return None, 0
+    if workspace is None:
+        workspace = torch.empty(nbytes, dtype=torch.uint8, device=device)
+    elif workspace.numel() * workspace.element_size() < nbytes:
+        raise SAError(3, f"workspace of {nbytes} bytes needed")
+    return workspace, workspace.numel() * workspace.element_size()
+
+
+def sketch_fwd(K, V, P, offsets, scale: Optional[float] = None, sketch=None, lse=None,
+               want_lse: bool = True, workspace=None, stream=None):
+    """sa_sketch_fwd on torch tensors.  Returns (sketch [B,H,M,d] fp32, lse [T,H] or None)."""
+    import torch
+    T, H, d = K.shape
+    M = P.shape[1]
+    B = offsets.shape[0] - 1
+    dev = K.device
+    code = _dtype_code(K)
+    _require(K, "K", (T, H, d), K.dtype, dev)
+    _require(V, "V", (T, H, d), K.dtype, dev)
+    _require(P, "P", (H, M, d), K.dtype, dev)
+    _require(offsets, "offsets", (B + 1,), torch.int64, dev)
+    if scale is None:
+        scale = 1.0 / math.sqrt(d)
+    if sketch is None:
+        sketch = torch.empty((B, H, M, d), dtype=torch.float32, device=dev)
+    _require(sketch, "sketch", (B, H, M, d), torch.float32, dev)
+    if lse is None and want_lse:
+        lse = torch.empty((T, H), dtype=torch.float32, device=dev)
+    if lse is not None:
+        _require(lse, "lse", (T, H), torch.float32, dev)
+    ws, nbytes = _workspace(fwd_workspace_size(B, T, H, M, d, code), dev, workspace)
+    rc = lib().sa_sketch_fwd(_ptr(K), _ptr(V), _ptr(P), _ptr(offsets), B, T, H, M, d,
+                             float(scale), code, _ptr(sketch), _ptr(lse), _ptr(ws), nbytes,
+                             _stream_handle(stream))
+    _check(rc)
+    return sketch, lse
+
+
+def sketch_bwd(K, V, P, offsets, dsketch, lse, scale: Optional[float] = None, dK=None,
+               dV=None, dP=None, workspace=None, stream=None) -> Tuple:
+    """sa_sketch_bwd on torch tensors.  dsketch: [B,R,H,M,d].  Returns (dK, dV, dP)."""
+    import torch
+    T, H, d = K.shape
+    M = P.shape[1]
+    B = offsets.shape[0] - 1
+    R = dsketch.shape[1]
+    dev = K.device
+    code = _dtype_code(K)
+    _require(K, "K", (T, H, d), K.dtype, dev)
+    _require(V, "V", (T, H, d), K.dtype, dev)
+    _require(P, "P", (H, M, d), K.dtype, dev)
+    _require(offsets, "offsets", (B + 1,), torch.int64, dev)
+    _require(dsketch, "dsketch", (B, R, H, M, d), torch.float32, dev)
+    _require(lse, "lse", (T, H), torch.float32, dev)
+    if scale is None:
+        scale = 1.0 / math.sqrt(d)
+    if dK is None:
+        dK = torch.empty((T, H, d), dtype=torch.float32, device=dev)
+    if dV is None:
+        dV = torch.empty((T, H, d), dtype=torch.float32, device=dev)
+    if dP is None:
+        dP = torch.empty((H, M, d), dtype=torch.float32, device=dev)
+    ws, nbytes = _workspace(bwd_workspace_size(B, T, H, M, d, code, R), dev, workspace)
+    rc = lib().sa_sketch_bwd(_ptr(K), _ptr(V), _ptr(P), _ptr(offsets), B, T, H, M, d,
+                             float(scale), code, _ptr(dsketch), R, _ptr(lse), _ptr(dK), _ptr(dV),
+                             _ptr(dP), _ptr(ws), nbytes, _stream_handle(stream))
+    _check(rc)
+    return dK, dV, dP
+
+
+def build_worklist(offsets, T: int, H: int, chunk_tokens: int, max_items: Optional[int] = None,
+                   stream=None):
+    """sa_build_worklist: returns the items as an int32 tensor [n_items, 8] on the device."""
+    import torch
+    B = offsets.shape[0] - 1
+    if max_items is None:
+        max_items = (H * T + chunk_tokens - 1) // chunk_tokens + H * B
+    items = torch.empty((max(max_items, 1), ITEM_WORDS), dtype=torch.int32, device=offsets.device)
+    n = torch.zeros(1, dtype=torch.int64, device=offsets.device)
+    rc = lib().sa_build_worklist(_ptr(offsets), B, T, H, chunk_tokens, _ptr(items), max_items,
+                                 _ptr(n), _stream_handle(stream))
+    _check(rc)
+    return items[: int(n.item())]

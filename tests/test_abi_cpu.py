@@ -1,0 +1,108 @@
+"""Host-side checks of the C-ABI library that need no GPU: it loads, exports
+every entry point include/sa_sketch.h declares, and rejects bad arguments
+before anything is enqueued."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from oracle import worklist as wlref
+from paper_2609_08443_amd import sa_sketch as sa
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "sa_sketch.h")
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(sa_[a-z_0-9]+)\s*\(", text)))
+
+
+def test_library_exports_every_declared_symbol():
+    L = sa.lib()
+    names = declared_functions()
+    assert len(names) >= 8, names
+    for n in names:
+        assert hasattr(L, n), n
+    assert set(names) == set(sa.EXPORTS)
+
+
+def test_status_strings():
+    L = sa.lib()
+    for code, name in sa._STATUS.items():
+        assert L.sa_status_string(code).decode() == name
+
+
+NULL = None
+
+
+def call_fwd(B=2, T=10, H=1, M=128, d=64, scale=0.125, dtype=sa.SA_BF16, K=1 << 12, V=1 << 12,
+             P=1 << 12, off=1 << 12, sketch=1 << 12, lse=NULL, ws=NULL, wsb=0):
+    return sa.lib().sa_sketch_fwd(K, V, P, off, B, T, H, M, d, scale, dtype, sketch, lse, ws, wsb, None)
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(B=-1), 1), (dict(H=0), 1), (dict(M=0), 1), (dict(d=0), 1), (dict(T=-5), 1),
+    (dict(d=96), 2), (dict(d=32), 2), (dict(M=5000), 2), (dict(T=1 << 31), 2),
+    (dict(scale=float("nan")), 1), (dict(scale=-1.0), 1), (dict(scale=float("inf")), 1),
+    (dict(dtype=7), 2),
+    (dict(K=NULL), 1), (dict(V=NULL), 1), (dict(P=NULL), 1), (dict(off=NULL), 1),
+    (dict(sketch=NULL), 1),
+    (dict(K=(1 << 12) + 4), 1), (dict(sketch=(1 << 12) + 8), 1), (dict(lse=(1 << 12) + 2), 1),
+])
+def test_fwd_rejects_bad_arguments(kw, code):
+    assert call_fwd(**kw) == code
+    assert sa.lib().sa_last_error().decode() != ""
+
+
+def test_fwd_zero_users_is_noop():
+    # B = 0 returns before touching any pointer
+    assert call_fwd(B=0, K=NULL, V=NULL, P=NULL, off=NULL, sketch=NULL) == 0
+
+
+def test_fwd_workspace_too_small():
+    need = sa.fwd_workspace_size(2, 10, 1, 128, 64, sa.SA_BF16)
+    assert need > 0
+    assert call_fwd(ws=NULL, wsb=0) == 3
+    assert call_fwd(ws=1 << 20, wsb=need - 1) == 3
+
+
+def test_bwd_rejects_bad_arguments():
+    L = sa.lib()
+    p = 1 << 12
+    args = dict(K=p, V=p, P=p, off=p, B=2, T=10, H=1, M=128, d=64, scale=0.125, dtype=0, ds=p,
+                R=1, lse=p, dK=p, dV=p, dP=p, ws=NULL, wsb=0)
+
+    def call(**kw):
+        a = dict(args, **kw)
+        return L.sa_sketch_bwd(a["K"], a["V"], a["P"], a["off"], a["B"], a["T"], a["H"], a["M"],
+                               a["d"], a["scale"], a["dtype"], a["ds"], a["R"], a["lse"], a["dK"],
+                               a["dV"], a["dP"], a["ws"], a["wsb"], None)
+    assert call(R=0) == 1
+    assert call(lse=NULL) == 1
+    assert call(ds=NULL) == 1
+    assert call(dP=NULL) == 1
+    assert call(d=80) == 2
+    assert call() == 3  # no workspace
+    assert sa.bwd_workspace_size(2, 10, 1, 128, 64, 0, 1) > 0
+
+
+def test_worklist_rejects_bad_arguments():
+    L = sa.lib()
+    assert L.sa_build_worklist(1 << 12, 2, 10, 1, 0, 1 << 12, 4, 1 << 12, None) == 1
+    assert L.sa_build_worklist(None, 2, 10, 1, 4, 1 << 12, 4, 1 << 12, None) == 1
+    assert L.sa_build_worklist(1 << 12, 2, 10, 1, 4, 1 << 12, 4, None, None) == 1
+
+
+@pytest.mark.parametrize("offsets,T,H,C", [
+    ([0, 5, 5, 17, 18], 18, 2, 4), ([0, 100], 100, 3, 32), ([0, 0, 0], 0, 2, 7),
+    ([0, 1, 2, 3], 3, 1, 1), ([0, 64, 64, 200], 200, 2, 64)])
+def test_reference_worklist_covers_every_token_once(offsets, T, H, C):
+    items = wlref.worklist(offsets, T, H, C)
+    assert wlref.coverage_ok(items, offsets, H)
+    n_ranges = (H * T + C - 1) // C
+    assert len(items) <= n_ranges + H * (len(offsets) - 1)
+    for (b, h, t0, t1, r, split, first, _) in items:
+        assert t1 > t0 and r * C <= h * T + t0 and h * T + t1 <= (r + 1) * C
