@@ -1,0 +1,235 @@
+"""Benchmark of the SA sketching step on one MI355X.
+
+    python bench.py [--steps K] [--warmup W] [--workload c5] [--no-cpu-baseline]
+
+A step is one pass of the whole hot path over one batch: sa_sketch_fwd
+(work list, fused forward, split-L merge) then sa_sketch_bwd (MRLB target sum,
+backward kernels).  The default workload is the ragged 100K batch trained with
+4 target instances per user (32 users, log-uniform lengths in [1e3, 1e5],
+H = 4, d = 128, M = 512, bf16, R = 4).  Inputs are synthetic, drawn on the
+device with fixed seeds, resident in HBM before timing starts.
+
+Prints one JSON line.  ``value`` is history tokens per second of the whole
+step; ``fwd_tokens_per_s`` is the forward alone.  ``roofline`` describes the
+kernel with the largest share of the step, with its algorithmic FLOPs (GEMM
+convention of Appendix G: 4 M d per (token, head) in the forward, 8 M d in the
+backward) over its live HIP-event time.  ``cpu_baseline`` times the CPU oracle
+on a bounded sample of the same batch.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+from paper_2609_08443_amd import workloads as wl  # noqa: E402
+
+PEAK_BF16_TFLOPS = 2500.0     # MI355X dense bf16 MFMA
+PEAK_HBM_GBS = 8000.0         # MI355X HBM3E
+METRIC = "history tokens sketched/sec (fwd+bwd step; fwd alone in fwd_tokens_per_s), ragged 100K batch"
+
+WORKLOADS = {"c1": 1, "c2": 2, "c3": 3, "c4": 4, "c5": 5}
+
+
+# ---------------------------------------------------------------- accounting
+def fwd_algorithmic_flops(w: wl.Workload) -> float:
+    """Affinity GEMM + aggregation GEMM, 2 L_s L d each, per head (Appendix G.3)."""
+    return 4.0 * w.M * w.d * float(w.T) * w.H
+
+
+def bwd_algorithmic_flops(w: wl.Workload) -> float:
+    """Four gradient GEMMs of the same size: dA = V dY^T, dV = A dY, dK = dS P, dP = dS^T K."""
+    return 8.0 * w.M * w.d * float(w.T) * w.H
+
+
+def fwd_algorithmic_bytes(w: wl.Workload) -> float:
+    el = 2 if w.dtype == "bf16" else 4
+    return (2.0 * w.T * w.H * w.d * el          # K, V read once
+            + w.H * w.M * w.d * el              # P
+            + 4.0 * w.B * w.H * w.M * w.d       # sketch written
+            + 4.0 * w.T * w.H)                  # lse written
+
+
+def bwd_algorithmic_bytes(w: wl.Workload) -> float:
+    el = 2 if w.dtype == "bf16" else 4
+    return (2.0 * w.T * w.H * w.d * el          # K, V
+            + 4.0 * w.T * w.H                   # lse
+            + 4.0 * w.B * w.R * w.H * w.M * w.d  # dsketch
+            + 2.0 * 4.0 * w.T * w.H * w.d       # dK, dV written (fp32)
+            + 4.0 * w.H * w.M * w.d)            # dP
+
+
+# kernel name -> (algorithmic flops, algorithmic bytes, bound) of one launch
+def kernel_work(name: str, w: wl.Workload):
+    if name == "fused_fwd":
+        return fwd_algorithmic_flops(w), fwd_algorithmic_bytes(w), "mfma"
+    if name in ("bwd_fused", "plain_bwd"):
+        return bwd_algorithmic_flops(w), bwd_algorithmic_bytes(w), "mfma" if name == "bwd_fused" else "alu"
+    if name == "plain_fwd":
+        return fwd_algorithmic_flops(w), fwd_algorithmic_bytes(w), "alu"
+    return None
+
+
+# ---------------------------------------------------------------- CPU baseline
+def cpu_baseline(w: wl.Workload, dev: dict, budget_tokens: int) -> dict:
+    """The fp64 oracle (fwd, plus bwd when the step has it) on the shortest users of the
+    batch whose total length reaches budget_tokens; reported in tokens/s."""
+    import numpy as np
+    import oracle
+
+    order = list(np.argsort(w.lengths, kind="stable"))
+    users, tot = [], 0
+    for b in order:
+        users.append(int(b))
+        tot += int(w.lengths[b])
+        if tot >= budget_tokens:
+            break
+    users.sort()
+    off = w.offsets
+    K = np.concatenate([dev["K"][off[b]:off[b + 1]].float().cpu().numpy() for b in users])
+    V = np.concatenate([dev["V"][off[b]:off[b + 1]].float().cpu().numpy() for b in users])
+    P = dev["P"].float().cpu().numpy()
+    lens = w.lengths[users]
+    o = np.zeros(len(users) + 1, np.int64)
+    np.cumsum(lens, out=o[1:])
+    threads = oracle.max_threads()
+    t0 = time.perf_counter()
+    oracle.fwd(K, V, P, o, w.scale)
+    if w.bwd:
+        dS = dev["dsketch"][users].cpu().numpy()
+        oracle.bwd(K, V, P, o, dS, w.scale)
+    dt = time.perf_counter() - t0
+    ntok = int(lens.sum())
+    return {"value": ntok / dt, "unit": "tokens/s", "cores": min(threads, len(users) * w.H),
+            "kind": "oracle",
+            "sample": f"{len(users)} shortest users ({ntok} tokens, all {w.H} heads, "
+                      f"{'fwd+bwd' if w.bwd else 'fwd'}) of the same batch, fp64, {dt:.1f} s"}
+
+
+# ---------------------------------------------------------------- main
+def main(argv=None) -> int:
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="c5", choices=sorted(WORKLOADS))
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-tokens", type=int, default=6000,
+                    help="tokens of the CPU-baseline sample")
+    args = ap.parse_args(argv)
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only (asked for {args.gpus}): the sketching step "
+              "shards by user with no exchange in the forward; multi-GPU runs are not part "
+              "of this build.", file=sys.stderr)
+        return 2
+
+    import torch
+
+    from paper_2609_08443_amd import sa_sketch as sa
+
+    torch.cuda.set_device(0)
+    w = wl.config(WORKLOADS[args.workload])
+    dev = wl.device_tensors(w, "cuda")
+    code = sa.SA_BF16 if w.dtype == "bf16" else sa.SA_FP32
+    B, T, H, M, d, R = w.B, w.T, w.H, w.M, w.d, w.R
+    sketch = torch.empty((B, H, M, d), dtype=torch.float32, device="cuda")
+    lse = torch.empty((T, H), dtype=torch.float32, device="cuda")
+    ws_f = torch.empty(max(sa.fwd_workspace_size(B, T, H, M, d, code), 1), dtype=torch.uint8,
+                       device="cuda")
+    if w.bwd:
+        dK = torch.empty((T, H, d), dtype=torch.float32, device="cuda")
+        dV = torch.empty((T, H, d), dtype=torch.float32, device="cuda")
+        dP = torch.empty((H, M, d), dtype=torch.float32, device="cuda")
+        ws_b = torch.empty(max(sa.bwd_workspace_size(B, T, H, M, d, code, R), 1),
+                           dtype=torch.uint8, device="cuda")
+
+    def step():
+        sa.sketch_fwd(dev["K"], dev["V"], dev["P"], dev["offsets"], w.scale, sketch=sketch,
+                      lse=lse, workspace=ws_f)
+        if w.bwd:
+            sa.sketch_bwd(dev["K"], dev["V"], dev["P"], dev["offsets"], dev["dsketch"], lse,
+                          w.scale, dK=dK, dV=dV, dP=dP, workspace=ws_b)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+
+    # timed region: outer events for the step, library events for each kernel
+    stream = torch.cuda.current_stream()
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    sa.kernel_times()  # clear
+    sa.profile_enable(True)
+    torch.cuda.synchronize()
+    wall0 = time.perf_counter()
+    e0.record(stream)
+    for _ in range(args.steps):
+        step()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - wall0
+    sa.profile_enable(False)
+    kt = sa.kernel_times()
+    ms_step = e0.elapsed_time(e1) / args.steps
+
+    # fwd-only rate from the per-kernel events of the forward's launches
+    fwd_names = ("worklist", "fused_fwd", "splitL_merge", "plain_fwd")
+    fwd_ms = sum(kt[n][1] for n in fwd_names if n in kt) / args.steps
+    kernels = {n: {"launches": c, "avg_ms": tot / c} for n, (c, tot) in kt.items()}
+
+    flops_step = fwd_algorithmic_flops(w) + (bwd_algorithmic_flops(w) if w.bwd else 0.0)
+    dom = max(kt.items(), key=lambda kv: kv[1][1])[0] if kt else None
+    roof = None
+    if dom is not None and kernel_work(dom, w) is not None:
+        fl, by, bound = kernel_work(dom, w)
+        avg_ms = kt[dom][1] / kt[dom][0]
+        if bound == "mfma":
+            ach, peak, unit = fl / (avg_ms * 1e-3) / 1e12, PEAK_BF16_TFLOPS, "TFLOP/s"
+        elif bound == "hbm":
+            ach, peak, unit = by / (avg_ms * 1e-3) / 1e9, PEAK_HBM_GBS, "GB/s"
+        else:  # plain fp32 vector arithmetic: fp32 vector peak
+            ach, peak, unit = fl / (avg_ms * 1e-3) / 1e12, 157.3, "TFLOP/s"
+        roof = {"kernel": dom, "bound": bound, "achieved": ach, "peak": peak, "unit": unit,
+                "frac": ach / peak, "traffic": None, "avg_ms": avg_ms,
+                "algorithmic_per_launch": fl if unit == "TFLOP/s" else by}
+
+    out = {
+        "metric": METRIC,
+        "value": T / (ms_step * 1e-3),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16" if w.dtype == "bf16" else "f32",
+        "data": "synthetic (seeded N(0,1) K/V/dSketch, N(0,1/d) P; paper-shaped lengths)",
+        "config": {"workload": w.name, "B": B, "T": T, "H": H, "M": M, "d": d, "R": R,
+                   "step": "sa_sketch_fwd + sa_sketch_bwd" if w.bwd else "sa_sketch_fwd"},
+        "fwd_tokens_per_s": T / (fwd_ms * 1e-3) if fwd_ms > 0 else None,
+        "token_heads_per_s": T * H / (ms_step * 1e-3),
+        "mfma_util_step": flops_step / (ms_step * 1e-3) / 1e12 / PEAK_BF16_TFLOPS,
+        "mfma_util_fwd": (fwd_algorithmic_flops(w) / (fwd_ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS
+                          if fwd_ms > 0 else None),
+        "wall_s_timed": wall,
+        "kernels": kernels,
+        "roofline": roof,
+        "cpu_baseline": None,
+    }
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(w, dev, args.cpu_tokens)
+    print(json.dumps(out), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

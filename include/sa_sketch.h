@@ -170,6 +170,19 @@ sa_status sa_build_worklist(const int64_t* offsets, int64_t B, int64_t T,
 int64_t sa_sketch_fwd_chunk_tokens(int64_t B, int64_t T, int32_t H, int32_t M,
                                    int32_t d, sa_dtype dtype);
 
+/*
+ * Kernel timing for benchmarks.  While enabled (on = 1) on the calling thread,
+ * every kernel the library launches from that thread is bracketed by two HIP
+ * events recorded on the launch stream.  sa_kernel_times() waits for those
+ * events and returns, for up to max_kernels distinct kernels, the name (NUL
+ * terminated, at most 47 characters, in names[i*48]), the number of launches
+ * and the total device time in milliseconds since the previous collection, then
+ * clears the record.  Returns the number of kernels written, or -1 on a HIP
+ * error.  Disabled by default; costs two event records per launch when on.
+ */
+void sa_profile_enable(int32_t on);
+int32_t sa_kernel_times(int32_t max_kernels, char* names, int64_t* launches, double* total_ms);
+
 /* Static text of a status code. */
 const char* sa_status_string(sa_status status);
 

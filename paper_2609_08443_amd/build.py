@@ -24,9 +24,6 @@ FLAGS = [
     "-Wno-unused-function",
     # packed fp32 VALU instructions are kept out of the device code
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
-    # let MFMA accumulate in VGPRs as well as AGPRs (keeps the large
-    # accumulators of the fused kernels out of scratch)
-    "-mllvm", "-amdgpu-mfma-vgpr-form",
     "-I", os.path.join(ROOT, "include"),
 ]
 

@@ -50,6 +50,47 @@ int device_cus() {
     return g_cu_count[dev];
 }
 
+// ---------------------------------------------------------------- kernel timing
+struct ProfRec {
+    const char* name;
+    hipEvent_t start, stop;
+};
+thread_local bool g_prof_on = false;
+thread_local std::vector<ProfRec> g_prof_recs;
+thread_local std::vector<hipEvent_t> g_prof_pool;
+
+hipEvent_t prof_event() {
+    if (!g_prof_pool.empty()) {
+        hipEvent_t e = g_prof_pool.back();
+        g_prof_pool.pop_back();
+        return e;
+    }
+    hipEvent_t e = nullptr;
+    if (hipEventCreate(&e) != hipSuccess) return nullptr;
+    return e;
+}
+
+// Brackets the launches made in its scope with events on `stream` (when enabled).
+class ProfScope {
+  public:
+    ProfScope(const char* name, hipStream_t stream) : stream_(stream) {
+        if (!g_prof_on) return;
+        rec_.name = name;
+        rec_.start = prof_event();
+        rec_.stop = prof_event();
+        if (rec_.start && rec_.stop && hipEventRecord(rec_.start, stream_) == hipSuccess) active_ = true;
+    }
+    ~ProfScope() {
+        if (!active_) return;
+        if (hipEventRecord(rec_.stop, stream_) == hipSuccess) g_prof_recs.push_back(rec_);
+    }
+
+  private:
+    hipStream_t stream_;
+    ProfRec rec_{};
+    bool active_ = false;
+};
+
 bool debug_validate() {
     const char* v = getenv("SA_DEBUG_VALIDATE");
     return v && v[0] && strcmp(v, "0") != 0;
@@ -139,22 +180,48 @@ FwdPlan plan_fwd(int64_t B, int64_t T, int32_t H, int32_t M, int32_t d, sa_dtype
 
 // ---------------------------------------------------------------- backward plan
 struct BwdPlan {
+    bool fused = false;
     int32_t n_chunks = 1;
-    size_t off_dY = 0, off_D = 0, off_part = 0, total = 0;
+    int64_t C = 0, n_ranges = 0, max_items = 0;
+    size_t off_dY = 0, off_D = 0, off_part = 0;
+    size_t off_nitems = 0, off_wgstart = 0, off_pairstart = 0, off_items = 0, off_ymj = 0,
+           off_yjm = 0, off_pjm = 0, total = 0;
 };
 
-BwdPlan plan_bwd(int64_t B, int64_t T, int32_t H, int32_t M, int32_t d) {
+BwdPlan plan_bwd(int64_t B, int64_t T, int32_t H, int32_t M, int32_t d, sa_dtype dtype) {
     BwdPlan p;
-    p.n_chunks = sa::generic_dp_chunks(T, H, M);
+    p.fused = dtype == SA_BF16 && sa::fused_bwd_supported(M, d);
     size_t off = 0;
     auto carve = [&](size_t bytes) {
         const size_t o = off;
         off = align_up(off + bytes, 256);
         return o;
     };
-    p.off_dY = carve(sizeof(float) * (size_t)B * H * M * d);
-    p.off_D = carve(sizeof(float) * (size_t)T * H);
-    p.off_part = carve(sizeof(float) * (size_t)p.n_chunks * H * M * d);
+    if (p.fused) {
+        // one workgroup range per CU; the dP kernel runs M / part workgroups per range
+        const int64_t HT = (int64_t)H * T;
+        const int64_t target = device_cus();
+        int64_t C = (HT + target - 1) / target;
+        C = (C + 127) / 128 * 128;
+        if (C < 128) C = 128;
+        p.C = C;
+        p.n_ranges = (HT + C - 1) / C;
+        p.max_items = p.n_ranges + (int64_t)H * B;
+        p.off_nitems = carve(sizeof(int64_t));
+        p.off_wgstart = carve(sizeof(int32_t) * (p.n_ranges + 1));
+        p.off_pairstart = carve(sizeof(int32_t) * ((int64_t)H * B + 1));
+        p.off_items = carve(sizeof(int32_t) * sa::IT_WORDS * p.max_items);
+        p.off_ymj = carve(sizeof(uint16_t) * (size_t)B * H * M * d);
+        p.off_yjm = carve(sizeof(uint16_t) * (size_t)B * H * M * d);
+        p.off_pjm = carve(sizeof(uint16_t) * (size_t)H * M * d);
+        p.off_D = carve(sizeof(float) * (size_t)T * H);
+        p.off_part = carve(sizeof(float) * (size_t)p.max_items * M * d);
+    } else {
+        p.n_chunks = sa::generic_dp_chunks(T, H, M);
+        p.off_dY = carve(sizeof(float) * (size_t)B * H * M * d);
+        p.off_D = carve(sizeof(float) * (size_t)T * H);
+        p.off_part = carve(sizeof(float) * (size_t)p.n_chunks * H * M * d);
+    }
     p.total = off;
     return p;
 }
@@ -221,8 +288,11 @@ sa_status sa_sketch_fwd(const void* K, const void* V, const void* P, const int64
         int32_t* pair_start = reinterpret_cast<int32_t*>(ws + plan.off_pairstart);
         int64_t* n_items = reinterpret_cast<int64_t*>(ws + plan.off_nitems);
         float* partials = reinterpret_cast<float*>(ws + plan.off_partials);
-        e = sa::launch_worklist(offsets, B, T, H, plan.C, plan.n_ranges, items, plan.max_items,
-                                wg_start, pair_start, n_items, stream);
+        {
+            ProfScope ps("worklist", stream);
+            e = sa::launch_worklist(offsets, B, T, H, plan.C, plan.n_ranges, items,
+                                    plan.max_items, wg_start, pair_start, n_items, stream);
+        }
         if (e != hipSuccess) return hip_fail(e, "work list launch");
         sa::FusedFwdArgs a;
         a.K = reinterpret_cast<const uint16_t*>(K);
@@ -241,16 +311,25 @@ sa_status sa_sketch_fwd(const void* K, const void* V, const void* P, const int64
         a.sketch = sketch;
         a.lse = lse;
         a.partials = partials;
-        e = sa::launch_fused_fwd(a, stream);
+        {
+            ProfScope ps("fused_fwd", stream);
+            e = sa::launch_fused_fwd(a, stream);
+        }
         if (e != hipSuccess) return hip_fail(e, "fused forward launch");
-        e = sa::launch_merge(pair_start, B, H, plan.max_items, partials, (int64_t)M * d, sketch,
-                             stream);
+        {
+            ProfScope ps("splitL_merge", stream);
+            e = sa::launch_merge(pair_start, B, H, plan.max_items, partials, (int64_t)M * d,
+                                 sketch, stream);
+        }
         if (e != hipSuccess) return hip_fail(e, "split-L merge launch");
         return SA_OK;
     }
     float* lse_out = lse ? lse : reinterpret_cast<float*>(ws + plan.off_lse);
-    e = sa::launch_generic_fwd(K, V, P, offsets, B, T, H, M, d, scale, dtype == SA_BF16, sketch,
-                               lse_out, stream);
+    {
+        ProfScope ps("plain_fwd", stream);
+        e = sa::launch_generic_fwd(K, V, P, offsets, B, T, H, M, d, scale, dtype == SA_BF16,
+                                   sketch, lse_out, stream);
+    }
     if (e != hipSuccess) return hip_fail(e, "fp32 forward launch");
     return SA_OK;
 }
@@ -258,7 +337,7 @@ sa_status sa_sketch_fwd(const void* K, const void* V, const void* P, const int64
 size_t sa_sketch_bwd_workspace_size(int64_t B, int64_t T, int32_t H, int32_t M, int32_t d,
                                     sa_dtype dtype, int32_t R) {
     if (check_common(B, T, H, M, d, 1.0f, dtype) != SA_OK || R < 1) return 0;
-    return plan_bwd(B, T, H, M, d).total;
+    return plan_bwd(B, T, H, M, d, dtype).total;
 }
 
 sa_status sa_sketch_bwd(const void* K, const void* V, const void* P, const int64_t* offsets,
@@ -277,7 +356,7 @@ sa_status sa_sketch_bwd(const void* K, const void* V, const void* P, const int64
         !aligned16(lse) || !aligned16(dK) || !aligned16(dV) || !aligned16(dP))
         return fail(SA_ERR_INVALID_ARG, "tensor arguments must be 16-byte aligned");
     hipStream_t stream = reinterpret_cast<hipStream_t>(stream_);
-    const BwdPlan plan = plan_bwd(B, T, H, M, d);
+    const BwdPlan plan = plan_bwd(B, T, H, M, d, dtype);
     if (plan.total > 0 && (!workspace || workspace_bytes < plan.total))
         return fail(SA_ERR_WORKSPACE, "workspace of %zu bytes needed, %zu given", plan.total,
                     workspace ? workspace_bytes : (size_t)0);
@@ -289,12 +368,101 @@ sa_status sa_sketch_bwd(const void* K, const void* V, const void* P, const int64
     float* dY = reinterpret_cast<float*>(ws + plan.off_dY);
     float* Dbuf = reinterpret_cast<float*>(ws + plan.off_D);
     float* part = reinterpret_cast<float*>(ws + plan.off_part);
-    hipError_t e = sa::launch_dy_reduce(dsketch, B, R, H, (int64_t)M * d, dY, stream);
+    hipError_t e;
+    if (plan.fused) {
+        sa::FusedBwdArgs f;
+        f.K = reinterpret_cast<const uint16_t*>(K);
+        f.V = reinterpret_cast<const uint16_t*>(V);
+        f.P = reinterpret_cast<const uint16_t*>(P);
+        f.dsketch = dsketch;
+        f.lse = lse;
+        f.items = reinterpret_cast<int32_t*>(ws + plan.off_items);
+        f.wg_start = reinterpret_cast<int32_t*>(ws + plan.off_wgstart);
+        f.pair_start = reinterpret_cast<int32_t*>(ws + plan.off_pairstart);
+        f.n_ranges = plan.n_ranges;
+        f.max_items = plan.max_items;
+        f.B = B;
+        f.T = T;
+        f.H = H;
+        f.M = M;
+        f.d = d;
+        f.R = R;
+        f.scale = scale;
+        f.Ymj = reinterpret_cast<uint16_t*>(ws + plan.off_ymj);
+        f.Yjm = reinterpret_cast<uint16_t*>(ws + plan.off_yjm);
+        f.Pjm = reinterpret_cast<uint16_t*>(ws + plan.off_pjm);
+        f.Dbuf = Dbuf;
+        f.partials = part;
+        f.dK = dK;
+        f.dV = dV;
+        f.dP = dP;
+        {
+            ProfScope ps("worklist", stream);
+            e = sa::launch_worklist(offsets, B, T, H, plan.C, plan.n_ranges,
+                                    const_cast<int32_t*>(f.items), plan.max_items,
+                                    const_cast<int32_t*>(f.wg_start),
+                                    const_cast<int32_t*>(f.pair_start),
+                                    reinterpret_cast<int64_t*>(ws + plan.off_nitems), stream);
+        }
+        if (e != hipSuccess) return hip_fail(e, "work list launch");
+        {
+            ProfScope ps("bwd_fused", stream);
+            e = sa::launch_fused_bwd(f, stream);
+        }
+        if (e != hipSuccess) return hip_fail(e, "fused backward launch");
+        return SA_OK;
+    }
+    {
+        ProfScope ps("dY_reduce", stream);
+        e = sa::launch_dy_reduce(dsketch, B, R, H, (int64_t)M * d, dY, stream);
+    }
     if (e != hipSuccess) return hip_fail(e, "dY reduce launch");
-    e = sa::launch_generic_bwd(K, V, P, offsets, B, T, H, M, d, scale, dtype == SA_BF16, dY, lse,
-                               Dbuf, dK, dV, dP, part, plan.n_chunks, stream);
+    {
+        ProfScope ps("plain_bwd", stream);
+        e = sa::launch_generic_bwd(K, V, P, offsets, B, T, H, M, d, scale, dtype == SA_BF16, dY,
+                                   lse, Dbuf, dK, dV, dP, part, plan.n_chunks, stream);
+    }
     if (e != hipSuccess) return hip_fail(e, "backward launch");
     return SA_OK;
+}
+
+void sa_profile_enable(int32_t on) { g_prof_on = on != 0; }
+
+int32_t sa_kernel_times(int32_t max_kernels, char* names, int64_t* launches, double* total_ms) {
+    struct Acc {
+        const char* name;
+        int64_t n;
+        double ms;
+    };
+    std::vector<Acc> acc;
+    bool ok = true;
+    for (const ProfRec& r : g_prof_recs) {
+        float ms = 0.f;
+        if (hipEventSynchronize(r.stop) != hipSuccess ||
+            hipEventElapsedTime(&ms, r.start, r.stop) != hipSuccess)
+            ok = false;
+        size_t i = 0;
+        while (i < acc.size() && strcmp(acc[i].name, r.name) != 0) ++i;
+        if (i == acc.size()) acc.push_back({r.name, 0, 0.0});
+        acc[i].n += 1;
+        acc[i].ms += ms;
+        g_prof_pool.push_back(r.start);
+        g_prof_pool.push_back(r.stop);
+    }
+    g_prof_recs.clear();
+    if (!ok) return -1;
+    int32_t n = 0;
+    for (const Acc& a : acc) {
+        if (n >= max_kernels) break;
+        if (names) {
+            strncpy(names + (size_t)n * 48, a.name, 47);
+            names[(size_t)n * 48 + 47] = 0;
+        }
+        if (launches) launches[n] = a.n;
+        if (total_ms) total_ms[n] = a.ms;
+        ++n;
+    }
+    return n;
 }
 
 sa_status sa_build_worklist(const int64_t* offsets, int64_t B, int64_t T, int32_t H,

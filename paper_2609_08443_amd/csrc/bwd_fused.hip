@@ -1,0 +1,591 @@
+// Backward of the SA sketching step on gfx950 matrix cores (bf16 inputs,
+// fp32 gradients).
+//
+// Chain rule of the forward (section 3.1: S = scale K P^T, A = softmax over
+// prototypes, sketch = A^T V), with the MRLB sum of section 4.2 done first
+// (dY = sum over the R target instances that reuse a user's sketch):
+//
+//   A[t,m]  = exp(scale * S[t,m] - lse[t])        (recomputed from the saved lse)
+//   dV_t    = sum_m A[t,m] dY_m
+//   D_t     = sum_m A[t,m] <V_t, dY_m>  =  <V_t, dV_t>
+//   dS[t,m] = A[t,m] (<V_t, dY_m> - D_t)
+//   dK_t    = scale sum_m dS[t,m] P_m
+//   dP_m    = scale sum_t dS[t,m] K_t             (over every user and token)
+//
+// Three device passes:
+//   prep   dY (fp32, R summed) -> bf16 in two layouts; P -> bf16 transposed.
+//   token  per token tile: dV (first sweep over the prototypes), D_t = <V_t, dV_t>,
+//          then dK (second sweep).  Works in the transposed orientation S^T (rows =
+//          prototypes, lanes = tokens) so that the reductions over prototypes are
+//          matrix-core contractions whose k slots are the register index of S^T.
+//          Prototype blocks of 32 are streamed through double-buffered LDS and
+//          shared by the four waves (each wave owns 32 tokens).
+//   proto  dP for a slice of the prototypes, in the forward's orientation (lanes =
+//          prototypes): the prototype slice and the user's dY slice stay in LDS,
+//          dS^T . K accumulates in registers; one partial per work-list segment,
+//          summed per head in segment order (deterministic).
+#include "sa_internal.h"
+
+namespace sa {
+
+namespace {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+
+constexpr float kLog2e = 1.4426950408889634f;
+
+__device__ inline float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
+__device__ inline float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
+__device__ inline uint32_t pack_bf16x2(float a, float b) {
+    bf16x2 v = __builtin_convertvector((f32x2){a, b}, bf16x2);
+    return __builtin_bit_cast(uint32_t, v);
+}
+__device__ inline uint16_t to_bf16(float a) { return (uint16_t)(pack_bf16x2(a, 0.f) & 0xffffu); }
+__device__ inline bf16x8 pack8(const float* e) {
+    uint4 pk;
+    pk.x = pack_bf16x2(e[0], e[1]);
+    pk.y = pack_bf16x2(e[2], e[3]);
+    pk.z = pack_bf16x2(e[4], e[5]);
+    pk.w = pack_bf16x2(e[6], e[7]);
+    return __builtin_bit_cast(bf16x8, pk);
+}
+template <int COLS>
+__device__ inline int swz(int r, int c) {
+    if constexpr (COLS == 32) {
+        return r * 32 + ((c ^ ((r >> 1) & 3)) << 3);
+    } else {
+        return r * COLS + ((c ^ (r & 7)) << 3);
+    }
+}
+__device__ inline bf16x8 lds_b128(const uint16_t* base, int off) {
+    return __builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4*>(base + off));
+}
+// position <-> index permutation inside each 16-group: swap bits 2 and 3.  The C
+// layout of a 32x32 tile read as the k slots of the next contraction visits its
+// rows in this order (an involution).
+__device__ inline int perm16(int t) { return (t & ~12) | ((t & 4) << 1) | ((t & 8) >> 1); }
+__device__ inline int srow(int r, int hl) { return 8 * (r >> 2) + 4 * hl + (r & 3); }
+
+__device__ inline float xhalf_sum(float v) {
+    const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+    return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+
+// ------------------------------------------------------------------ prep
+// dY[b,h] = sum_r dsketch[b,r,h] (fp32) written as bf16 row-major Ymj[b,h,m,j]
+// and transposed Yjm[b,h,j,p] with p = perm16(m); P -> Pjm[h,j,p] likewise.
+__global__ __launch_bounds__(256) void prep_kernel(const float* __restrict__ ds, int64_t B,
+                                                   int32_t R, int32_t H, int32_t M, int32_t D,
+                                                   const uint16_t* __restrict__ P,
+                                                   uint16_t* __restrict__ Ymj,
+                                                   uint16_t* __restrict__ Yjm,
+                                                   uint16_t* __restrict__ Pjm) {
+    const int64_t MD = (int64_t)M * D;
+    const int64_t nY = B * H * MD;
+    const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    if (i < nY) {
+        const int64_t bh = i / MD, rest = i % MD;
+        const int64_t b = bh / H, h = bh % H;
+        const int m = (int)(rest / D), j = (int)(rest % D);
+        float s = 0.f;
+        for (int r = 0; r < R; ++r) s += ds[((b * R + r) * H + h) * MD + rest];
+        const uint16_t v = to_bf16(s);
+        Ymj[i] = v;
+        Yjm[bh * MD + (int64_t)j * M + perm16(m)] = v;
+    } else if (i < nY + (int64_t)H * MD) {
+        const int64_t k = i - nY;
+        const int64_t h = k / MD, rest = k % MD;
+        const int m = (int)(rest / D), j = (int)(rest % D);
+        Pjm[h * MD + (int64_t)j * M + perm16(m)] = P[k];
+    }
+}
+
+// ------------------------------------------------------------------ token side
+template <int D>
+struct TokCfg {
+    static constexpr int NW = 4;
+    static constexpr int THREADS = 256;
+    static constexpr int KS = D / 16;
+    static constexpr int JT = D / 32;
+    static constexpr int BLK = 32 * D;                 // bf16 elements of one 32-row block
+    // LDS: two buffers of {Pmj, Pjm, Ymj, Yjm} prototype blocks
+    static constexpr int BUF = 4 * BLK;
+    static constexpr int LDS = 2 * BUF * 2;
+    static constexpr int CH_MJ = BLK / 8 / THREADS;    // 16-byte chunks per thread, [32][D] block
+    static constexpr int CH_JM = BLK / 8 / THREADS;    // [D][32] block
+};
+
+struct TokArgs {
+    const uint16_t* K;
+    const uint16_t* V;
+    const uint16_t* P;
+    const uint16_t* Pjm;
+    const uint16_t* Ymj;
+    const uint16_t* Yjm;
+    const float* lse;
+    const int32_t* items;
+    const int32_t* wg_start;
+    int64_t max_items;
+    int64_t T;
+    int32_t B, H, M;
+    float scale;
+    float* dK;
+    float* dV;
+    float* Dbuf;
+};
+
+template <int D>
+__global__ __launch_bounds__(256, 1) void bwd_token_kernel(TokArgs a) {
+    using C = TokCfg<D>;
+    extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
+    uint16_t* lds = reinterpret_cast<uint16_t*>(smem);
+    const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+    const int l32 = lane & 31, hl = lane >> 5;
+
+    const int64_t range = blockIdx.x;
+    const int64_t k0 = a.wg_start[range], k1 = a.wg_start[range + 1];
+    if (k0 < 0 || k1 < k0 || k1 > a.max_items) return;
+    const float ks2 = a.scale * kLog2e;
+    const int nblk = a.M / 32;
+    const int64_t MD = (int64_t)a.M * D;
+
+    for (int64_t k = k0; k < k1; ++k) {
+        const int32_t* it = a.items + k * IT_WORDS;
+        const int b = it[IT_B], h = it[IT_H], t0 = it[IT_T0], t1 = it[IT_T1];
+        if (b < 0 || b >= a.B || h < 0 || h >= a.H || t0 < 0 || t1 < t0 || t1 > a.T) continue;
+        const uint16_t* Pmj_g = a.P + (int64_t)h * MD;
+        const uint16_t* Pjm_g = a.Pjm + (int64_t)h * MD;
+        const uint16_t* Ymj_g = a.Ymj + ((int64_t)b * a.H + h) * MD;
+        const uint16_t* Yjm_g = a.Yjm + ((int64_t)b * a.H + h) * MD;
+
+        for (int tb = t0; tb < t1; tb += 128) {
+            const int tok = tb + 32 * w + l32;   // this lane's token (column of S^T)
+            const bool tv = tok < t1;
+            // K and V as B operands: lane (hl, t) holds 8 consecutive j of its token
+            bf16x8 kb[C::KS], vb[C::KS];
+            {
+                const uint16_t* kr = a.K + ((int64_t)(tv ? tok : t0) * a.H + h) * D;
+                const uint16_t* vr = a.V + ((int64_t)(tv ? tok : t0) * a.H + h) * D;
+#pragma unroll
+                for (int kk = 0; kk < C::KS; ++kk) {
+                    uint4 x = *reinterpret_cast<const uint4*>(kr + 16 * kk + 8 * hl);
+                    uint4 y = *reinterpret_cast<const uint4*>(vr + 16 * kk + 8 * hl);
+                    if (!tv) x = y = make_uint4(0, 0, 0, 0);
+                    kb[kk] = __builtin_bit_cast(bf16x8, x);
+                    vb[kk] = __builtin_bit_cast(bf16x8, y);
+                }
+            }
+            const float nl = tv ? -a.lse[(int64_t)tok * a.H + h] * kLog2e : 0.f;
+
+            // stage prototype block mb of the requested matrices into buffer `buf`
+            // (sweep 0: Pmj, Yjm; sweep 1: Pmj, Pjm, Ymj)
+            auto stage = [&](int mb, int buf, int sweep) {
+                uint16_t* L = lds + buf * C::BUF;
+#pragma unroll
+                for (int c = 0; c < C::CH_MJ; ++c) {
+                    const int i = tid + c * C::THREADS;
+                    const int r = i / (D / 8), ch = i % (D / 8);
+                    const int64_t src = (int64_t)(mb * 32 + r) * D + ch * 8;
+                    *reinterpret_cast<uint4*>(L + swz<D>(r, ch)) = *reinterpret_cast<const uint4*>(Pmj_g + src);
+                    if (sweep == 1)
+                        *reinterpret_cast<uint4*>(L + 2 * C::BLK + swz<D>(r, ch)) =
+                            *reinterpret_cast<const uint4*>(Ymj_g + src);
+                }
+#pragma unroll
+                for (int c = 0; c < C::CH_JM; ++c) {
+                    const int i = tid + c * C::THREADS;
+                    const int j = i / 4, ch = i % 4;
+                    const int64_t src = (int64_t)j * a.M + mb * 32 + ch * 8;
+                    if (sweep == 1)
+                        *reinterpret_cast<uint4*>(L + C::BLK + swz<32>(j, ch)) =
+                            *reinterpret_cast<const uint4*>(Pjm_g + src);
+                    else
+                        *reinterpret_cast<uint4*>(L + 3 * C::BLK + swz<32>(j, ch)) =
+                            *reinterpret_cast<const uint4*>(Yjm_g + src);
+                }
+            };
+            // S^T tile of block mb (rows = the block's 32 prototypes, cols = tokens)
+            auto st_tile = [&](const uint16_t* L) {
+                f32x16 s;
+#pragma unroll
+                for (int r = 0; r < 16; ++r) s[r] = 0.f;
+#pragma unroll
+                for (int kk = 0; kk < C::KS; ++kk)
+                    s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(lds_b128(L, swz<D>(l32, 2 * kk + hl)), kb[kk], s, 0, 0, 0);
+                return s;
+            };
+
+            // ---------------- sweep 1: dV^T[j, t] = sum_m dY[m, j] A[t, m]
+            f32x16 dvt[C::JT];
+#pragma unroll
+            for (int jt = 0; jt < C::JT; ++jt)
+#pragma unroll
+                for (int r = 0; r < 16; ++r) dvt[jt][r] = 0.f;
+            __syncthreads();  // previous users of the buffers are done
+            stage(0, 0, 0);
+            __syncthreads();
+            for (int mb = 0; mb < nblk; ++mb) {
+                const uint16_t* L = lds + (mb & 1) * C::BUF;
+                if (mb + 1 < nblk) stage(mb + 1, (mb + 1) & 1, 0);
+                const f32x16 s = st_tile(L);
+                float e[16];
+#pragma unroll
+                for (int r = 0; r < 16; ++r) e[r] = __builtin_amdgcn_exp2f(__builtin_fmaf(s[r], ks2, nl));
+                const bf16x8 ab0 = pack8(e), ab1 = pack8(e + 8);
+#pragma unroll
+                for (int jt = 0; jt < C::JT; ++jt) {
+                    const uint16_t* Y = L + 3 * C::BLK;
+                    dvt[jt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(lds_b128(Y, swz<32>(jt * 32 + l32, 0 + hl)), ab0, dvt[jt], 0, 0, 0);
+                    dvt[jt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(lds_b128(Y, swz<32>(jt * 32 + l32, 2 + hl)), ab1, dvt[jt], 0, 0, 0);
+                }
+                __syncthreads();
+            }
+            // D_t = <V_t, dV_t>: this lane holds dV[t, j] for j = jt*32 + srow(r, hl)
+            float Dt = 0.f;
+            {
+                const uint16_t* vr = a.V + ((int64_t)(tv ? tok : t0) * a.H + h) * D;
+#pragma unroll
+                for (int jt = 0; jt < C::JT; ++jt)
+#pragma unroll
+                    for (int g = 0; g < 4; ++g) {
+                        const uint2 v4 = *reinterpret_cast<const uint2*>(vr + jt * 32 + 8 * g + 4 * hl);
+                        Dt = __builtin_fmaf(bf16_lo(v4.x), dvt[jt][4 * g + 0], Dt);
+                        Dt = __builtin_fmaf(bf16_hi(v4.x), dvt[jt][4 * g + 1], Dt);
+                        Dt = __builtin_fmaf(bf16_lo(v4.y), dvt[jt][4 * g + 2], Dt);
+                        Dt = __builtin_fmaf(bf16_hi(v4.y), dvt[jt][4 * g + 3], Dt);
+                    }
+                Dt = tv ? xhalf_sum(Dt) : 0.f;
+            }
+            // write dV now (frees its registers)
+            if (tv) {
+                float* out = a.dV + ((int64_t)tok * a.H + h) * D;
+#pragma unroll
+                for (int jt = 0; jt < C::JT; ++jt)
+#pragma unroll
+                    for (int r = 0; r < 16; ++r) out[jt * 32 + srow(r, hl)] = dvt[jt][r];
+                if (hl == 0) a.Dbuf[(int64_t)tok * a.H + h] = Dt;
+            }
+
+            // ---------------- sweep 2: dK^T[j, t] = scale sum_m P[m, j] dS[t, m]
+            f32x16 dkt[C::JT];
+#pragma unroll
+            for (int jt = 0; jt < C::JT; ++jt)
+#pragma unroll
+                for (int r = 0; r < 16; ++r) dkt[jt][r] = 0.f;
+            stage(0, 0, 1);
+            __syncthreads();
+            for (int mb = 0; mb < nblk; ++mb) {
+                const uint16_t* L = lds + (mb & 1) * C::BUF;
+                if (mb + 1 < nblk) stage(mb + 1, (mb + 1) & 1, 1);
+                const f32x16 s = st_tile(L);
+                f32x16 da;
+#pragma unroll
+                for (int r = 0; r < 16; ++r) da[r] = 0.f;
+                const uint16_t* Ym = L + 2 * C::BLK;
+#pragma unroll
+                for (int kk = 0; kk < C::KS; ++kk)
+                    da = __builtin_amdgcn_mfma_f32_32x32x16_bf16(lds_b128(Ym, swz<D>(l32, 2 * kk + hl)), vb[kk], da, 0, 0, 0);
+                float e[16];
+#pragma unroll
+                for (int r = 0; r < 16; ++r) {
+                    const float A = __builtin_amdgcn_exp2f(__builtin_fmaf(s[r], ks2, nl));
+                    e[r] = A * (da[r] - Dt);
+                }
+                const bf16x8 d0 = pack8(e), d1 = pack8(e + 8);
+                const uint16_t* Pj = L + C::BLK;
+#pragma unroll
+                for (int jt = 0; jt < C::JT; ++jt) {
+                    dkt[jt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(lds_b128(Pj, swz<32>(jt * 32 + l32, 0 + hl)), d0, dkt[jt], 0, 0, 0);
+                    dkt[jt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(lds_b128(Pj, swz<32>(jt * 32 + l32, 2 + hl)), d1, dkt[jt], 0, 0, 0);
+                }
+                __syncthreads();
+            }
+            if (tv) {
+                float* out = a.dK + ((int64_t)tok * a.H + h) * D;
+#pragma unroll
+                for (int jt = 0; jt < C::JT; ++jt)
+#pragma unroll
+                    for (int r = 0; r < 16; ++r) out[jt * 32 + srow(r, hl)] = a.scale * dkt[jt][r];
+            }
+        }
+    }
+}
+
+// ------------------------------------------------------------------ prototype side
+template <int D, int MW>
+struct ProtoCfg {
+    static constexpr int NW = 4;
+    static constexpr int THREADS = 256;
+    static constexpr int MP = MW * NW;      // prototypes of one part
+    static constexpr int MT = MW / 32;
+    static constexpr int KS = D / 16;
+    static constexpr int JT = D / 32;
+    static constexpr int KCH = D / 8;
+    static constexpr int LD_CHUNKS = 32 * KCH;
+    static constexpr int NLD = LD_CHUNKS / THREADS;
+    static constexpr int OFF_P = 0;                        // [MP][D]
+    static constexpr int OFF_Y = OFF_P + MP * D * 2;       // [MP][D]
+    static constexpr int OFF_K = OFF_Y + MP * D * 2;       // [32][D] token-major K tile
+    static constexpr int OFF_V = OFF_K + 32 * D * 2;       // [32][D] V tile
+    static constexpr int OFF_KT = OFF_V + 32 * D * 2;      // [D][32] K^T, permuted tokens
+    static constexpr int OFF_L = OFF_KT + D * 32 * 2;      // [32] -lse*log2e
+    static constexpr int OFF_D = OFF_L + 32 * 4;           // [32] D_t
+    static constexpr int LDS = OFF_D + 32 * 4;
+};
+
+struct ProtoArgs {
+    const uint16_t* K;
+    const uint16_t* V;
+    const uint16_t* P;
+    const uint16_t* Ymj;
+    const float* lse;
+    const float* Dbuf;
+    const int32_t* items;
+    const int32_t* wg_start;
+    int64_t max_items;
+    int64_t T;
+    int32_t B, H, M;
+    float scale;
+    float* partials;  // [max_items][M][D]
+};
+
+template <int D, int MW>
+__global__ __launch_bounds__(256, 1) void bwd_proto_kernel(ProtoArgs a) {
+    using C = ProtoCfg<D, MW>;
+    extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
+    uint16_t* Ps = reinterpret_cast<uint16_t*>(smem + C::OFF_P);
+    uint16_t* Ys = reinterpret_cast<uint16_t*>(smem + C::OFF_Y);
+    uint16_t* Ks = reinterpret_cast<uint16_t*>(smem + C::OFF_K);
+    uint16_t* Vs = reinterpret_cast<uint16_t*>(smem + C::OFF_V);
+    uint16_t* Kt = reinterpret_cast<uint16_t*>(smem + C::OFF_KT);
+    float* nls = reinterpret_cast<float*>(smem + C::OFF_L);
+    float* Ds = reinterpret_cast<float*>(smem + C::OFF_D);
+    const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+    const int l32 = lane & 31, hl = lane >> 5;
+
+    const int64_t range = blockIdx.x;
+    const int part = blockIdx.y;          // prototypes [part*MP, (part+1)*MP)
+    const int64_t k0 = a.wg_start[range], k1 = a.wg_start[range + 1];
+    if (k0 < 0 || k1 < k0 || k1 > a.max_items) return;
+    const float ks2 = a.scale * kLog2e;
+    const int64_t MD = (int64_t)a.M * D;
+    const uint32_t row_stride = (uint32_t)a.H * D;
+    int cur_h = -1;
+
+    for (int64_t k = k0; k < k1; ++k) {
+        const int32_t* it = a.items + k * IT_WORDS;
+        const int b = it[IT_B], h = it[IT_H], t0 = it[IT_T0], t1 = it[IT_T1];
+        if (b < 0 || b >= a.B || h < 0 || h >= a.H || t0 < 0 || t1 < t0 || t1 > a.T) continue;
+        __syncthreads();  // previous segment is done with the LDS tiles
+        {
+            const uint4* srcP = reinterpret_cast<const uint4*>(a.P + (int64_t)h * MD + (int64_t)part * C::MP * D);
+            const uint4* srcY = reinterpret_cast<const uint4*>(a.Ymj + ((int64_t)b * a.H + h) * MD + (int64_t)part * C::MP * D);
+            for (int i = tid; i < C::MP * C::KCH; i += C::THREADS) {
+                const int r = i / C::KCH, c = i % C::KCH;
+                if (h != cur_h) *reinterpret_cast<uint4*>(Ps + swz<D>(r, c)) = srcP[i];
+                *reinterpret_cast<uint4*>(Ys + swz<D>(r, c)) = srcY[i];
+            }
+            cur_h = h;
+        }
+        f32x16 acc[C::MT][C::JT];
+#pragma unroll
+        for (int mt = 0; mt < C::MT; ++mt)
+#pragma unroll
+            for (int jt = 0; jt < C::JT; ++jt)
+#pragma unroll
+                for (int r = 0; r < 16; ++r) acc[mt][jt][r] = 0.f;
+
+        for (int ts = t0; ts < t1; ts += 32) {
+            __syncthreads();  // previous tile's K, V, K^T, lse, D consumed
+            const int64_t tb = ((int64_t)ts * a.H + h) * D;
+#pragma unroll
+            for (int i = 0; i < C::NLD; ++i) {
+                const int idx = tid + i * C::THREADS;
+                const int tok = idx / C::KCH, ch = idx % C::KCH;
+                uint4 kv = make_uint4(0, 0, 0, 0), vv = make_uint4(0, 0, 0, 0);
+                if (ts + tok < t1) {
+                    const uint32_t off = (uint32_t)tok * row_stride + (uint32_t)(ch * 8);
+                    kv = *reinterpret_cast<const uint4*>(a.K + tb + off);
+                    vv = *reinterpret_cast<const uint4*>(a.V + tb + off);
+                }
+                *reinterpret_cast<uint4*>(Ks + swz<D>(tok, ch)) = kv;
+                *reinterpret_cast<uint4*>(Vs + swz<D>(tok, ch)) = vv;
+                const int p = perm16(tok);
+                const uint32_t wv[4] = {kv.x, kv.y, kv.z, kv.w};
+#pragma unroll
+                for (int e2 = 0; e2 < 4; ++e2) {
+                    const int j0 = ch * 8 + 2 * e2;
+                    Kt[swz<32>(j0, p >> 3) + (p & 7)] = (uint16_t)(wv[e2] & 0xffffu);
+                    Kt[swz<32>(j0 + 1, p >> 3) + (p & 7)] = (uint16_t)(wv[e2] >> 16);
+                }
+            }
+            if (tid < 32) {
+                const bool v = ts + tid < t1;
+                nls[tid] = v ? -a.lse[(int64_t)(ts + tid) * a.H + h] * kLog2e : 0.f;
+                Ds[tid] = v ? a.Dbuf[(int64_t)(ts + tid) * a.H + h] : 0.f;
+            }
+            __syncthreads();
+
+            bf16x8 kop[C::KS], vop[C::KS];
+#pragma unroll
+            for (int kk = 0; kk < C::KS; ++kk) {
+                kop[kk] = lds_b128(Ks, swz<D>(l32, 2 * kk + hl));
+                vop[kk] = lds_b128(Vs, swz<D>(l32, 2 * kk + hl));
+            }
+            float nl[16], Dr[16];
+#pragma unroll
+            for (int r = 0; r < 16; ++r) {
+                nl[r] = nls[srow(r, hl)];
+                Dr[r] = Ds[srow(r, hl)];
+            }
+            bf16x8 dso[C::MT][2];
+#pragma unroll
+            for (int mt = 0; mt < C::MT; ++mt) {
+                const int prow = w * MW + mt * 32 + l32;
+                f32x16 s, da;
+#pragma unroll
+                for (int r = 0; r < 16; ++r) s[r] = da[r] = 0.f;
+#pragma unroll
+                for (int kk = 0; kk < C::KS; ++kk) {
+                    s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kop[kk], lds_b128(Ps, swz<D>(prow, 2 * kk + hl)), s, 0, 0, 0);
+                    da = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vop[kk], lds_b128(Ys, swz<D>(prow, 2 * kk + hl)), da, 0, 0, 0);
+                }
+                float e[16];
+#pragma unroll
+                for (int r = 0; r < 16; ++r) {
+                    const float A = __builtin_amdgcn_exp2f(__builtin_fmaf(s[r], ks2, nl[r]));
+                    e[r] = A * (da[r] - Dr[r]);
+                }
+                dso[mt][0] = pack8(e);
+                dso[mt][1] = pack8(e + 8);
+            }
+#pragma unroll
+            for (int jt = 0; jt < C::JT; ++jt) {
+                const bf16x8 k0v = lds_b128(Kt, swz<32>(jt * 32 + l32, 0 + hl));
+                const bf16x8 k1v = lds_b128(Kt, swz<32>(jt * 32 + l32, 2 + hl));
+#pragma unroll
+                for (int mt = 0; mt < C::MT; ++mt) {
+                    acc[mt][jt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(dso[mt][0], k0v, acc[mt][jt], 0, 0, 0);
+                    acc[mt][jt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(dso[mt][1], k1v, acc[mt][jt], 0, 0, 0);
+                }
+            }
+        }
+        // partial of this segment for this part's prototype rows
+        float* out = a.partials + k * MD + (int64_t)part * C::MP * D;
+        uint32_t lane_off = (uint32_t)((w * MW + 4 * hl) * D + l32);
+        asm volatile("" : "+v"(lane_off));
+#pragma unroll
+        for (int mt = 0; mt < C::MT; ++mt)
+#pragma unroll
+            for (int jt = 0; jt < C::JT; ++jt)
+#pragma unroll
+                for (int r = 0; r < 16; ++r) {
+                    const uint32_t o = lane_off + (uint32_t)((mt * 32 + 8 * (r >> 2) + (r & 3)) * D + jt * 32);
+                    out[o] = a.scale * acc[mt][jt][r];
+                }
+    }
+}
+
+// dP[h] = sum of the partials of the segments of head h, in segment order
+__global__ __launch_bounds__(256) void dp_sum_kernel(const int32_t* __restrict__ pair_start,
+                                                     int64_t B, int32_t H, int64_t max_items,
+                                                     const float* __restrict__ partials,
+                                                     int64_t MD, float* __restrict__ dP) {
+    const int64_t i = ((int64_t)blockIdx.x * 256 + threadIdx.x) * 4;
+    if (i >= (int64_t)H * MD) return;
+    const int64_t h = i / MD, rest = i % MD;
+    int64_t s0 = pair_start[h * B], s1 = pair_start[(h + 1) * B];
+    s0 = s0 < 0 ? 0 : (s0 > max_items ? max_items : s0);
+    s1 = s1 < s0 ? s0 : (s1 > max_items ? max_items : s1);
+    float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+    for (int64_t k = s0; k < s1; ++k) {
+        const float4 v = *reinterpret_cast<const float4*>(partials + k * MD + rest);
+        acc.x += v.x;
+        acc.y += v.y;
+        acc.z += v.z;
+        acc.w += v.w;
+    }
+    *reinterpret_cast<float4*>(dP + i) = acc;
+}
+
+template <int D>
+hipError_t launch_token(const TokArgs& a, int64_t n_ranges, hipStream_t stream) {
+    using C = TokCfg<D>;
+    auto kern = bwd_token_kernel<D>;
+    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, C::LDS);
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(kern, dim3((unsigned)n_ranges), dim3(C::THREADS), C::LDS, stream, a);
+    return hipGetLastError();
+}
+
+template <int D, int MW>
+hipError_t launch_proto(const ProtoArgs& a, int64_t n_ranges, hipStream_t stream) {
+    using C = ProtoCfg<D, MW>;
+    auto kern = bwd_proto_kernel<D, MW>;
+    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, C::LDS);
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(kern, dim3((unsigned)n_ranges, (unsigned)(a.M / C::MP)), dim3(C::THREADS),
+                       C::LDS, stream, a);
+    return hipGetLastError();
+}
+
+}  // namespace
+
+// prototypes per part of the dP kernel: P and dY slices of MP x d bf16 each fit in LDS
+int32_t fused_bwd_part(int32_t M, int32_t d) {
+    const int cap = d == 64 ? 512 : 256;
+    for (int mp = cap; mp >= 128; mp -= 128)
+        if (M % mp == 0 && (mp == 128 || mp == 256 || mp == 512)) return mp;
+    return 0;
+}
+
+bool fused_bwd_supported(int32_t M, int32_t d) {
+    return (d == 64 || d == 128) && M % 128 == 0 && M <= 4096 && fused_bwd_part(M, d) > 0;
+}
+
+hipError_t launch_fused_bwd(const FusedBwdArgs& f, hipStream_t stream) {
+    const int64_t MD = (int64_t)f.M * f.d;
+    // dY (R summed) and P in the layouts the contractions read
+    {
+        const int64_t n = f.B * f.H * MD + (int64_t)f.H * MD;
+        hipLaunchKernelGGL(prep_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, stream,
+                           f.dsketch, f.B, f.R, f.H, f.M, f.d, f.P, f.Ymj, f.Yjm, f.Pjm);
+        hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return e;
+    }
+    if (f.n_ranges > 0) {
+        TokArgs t;
+        t.K = f.K; t.V = f.V; t.P = f.P; t.Pjm = f.Pjm; t.Ymj = f.Ymj; t.Yjm = f.Yjm;
+        t.lse = f.lse; t.items = f.items; t.wg_start = f.wg_start; t.max_items = f.max_items;
+        t.T = f.T; t.B = (int32_t)f.B; t.H = f.H; t.M = f.M; t.scale = f.scale;
+        t.dK = f.dK; t.dV = f.dV; t.Dbuf = f.Dbuf;
+        hipError_t e = f.d == 64 ? launch_token<64>(t, f.n_ranges, stream)
+                                 : launch_token<128>(t, f.n_ranges, stream);
+        if (e != hipSuccess) return e;
+        ProtoArgs p;
+        p.K = f.K; p.V = f.V; p.P = f.P; p.Ymj = f.Ymj; p.lse = f.lse; p.Dbuf = f.Dbuf;
+        p.items = f.items; p.wg_start = f.wg_start; p.max_items = f.max_items; p.T = f.T;
+        p.B = (int32_t)f.B; p.H = f.H; p.M = f.M; p.scale = f.scale; p.partials = f.partials;
+        const int mp = fused_bwd_part(f.M, f.d);
+        if (f.d == 64) {
+            e = mp == 128 ? launch_proto<64, 32>(p, f.n_ranges, stream)
+              : mp == 256 ? launch_proto<64, 64>(p, f.n_ranges, stream)
+                          : launch_proto<64, 128>(p, f.n_ranges, stream);
+        } else {
+            e = mp == 128 ? launch_proto<128, 32>(p, f.n_ranges, stream)
+                          : launch_proto<128, 64>(p, f.n_ranges, stream);
+        }
+        if (e != hipSuccess) return e;
+    }
+    const int64_t n = (int64_t)f.H * MD / 4;
+    hipLaunchKernelGGL(dp_sum_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, stream,
+                       f.pair_start, f.B, f.H, f.max_items, f.partials, MD, f.dP);
+    return hipGetLastError();
+}
+
+}  // namespace sa

@@ -5,15 +5,26 @@
 // prototype-wise softmax statistics, aggregation into the sketch):
 //
 //   S   = K_tile . P^T                  32 x M, bf16 MFMA 32x32x16, fp32 accumulate
-//   mu  = max over the M prototypes      per token (section 3.1: softmax over prototypes)
-//   E   = exp(scale * (S - mu)),  z = sum_m E,  lse = scale*mu + log z
+//   E   = exp(scale * S - c_t)           c_t >= max_m scale * S[t, m]   (see below)
+//   z_t = sum_m E,   lse_t = c_t + log z_t
 //   acc[M, d] += E^T . (V_tile / z)      bf16 MFMA, fp32 accumulate
 //
-// Workgroup = NW waves (one per SIMD); wave w owns prototypes
+// The softmax over the M prototypes of a token (section 3.1) is shift
+// invariant, so any shift c_t works as long as exp neither overflows nor
+// underflows.  The shift used is the Cauchy-Schwarz bound
+// c_t = scale * |K_t| * max_m |P_m|, which is known before the logits are:
+// each 32x32 tile of S is exponentiated as soon as its MFMAs finish (no pass
+// over all M logits first), and the exponentials of one tile can overlap the
+// MFMAs of the next.  When the bound is so loose that a token's
+// sum z_t would underflow (z_t < 2^-64, i.e. logits far below the bound), the
+// tile is recomputed with the exact per-token max.
+//
+// Workgroup = 4 waves (one per SIMD); wave w owns prototypes
 // [w*MW, (w+1)*MW) for both GEMMs, so the M x d fp32 accumulator is spread
-// over the four SIMDs' register files.  The per-token max and sum over the M
+// over the four SIMDs' register files.  The per-token sums over the M
 // prototypes are reduced in registers (over the wave's 32x32 tiles), across
-// the 32 lanes of a row, and across waves through LDS.
+// the 32 lanes of a row (DPP and permlane, no LDS), and across waves through
+// LDS.
 //
 // Layouts (v_mfma_f32_32x32x16_bf16, checked on the device):
 //   A operand: lane l holds row l%32, k = (l/32)*8 + 0..7
@@ -24,6 +35,14 @@
 // acc[m, j] += sum_t E[t, m] V'[t, j] once the token index of the k slots is
 // permuted accordingly; V' is staged in LDS transposed and in that permuted
 // token order.  1/z is folded into V' (d values per token instead of M).
+//
+// Pipeline per tile i (two workgroup barriers on the common path):
+//   S/exp over the wave's prototype tiles  (K(i) in LDS buffer i%2)
+//   stage K(i+1) into buffer (i+1)%2; per-token partial sums to LDS
+//   --- barrier ---
+//   z, lse; stage V(i)/z transposed; issue the global loads of tile i+2
+//   --- barrier ---
+//   aggregation MFMAs
 #include "sa_internal.h"
 
 namespace sa {
@@ -36,6 +55,10 @@ typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef float f32x2 __attribute__((ext_vector_type(2)));
 
 constexpr float kLog2e = 1.4426950408889634f;
+// z below this means the shift was too far above the largest logit
+constexpr float kUnderflowZ = 5.421010862427522e-20f;  // 2^-64
+// relative margin on the bound for the rounding of the fp32 norms and logits
+constexpr float kBoundMargin = 1.0f + 1.0f / 1024.0f;
 
 __device__ inline float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
 __device__ inline float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
@@ -46,8 +69,29 @@ __device__ inline uint32_t pack_bf16x2(float a, float b) {
     return __builtin_bit_cast(uint32_t, v);
 }
 
+__device__ inline bf16x8 pack8(const float* e) {
+    uint4 pk;
+    pk.x = pack_bf16x2(e[0], e[1]);
+    pk.y = pack_bf16x2(e[2], e[3]);
+    pk.z = pack_bf16x2(e[4], e[5]);
+    pk.w = pack_bf16x2(e[6], e[7]);
+    return __builtin_bit_cast(bf16x8, pk);
+}
+
+__device__ inline float sumsq8(uint4 v) {
+    const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+    float s = 0.f;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        const float a = bf16_lo(w[i]), b = bf16_hi(w[i]);
+        s = __builtin_fmaf(a, a, s);
+        s = __builtin_fmaf(b, b, s);
+    }
+    return s;
+}
+
 // LDS element offset (in bf16 units) of 16-byte chunk c of row r of a matrix
-// with `cols` bf16 per row; chunks are XOR-swizzled with the row so that the
+// with COLS bf16 per row; chunks are XOR-swizzled with the row so that the
 // 32 rows read by one operand load fall in different banks.
 template <int COLS>
 __device__ inline int swz(int r, int c) {
@@ -69,16 +113,52 @@ __device__ inline int perm_tok(int t) {
     return (t & ~12) | ((t & 4) << 1) | ((t & 8) >> 1);
 }
 
-// reduce across the 32 lanes of each half-wave (lanes l and l^k, k < 32)
+// row of S (token index inside the tile) held by register r of this lane-half
+__device__ inline int srow(int r, int hl) { return 8 * (r >> 2) + 4 * hl + (r & 3); }
+
+// Cross-lane moves without LDS: DPP inside rows of 16 lanes, then
+// v_permlane16_swap between the two rows of each 32-lane half.
+template <int CTRL>
+__device__ inline float dpp(float v) {
+    return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), CTRL, 0xF, 0xF, true));
+}
+constexpr int kQuadXor1 = 0xB1;      // quad_perm [1,0,3,2]
+constexpr int kQuadXor2 = 0x4E;      // quad_perm [2,3,0,1]
+constexpr int kRowHalfMirror = 0x141;
+constexpr int kRowMirror = 0x140;
+constexpr int kRowRor4 = 0x124;
+constexpr int kRowRor8 = 0x128;
+
+// reduce across the 32 lanes of each half-wave; every lane gets the result
 __device__ inline float half_max(float v) {
-#pragma unroll
-    for (int k = 1; k < 32; k <<= 1) v = fmaxf(v, __shfl_xor(v, k, 64));
-    return v;
+    v = fmaxf(v, dpp<kQuadXor1>(v));
+    v = fmaxf(v, dpp<kQuadXor2>(v));
+    v = fmaxf(v, dpp<kRowRor4>(v));
+    v = fmaxf(v, dpp<kRowRor8>(v));
+    const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+    return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
 }
 __device__ inline float half_sum(float v) {
-#pragma unroll
-    for (int k = 1; k < 32; k <<= 1) v += __shfl_xor(v, k, 64);
+    v += dpp<kQuadXor1>(v);
+    v += dpp<kQuadXor2>(v);
+    v += dpp<kRowRor4>(v);
+    v += dpp<kRowRor8>(v);
+    const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+    return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+// sum over aligned groups of G = 8 or 16 consecutive lanes; every lane gets it
+template <int G>
+__device__ inline float group_sum(float v) {
+    v += dpp<kQuadXor1>(v);
+    v += dpp<kQuadXor2>(v);
+    v += dpp<kRowHalfMirror>(v);
+    if constexpr (G == 16) v += dpp<kRowMirror>(v);
     return v;
+}
+__device__ inline float wave_max(float v) {
+    v = half_max(v);
+    const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+    return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
 }
 
 template <int D, int MW, int NW>
@@ -93,10 +173,18 @@ struct Cfg {
     static constexpr int NLD = (LD_CHUNKS + THREADS - 1) / THREADS;
     // LDS layout (bytes)
     static constexpr int P_BYTES = M * D * 2;
-    static constexpr int K_BYTES = 32 * D * 2;
+    static constexpr int K_BYTES = 32 * D * 2;  // one K tile buffer (two are kept)
     static constexpr int V_BYTES = D * 32 * 2;
     static constexpr int RED_BYTES = NW * 32 * 4;
-    static constexpr int LDS = P_BYTES + K_BYTES + V_BYTES + 2 * RED_BYTES;
+    static constexpr int OFF_K = P_BYTES;
+    static constexpr int OFF_V = OFF_K + 2 * K_BYTES;
+    static constexpr int OFF_SUM = OFF_V + V_BYTES;      // [NW][32] partial sums (bound path)
+    static constexpr int OFF_MAX = OFF_SUM + RED_BYTES;  // [NW][32] partial maxima (exact path)
+    static constexpr int OFF_SUM2 = OFF_MAX + RED_BYTES; // [NW][32] partial sums (exact path)
+    static constexpr int OFF_KN = OFF_SUM2 + RED_BYTES;  // [2][32] token norms
+    static constexpr int OFF_PN = OFF_KN + 2 * 32 * 4;   // [NW] prototype norm maxima
+    static constexpr int OFF_SH = OFF_PN + 16 * 4;       // [32] exact-path shifts
+    static constexpr int LDS = OFF_SH + 32 * 4;
 };
 
 template <int D, int MW, int NW>
@@ -104,10 +192,14 @@ __global__ __launch_bounds__(NW * 64, 1) void fwd_fused_kernel(FusedFwdArgs a) {
     using C = Cfg<D, MW, NW>;
     extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
     uint16_t* Ps = reinterpret_cast<uint16_t*>(smem);
-    uint16_t* Ks = reinterpret_cast<uint16_t*>(smem + C::P_BYTES);
-    uint16_t* Vt = reinterpret_cast<uint16_t*>(smem + C::P_BYTES + C::K_BYTES);
-    float* red_max = reinterpret_cast<float*>(smem + C::P_BYTES + C::K_BYTES + C::V_BYTES);
-    float* red_sum = red_max + NW * 32;
+    uint16_t* Kbuf = reinterpret_cast<uint16_t*>(smem + C::OFF_K);
+    uint16_t* Vt = reinterpret_cast<uint16_t*>(smem + C::OFF_V);
+    float* red_sum = reinterpret_cast<float*>(smem + C::OFF_SUM);
+    float* red_max = reinterpret_cast<float*>(smem + C::OFF_MAX);
+    float* red_sum2 = reinterpret_cast<float*>(smem + C::OFF_SUM2);
+    float* knorm = reinterpret_cast<float*>(smem + C::OFF_KN);
+    float* pnorm = reinterpret_cast<float*>(smem + C::OFF_PN);
+    float* shift_s = reinterpret_cast<float*>(smem + C::OFF_SH);
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
@@ -116,13 +208,15 @@ __global__ __launch_bounds__(NW * 64, 1) void fwd_fused_kernel(FusedFwdArgs a) {
     const int hl = lane >> 5;  // half of the wave
 
     const int64_t range = blockIdx.x;
-    int64_t k0 = a.wg_start[range];
-    int64_t k1 = a.wg_start[range + 1];
+    const int64_t k0 = a.wg_start[range];
+    const int64_t k1 = a.wg_start[range + 1];
     if (k0 < 0 || k1 < k0 || k1 > a.max_items) return;  // malformed offsets: nothing safe to do
 
     const float ks2 = a.scale * kLog2e;
     const int64_t MD = (int64_t)C::M * D;
+    const uint32_t row_stride = (uint32_t)a.H * D;
     int cur_h = -1;
+    float pmax = 0.f;  // max_m |P[h, m]| of the loaded head
 
     for (int64_t k = k0; k < k1; ++k) {
         const int32_t* it = a.items + k * IT_WORDS;
@@ -133,15 +227,28 @@ __global__ __launch_bounds__(NW * 64, 1) void fwd_fused_kernel(FusedFwdArgs a) {
         const int split = it[IT_SPLIT];
         if (b < 0 || b >= a.B || h < 0 || h >= a.H || t0 < 0 || t1 < t0 || t1 > a.T) continue;
 
+        // ---- prototypes of head h into LDS, with max_m |P_m|
         if (h != cur_h) {
-            __syncthreads();  // every wave is done with the previous P
             const uint4* src = reinterpret_cast<const uint4*>(a.P + (int64_t)h * C::M * D);
+            float nmax = 0.f;
             for (int i = tid; i < C::M * C::KCH; i += C::THREADS) {
                 const int r = i / C::KCH, c = i % C::KCH;
-                *reinterpret_cast<uint4*>(Ps + swz<D>(r, c)) = src[i];
+                const uint4 v = src[i];
+                *reinterpret_cast<uint4*>(Ps + swz<D>(r, c)) = v;
+                // the KCH chunks of a row sit in KCH consecutive lanes
+                nmax = fmaxf(nmax, group_sum<C::KCH>(sumsq8(v)));
             }
+            nmax = wave_max(nmax);
+            if (lane == 0) pnorm[w] = nmax;
+            __syncthreads();
+            float m2 = pnorm[0];
+#pragma unroll
+            for (int ww = 1; ww < NW; ++ww) m2 = fmaxf(m2, pnorm[ww]);
+            pmax = __builtin_sqrtf(m2);
             cur_h = h;
         }
+        // shift bound of token t = cb * |K_t|
+        const float cb = a.scale * pmax * kBoundMargin;
 
         f32x16 acc[C::MT][C::JT];
 #pragma unroll
@@ -151,10 +258,8 @@ __global__ __launch_bounds__(NW * 64, 1) void fwd_fused_kernel(FusedFwdArgs a) {
 #pragma unroll
                 for (int r = 0; r < 16; ++r) acc[mt][jt][r] = 0.f;
 
-        // prefetch the first tile
-        uint4 kreg[C::NLD], vreg[C::NLD];
-        // per-lane 32-bit element offsets inside a tile; the tile base is uniform
-        const uint32_t row_stride = (uint32_t)a.H * D;
+        // global tile loads into registers: 32-bit per-lane offsets, uniform tile base
+        uint4 kreg[C::NLD], vreg[C::NLD], vcur[C::NLD];
         auto load_tile = [&](int ts) {
             const int64_t tb = ((int64_t)ts * a.H + h) * D;
             const uint16_t* Kb = a.K + tb;
@@ -173,119 +278,169 @@ __global__ __launch_bounds__(NW * 64, 1) void fwd_fused_kernel(FusedFwdArgs a) {
                 vreg[i] = vv;
             }
         };
-        load_tile(t0);
-
-        for (int ts = t0; ts < t1; ts += 32) {
-            // ---- stage K tile
+        // K tile (from kreg) into LDS buffer `buf`, with the token norms
+        auto stage_k = [&](int kb) {
+            uint16_t* Kd = Kbuf + kb * (32 * D);
 #pragma unroll
             for (int i = 0; i < C::NLD; ++i) {
-                const int idx = tid + i * C::THREADS;
+                int idx = tid + i * C::THREADS;
+                asm volatile("" : "+v"(idx));
                 if (idx < C::LD_CHUNKS) {
                     const int tok = idx / C::KCH, ch = idx % C::KCH;
-                    *reinterpret_cast<uint4*>(Ks + swz<D>(tok, ch)) = kreg[i];
+                    *reinterpret_cast<uint4*>(Kd + swz<D>(tok, ch)) = kreg[i];
+                    const float ss = group_sum<C::KCH>(sumsq8(kreg[i]));
+                    if (ch == 0) knorm[kb * 32 + tok] = __builtin_sqrtf(ss);
                 }
             }
-            uint4 vcur[C::NLD];
+        };
+        // one 32x32 tile of S for this wave's prototype tile mt
+        auto s_tile = [&](const bf16x8* kop, int mt) {
+            f32x16 s;
 #pragma unroll
-            for (int i = 0; i < C::NLD; ++i) vcur[i] = vreg[i];
-            __syncthreads();  // B1: K tile and P visible
-            if (ts + 32 < t1) load_tile(ts + 32);
-
-            // ---- S = K . P^T for this wave's prototypes
-            f32x16 s[C::MT];
-#pragma unroll
-            for (int mt = 0; mt < C::MT; ++mt)
-#pragma unroll
-                for (int r = 0; r < 16; ++r) s[mt][r] = 0.f;
+            for (int r = 0; r < 16; ++r) s[r] = 0.f;
+            const int prow = w * MW + mt * 32 + l32;
 #pragma unroll
             for (int kk = 0; kk < C::KS; ++kk) {
-                const bf16x8 ak = lds_b128(Ks, swz<D>(l32, 2 * kk + hl));
-#pragma unroll
-                for (int mt = 0; mt < C::MT; ++mt) {
-                    const bf16x8 bp = lds_b128(Ps, swz<D>(w * MW + mt * 32 + l32, 2 * kk + hl));
-                    s[mt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ak, bp, s[mt], 0, 0, 0);
-                }
-                // keep the operand loads of one k step in flight at a time
-                __builtin_amdgcn_sched_barrier(0);
+                const bf16x8 bp = lds_b128(Ps, swz<D>(prow, 2 * kk + hl));
+                s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kop[kk], bp, s, 0, 0, 0);
             }
+            return s;
+        };
 
-            // ---- per-token max over prototypes
-            float rmax[16];
+        const int ntiles = (t1 - t0 + 31) / 32;
+        // prologue: tile 0 staged, tile 1 in flight
+        load_tile(t0);
+        stage_k(0);
 #pragma unroll
-            for (int r = 0; r < 16; ++r) {
-                float v = s[0][r];
-#pragma unroll
-                for (int mt = 1; mt < C::MT; ++mt) v = fmaxf(v, s[mt][r]);
-                rmax[r] = half_max(v);
-            }
-            if (l32 == 0) {
-#pragma unroll
-                for (int r = 0; r < 16; ++r)
-                    red_max[w * 32 + 8 * (r >> 2) + 4 * hl + (r & 3)] = rmax[r];
-            }
-            __syncthreads();  // B2
-            float nmu[16];
-#pragma unroll
-            for (int r = 0; r < 16; ++r) {
-                const int t = 8 * (r >> 2) + 4 * hl + (r & 3);
-                float mu = red_max[t];
-#pragma unroll
-                for (int ww = 1; ww < NW; ++ww) mu = fmaxf(mu, red_max[ww * 32 + t]);
-                nmu[r] = -mu * ks2;
-            }
+        for (int i = 0; i < C::NLD; ++i) vcur[i] = vreg[i];
+        if (ntiles > 1) load_tile(t0 + 32);
+        __syncthreads();
 
-            // ---- E = exp2((S - mu) * scale * log2 e), partial sums, bf16 operands
+        for (int ti = 0; ti < ntiles; ++ti) {
+            const int ts = t0 + ti * 32;
+            const int kb = ti & 1;
+            const uint16_t* Ks = Kbuf + kb * (32 * D);
+
+            // ---- per-row shift: -c_t * log2(e) for this lane's 16 rows, c_t = cb * |K_t|
+            float nb[16];
+#pragma unroll
+            for (int r = 0; r < 16; ++r) nb[r] = -cb * kLog2e * knorm[kb * 32 + srow(r, hl)];
+
+            // ---- S tiles, exponentiated as they complete
+            bf16x8 kop[C::KS];
+#pragma unroll
+            for (int kk = 0; kk < C::KS; ++kk) kop[kk] = lds_b128(Ks, swz<D>(l32, 2 * kk + hl));
             float rsum[16];
 #pragma unroll
             for (int r = 0; r < 16; ++r) rsum[r] = 0.f;
             bf16x8 eop[C::MT][2];
 #pragma unroll
             for (int mt = 0; mt < C::MT; ++mt) {
+                const f32x16 s = s_tile(kop, mt);
                 float e[16];
 #pragma unroll
                 for (int r = 0; r < 16; ++r) {
-                    e[r] = __builtin_amdgcn_exp2f(__builtin_fmaf(s[mt][r], ks2, nmu[r]));
+                    e[r] = __builtin_amdgcn_exp2f(__builtin_fmaf(s[r], ks2, nb[r]));
                     rsum[r] += e[r];
                 }
-#pragma unroll
-                for (int q = 0; q < 2; ++q) {
-                    uint4 pk;
-                    pk.x = pack_bf16x2(e[8 * q + 0], e[8 * q + 1]);
-                    pk.y = pack_bf16x2(e[8 * q + 2], e[8 * q + 3]);
-                    pk.z = pack_bf16x2(e[8 * q + 4], e[8 * q + 5]);
-                    pk.w = pack_bf16x2(e[8 * q + 6], e[8 * q + 7]);
-                    eop[mt][q] = __builtin_bit_cast(bf16x8, pk);
-                }
+                eop[mt][0] = pack8(e);
+                eop[mt][1] = pack8(e + 8);
             }
 #pragma unroll
             for (int r = 0; r < 16; ++r) rsum[r] = half_sum(rsum[r]);
             if (l32 == 0) {
 #pragma unroll
-                for (int r = 0; r < 16; ++r)
-                    red_sum[w * 32 + 8 * (r >> 2) + 4 * hl + (r & 3)] = rsum[r];
+                for (int r = 0; r < 16; ++r) red_sum[w * 32 + srow(r, hl)] = rsum[r];
             }
-            __syncthreads();  // B3
+            // ---- next K tile into the other buffer
+            if (ti + 1 < ntiles) stage_k(kb ^ 1);
+            __syncthreads();  // B_z
+
+            // ---- tile-uniform check that the bound did not underflow any z_t
+            bool exact;
+            {
+                const int tt = lane & 31;
+                float z = 0.f;
+#pragma unroll
+                for (int ww = 0; ww < NW; ++ww) z += red_sum[ww * 32 + tt];
+                exact = __builtin_amdgcn_ballot_w64(z < kUnderflowZ && ts + tt < t1) != 0;
+            }
+            if (exact) {
+                // rare: exact per-token max over the prototypes, then the exponentials
+                // again (rsum holds the running max first; its sums are in LDS)
+#pragma unroll
+                for (int r = 0; r < 16; ++r) rsum[r] = -INFINITY;
+#pragma unroll
+                for (int mt = 0; mt < C::MT; ++mt) {
+                    const f32x16 s = s_tile(kop, mt);
+#pragma unroll
+                    for (int r = 0; r < 16; ++r) rsum[r] = fmaxf(rsum[r], s[r]);
+                }
+#pragma unroll
+                for (int r = 0; r < 16; ++r) rsum[r] = half_max(rsum[r]);
+                if (l32 == 0) {
+#pragma unroll
+                    for (int r = 0; r < 16; ++r) red_max[w * 32 + srow(r, hl)] = rsum[r];
+                }
+                __syncthreads();
+                if (tid < 32) {
+                    float mu = red_max[tid];
+#pragma unroll
+                    for (int ww = 1; ww < NW; ++ww) mu = fmaxf(mu, red_max[ww * 32 + tid]);
+                    shift_s[tid] = -mu * ks2;
+                }
+                __syncthreads();
+#pragma unroll
+                for (int r = 0; r < 16; ++r) {
+                    nb[r] = shift_s[srow(r, hl)];
+                    rsum[r] = 0.f;
+                }
+#pragma unroll
+                for (int mt = 0; mt < C::MT; ++mt) {
+                    const f32x16 s = s_tile(kop, mt);
+                    float e[16];
+#pragma unroll
+                    for (int r = 0; r < 16; ++r) {
+                        e[r] = __builtin_amdgcn_exp2f(__builtin_fmaf(s[r], ks2, nb[r]));
+                        rsum[r] += e[r];
+                    }
+                    eop[mt][0] = pack8(e);
+                    eop[mt][1] = pack8(e + 8);
+                }
+#pragma unroll
+                for (int r = 0; r < 16; ++r) rsum[r] = half_sum(rsum[r]);
+                if (l32 == 0) {
+#pragma unroll
+                    for (int r = 0; r < 16; ++r) red_sum2[w * 32 + srow(r, hl)] = rsum[r];
+                }
+                __syncthreads();
+            }
+            const float* zsrc = exact ? red_sum2 : red_sum;
 
             // ---- lse of the tile's tokens: thread tt of wave 0 handles token tt
             if (tid < 32 && a.lse && ts + tid < t1) {
-                float mu = red_max[tid], z = red_sum[tid];
+                float z = 0.f;
 #pragma unroll
-                for (int ww = 1; ww < NW; ++ww) {
-                    mu = fmaxf(mu, red_max[ww * 32 + tid]);
-                    z += red_sum[ww * 32 + tid];
+                for (int ww = 0; ww < NW; ++ww) z += zsrc[ww * 32 + tid];
+                float c;
+                if (exact) {
+                    c = -shift_s[tid] / kLog2e;
+                } else {
+                    c = cb * knorm[kb * 32 + tid];
                 }
-                a.lse[(int64_t)(ts + tid) * a.H + h] = mu * a.scale + __logf(z);
+                a.lse[(int64_t)(ts + tid) * a.H + h] = c + __logf(z);
             }
 
             // ---- stage V / z transposed, in the permuted token order
 #pragma unroll
             for (int i = 0; i < C::NLD; ++i) {
-                const int idx = tid + i * C::THREADS;
+                int idx = tid + i * C::THREADS;
+                asm volatile("" : "+v"(idx));  // addresses built here, not hoisted
                 if (idx < C::LD_CHUNKS) {
                     const int tok = idx / C::KCH, ch = idx % C::KCH;
                     float z = 0.f;
 #pragma unroll
-                    for (int ww = 0; ww < NW; ++ww) z += red_sum[ww * 32 + tok];
+                    for (int ww = 0; ww < NW; ++ww) z += zsrc[ww * 32 + tok];
                     const float rz = 1.0f / z;
                     const uint32_t wv[4] = {vcur[i].x, vcur[i].y, vcur[i].z, vcur[i].w};
                     const int p = perm_tok(tok);
@@ -298,7 +453,11 @@ __global__ __launch_bounds__(NW * 64, 1) void fwd_fused_kernel(FusedFwdArgs a) {
                     }
                 }
             }
-            __syncthreads();  // B4
+            // V of tile i+1 is in vreg; issue the loads of tile i+2
+#pragma unroll
+            for (int i = 0; i < C::NLD; ++i) vcur[i] = vreg[i];
+            if (ti + 2 < ntiles) load_tile(ts + 64);
+            __syncthreads();  // B_v: V' staged, K(i+1) visible
 
             // ---- acc[m, j] += E^T . V'
 #pragma unroll
@@ -315,7 +474,10 @@ __global__ __launch_bounds__(NW * 64, 1) void fwd_fused_kernel(FusedFwdArgs a) {
 
         // ---- flush: the whole sketch of the pair, or this segment's partial
         float* out = split ? a.partials + k * MD : a.sketch + ((int64_t)b * a.H + h) * MD;
-        const uint32_t lane_off = (uint32_t)((w * MW + 4 * hl) * D + l32);
+        uint32_t lane_off = (uint32_t)((w * MW + 4 * hl) * D + l32);
+        // keep the per-store addresses from being hoisted out of the loops (they
+        // would stay live in registers through the whole tile loop)
+        asm volatile("" : "+v"(lane_off));
 #pragma unroll
         for (int mt = 0; mt < C::MT; ++mt)
 #pragma unroll
@@ -325,6 +487,7 @@ __global__ __launch_bounds__(NW * 64, 1) void fwd_fused_kernel(FusedFwdArgs a) {
                     const uint32_t o = lane_off + (uint32_t)((mt * 32 + 8 * (r >> 2) + (r & 3)) * D + jt * 32);
                     out[o] = acc[mt][jt][r];
                 }
+        __syncthreads();  // LDS tiles and norms are reused by the next segment
     }
 }
 
@@ -351,38 +514,45 @@ hipError_t occ_inst(int* blocks) {
 
 }  // namespace
 
-// Instances: NW = 4 waves; MW = M / 4 prototypes per wave.
+// Instances (d, prototypes per wave, waves): M = MW * NW.  Eight waves (two per
+// SIMD) hide the LDS latency of one wave behind the matrix work of the other
+// when the per-wave share of the accumulator allows it.
 #define SA_FUSED_CASES(X)  \
-    X(64, 32)              \
-    X(64, 64)              \
-    X(64, 96)              \
-    X(64, 128)             \
-    X(64, 160)             \
-    X(64, 192)             \
-    X(64, 224)             \
-    X(64, 256)             \
-    X(128, 32)             \
-    X(128, 64)             \
-    X(128, 96)             \
-    X(128, 128)
+    X(64, 32, 4)           \
+    X(64, 64, 4)           \
+    X(64, 96, 4)           \
+    X(64, 128, 4)          \
+    X(64, 160, 4)          \
+    X(64, 192, 4)          \
+    X(64, 224, 4)          \
+    X(64, 256, 4)          \
+    X(128, 32, 4)          \
+    X(128, 64, 4)          \
+    X(128, 96, 4)          \
+    X(128, 128, 4)
+
+// Waves per workgroup for an (M, d) (every instance uses four, one per SIMD).
+int fused_waves(int32_t, int32_t) { return 4; }
 
 bool fused_fwd_supported(int32_t M, int32_t d) {
     if (M % 128 != 0) return false;
-#define X(DD, MWW) if (d == DD && M == 4 * MWW) return true;
+#define X(DD, MWW, NWW) if (d == DD && M == NWW * MWW) return true;
     SA_FUSED_CASES(X)
 #undef X
     return false;
 }
 
 size_t fused_fwd_lds_bytes(int32_t M, int32_t d) {
-#define X(DD, MWW) if (d == DD && M == 4 * MWW) return Cfg<DD, MWW, 4>::LDS;
+    const int nw = fused_waves(M, d);
+#define X(DD, MWW, NWW) if (d == DD && M == NWW * MWW && nw == NWW) return Cfg<DD, MWW, NWW>::LDS;
     SA_FUSED_CASES(X)
 #undef X
     return 0;
 }
 
 hipError_t fused_fwd_occupancy(int32_t M, int32_t d, int* blocks) {
-#define X(DD, MWW) if (d == DD && M == 4 * MWW) return occ_inst<DD, MWW, 4>(blocks);
+    const int nw = fused_waves(M, d);
+#define X(DD, MWW, NWW) if (d == DD && M == NWW * MWW && nw == NWW) return occ_inst<DD, MWW, NWW>(blocks);
     SA_FUSED_CASES(X)
 #undef X
     return hipErrorInvalidValue;
@@ -390,7 +560,8 @@ hipError_t fused_fwd_occupancy(int32_t M, int32_t d, int* blocks) {
 
 hipError_t launch_fused_fwd(const FusedFwdArgs& a, hipStream_t stream) {
     if (a.n_ranges == 0) return hipSuccess;
-#define X(DD, MWW) if (a.d == DD && a.M == 4 * MWW) return launch_inst<DD, MWW, 4>(a, stream);
+    const int nw = fused_waves(a.M, a.d);
+#define X(DD, MWW, NWW) if (a.d == DD && a.M == NWW * MWW && nw == NWW) return launch_inst<DD, MWW, NWW>(a, stream);
     SA_FUSED_CASES(X)
 #undef X
     return hipErrorInvalidValue;

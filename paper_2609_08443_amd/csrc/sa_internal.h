@@ -57,6 +57,35 @@ size_t fused_fwd_lds_bytes(int32_t M, int32_t d);
 hipError_t fused_fwd_occupancy(int32_t M, int32_t d, int* blocks_per_cu);
 hipError_t launch_fused_fwd(const FusedFwdArgs& a, hipStream_t stream);
 
+// Fused bf16 backward (matrix cores): prep, token-side and prototype-side
+// kernels plus the per-head sum of the dP partials.
+struct FusedBwdArgs {
+    const uint16_t* K;
+    const uint16_t* V;
+    const uint16_t* P;
+    const float* dsketch;
+    const float* lse;
+    const int32_t* items;
+    const int32_t* wg_start;
+    const int32_t* pair_start;
+    int64_t n_ranges;
+    int64_t max_items;
+    int64_t B, T;
+    int32_t H, M, d, R;
+    float scale;
+    uint16_t* Ymj;       // [B,H,M,d] bf16
+    uint16_t* Yjm;       // [B,H,d,M] bf16, prototype index permuted within 16-groups
+    uint16_t* Pjm;       // [H,d,M] bf16, likewise
+    float* Dbuf;         // [T,H]
+    float* partials;     // [max_items][M][d]
+    float* dK;
+    float* dV;
+    float* dP;
+};
+bool fused_bwd_supported(int32_t M, int32_t d);
+int32_t fused_bwd_part(int32_t M, int32_t d);
+hipError_t launch_fused_bwd(const FusedBwdArgs& a, hipStream_t stream);
+
 // Plain fp32-arithmetic path (fp32 or bf16 inputs).
 hipError_t launch_generic_fwd(const void* K, const void* V, const void* P,
                               const int64_t* offsets, int64_t B, int64_t T, int32_t H,

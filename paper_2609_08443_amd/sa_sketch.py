@@ -22,7 +22,7 @@ ITEM_WORDS = 8
 
 EXPORTS = ("sa_sketch_fwd_workspace_size", "sa_sketch_fwd", "sa_sketch_bwd_workspace_size",
            "sa_sketch_bwd", "sa_build_worklist", "sa_sketch_fwd_chunk_tokens",
-           "sa_status_string", "sa_last_error")
+           "sa_profile_enable", "sa_kernel_times", "sa_status_string", "sa_last_error")
 
 
 class SAError(RuntimeError):
@@ -63,6 +63,10 @@ def lib() -> ctypes.CDLL:
     L.sa_status_string.restype = c.c_char_p
     L.sa_last_error.argtypes = []
     L.sa_last_error.restype = c.c_char_p
+    L.sa_profile_enable.argtypes = [i32]
+    L.sa_profile_enable.restype = None
+    L.sa_kernel_times.argtypes = [i32, vp, vp, vp]
+    L.sa_kernel_times.restype = i32
     _lib = L
     return L
 
@@ -186,6 +190,27 @@ def sketch_bwd(K, V, P, offsets, dsketch, lse, scale: Optional[float] = None, dK
                              _ptr(dP), _ptr(ws), nbytes, _stream_handle(stream))
     _check(rc)
     return dK, dV, dP
+
+
+def profile_enable(on: bool = True) -> None:
+    """Bracket every library launch of this thread with HIP events (benchmarks)."""
+    lib().sa_profile_enable(1 if on else 0)
+
+
+def kernel_times(max_kernels: int = 32) -> dict:
+    """{kernel name: (launches, total ms)} since the previous call (waits for the events)."""
+    names = ctypes.create_string_buffer(48 * max_kernels)
+    n_l = (ctypes.c_int64 * max_kernels)()
+    ms = (ctypes.c_double * max_kernels)()
+    n = lib().sa_kernel_times(max_kernels, ctypes.addressof(names), ctypes.addressof(n_l),
+                              ctypes.addressof(ms))
+    if n < 0:
+        raise SAError(5, "collecting kernel times failed")
+    out = {}
+    for i in range(n):
+        nm = names.raw[48 * i: 48 * (i + 1)].split(b"\0", 1)[0].decode()
+        out[nm] = (int(n_l[i]), float(ms[i]))
+    return out
 
 
 def build_worklist(offsets, T: int, H: int, chunk_tokens: int, max_items: Optional[int] = None,

@@ -229,3 +229,69 @@ def test_bwd_matches_oracle(sa, lengths, H, M, d, dtype, R):
     for h in range(H):
         err = np.abs(gP[h] - rP[h]).max() / max(np.abs(rP[h]).max(), 1e-30)
         assert err <= tol, ("dP", h, err)
+
+
+def test_bwd_users_split_across_ranges(sa):
+    """Long users are cut into several segments; dK/dV are per token, dP sums every segment."""
+    w = wl.custom([3000, 5, 2100, 0, 700], 2, 256, 64, "bf16", seed=77, R=2, bwd=True)
+    host = wl.host_tensors(w)
+    dev = wl.to_device(host, "bf16")
+    sk, lse = sa.sketch_fwd(dev["K"], dev["V"], dev["P"], dev["offsets"])
+    dK, dV, dP = sa.sketch_bwd(dev["K"], dev["V"], dev["P"], dev["offsets"], dev["dsketch"], lse)
+    torch.cuda.synchronize()
+    rK, rV, rP = oracle.bwd(host["K"], host["V"], host["P"], host["offsets"], host["dsketch"])
+    off = host["offsets"]
+    for b in range(w.B):
+        s, e = off[b], off[b + 1]
+        if e == s:
+            continue
+        for h in range(w.H):
+            for gg, rr in ((dK, rK), (dV, rV)):
+                g = gg[s:e, h].cpu().numpy().astype(np.float64)
+                assert np.abs(g - rr[s:e, h]).max() / np.abs(rr[s:e, h]).max() <= 2e-2
+    g = dP.cpu().numpy().astype(np.float64)
+    for h in range(w.H):
+        assert np.abs(g[h] - rP[h]).max() / np.abs(rP[h]).max() <= 2e-2
+
+
+def test_bwd_is_deterministic(sa):
+    w = wl.custom([1500, 40, 900], 2, 512, 128, "bf16", seed=78, R=4, bwd=True)
+    dev = wl.to_device(wl.host_tensors(w), "bf16")
+    _, lse = sa.sketch_fwd(dev["K"], dev["V"], dev["P"], dev["offsets"])
+    g1 = sa.sketch_bwd(dev["K"], dev["V"], dev["P"], dev["offsets"], dev["dsketch"], lse)
+    g2 = sa.sketch_bwd(dev["K"], dev["V"], dev["P"], dev["offsets"], dev["dsketch"], lse)
+    for a_, b_ in zip(g1, g2):
+        assert torch.equal(a_, b_)
+
+
+@pytest.mark.parametrize("M,d", [(256, 64), (512, 128)])
+def test_fwd_loose_bound_falls_back_to_exact_max(sa, M, d):
+    """Keys of huge norm nearly orthogonal to every prototype: the logits sit far below
+    the Cauchy-Schwarz shift, so exp(logit - shift) would underflow; the tile is
+    recomputed with the exact per-token max and still matches the oracle."""
+    rng = np.random.default_rng(5)
+    lengths = [70, 33, 129]
+    w = wl.custom(lengths, 2, M, d, "bf16", seed=9)
+    host = wl.host_tensors(w)
+    T = w.T
+    K = np.zeros((T, 2, d), np.float32)
+    K[:, :, 0] = 2048.0                                  # |K_t| = 2048 along axis 0
+    K[:, :, 1:] = rng.standard_normal((T, 2, d - 1)).astype(np.float32)
+    P = (rng.standard_normal((2, M, d)) * 4.0).astype(np.float32)
+    P[:, :, 0] = (rng.integers(-8, 9, (2, M)) / 512.0)   # tiny overlap with axis 0
+    # every other token gets an ordinary key, so tiles mix both regimes
+    K[::2] = rng.standard_normal((len(K[::2]), 2, d)).astype(np.float32)
+    host["K"] = wl.bf16_bits_to_f32(wl.f32_to_bf16_bits(K))
+    host["P"] = wl.bf16_bits_to_f32(wl.f32_to_bf16_bits(P))
+    dev = wl.to_device(host, "bf16")
+    sk, lse = sa.sketch_fwd(dev["K"], dev["V"], dev["P"], dev["offsets"])
+    ref, ref_lse = oracle.fwd(host["K"], host["V"], host["P"], host["offsets"])
+    # the bound is far above the logits (otherwise this case tests nothing)
+    s_max = np.max(np.einsum("thd,hmd->thm", host["K"].astype(np.float64),
+                             host["P"].astype(np.float64)), axis=2) / math.sqrt(d)
+    bound = np.linalg.norm(host["K"], axis=2) * np.linalg.norm(host["P"], axis=2).max(axis=1) / math.sqrt(d)
+    assert (bound - s_max).max() > 200
+    g = sk.cpu().numpy()
+    assert np.all(np.isfinite(g)) and np.all(np.isfinite(lse.cpu().numpy()))
+    assert normwise(g, ref, (2, 3)).max() <= 2e-2
+    assert np.abs(lse.cpu().numpy() - ref_lse).max() <= 1e-3 * max(1.0, np.abs(ref_lse).max())
