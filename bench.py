@@ -37,6 +37,37 @@ METRIC = "history tokens sketched/sec (fwd+bwd step; fwd alone in fwd_tokens_per
 
 WORKLOADS = {"c1": 1, "c2": 2, "c3": 3, "c4": 4, "c5": 5}
 
+# HBM bytes per launch measured with rocprofv3 FETCH_SIZE / WRITE_SIZE (scaled by the
+# same counters on a plain 1 GiB copy) on the default workload, keyed by the sha256 of
+# the kernel's source file at the time: a changed kernel reports traffic = null.
+# Source: profiles/hbm_bytes_c5_ragged100k_fwd_bwd.md
+MEASURED_TRAFFIC = {
+    "bwd_token": ("paper_2609_08443_amd/csrc/bwd_fused.hip",
+                  "d1ca8cfbe428379d7a806233f5ab8524c8c6f5f02cf5d17437136b55c4b8b27e",
+                  6.702e9 + 2.250e9),
+    "bwd_proto": ("paper_2609_08443_amd/csrc/bwd_fused.hip",
+                  "d1ca8cfbe428379d7a806233f5ab8524c8c6f5f02cf5d17437136b55c4b8b27e",
+                  2.408e9 + 0.100e9),
+    "fused_fwd": ("paper_2609_08443_amd/csrc/fwd_fused.hip",
+                  "e2d6b8407c99024b7c302050319d8e93895edc87e7e0d8b065bad6ee7a7457b4",
+                  1.114e9 + 0.135e9),
+}
+
+
+def measured_traffic(kernel: str, workload: str):
+    """Bytes per launch if counters were taken on this workload and kernel source."""
+    import hashlib
+    if workload != "c5" or kernel not in MEASURED_TRAFFIC:
+        return None
+    path, digest, nbytes = MEASURED_TRAFFIC[kernel]
+    try:
+        with open(os.path.join(ROOT, path), "rb") as f:
+            if hashlib.sha256(f.read()).hexdigest() != digest:
+                return None
+    except OSError:
+        return None
+    return nbytes
+
 
 # ---------------------------------------------------------------- accounting
 def fwd_algorithmic_flops(w: wl.Workload) -> float:
@@ -66,14 +97,23 @@ def bwd_algorithmic_bytes(w: wl.Workload) -> float:
             + 4.0 * w.H * w.M * w.d)            # dP
 
 
-# kernel name -> (algorithmic flops, algorithmic bytes, bound) of one launch
+# kernel name -> (algorithmic flops, executed matrix flops, algorithmic bytes, bound) of one
+# launch.  Algorithmic = the GEMMs of the method (Appendix G convention); executed also
+# counts the recomputation of S (and of dA) that the backward kernels do instead of storing.
 def kernel_work(name: str, w: wl.Workload):
+    th = float(w.T) * w.H
+    md = float(w.M) * w.d
+    el = 2 if w.dtype == "bf16" else 4
     if name == "fused_fwd":
-        return fwd_algorithmic_flops(w), fwd_algorithmic_bytes(w), "mfma"
-    if name in ("bwd_fused", "plain_bwd"):
-        return bwd_algorithmic_flops(w), bwd_algorithmic_bytes(w), "mfma" if name == "bwd_fused" else "alu"
+        return 4 * md * th, 4 * md * th, fwd_algorithmic_bytes(w), "mfma"
+    if name == "bwd_token":   # dA, dV, dK (+ S twice)
+        return 6 * md * th, 10 * md * th, th * w.d * (2 * el + 8) + 4 * th, "mfma"
+    if name == "bwd_proto":   # dP (+ S and dA)
+        return 2 * md * th, 6 * md * th, th * w.d * 2 * el + 8 * th, "mfma"
     if name == "plain_fwd":
-        return fwd_algorithmic_flops(w), fwd_algorithmic_bytes(w), "alu"
+        return 4 * md * th, 0.0, fwd_algorithmic_bytes(w), "alu"
+    if name == "plain_bwd":
+        return 8 * md * th, 0.0, bwd_algorithmic_bytes(w), "alu"
     return None
 
 
@@ -121,8 +161,10 @@ def main(argv=None) -> int:
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="c5", choices=sorted(WORKLOADS))
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-tokens", type=int, default=6000,
-                    help="tokens of the CPU-baseline sample")
+    ap.add_argument("--cpu-tokens", type=int, default=300000,
+                    help="tokens of the CPU-baseline sample (shortest users first)")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="only run a plain device copy of 1 GiB (to scale HBM byte counters)")
     args = ap.parse_args(argv)
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (asked for {args.gpus}): the sketching step "
@@ -135,6 +177,15 @@ def main(argv=None) -> int:
     from paper_2609_08443_amd import sa_sketch as sa
 
     torch.cuda.set_device(0)
+    if args.copy_calibration:
+        n = 1 << 28  # 2^28 fp32 = 1 GiB read + 1 GiB written per copy
+        src = torch.ones(n, dtype=torch.float32, device="cuda")
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_bytes_read": 4 * n, "copy_bytes_written": 4 * n, "copies": 3}))
+        return 0
     w = wl.config(WORKLOADS[args.workload])
     dev = wl.device_tensors(w, "cuda")
     code = sa.SA_BF16 if w.dtype == "bf16" else sa.SA_FP32
@@ -185,10 +236,11 @@ def main(argv=None) -> int:
     kernels = {n: {"launches": c, "avg_ms": tot / c} for n, (c, tot) in kt.items()}
 
     flops_step = fwd_algorithmic_flops(w) + (bwd_algorithmic_flops(w) if w.bwd else 0.0)
-    dom = max(kt.items(), key=lambda kv: kv[1][1])[0] if kt else None
+    known = {n: v for n, v in kt.items() if kernel_work(n, w) is not None}
+    dom = max(known.items(), key=lambda kv: kv[1][1])[0] if known else None
     roof = None
-    if dom is not None and kernel_work(dom, w) is not None:
-        fl, by, bound = kernel_work(dom, w)
+    if dom is not None:
+        fl, fl_exec, by, bound = kernel_work(dom, w)
         avg_ms = kt[dom][1] / kt[dom][0]
         if bound == "mfma":
             ach, peak, unit = fl / (avg_ms * 1e-3) / 1e12, PEAK_BF16_TFLOPS, "TFLOP/s"
@@ -197,8 +249,10 @@ def main(argv=None) -> int:
         else:  # plain fp32 vector arithmetic: fp32 vector peak
             ach, peak, unit = fl / (avg_ms * 1e-3) / 1e12, 157.3, "TFLOP/s"
         roof = {"kernel": dom, "bound": bound, "achieved": ach, "peak": peak, "unit": unit,
-                "frac": ach / peak, "traffic": None, "avg_ms": avg_ms,
-                "algorithmic_per_launch": fl if unit == "TFLOP/s" else by}
+                "frac": ach / peak, "traffic": measured_traffic(dom, args.workload),
+                "avg_ms": avg_ms,
+                "algorithmic_flops_per_launch": fl, "algorithmic_bytes_per_launch": by,
+                "executed_mfma_tflops": fl_exec / (avg_ms * 1e-3) / 1e12 if fl_exec else None}
 
     out = {
         "metric": METRIC,

@@ -70,27 +70,6 @@ hipEvent_t prof_event() {
     return e;
 }
 
-// Brackets the launches made in its scope with events on `stream` (when enabled).
-class ProfScope {
-  public:
-    ProfScope(const char* name, hipStream_t stream) : stream_(stream) {
-        if (!g_prof_on) return;
-        rec_.name = name;
-        rec_.start = prof_event();
-        rec_.stop = prof_event();
-        if (rec_.start && rec_.stop && hipEventRecord(rec_.start, stream_) == hipSuccess) active_ = true;
-    }
-    ~ProfScope() {
-        if (!active_) return;
-        if (hipEventRecord(rec_.stop, stream_) == hipSuccess) g_prof_recs.push_back(rec_);
-    }
-
-  private:
-    hipStream_t stream_;
-    ProfRec rec_{};
-    bool active_ = false;
-};
-
 bool debug_validate() {
     const char* v = getenv("SA_DEBUG_VALIDATE");
     return v && v[0] && strcmp(v, "0") != 0;
@@ -228,6 +207,23 @@ BwdPlan plan_bwd(int64_t B, int64_t T, int32_t H, int32_t M, int32_t d, sa_dtype
 
 }  // namespace
 
+namespace sa {
+
+ProfScope::ProfScope(const char* name, hipStream_t stream) : stream_(stream) {
+    if (!g_prof_on) return;
+    name_ = name;
+    start_ = prof_event();
+    stop_ = prof_event();
+    if (start_ && stop_ && hipEventRecord(start_, stream_) == hipSuccess) active_ = true;
+}
+
+ProfScope::~ProfScope() {
+    if (!active_) return;
+    if (hipEventRecord(stop_, stream_) == hipSuccess) g_prof_recs.push_back({name_, start_, stop_});
+}
+
+}  // namespace sa
+
 extern "C" {
 
 const char* sa_status_string(sa_status s) {
@@ -289,7 +285,7 @@ sa_status sa_sketch_fwd(const void* K, const void* V, const void* P, const int64
         int64_t* n_items = reinterpret_cast<int64_t*>(ws + plan.off_nitems);
         float* partials = reinterpret_cast<float*>(ws + plan.off_partials);
         {
-            ProfScope ps("worklist", stream);
+            sa::ProfScope ps("worklist", stream);
             e = sa::launch_worklist(offsets, B, T, H, plan.C, plan.n_ranges, items,
                                     plan.max_items, wg_start, pair_start, n_items, stream);
         }
@@ -312,12 +308,12 @@ sa_status sa_sketch_fwd(const void* K, const void* V, const void* P, const int64
         a.lse = lse;
         a.partials = partials;
         {
-            ProfScope ps("fused_fwd", stream);
+            sa::ProfScope ps("fused_fwd", stream);
             e = sa::launch_fused_fwd(a, stream);
         }
         if (e != hipSuccess) return hip_fail(e, "fused forward launch");
         {
-            ProfScope ps("splitL_merge", stream);
+            sa::ProfScope ps("splitL_merge", stream);
             e = sa::launch_merge(pair_start, B, H, plan.max_items, partials, (int64_t)M * d,
                                  sketch, stream);
         }
@@ -326,7 +322,7 @@ sa_status sa_sketch_fwd(const void* K, const void* V, const void* P, const int64
     }
     float* lse_out = lse ? lse : reinterpret_cast<float*>(ws + plan.off_lse);
     {
-        ProfScope ps("plain_fwd", stream);
+        sa::ProfScope ps("plain_fwd", stream);
         e = sa::launch_generic_fwd(K, V, P, offsets, B, T, H, M, d, scale, dtype == SA_BF16,
                                    sketch, lse_out, stream);
     }
@@ -397,7 +393,7 @@ sa_status sa_sketch_bwd(const void* K, const void* V, const void* P, const int64
         f.dV = dV;
         f.dP = dP;
         {
-            ProfScope ps("worklist", stream);
+            sa::ProfScope ps("worklist", stream);
             e = sa::launch_worklist(offsets, B, T, H, plan.C, plan.n_ranges,
                                     const_cast<int32_t*>(f.items), plan.max_items,
                                     const_cast<int32_t*>(f.wg_start),
@@ -405,20 +401,17 @@ sa_status sa_sketch_bwd(const void* K, const void* V, const void* P, const int64
                                     reinterpret_cast<int64_t*>(ws + plan.off_nitems), stream);
         }
         if (e != hipSuccess) return hip_fail(e, "work list launch");
-        {
-            ProfScope ps("bwd_fused", stream);
-            e = sa::launch_fused_bwd(f, stream);
-        }
+        e = sa::launch_fused_bwd(f, stream);
         if (e != hipSuccess) return hip_fail(e, "fused backward launch");
         return SA_OK;
     }
     {
-        ProfScope ps("dY_reduce", stream);
+        sa::ProfScope ps("dY_reduce", stream);
         e = sa::launch_dy_reduce(dsketch, B, R, H, (int64_t)M * d, dY, stream);
     }
     if (e != hipSuccess) return hip_fail(e, "dY reduce launch");
     {
-        ProfScope ps("plain_bwd", stream);
+        sa::ProfScope ps("plain_bwd", stream);
         e = sa::launch_generic_bwd(K, V, P, offsets, B, T, H, M, d, scale, dtype == SA_BF16, dY,
                                    lse, Dbuf, dK, dV, dP, part, plan.n_chunks, stream);
     }

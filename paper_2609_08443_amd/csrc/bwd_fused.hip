@@ -552,6 +552,7 @@ hipError_t launch_fused_bwd(const FusedBwdArgs& f, hipStream_t stream) {
     const int64_t MD = (int64_t)f.M * f.d;
     // dY (R summed) and P in the layouts the contractions read
     {
+        ProfScope ps("bwd_prep", stream);
         const int64_t n = f.B * f.H * MD + (int64_t)f.H * MD;
         hipLaunchKernelGGL(prep_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, stream,
                            f.dsketch, f.B, f.R, f.H, f.M, f.d, f.P, f.Ymj, f.Yjm, f.Pjm);
@@ -564,14 +565,19 @@ hipError_t launch_fused_bwd(const FusedBwdArgs& f, hipStream_t stream) {
         t.lse = f.lse; t.items = f.items; t.wg_start = f.wg_start; t.max_items = f.max_items;
         t.T = f.T; t.B = (int32_t)f.B; t.H = f.H; t.M = f.M; t.scale = f.scale;
         t.dK = f.dK; t.dV = f.dV; t.Dbuf = f.Dbuf;
-        hipError_t e = f.d == 64 ? launch_token<64>(t, f.n_ranges, stream)
-                                 : launch_token<128>(t, f.n_ranges, stream);
+        hipError_t e;
+        {
+            ProfScope ps("bwd_token", stream);
+            e = f.d == 64 ? launch_token<64>(t, f.n_ranges, stream)
+                          : launch_token<128>(t, f.n_ranges, stream);
+        }
         if (e != hipSuccess) return e;
         ProtoArgs p;
         p.K = f.K; p.V = f.V; p.P = f.P; p.Ymj = f.Ymj; p.lse = f.lse; p.Dbuf = f.Dbuf;
         p.items = f.items; p.wg_start = f.wg_start; p.max_items = f.max_items; p.T = f.T;
         p.B = (int32_t)f.B; p.H = f.H; p.M = f.M; p.scale = f.scale; p.partials = f.partials;
         const int mp = fused_bwd_part(f.M, f.d);
+        ProfScope ps("bwd_proto", stream);
         if (f.d == 64) {
             e = mp == 128 ? launch_proto<64, 32>(p, f.n_ranges, stream)
               : mp == 256 ? launch_proto<64, 64>(p, f.n_ranges, stream)
@@ -583,6 +589,7 @@ hipError_t launch_fused_bwd(const FusedBwdArgs& f, hipStream_t stream) {
         if (e != hipSuccess) return e;
     }
     const int64_t n = (int64_t)f.H * MD / 4;
+    ProfScope ps("bwd_dp_sum", stream);
     hipLaunchKernelGGL(dp_sum_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, stream,
                        f.pair_start, f.B, f.H, f.max_items, f.partials, MD, f.dP);
     return hipGetLastError();

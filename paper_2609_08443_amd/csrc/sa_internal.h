@@ -19,6 +19,22 @@ enum : int { IT_B = 0, IT_H = 1, IT_T0 = 2, IT_T1 = 3, IT_RANGE = 4, IT_SPLIT = 
 constexpr int kTileTokens = 32;     // tokens per MFMA tile (rows of the 32x32 output)
 constexpr int kWorklistThreads = 1024;
 
+// Brackets the launches made in its scope with HIP events on `stream` when
+// kernel timing is enabled on the calling thread (sa_profile_enable).
+class ProfScope {
+  public:
+    ProfScope(const char* name, hipStream_t stream);
+    ~ProfScope();
+    ProfScope(const ProfScope&) = delete;
+    ProfScope& operator=(const ProfScope&) = delete;
+
+  private:
+    hipStream_t stream_;
+    const char* name_ = nullptr;
+    hipEvent_t start_ = nullptr, stop_ = nullptr;
+    bool active_ = false;
+};
+
 // ---------------------------------------------------------------------------
 // launchers (each returns hipSuccess or the launch error)
 // ---------------------------------------------------------------------------
