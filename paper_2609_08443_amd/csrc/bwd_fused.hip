@@ -104,18 +104,18 @@ __global__ __launch_bounds__(256) void prep_kernel(const float* __restrict__ ds,
 }
 
 // ------------------------------------------------------------------ token side
-template <int D>
+template <int D, int NW_>
 struct TokCfg {
-    static constexpr int NW = 4;
-    static constexpr int THREADS = 256;
+    static constexpr int NW = NW_;
+    static constexpr int THREADS = NW * 64;
+    static constexpr int TB = 32 * NW;                 // tokens per block (32 per wave)
     static constexpr int KS = D / 16;
     static constexpr int JT = D / 32;
     static constexpr int BLK = 32 * D;                 // bf16 elements of one 32-row block
     // LDS: two buffers of {Pmj, Pjm, Ymj, Yjm} prototype blocks
     static constexpr int BUF = 4 * BLK;
     static constexpr int LDS = 2 * BUF * 2;
-    static constexpr int CH_MJ = BLK / 8 / THREADS;    // 16-byte chunks per thread, [32][D] block
-    static constexpr int CH_JM = BLK / 8 / THREADS;    // [D][32] block
+    static constexpr int CHUNKS = BLK / 8;             // 16-byte chunks of one block
 };
 
 struct TokArgs {
@@ -137,9 +137,9 @@ struct TokArgs {
     float* Dbuf;
 };
 
-template <int D>
-__global__ __launch_bounds__(256, 1) void bwd_token_kernel(TokArgs a) {
-    using C = TokCfg<D>;
+template <int D, int NW>
+__global__ __launch_bounds__(NW * 64, 1) void bwd_token_kernel(TokArgs a) {
+    using C = TokCfg<D, NW>;
     extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
     uint16_t* lds = reinterpret_cast<uint16_t*>(smem);
     const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
@@ -161,7 +161,7 @@ __global__ __launch_bounds__(256, 1) void bwd_token_kernel(TokArgs a) {
         const uint16_t* Ymj_g = a.Ymj + ((int64_t)b * a.H + h) * MD;
         const uint16_t* Yjm_g = a.Yjm + ((int64_t)b * a.H + h) * MD;
 
-        for (int tb = t0; tb < t1; tb += 128) {
+        for (int tb = t0; tb < t1; tb += C::TB) {
             const int tok = tb + 32 * w + l32;   // this lane's token (column of S^T)
             const bool tv = tok < t1;
             // K and V as B operands: lane (hl, t) holds 8 consecutive j of its token
@@ -182,29 +182,38 @@ __global__ __launch_bounds__(256, 1) void bwd_token_kernel(TokArgs a) {
 
             // stage prototype block mb of the requested matrices into buffer `buf`
             // (sweep 0: Pmj, Yjm; sweep 1: Pmj, Pjm, Ymj)
-            auto stage = [&](int mb, int buf, int sweep) {
+            // prototype block mb of the requested matrices: global -> registers,
+            // then registers -> LDS buffer `buf` after the current block's compute
+            // (sweep 0: Pmj, Yjm; sweep 1: Pmj, Pjm, Ymj)
+            constexpr int NCH = (C::CHUNKS + C::THREADS - 1) / C::THREADS;
+            uint4 rg_mj[NCH], rg_y[NCH], rg_jm[NCH];
+            auto fetch = [&](int mb, int sweep) {
+#pragma unroll
+                for (int c = 0; c < NCH; ++c) {
+                    const int i = tid + c * C::THREADS;
+                    if (i < C::CHUNKS) {
+                        const int r = i / (D / 8), ch = i % (D / 8);
+                        const int64_t src = (int64_t)(mb * 32 + r) * D + ch * 8;
+                        rg_mj[c] = *reinterpret_cast<const uint4*>(Pmj_g + src);
+                        if (sweep == 1) rg_y[c] = *reinterpret_cast<const uint4*>(Ymj_g + src);
+                        const int j = i / 4, cj = i % 4;
+                        const int64_t srcj = (int64_t)j * a.M + mb * 32 + cj * 8;
+                        rg_jm[c] = *reinterpret_cast<const uint4*>((sweep == 1 ? Pjm_g : Yjm_g) + srcj);
+                    }
+                }
+            };
+            auto store = [&](int buf, int sweep) {
                 uint16_t* L = lds + buf * C::BUF;
 #pragma unroll
-                for (int c = 0; c < C::CH_MJ; ++c) {
+                for (int c = 0; c < NCH; ++c) {
                     const int i = tid + c * C::THREADS;
-                    const int r = i / (D / 8), ch = i % (D / 8);
-                    const int64_t src = (int64_t)(mb * 32 + r) * D + ch * 8;
-                    *reinterpret_cast<uint4*>(L + swz<D>(r, ch)) = *reinterpret_cast<const uint4*>(Pmj_g + src);
-                    if (sweep == 1)
-                        *reinterpret_cast<uint4*>(L + 2 * C::BLK + swz<D>(r, ch)) =
-                            *reinterpret_cast<const uint4*>(Ymj_g + src);
-                }
-#pragma unroll
-                for (int c = 0; c < C::CH_JM; ++c) {
-                    const int i = tid + c * C::THREADS;
-                    const int j = i / 4, ch = i % 4;
-                    const int64_t src = (int64_t)j * a.M + mb * 32 + ch * 8;
-                    if (sweep == 1)
-                        *reinterpret_cast<uint4*>(L + C::BLK + swz<32>(j, ch)) =
-                            *reinterpret_cast<const uint4*>(Pjm_g + src);
-                    else
-                        *reinterpret_cast<uint4*>(L + 3 * C::BLK + swz<32>(j, ch)) =
-                            *reinterpret_cast<const uint4*>(Yjm_g + src);
+                    if (i < C::CHUNKS) {
+                        const int r = i / (D / 8), ch = i % (D / 8);
+                        *reinterpret_cast<uint4*>(L + swz<D>(r, ch)) = rg_mj[c];
+                        if (sweep == 1) *reinterpret_cast<uint4*>(L + 2 * C::BLK + swz<D>(r, ch)) = rg_y[c];
+                        const int j = i / 4, cj = i % 4;
+                        *reinterpret_cast<uint4*>(L + (sweep == 1 ? C::BLK : 3 * C::BLK) + swz<32>(j, cj)) = rg_jm[c];
+                    }
                 }
             };
             // S^T tile of block mb (rows = the block's 32 prototypes, cols = tokens)
@@ -225,11 +234,12 @@ __global__ __launch_bounds__(256, 1) void bwd_token_kernel(TokArgs a) {
 #pragma unroll
                 for (int r = 0; r < 16; ++r) dvt[jt][r] = 0.f;
             __syncthreads();  // previous users of the buffers are done
-            stage(0, 0, 0);
+            fetch(0, 0);
+            store(0, 0);
             __syncthreads();
             for (int mb = 0; mb < nblk; ++mb) {
                 const uint16_t* L = lds + (mb & 1) * C::BUF;
-                if (mb + 1 < nblk) stage(mb + 1, (mb + 1) & 1, 0);
+                if (mb + 1 < nblk) fetch(mb + 1, 0);
                 const f32x16 s = st_tile(L);
                 float e[16];
 #pragma unroll
@@ -241,6 +251,7 @@ __global__ __launch_bounds__(256, 1) void bwd_token_kernel(TokArgs a) {
                     dvt[jt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(lds_b128(Y, swz<32>(jt * 32 + l32, 0 + hl)), ab0, dvt[jt], 0, 0, 0);
                     dvt[jt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(lds_b128(Y, swz<32>(jt * 32 + l32, 2 + hl)), ab1, dvt[jt], 0, 0, 0);
                 }
+                if (mb + 1 < nblk) store((mb + 1) & 1, 0);
                 __syncthreads();
             }
             // D_t = <V_t, dV_t>: this lane holds dV[t, j] for j = jt*32 + srow(r, hl)
@@ -275,11 +286,12 @@ __global__ __launch_bounds__(256, 1) void bwd_token_kernel(TokArgs a) {
             for (int jt = 0; jt < C::JT; ++jt)
 #pragma unroll
                 for (int r = 0; r < 16; ++r) dkt[jt][r] = 0.f;
-            stage(0, 0, 1);
+            fetch(0, 1);
+            store(0, 1);
             __syncthreads();
             for (int mb = 0; mb < nblk; ++mb) {
                 const uint16_t* L = lds + (mb & 1) * C::BUF;
-                if (mb + 1 < nblk) stage(mb + 1, (mb + 1) & 1, 1);
+                if (mb + 1 < nblk) fetch(mb + 1, 1);
                 const f32x16 s = st_tile(L);
                 f32x16 da;
 #pragma unroll
@@ -301,6 +313,7 @@ __global__ __launch_bounds__(256, 1) void bwd_token_kernel(TokArgs a) {
                     dkt[jt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(lds_b128(Pj, swz<32>(jt * 32 + l32, 0 + hl)), d0, dkt[jt], 0, 0, 0);
                     dkt[jt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(lds_b128(Pj, swz<32>(jt * 32 + l32, 2 + hl)), d1, dkt[jt], 0, 0, 0);
                 }
+                if (mb + 1 < nblk) store((mb + 1) & 1, 1);
                 __syncthreads();
             }
             if (tv) {
@@ -315,17 +328,16 @@ __global__ __launch_bounds__(256, 1) void bwd_token_kernel(TokArgs a) {
 }
 
 // ------------------------------------------------------------------ prototype side
-template <int D, int MW>
+template <int D, int MW, int NW_>
 struct ProtoCfg {
-    static constexpr int NW = 4;
-    static constexpr int THREADS = 256;
+    static constexpr int NW = NW_;
+    static constexpr int THREADS = NW * 64;
     static constexpr int MP = MW * NW;      // prototypes of one part
     static constexpr int MT = MW / 32;
     static constexpr int KS = D / 16;
     static constexpr int JT = D / 32;
     static constexpr int KCH = D / 8;
     static constexpr int LD_CHUNKS = 32 * KCH;
-    static constexpr int NLD = LD_CHUNKS / THREADS;
     static constexpr int OFF_P = 0;                        // [MP][D]
     static constexpr int OFF_Y = OFF_P + MP * D * 2;       // [MP][D]
     static constexpr int OFF_K = OFF_Y + MP * D * 2;       // [32][D] token-major K tile
@@ -352,9 +364,9 @@ struct ProtoArgs {
     float* partials;  // [max_items][M][D]
 };
 
-template <int D, int MW>
-__global__ __launch_bounds__(256, 1) void bwd_proto_kernel(ProtoArgs a) {
-    using C = ProtoCfg<D, MW>;
+template <int D, int MW, int NW>
+__global__ __launch_bounds__(NW * 64, 1) void bwd_proto_kernel(ProtoArgs a) {
+    using C = ProtoCfg<D, MW, NW>;
     extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
     uint16_t* Ps = reinterpret_cast<uint16_t*>(smem + C::OFF_P);
     uint16_t* Ys = reinterpret_cast<uint16_t*>(smem + C::OFF_Y);
@@ -398,36 +410,58 @@ __global__ __launch_bounds__(256, 1) void bwd_proto_kernel(ProtoArgs a) {
 #pragma unroll
                 for (int r = 0; r < 16; ++r) acc[mt][jt][r] = 0.f;
 
-        for (int ts = t0; ts < t1; ts += 32) {
-            __syncthreads();  // previous tile's K, V, K^T, lse, D consumed
+        // token tiles: global -> registers one tile ahead, registers -> LDS per tile
+        constexpr int NCH = (C::LD_CHUNKS + C::THREADS - 1) / C::THREADS;
+        uint4 kreg[NCH], vreg[NCH];
+        float lse_r = 0.f, d_r = 0.f;
+        auto fetch = [&](int ts) {
             const int64_t tb = ((int64_t)ts * a.H + h) * D;
 #pragma unroll
-            for (int i = 0; i < C::NLD; ++i) {
-                const int idx = tid + i * C::THREADS;
+            for (int c = 0; c < NCH; ++c) {
+                const int idx = tid + c * C::THREADS;
                 const int tok = idx / C::KCH, ch = idx % C::KCH;
                 uint4 kv = make_uint4(0, 0, 0, 0), vv = make_uint4(0, 0, 0, 0);
-                if (ts + tok < t1) {
+                if (idx < C::LD_CHUNKS && ts + tok < t1) {
                     const uint32_t off = (uint32_t)tok * row_stride + (uint32_t)(ch * 8);
                     kv = *reinterpret_cast<const uint4*>(a.K + tb + off);
                     vv = *reinterpret_cast<const uint4*>(a.V + tb + off);
                 }
-                *reinterpret_cast<uint4*>(Ks + swz<D>(tok, ch)) = kv;
-                *reinterpret_cast<uint4*>(Vs + swz<D>(tok, ch)) = vv;
-                const int p = perm16(tok);
-                const uint32_t wv[4] = {kv.x, kv.y, kv.z, kv.w};
-#pragma unroll
-                for (int e2 = 0; e2 < 4; ++e2) {
-                    const int j0 = ch * 8 + 2 * e2;
-                    Kt[swz<32>(j0, p >> 3) + (p & 7)] = (uint16_t)(wv[e2] & 0xffffu);
-                    Kt[swz<32>(j0 + 1, p >> 3) + (p & 7)] = (uint16_t)(wv[e2] >> 16);
-                }
+                kreg[c] = kv;
+                vreg[c] = vv;
             }
             if (tid < 32) {
                 const bool v = ts + tid < t1;
-                nls[tid] = v ? -a.lse[(int64_t)(ts + tid) * a.H + h] * kLog2e : 0.f;
-                Ds[tid] = v ? a.Dbuf[(int64_t)(ts + tid) * a.H + h] : 0.f;
+                lse_r = v ? -a.lse[(int64_t)(ts + tid) * a.H + h] * kLog2e : 0.f;
+                d_r = v ? a.Dbuf[(int64_t)(ts + tid) * a.H + h] : 0.f;
+            }
+        };
+        fetch(t0);
+        for (int ts = t0; ts < t1; ts += 32) {
+            __syncthreads();  // previous tile's K, V, K^T, lse, D consumed
+#pragma unroll
+            for (int c = 0; c < NCH; ++c) {
+                const int idx = tid + c * C::THREADS;
+                if (idx < C::LD_CHUNKS) {
+                    const int tok = idx / C::KCH, ch = idx % C::KCH;
+                    const uint4 kv = kreg[c], vv = vreg[c];
+                    *reinterpret_cast<uint4*>(Ks + swz<D>(tok, ch)) = kv;
+                    *reinterpret_cast<uint4*>(Vs + swz<D>(tok, ch)) = vv;
+                    const int p = perm16(tok);
+                    const uint32_t wv[4] = {kv.x, kv.y, kv.z, kv.w};
+#pragma unroll
+                    for (int e2 = 0; e2 < 4; ++e2) {
+                        const int j0 = ch * 8 + 2 * e2;
+                        Kt[swz<32>(j0, p >> 3) + (p & 7)] = (uint16_t)(wv[e2] & 0xffffu);
+                        Kt[swz<32>(j0 + 1, p >> 3) + (p & 7)] = (uint16_t)(wv[e2] >> 16);
+                    }
+                }
+            }
+            if (tid < 32) {
+                nls[tid] = lse_r;
+                Ds[tid] = d_r;
             }
             __syncthreads();
+            if (ts + 32 < t1) fetch(ts + 32);
 
             bf16x8 kop[C::KS], vop[C::KS];
 #pragma unroll
@@ -511,10 +545,10 @@ __global__ __launch_bounds__(256) void dp_sum_kernel(const int32_t* __restrict__
     *reinterpret_cast<float4*>(dP + i) = acc;
 }
 
-template <int D>
+template <int D, int NW>
 hipError_t launch_token(const TokArgs& a, int64_t n_ranges, hipStream_t stream) {
-    using C = TokCfg<D>;
-    auto kern = bwd_token_kernel<D>;
+    using C = TokCfg<D, NW>;
+    auto kern = bwd_token_kernel<D, NW>;
     hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
                                        hipFuncAttributeMaxDynamicSharedMemorySize, C::LDS);
     if (e != hipSuccess) return e;
@@ -522,10 +556,10 @@ hipError_t launch_token(const TokArgs& a, int64_t n_ranges, hipStream_t stream) 
     return hipGetLastError();
 }
 
-template <int D, int MW>
+template <int D, int MW, int NW>
 hipError_t launch_proto(const ProtoArgs& a, int64_t n_ranges, hipStream_t stream) {
-    using C = ProtoCfg<D, MW>;
-    auto kern = bwd_proto_kernel<D, MW>;
+    using C = ProtoCfg<D, MW, NW>;
+    auto kern = bwd_proto_kernel<D, MW, NW>;
     hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
                                        hipFuncAttributeMaxDynamicSharedMemorySize, C::LDS);
     if (e != hipSuccess) return e;
@@ -535,6 +569,9 @@ hipError_t launch_proto(const ProtoArgs& a, int64_t n_ranges, hipStream_t stream
 }
 
 }  // namespace
+
+// waves of the token-side kernel: two per SIMD
+constexpr int kTokWaves = 8;
 
 // prototypes per part of the dP kernel: P and dY slices of MP x d bf16 each fit in LDS
 int32_t fused_bwd_part(int32_t M, int32_t d) {
@@ -568,8 +605,8 @@ hipError_t launch_fused_bwd(const FusedBwdArgs& f, hipStream_t stream) {
         hipError_t e;
         {
             ProfScope ps("bwd_token", stream);
-            e = f.d == 64 ? launch_token<64>(t, f.n_ranges, stream)
-                          : launch_token<128>(t, f.n_ranges, stream);
+            e = f.d == 64 ? launch_token<64, kTokWaves>(t, f.n_ranges, stream)
+                          : launch_token<128, kTokWaves>(t, f.n_ranges, stream);
         }
         if (e != hipSuccess) return e;
         ProtoArgs p;
@@ -578,13 +615,14 @@ hipError_t launch_fused_bwd(const FusedBwdArgs& f, hipStream_t stream) {
         p.B = (int32_t)f.B; p.H = f.H; p.M = f.M; p.scale = f.scale; p.partials = f.partials;
         const int mp = fused_bwd_part(f.M, f.d);
         ProfScope ps("bwd_proto", stream);
+        // eight waves (two per SIMD) when the part has at least 32 prototypes per wave
         if (f.d == 64) {
-            e = mp == 128 ? launch_proto<64, 32>(p, f.n_ranges, stream)
-              : mp == 256 ? launch_proto<64, 64>(p, f.n_ranges, stream)
-                          : launch_proto<64, 128>(p, f.n_ranges, stream);
+            e = mp == 128 ? launch_proto<64, 32, 4>(p, f.n_ranges, stream)
+              : mp == 256 ? launch_proto<64, 32, 8>(p, f.n_ranges, stream)
+                          : launch_proto<64, 64, 8>(p, f.n_ranges, stream);
         } else {
-            e = mp == 128 ? launch_proto<128, 32>(p, f.n_ranges, stream)
-                          : launch_proto<128, 64>(p, f.n_ranges, stream);
+            e = mp == 128 ? launch_proto<128, 32, 4>(p, f.n_ranges, stream)
+                          : launch_proto<128, 32, 8>(p, f.n_ranges, stream);
         }
         if (e != hipSuccess) return e;
     }
