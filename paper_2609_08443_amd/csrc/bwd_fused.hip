@@ -19,55 +19,21 @@
 //          prototypes, lanes = tokens) so that the reductions over prototypes are
 //          matrix-core contractions whose k slots are the register index of S^T.
 //          Prototype blocks of 32 are streamed through double-buffered LDS and
-//          shared by the four waves (each wave owns 32 tokens).
+//          shared by the eight waves (each wave owns 32 tokens).
 //   proto  dP for a slice of the prototypes, in the forward's orientation (lanes =
-//          prototypes): the prototype slice and the user's dY slice stay in LDS,
-//          dS^T . K accumulates in registers; one partial per work-list segment,
-//          summed per head in segment order (deterministic).
+//          prototypes): the prototype slice and the user's dY slice stay in LDS
+//          (or in registers with one 32-prototype tile per wave), dS^T . K
+//          accumulates in registers with K^T read by the transposing LDS load;
+//          one partial per work-list segment, summed per head in segment order
+//          (deterministic).
 #include "sa_internal.h"
+#include "tile_ops.h"
 
 namespace sa {
 
 namespace {
 
-typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
-typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
-typedef float f32x16 __attribute__((ext_vector_type(16)));
-typedef float f32x2 __attribute__((ext_vector_type(2)));
-
-constexpr float kLog2e = 1.4426950408889634f;
-
-__device__ inline float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
-__device__ inline float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
-__device__ inline uint32_t pack_bf16x2(float a, float b) {
-    bf16x2 v = __builtin_convertvector((f32x2){a, b}, bf16x2);
-    return __builtin_bit_cast(uint32_t, v);
-}
-__device__ inline uint16_t to_bf16(float a) { return (uint16_t)(pack_bf16x2(a, 0.f) & 0xffffu); }
-__device__ inline bf16x8 pack8(const float* e) {
-    uint4 pk;
-    pk.x = pack_bf16x2(e[0], e[1]);
-    pk.y = pack_bf16x2(e[2], e[3]);
-    pk.z = pack_bf16x2(e[4], e[5]);
-    pk.w = pack_bf16x2(e[6], e[7]);
-    return __builtin_bit_cast(bf16x8, pk);
-}
-template <int COLS>
-__device__ inline int swz(int r, int c) {
-    if constexpr (COLS == 32) {
-        return r * 32 + ((c ^ ((r >> 1) & 3)) << 3);
-    } else {
-        return r * COLS + ((c ^ (r & 7)) << 3);
-    }
-}
-__device__ inline bf16x8 lds_b128(const uint16_t* base, int off) {
-    return __builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4*>(base + off));
-}
-// position <-> index permutation inside each 16-group: swap bits 2 and 3.  The C
-// layout of a 32x32 tile read as the k slots of the next contraction visits its
-// rows in this order (an involution).
-__device__ inline int perm16(int t) { return (t & ~12) | ((t & 4) << 1) | ((t & 8) >> 1); }
-__device__ inline int srow(int r, int hl) { return 8 * (r >> 2) + 4 * hl + (r & 3); }
+using namespace tile;
 
 __device__ inline float xhalf_sum(float v) {
     const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
@@ -342,8 +308,7 @@ struct ProtoCfg {
     static constexpr int OFF_Y = OFF_P + MP * D * 2;       // [MP][D]
     static constexpr int OFF_K = OFF_Y + MP * D * 2;       // [32][D] token-major K tile
     static constexpr int OFF_V = OFF_K + 32 * D * 2;       // [32][D] V tile
-    static constexpr int OFF_KT = OFF_V + 32 * D * 2;      // [D][32] K^T, permuted tokens
-    static constexpr int OFF_L = OFF_KT + D * 32 * 2;      // [32] -lse*log2e
+    static constexpr int OFF_L = OFF_V + 32 * D * 2;       // [32] -lse*log2e
     static constexpr int OFF_D = OFF_L + 32 * 4;           // [32] D_t
     static constexpr int LDS = OFF_D + 32 * 4;
 };
@@ -372,7 +337,6 @@ __global__ __launch_bounds__(NW * 64, 1) void bwd_proto_kernel(ProtoArgs a) {
     uint16_t* Ys = reinterpret_cast<uint16_t*>(smem + C::OFF_Y);
     uint16_t* Ks = reinterpret_cast<uint16_t*>(smem + C::OFF_K);
     uint16_t* Vs = reinterpret_cast<uint16_t*>(smem + C::OFF_V);
-    uint16_t* Kt = reinterpret_cast<uint16_t*>(smem + C::OFF_KT);
     float* nls = reinterpret_cast<float*>(smem + C::OFF_L);
     float* Ds = reinterpret_cast<float*>(smem + C::OFF_D);
     const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
@@ -436,24 +400,30 @@ __global__ __launch_bounds__(NW * 64, 1) void bwd_proto_kernel(ProtoArgs a) {
             }
         };
         fetch(t0);
+        __syncthreads();  // the P and dY slices are in LDS
+        // With one prototype tile per wave, this wave's rows of P and dY are held in
+        // registers as B operands for the whole segment (each K / V operand is then
+        // used once); with more, K and V operands are read once per tile and reused.
+        constexpr bool kHold = C::MT == 1;
+        constexpr int HM = kHold ? C::MT : 1, HK = kHold ? C::KS : 1;
+        bf16x8 pop[HM][HK], yop[HM][HK];
+        if constexpr (kHold) {
+#pragma unroll
+            for (int kk = 0; kk < C::KS; ++kk) {
+                const int prow = w * MW + l32;
+                pop[0][kk] = lds_b128(Ps, swz<D>(prow, 2 * kk + hl));
+                yop[0][kk] = lds_b128(Ys, swz<D>(prow, 2 * kk + hl));
+            }
+        }
         for (int ts = t0; ts < t1; ts += 32) {
-            __syncthreads();  // previous tile's K, V, K^T, lse, D consumed
+            __syncthreads();  // previous tile's K, V, lse, D consumed
 #pragma unroll
             for (int c = 0; c < NCH; ++c) {
                 const int idx = tid + c * C::THREADS;
                 if (idx < C::LD_CHUNKS) {
                     const int tok = idx / C::KCH, ch = idx % C::KCH;
-                    const uint4 kv = kreg[c], vv = vreg[c];
-                    *reinterpret_cast<uint4*>(Ks + swz<D>(tok, ch)) = kv;
-                    *reinterpret_cast<uint4*>(Vs + swz<D>(tok, ch)) = vv;
-                    const int p = perm16(tok);
-                    const uint32_t wv[4] = {kv.x, kv.y, kv.z, kv.w};
-#pragma unroll
-                    for (int e2 = 0; e2 < 4; ++e2) {
-                        const int j0 = ch * 8 + 2 * e2;
-                        Kt[swz<32>(j0, p >> 3) + (p & 7)] = (uint16_t)(wv[e2] & 0xffffu);
-                        Kt[swz<32>(j0 + 1, p >> 3) + (p & 7)] = (uint16_t)(wv[e2] >> 16);
-                    }
+                    *reinterpret_cast<uint4*>(Ks + swz<D>(tok, ch)) = kreg[c];
+                    *reinterpret_cast<uint4*>(Vs + swz<D>(tok, ch)) = vreg[c];
                 }
             }
             if (tid < 32) {
@@ -463,43 +433,47 @@ __global__ __launch_bounds__(NW * 64, 1) void bwd_proto_kernel(ProtoArgs a) {
             __syncthreads();
             if (ts + 32 < t1) fetch(ts + 32);
 
-            bf16x8 kop[C::KS], vop[C::KS];
+            constexpr int OK = kHold ? 1 : C::KS;
+            bf16x8 kop[OK], vop[OK];
+            if constexpr (!kHold) {
 #pragma unroll
-            for (int kk = 0; kk < C::KS; ++kk) {
-                kop[kk] = lds_b128(Ks, swz<D>(l32, 2 * kk + hl));
-                vop[kk] = lds_b128(Vs, swz<D>(l32, 2 * kk + hl));
-            }
-            float nl[16], Dr[16];
-#pragma unroll
-            for (int r = 0; r < 16; ++r) {
-                nl[r] = nls[srow(r, hl)];
-                Dr[r] = Ds[srow(r, hl)];
+                for (int kk = 0; kk < C::KS; ++kk) {
+                    kop[kk] = lds_b128(Ks, swz<D>(l32, 2 * kk + hl));
+                    vop[kk] = lds_b128(Vs, swz<D>(l32, 2 * kk + hl));
+                }
             }
             bf16x8 dso[C::MT][2];
 #pragma unroll
             for (int mt = 0; mt < C::MT; ++mt) {
-                const int prow = w * MW + mt * 32 + l32;
                 f32x16 s, da;
 #pragma unroll
                 for (int r = 0; r < 16; ++r) s[r] = da[r] = 0.f;
+                const int prow = w * MW + mt * 32 + l32;
 #pragma unroll
                 for (int kk = 0; kk < C::KS; ++kk) {
-                    s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kop[kk], lds_b128(Ps, swz<D>(prow, 2 * kk + hl)), s, 0, 0, 0);
-                    da = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vop[kk], lds_b128(Ys, swz<D>(prow, 2 * kk + hl)), da, 0, 0, 0);
+                    if constexpr (kHold) {
+                        s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(lds_b128(Ks, swz<D>(l32, 2 * kk + hl)), pop[0][kk], s, 0, 0, 0);
+                        da = __builtin_amdgcn_mfma_f32_32x32x16_bf16(lds_b128(Vs, swz<D>(l32, 2 * kk + hl)), yop[0][kk], da, 0, 0, 0);
+                    } else {
+                        s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kop[kk], lds_b128(Ps, swz<D>(prow, 2 * kk + hl)), s, 0, 0, 0);
+                        da = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vop[kk], lds_b128(Ys, swz<D>(prow, 2 * kk + hl)), da, 0, 0, 0);
+                    }
                 }
                 float e[16];
 #pragma unroll
                 for (int r = 0; r < 16; ++r) {
-                    const float A = __builtin_amdgcn_exp2f(__builtin_fmaf(s[r], ks2, nl[r]));
-                    e[r] = A * (da[r] - Dr[r]);
+                    const int t = srow(r, hl);
+                    const float A = __builtin_amdgcn_exp2f(__builtin_fmaf(s[r], ks2, nls[t]));
+                    e[r] = A * (da[r] - Ds[t]);
                 }
                 dso[mt][0] = pack8(e);
                 dso[mt][1] = pack8(e + 8);
             }
+            // dP[m, j] += dS^T[m, t] K[t, j]: K^T operands straight from the row-major tile
 #pragma unroll
             for (int jt = 0; jt < C::JT; ++jt) {
-                const bf16x8 k0v = lds_b128(Kt, swz<32>(jt * 32 + l32, 0 + hl));
-                const bf16x8 k1v = lds_b128(Kt, swz<32>(jt * 32 + l32, 2 + hl));
+                const bf16x8 k0v = lds_tr_tokens<D>(Ks, lane, jt, 0);
+                const bf16x8 k1v = lds_tr_tokens<D>(Ks, lane, jt, 1);
 #pragma unroll
                 for (int mt = 0; mt < C::MT; ++mt) {
                     acc[mt][jt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(dso[mt][0], k0v, acc[mt][jt], 0, 0, 0);

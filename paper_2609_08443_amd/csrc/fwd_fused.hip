@@ -26,57 +26,33 @@
 // the 32 lanes of a row (DPP and permlane, no LDS), and across waves through
 // LDS.
 //
-// Layouts (v_mfma_f32_32x32x16_bf16, checked on the device):
-//   A operand: lane l holds row l%32, k = (l/32)*8 + 0..7
-//   B operand: lane l holds col l%32, k = (l/32)*8 + 0..7
-//   C/D      : lane l holds col l%32, rows 8*(r/4) + 4*(l/32) + r%4, r = 0..15
-// S is computed with tokens as rows, so its C layout (lane = prototype,
-// register = token) is directly the A operand of the aggregation
-// acc[m, j] += sum_t E[t, m] V'[t, j] once the token index of the k slots is
-// permuted accordingly; V' is staged in LDS transposed and in that permuted
-// token order.  1/z is folded into V' (d values per token instead of M).
+// Layouts: see tile_ops.h.  S is computed with tokens as rows, so its C layout
+// (lane = prototype, register = token) is directly the A operand of the
+// aggregation acc[m, j] += sum_t E[t, m] V'[t, j], with the k slots in the perm16
+// token order; V' is staged row-major in LDS and read as the matching B operand
+// with the transposing LDS load.  1/z is folded into V' (d values per token
+// instead of M).
 //
 // Pipeline per tile i (two workgroup barriers on the common path):
 //   S/exp over the wave's prototype tiles  (K(i) in LDS buffer i%2)
 //   stage K(i+1) into buffer (i+1)%2; per-token partial sums to LDS
 //   --- barrier ---
-//   z, lse; stage V(i)/z transposed; issue the global loads of tile i+2
+//   z, lse; stage V(i)/z; issue the global loads of tile i+2
 //   --- barrier ---
 //   aggregation MFMAs
 #include "sa_internal.h"
+#include "tile_ops.h"
 
 namespace sa {
 
 namespace {
 
-typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
-typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
-typedef float f32x16 __attribute__((ext_vector_type(16)));
-typedef float f32x2 __attribute__((ext_vector_type(2)));
+using namespace tile;
 
-constexpr float kLog2e = 1.4426950408889634f;
 // z below this means the shift was too far above the largest logit
 constexpr float kUnderflowZ = 5.421010862427522e-20f;  // 2^-64
 // relative margin on the bound for the rounding of the fp32 norms and logits
 constexpr float kBoundMargin = 1.0f + 1.0f / 1024.0f;
-
-__device__ inline float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
-__device__ inline float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
-
-// Two fp32 -> packed bf16x2 (round to nearest even), first value in the low half.
-__device__ inline uint32_t pack_bf16x2(float a, float b) {
-    bf16x2 v = __builtin_convertvector((f32x2){a, b}, bf16x2);
-    return __builtin_bit_cast(uint32_t, v);
-}
-
-__device__ inline bf16x8 pack8(const float* e) {
-    uint4 pk;
-    pk.x = pack_bf16x2(e[0], e[1]);
-    pk.y = pack_bf16x2(e[2], e[3]);
-    pk.z = pack_bf16x2(e[4], e[5]);
-    pk.w = pack_bf16x2(e[6], e[7]);
-    return __builtin_bit_cast(bf16x8, pk);
-}
 
 __device__ inline float sumsq8(uint4 v) {
     const uint32_t w[4] = {v.x, v.y, v.z, v.w};
@@ -89,32 +65,6 @@ __device__ inline float sumsq8(uint4 v) {
     }
     return s;
 }
-
-// LDS element offset (in bf16 units) of 16-byte chunk c of row r of a matrix
-// with COLS bf16 per row; chunks are XOR-swizzled with the row so that the
-// 32 rows read by one operand load fall in different banks.
-template <int COLS>
-__device__ inline int swz(int r, int c) {
-    if constexpr (COLS == 32) {
-        return r * 32 + ((c ^ ((r >> 1) & 3)) << 3);
-    } else {
-        return r * COLS + ((c ^ (r & 7)) << 3);
-    }
-}
-
-__device__ inline bf16x8 lds_b128(const uint16_t* base, int off) {
-    uint4 v = *reinterpret_cast<const uint4*>(base + off);
-    return __builtin_bit_cast(bf16x8, v);
-}
-
-// token position of tile row t inside the k slots of the aggregation MFMA:
-// swap bits 2 and 3 of t (see the header comment)
-__device__ inline int perm_tok(int t) {
-    return (t & ~12) | ((t & 4) << 1) | ((t & 8) >> 1);
-}
-
-// row of S (token index inside the tile) held by register r of this lane-half
-__device__ inline int srow(int r, int hl) { return 8 * (r >> 2) + 4 * hl + (r & 3); }
 
 // Cross-lane moves without LDS: DPP inside rows of 16 lanes, then
 // v_permlane16_swap between the two rows of each 32-lane half.
@@ -431,7 +381,7 @@ __global__ __launch_bounds__(NW * 64, 1) void fwd_fused_kernel(FusedFwdArgs a) {
                 a.lse[(int64_t)(ts + tid) * a.H + h] = c + __logf(z);
             }
 
-            // ---- stage V / z transposed, in the permuted token order
+            // ---- stage V / z (row-major; the aggregation reads it transposed)
 #pragma unroll
             for (int i = 0; i < C::NLD; ++i) {
                 int idx = tid + i * C::THREADS;
@@ -441,16 +391,7 @@ __global__ __launch_bounds__(NW * 64, 1) void fwd_fused_kernel(FusedFwdArgs a) {
                     float z = 0.f;
 #pragma unroll
                     for (int ww = 0; ww < NW; ++ww) z += zsrc[ww * 32 + tok];
-                    const float rz = 1.0f / z;
-                    const uint32_t wv[4] = {vcur[i].x, vcur[i].y, vcur[i].z, vcur[i].w};
-                    const int p = perm_tok(tok);
-#pragma unroll
-                    for (int e2 = 0; e2 < 4; ++e2) {
-                        const uint32_t pk = pack_bf16x2(bf16_lo(wv[e2]) * rz, bf16_hi(wv[e2]) * rz);
-                        const int j0 = ch * 8 + 2 * e2;
-                        Vt[swz<32>(j0, p >> 3) + (p & 7)] = (uint16_t)(pk & 0xffffu);
-                        Vt[swz<32>(j0 + 1, p >> 3) + (p & 7)] = (uint16_t)(pk >> 16);
-                    }
+                    *reinterpret_cast<uint4*>(Vt + swz<D>(tok, ch)) = scale8(vcur[i], 1.0f / z);
                 }
             }
             // V of tile i+1 is in vreg; issue the loads of tile i+2
@@ -462,8 +403,8 @@ __global__ __launch_bounds__(NW * 64, 1) void fwd_fused_kernel(FusedFwdArgs a) {
             // ---- acc[m, j] += E^T . V'
 #pragma unroll
             for (int jt = 0; jt < C::JT; ++jt) {
-                const bf16x8 v0 = lds_b128(Vt, swz<32>(jt * 32 + l32, 0 + hl));
-                const bf16x8 v1 = lds_b128(Vt, swz<32>(jt * 32 + l32, 2 + hl));
+                const bf16x8 v0 = lds_tr_tokens<D>(Vt, lane, jt, 0);
+                const bf16x8 v1 = lds_tr_tokens<D>(Vt, lane, jt, 1);
 #pragma unroll
                 for (int mt = 0; mt < C::MT; ++mt) {
                     acc[mt][jt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(eop[mt][0], v0, acc[mt][jt], 0, 0, 0);
