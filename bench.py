@@ -43,13 +43,13 @@ WORKLOADS = {"c1": 1, "c2": 2, "c3": 3, "c4": 4, "c5": 5}
 # Source: profiles/hbm_bytes_c5_ragged100k_fwd_bwd.md
 MEASURED_TRAFFIC = {
     "bwd_token": ("paper_2609_08443_amd/csrc/bwd_fused.hip",
-                  "d1ca8cfbe428379d7a806233f5ab8524c8c6f5f02cf5d17437136b55c4b8b27e",
-                  6.702e9 + 2.250e9),
+                  "533282ec166fefbb35822ab13b3ce445882926257102688843bd37b37e36e7de",
+                  4.349e9 + 2.272e9),
     "bwd_proto": ("paper_2609_08443_amd/csrc/bwd_fused.hip",
-                  "d1ca8cfbe428379d7a806233f5ab8524c8c6f5f02cf5d17437136b55c4b8b27e",
-                  2.408e9 + 0.100e9),
+                  "533282ec166fefbb35822ab13b3ce445882926257102688843bd37b37e36e7de",
+                  2.407e9 + 0.100e9),
     "fused_fwd": ("paper_2609_08443_amd/csrc/fwd_fused.hip",
-                  "e2d6b8407c99024b7c302050319d8e93895edc87e7e0d8b065bad6ee7a7457b4",
+                  "905bf9def0c09f646691982ffa18bdd74941166efeaa1ce06a8cc30c850563c2",
                   1.114e9 + 0.135e9),
 }
 

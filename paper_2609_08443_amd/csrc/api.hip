@@ -177,9 +177,10 @@ BwdPlan plan_bwd(int64_t B, int64_t T, int32_t H, int32_t M, int32_t d, sa_dtype
         return o;
     };
     if (p.fused) {
-        // one workgroup range per CU; the dP kernel runs M / part workgroups per range
+        // token-side workgroup ranges: as many as fit on the CUs at once; the dP
+        // kernel runs M / part workgroups per range
         const int64_t HT = (int64_t)H * T;
-        const int64_t target = device_cus();
+        const int64_t target = (int64_t)device_cus() * sa::fused_bwd_ranges_per_cu();
         int64_t C = (HT + target - 1) / target;
         C = (C + 127) / 128 * 128;
         if (C < 128) C = 128;

@@ -104,7 +104,7 @@ struct TokArgs {
 };
 
 template <int D, int NW>
-__global__ __launch_bounds__(NW * 64, 1) void bwd_token_kernel(TokArgs a) {
+__global__ __launch_bounds__(NW * 64, 8 / NW) void bwd_token_kernel(TokArgs a) {
     using C = TokCfg<D, NW>;
     extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
     uint16_t* lds = reinterpret_cast<uint16_t*>(smem);
@@ -152,7 +152,7 @@ __global__ __launch_bounds__(NW * 64, 1) void bwd_token_kernel(TokArgs a) {
             // then registers -> LDS buffer `buf` after the current block's compute
             // (sweep 0: Pmj, Yjm; sweep 1: Pmj, Pjm, Ymj)
             constexpr int NCH = (C::CHUNKS + C::THREADS - 1) / C::THREADS;
-            uint4 rg_mj[NCH], rg_y[NCH], rg_jm[NCH];
+            u32x4 rg_mj[NCH], rg_y[NCH], rg_jm[NCH];  // native vectors stay in registers
             auto fetch = [&](int mb, int sweep) {
 #pragma unroll
                 for (int c = 0; c < NCH; ++c) {
@@ -160,11 +160,11 @@ __global__ __launch_bounds__(NW * 64, 1) void bwd_token_kernel(TokArgs a) {
                     if (i < C::CHUNKS) {
                         const int r = i / (D / 8), ch = i % (D / 8);
                         const int64_t src = (int64_t)(mb * 32 + r) * D + ch * 8;
-                        rg_mj[c] = *reinterpret_cast<const uint4*>(Pmj_g + src);
-                        if (sweep == 1) rg_y[c] = *reinterpret_cast<const uint4*>(Ymj_g + src);
+                        rg_mj[c] = *reinterpret_cast<const u32x4*>(Pmj_g + src);
+                        if (sweep == 1) rg_y[c] = *reinterpret_cast<const u32x4*>(Ymj_g + src);
                         const int j = i / 4, cj = i % 4;
                         const int64_t srcj = (int64_t)j * a.M + mb * 32 + cj * 8;
-                        rg_jm[c] = *reinterpret_cast<const uint4*>((sweep == 1 ? Pjm_g : Yjm_g) + srcj);
+                        rg_jm[c] = *reinterpret_cast<const u32x4*>((sweep == 1 ? Pjm_g : Yjm_g) + srcj);
                     }
                 }
             };
@@ -175,10 +175,10 @@ __global__ __launch_bounds__(NW * 64, 1) void bwd_token_kernel(TokArgs a) {
                     const int i = tid + c * C::THREADS;
                     if (i < C::CHUNKS) {
                         const int r = i / (D / 8), ch = i % (D / 8);
-                        *reinterpret_cast<uint4*>(L + swz<D>(r, ch)) = rg_mj[c];
-                        if (sweep == 1) *reinterpret_cast<uint4*>(L + 2 * C::BLK + swz<D>(r, ch)) = rg_y[c];
+                        *reinterpret_cast<u32x4*>(L + swz<D>(r, ch)) = rg_mj[c];
+                        if (sweep == 1) *reinterpret_cast<u32x4*>(L + 2 * C::BLK + swz<D>(r, ch)) = rg_y[c];
                         const int j = i / 4, cj = i % 4;
-                        *reinterpret_cast<uint4*>(L + (sweep == 1 ? C::BLK : 3 * C::BLK) + swz<32>(j, cj)) = rg_jm[c];
+                        *reinterpret_cast<u32x4*>(L + (sweep == 1 ? C::BLK : 3 * C::BLK) + swz<32>(j, cj)) = rg_jm[c];
                     }
                 }
             };
@@ -239,10 +239,13 @@ __global__ __launch_bounds__(NW * 64, 1) void bwd_token_kernel(TokArgs a) {
             // write dV now (frees its registers)
             if (tv) {
                 float* out = a.dV + ((int64_t)tok * a.H + h) * D;
+                // registers 4g..4g+3 hold 4 consecutive columns: 16-byte stores
 #pragma unroll
                 for (int jt = 0; jt < C::JT; ++jt)
 #pragma unroll
-                    for (int r = 0; r < 16; ++r) out[jt * 32 + srow(r, hl)] = dvt[jt][r];
+                    for (int g = 0; g < 4; ++g)
+                        *reinterpret_cast<float4*>(out + jt * 32 + 8 * g + 4 * hl) =
+                            make_float4(dvt[jt][4 * g], dvt[jt][4 * g + 1], dvt[jt][4 * g + 2], dvt[jt][4 * g + 3]);
                 if (hl == 0) a.Dbuf[(int64_t)tok * a.H + h] = Dt;
             }
 
@@ -287,7 +290,10 @@ __global__ __launch_bounds__(NW * 64, 1) void bwd_token_kernel(TokArgs a) {
 #pragma unroll
                 for (int jt = 0; jt < C::JT; ++jt)
 #pragma unroll
-                    for (int r = 0; r < 16; ++r) out[jt * 32 + srow(r, hl)] = a.scale * dkt[jt][r];
+                    for (int g = 0; g < 4; ++g)
+                        *reinterpret_cast<float4*>(out + jt * 32 + 8 * g + 4 * hl) =
+                            make_float4(a.scale * dkt[jt][4 * g], a.scale * dkt[jt][4 * g + 1],
+                                        a.scale * dkt[jt][4 * g + 2], a.scale * dkt[jt][4 * g + 3]);
             }
         }
     }
@@ -544,8 +550,10 @@ hipError_t launch_proto(const ProtoArgs& a, int64_t n_ranges, hipStream_t stream
 
 }  // namespace
 
-// waves of the token-side kernel: two per SIMD
+// waves of the token-side kernel: two per SIMD, one workgroup per CU
 constexpr int kTokWaves = 8;
+
+int32_t fused_bwd_ranges_per_cu() { return 8 / kTokWaves; }
 
 // prototypes per part of the dP kernel: P and dY slices of MP x d bf16 each fit in LDS
 int32_t fused_bwd_part(int32_t M, int32_t d) {

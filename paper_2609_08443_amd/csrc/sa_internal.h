@@ -100,6 +100,8 @@ struct FusedBwdArgs {
 };
 bool fused_bwd_supported(int32_t M, int32_t d);
 int32_t fused_bwd_part(int32_t M, int32_t d);
+// token-side workgroups resident per CU (sizes the work-list ranges)
+int32_t fused_bwd_ranges_per_cu();
 hipError_t launch_fused_bwd(const FusedBwdArgs& a, hipStream_t stream);
 
 // Plain fp32-arithmetic path (fp32 or bf16 inputs).
