@@ -35,6 +35,15 @@ namespace {
 
 using namespace tile;
 
+// A wave raises its issue priority for the length of a matrix-core chain and
+// drops it for its exponential / elementwise phase, so that the two waves of a
+// SIMD drift into opposite phases (one feeds the matrix core while the other
+// runs VALU and LDS work) instead of contending for the same unit in lockstep.
+// The changes take registers of the chain as operands, which orders the raise
+// before the chain's first MFMA and the drop after its results.
+__device__ inline void prio_up(const bf16x8& a) { asm volatile("s_setprio 1" :: "v"(a)); }
+__device__ inline void prio_down(f32x16& a) { asm volatile("s_setprio 0" : "+v"(a)); }
+
 __device__ inline float xhalf_sum(float v) {
     const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
     return __uint_as_float(r[0]) + __uint_as_float(r[1]);
@@ -77,6 +86,7 @@ struct TokCfg {
     static constexpr int TB = 32 * NW;                 // tokens per block (32 per wave)
     static constexpr int KS = D / 16;
     static constexpr int JT = D / 32;
+    static constexpr int KCH = D / 8;                  // 16-byte chunks per row
     static constexpr int BLK = 32 * D;                 // bf16 elements of one 32-row block
     // LDS: two buffers of {Pmj, Pjm, Ymj, Yjm} prototype blocks
     static constexpr int BUF = 4 * BLK;
@@ -111,13 +121,17 @@ __global__ __launch_bounds__(NW * 64, 8 / NW) void bwd_token_kernel(TokArgs a) {
     const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
     const int l32 = lane & 31, hl = lane >> 5;
 
-    const int64_t range = blockIdx.x;
+    const int64_t range = xcd_range(blockIdx.x, gridDim.x);
     const int64_t k0 = a.wg_start[range], k1 = a.wg_start[range + 1];
     if (k0 < 0 || k1 < k0 || k1 > a.max_items) return;
     const float ks2 = a.scale * kLog2e;
     const int nblk = a.M / 32;
     const int64_t MD = (int64_t)a.M * D;
 
+    // The workgroup's first token block is shortened by (range % 4) quarter blocks:
+    // workgroups then reach their HBM phases (K/V loads, dV/dK stores) at staggered
+    // times, overlapping other workgroups' matrix work, instead of all at once.
+    int first_cut = (int)(range % 4) * (C::TB / 4);
     for (int64_t k = k0; k < k1; ++k) {
         const int32_t* it = a.items + k * IT_WORDS;
         const int b = it[IT_B], h = it[IT_H], t0 = it[IT_T0], t1 = it[IT_T1];
@@ -127,9 +141,12 @@ __global__ __launch_bounds__(NW * 64, 8 / NW) void bwd_token_kernel(TokArgs a) {
         const uint16_t* Ymj_g = a.Ymj + ((int64_t)b * a.H + h) * MD;
         const uint16_t* Yjm_g = a.Yjm + ((int64_t)b * a.H + h) * MD;
 
-        for (int tb = t0; tb < t1; tb += C::TB) {
+        for (int tb = t0, te = t0; tb < t1; tb = te) {
+            te = tb + C::TB - first_cut;
+            first_cut = 0;
+            if (te > t1) te = t1;
             const int tok = tb + 32 * w + l32;   // this lane's token (column of S^T)
-            const bool tv = tok < t1;
+            const bool tv = tok < te;
             // K and V as B operands: lane (hl, t) holds 8 consecutive j of its token
             bf16x8 kb[C::KS], vb[C::KS];
             {
@@ -146,39 +163,25 @@ __global__ __launch_bounds__(NW * 64, 8 / NW) void bwd_token_kernel(TokArgs a) {
             }
             const float nl = tv ? -a.lse[(int64_t)tok * a.H + h] * kLog2e : 0.f;
 
-            // stage prototype block mb of the requested matrices into buffer `buf`
-            // (sweep 0: Pmj, Yjm; sweep 1: Pmj, Pjm, Ymj)
-            // prototype block mb of the requested matrices: global -> registers,
-            // then registers -> LDS buffer `buf` after the current block's compute
-            // (sweep 0: Pmj, Yjm; sweep 1: Pmj, Pjm, Ymj)
-            constexpr int NCH = (C::CHUNKS + C::THREADS - 1) / C::THREADS;
-            u32x4 rg_mj[NCH], rg_y[NCH], rg_jm[NCH];  // native vectors stay in registers
-            auto fetch = [&](int mb, int sweep) {
-#pragma unroll
-                for (int c = 0; c < NCH; ++c) {
-                    const int i = tid + c * C::THREADS;
-                    if (i < C::CHUNKS) {
-                        const int r = i / (D / 8), ch = i % (D / 8);
-                        const int64_t src = (int64_t)(mb * 32 + r) * D + ch * 8;
-                        rg_mj[c] = *reinterpret_cast<const u32x4*>(Pmj_g + src);
-                        if (sweep == 1) rg_y[c] = *reinterpret_cast<const u32x4*>(Ymj_g + src);
-                        const int j = i / 4, cj = i % 4;
-                        const int64_t srcj = (int64_t)j * a.M + mb * 32 + cj * 8;
-                        rg_jm[c] = *reinterpret_cast<const u32x4*>((sweep == 1 ? Pjm_g : Yjm_g) + srcj);
-                    }
-                }
-            };
-            auto store = [&](int buf, int sweep) {
+            // prototype block mb of the requested matrices straight into LDS buffer
+            // `buf` (sweep 0: Pmj, Yjm; sweep 1: Pmj, Pjm, Ymj).  Lane l of a wave
+            // fetches the global chunk that belongs at LDS chunk position p = 64 q + l
+            // of the swizzled layout (the XOR swizzle is its own inverse).
+            auto fetch = [&](int mb, int sweep, int buf) __attribute__((always_inline)) {
                 uint16_t* L = lds + buf * C::BUF;
-#pragma unroll
-                for (int c = 0; c < NCH; ++c) {
-                    const int i = tid + c * C::THREADS;
-                    if (i < C::CHUNKS) {
-                        const int r = i / (D / 8), ch = i % (D / 8);
-                        *reinterpret_cast<u32x4*>(L + swz<D>(r, ch)) = rg_mj[c];
-                        if (sweep == 1) *reinterpret_cast<u32x4*>(L + 2 * C::BLK + swz<D>(r, ch)) = rg_y[c];
-                        const int j = i / 4, cj = i % 4;
-                        *reinterpret_cast<u32x4*>(L + (sweep == 1 ? C::BLK : 3 * C::BLK) + swz<32>(j, cj)) = rg_jm[c];
+                constexpr int NQ = C::CHUNKS / 64;   // wave-loads per matrix block
+                for (int q = w; q < NQ; q += NW) {
+                    const int p = q * 64 + lane;
+                    {   // row-major [32 prototypes][D]: Pmj, and Ymj in sweep 1
+                        const int r = p / C::KCH, c = (p % C::KCH) ^ swz_x<D>(r);
+                        const int64_t src = (int64_t)(mb * 32 + r) * D + c * 8;
+                        load_lds16(Pmj_g + src, L + q * 512);
+                        if (sweep == 1) load_lds16(Ymj_g + src, L + 2 * C::BLK + q * 512);
+                    }
+                    {   // [D][32 prototypes], prototype index permuted: Yjm or Pjm
+                        const int j = p / 4, c = (p % 4) ^ swz_x<32>(j);
+                        const int64_t srcj = (int64_t)j * a.M + mb * 32 + c * 8;
+                        load_lds16((sweep == 1 ? Pjm_g : Yjm_g) + srcj, L + (sweep == 1 ? C::BLK : 3 * C::BLK) + q * 512);
                     }
                 }
             };
@@ -200,24 +203,28 @@ __global__ __launch_bounds__(NW * 64, 8 / NW) void bwd_token_kernel(TokArgs a) {
 #pragma unroll
                 for (int r = 0; r < 16; ++r) dvt[jt][r] = 0.f;
             __syncthreads();  // previous users of the buffers are done
-            fetch(0, 0);
-            store(0, 0);
+            fetch(0, 0, 0);
+            wait_vmem();
             __syncthreads();
             for (int mb = 0; mb < nblk; ++mb) {
                 const uint16_t* L = lds + (mb & 1) * C::BUF;
-                if (mb + 1 < nblk) fetch(mb + 1, 0);
-                const f32x16 s = st_tile(L);
+                if (mb + 1 < nblk) fetch(mb + 1, 0, (mb + 1) & 1);
+                prio_up(kb[0]);
+                f32x16 s = st_tile(L);
+                prio_down(s);
                 float e[16];
 #pragma unroll
                 for (int r = 0; r < 16; ++r) e[r] = __builtin_amdgcn_exp2f(__builtin_fmaf(s[r], ks2, nl));
                 const bf16x8 ab0 = pack8(e), ab1 = pack8(e + 8);
+                prio_up(ab1);
 #pragma unroll
                 for (int jt = 0; jt < C::JT; ++jt) {
                     const uint16_t* Y = L + 3 * C::BLK;
                     dvt[jt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(lds_b128(Y, swz<32>(jt * 32 + l32, 0 + hl)), ab0, dvt[jt], 0, 0, 0);
                     dvt[jt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(lds_b128(Y, swz<32>(jt * 32 + l32, 2 + hl)), ab1, dvt[jt], 0, 0, 0);
                 }
-                if (mb + 1 < nblk) store((mb + 1) & 1, 0);
+                prio_down(dvt[C::JT - 1]);
+                wait_vmem();   // block mb + 1 has landed in LDS
                 __syncthreads();
             }
             // D_t = <V_t, dV_t>: this lane holds dV[t, j] for j = jt*32 + srow(r, hl)
@@ -255,13 +262,14 @@ __global__ __launch_bounds__(NW * 64, 8 / NW) void bwd_token_kernel(TokArgs a) {
             for (int jt = 0; jt < C::JT; ++jt)
 #pragma unroll
                 for (int r = 0; r < 16; ++r) dkt[jt][r] = 0.f;
-            fetch(0, 1);
-            store(0, 1);
+            fetch(0, 1, 0);
+            wait_vmem();
             __syncthreads();
             for (int mb = 0; mb < nblk; ++mb) {
                 const uint16_t* L = lds + (mb & 1) * C::BUF;
-                if (mb + 1 < nblk) fetch(mb + 1, 1);
-                const f32x16 s = st_tile(L);
+                if (mb + 1 < nblk) fetch(mb + 1, 1, (mb + 1) & 1);
+                prio_up(kb[0]);
+                f32x16 s = st_tile(L);
                 f32x16 da;
 #pragma unroll
                 for (int r = 0; r < 16; ++r) da[r] = 0.f;
@@ -269,6 +277,8 @@ __global__ __launch_bounds__(NW * 64, 8 / NW) void bwd_token_kernel(TokArgs a) {
 #pragma unroll
                 for (int kk = 0; kk < C::KS; ++kk)
                     da = __builtin_amdgcn_mfma_f32_32x32x16_bf16(lds_b128(Ym, swz<D>(l32, 2 * kk + hl)), vb[kk], da, 0, 0, 0);
+                prio_down(s);
+                prio_down(da);
                 float e[16];
 #pragma unroll
                 for (int r = 0; r < 16; ++r) {
@@ -276,13 +286,15 @@ __global__ __launch_bounds__(NW * 64, 8 / NW) void bwd_token_kernel(TokArgs a) {
                     e[r] = A * (da[r] - Dt);
                 }
                 const bf16x8 d0 = pack8(e), d1 = pack8(e + 8);
+                prio_up(d1);
                 const uint16_t* Pj = L + C::BLK;
 #pragma unroll
                 for (int jt = 0; jt < C::JT; ++jt) {
                     dkt[jt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(lds_b128(Pj, swz<32>(jt * 32 + l32, 0 + hl)), d0, dkt[jt], 0, 0, 0);
                     dkt[jt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(lds_b128(Pj, swz<32>(jt * 32 + l32, 2 + hl)), d1, dkt[jt], 0, 0, 0);
                 }
-                if (mb + 1 < nblk) store((mb + 1) & 1, 1);
+                prio_down(dkt[C::JT - 1]);
+                wait_vmem();
                 __syncthreads();
             }
             if (tv) {
@@ -310,13 +322,20 @@ struct ProtoCfg {
     static constexpr int JT = D / 32;
     static constexpr int KCH = D / 8;
     static constexpr int LD_CHUNKS = 32 * KCH;
+    static constexpr int NCH = (LD_CHUNKS + THREADS - 1) / THREADS;
+    // With one 32-prototype tile per wave the wave's P and dY rows are held in
+    // registers for the segment (loaded from global memory); otherwise the part's
+    // P and dY slices stay in LDS.
+    static constexpr bool HOLD = MT == 1;
+    static constexpr int SLICE = HOLD ? 0 : MP * D * 2;
+    static constexpr int TILE = 32 * D * 2;                // one [32][D] bf16 token tile
     static constexpr int OFF_P = 0;                        // [MP][D]
-    static constexpr int OFF_Y = OFF_P + MP * D * 2;       // [MP][D]
-    static constexpr int OFF_K = OFF_Y + MP * D * 2;       // [32][D] token-major K tile
-    static constexpr int OFF_V = OFF_K + 32 * D * 2;       // [32][D] V tile
-    static constexpr int OFF_L = OFF_V + 32 * D * 2;       // [32] -lse*log2e
-    static constexpr int OFF_D = OFF_L + 32 * 4;           // [32] D_t
-    static constexpr int LDS = OFF_D + 32 * 4;
+    static constexpr int OFF_Y = OFF_P + SLICE;            // [MP][D]
+    static constexpr int OFF_K = OFF_Y + SLICE;            // 2 x [32][D] token-major K tiles
+    static constexpr int OFF_V = OFF_K + 2 * TILE;         // 2 x [32][D] V tiles
+    static constexpr int OFF_L = OFF_V + 2 * TILE;         // 2 x [32] -lse*log2e
+    static constexpr int OFF_D = OFF_L + 2 * 32 * 4;       // 2 x [32] D_t
+    static constexpr int LDS = OFF_D + 2 * 32 * 4;
 };
 
 struct ProtoArgs {
@@ -338,17 +357,14 @@ struct ProtoArgs {
 template <int D, int MW, int NW>
 __global__ __launch_bounds__(NW * 64, 1) void bwd_proto_kernel(ProtoArgs a) {
     using C = ProtoCfg<D, MW, NW>;
+    constexpr bool kHold = C::HOLD;
     extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
     uint16_t* Ps = reinterpret_cast<uint16_t*>(smem + C::OFF_P);
     uint16_t* Ys = reinterpret_cast<uint16_t*>(smem + C::OFF_Y);
-    uint16_t* Ks = reinterpret_cast<uint16_t*>(smem + C::OFF_K);
-    uint16_t* Vs = reinterpret_cast<uint16_t*>(smem + C::OFF_V);
-    float* nls = reinterpret_cast<float*>(smem + C::OFF_L);
-    float* Ds = reinterpret_cast<float*>(smem + C::OFF_D);
     const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
     const int l32 = lane & 31, hl = lane >> 5;
 
-    const int64_t range = blockIdx.x;
+    const int64_t range = xcd_range(blockIdx.x, gridDim.x);
     const int part = blockIdx.y;          // prototypes [part*MP, (part+1)*MP)
     const int64_t k0 = a.wg_start[range], k1 = a.wg_start[range + 1];
     if (k0 < 0 || k1 < k0 || k1 > a.max_items) return;
@@ -361,40 +377,23 @@ __global__ __launch_bounds__(NW * 64, 1) void bwd_proto_kernel(ProtoArgs a) {
         const int32_t* it = a.items + k * IT_WORDS;
         const int b = it[IT_B], h = it[IT_H], t0 = it[IT_T0], t1 = it[IT_T1];
         if (b < 0 || b >= a.B || h < 0 || h >= a.H || t0 < 0 || t1 < t0 || t1 > a.T) continue;
-        __syncthreads();  // previous segment is done with the LDS tiles
-        {
-            const uint4* srcP = reinterpret_cast<const uint4*>(a.P + (int64_t)h * MD + (int64_t)part * C::MP * D);
-            const uint4* srcY = reinterpret_cast<const uint4*>(a.Ymj + ((int64_t)b * a.H + h) * MD + (int64_t)part * C::MP * D);
-            for (int i = tid; i < C::MP * C::KCH; i += C::THREADS) {
-                const int r = i / C::KCH, c = i % C::KCH;
-                if (h != cur_h) *reinterpret_cast<uint4*>(Ps + swz<D>(r, c)) = srcP[i];
-                *reinterpret_cast<uint4*>(Ys + swz<D>(r, c)) = srcY[i];
-            }
-            cur_h = h;
-        }
-        f32x16 acc[C::MT][C::JT];
-#pragma unroll
-        for (int mt = 0; mt < C::MT; ++mt)
-#pragma unroll
-            for (int jt = 0; jt < C::JT; ++jt)
-#pragma unroll
-                for (int r = 0; r < 16; ++r) acc[mt][jt][r] = 0.f;
+        const uint16_t* Pg = a.P + (int64_t)h * MD + (int64_t)part * C::MP * D;
+        const uint16_t* Yg = a.Ymj + ((int64_t)b * a.H + h) * MD + (int64_t)part * C::MP * D;
 
-        // token tiles: global -> registers one tile ahead, registers -> LDS per tile
-        constexpr int NCH = (C::LD_CHUNKS + C::THREADS - 1) / C::THREADS;
-        uint4 kreg[NCH], vreg[NCH];
+        // token tiles: global -> registers one tile ahead, registers -> LDS buffer
+        u32x4 kreg[C::NCH], vreg[C::NCH];
         float lse_r = 0.f, d_r = 0.f;
-        auto fetch = [&](int ts) {
+        auto fetch = [&](int ts) __attribute__((always_inline)) {
             const int64_t tb = ((int64_t)ts * a.H + h) * D;
 #pragma unroll
-            for (int c = 0; c < NCH; ++c) {
+            for (int c = 0; c < C::NCH; ++c) {
                 const int idx = tid + c * C::THREADS;
                 const int tok = idx / C::KCH, ch = idx % C::KCH;
-                uint4 kv = make_uint4(0, 0, 0, 0), vv = make_uint4(0, 0, 0, 0);
+                u32x4 kv = (u32x4){0u, 0u, 0u, 0u}, vv = kv;
                 if (idx < C::LD_CHUNKS && ts + tok < t1) {
                     const uint32_t off = (uint32_t)tok * row_stride + (uint32_t)(ch * 8);
-                    kv = *reinterpret_cast<const uint4*>(a.K + tb + off);
-                    vv = *reinterpret_cast<const uint4*>(a.V + tb + off);
+                    kv = *reinterpret_cast<const u32x4*>(a.K + tb + off);
+                    vv = *reinterpret_cast<const u32x4*>(a.V + tb + off);
                 }
                 kreg[c] = kv;
                 vreg[c] = vv;
@@ -405,39 +404,67 @@ __global__ __launch_bounds__(NW * 64, 1) void bwd_proto_kernel(ProtoArgs a) {
                 d_r = v ? a.Dbuf[(int64_t)(ts + tid) * a.H + h] : 0.f;
             }
         };
-        fetch(t0);
-        __syncthreads();  // the P and dY slices are in LDS
-        // With one prototype tile per wave, this wave's rows of P and dY are held in
-        // registers as B operands for the whole segment (each K / V operand is then
-        // used once); with more, K and V operands are read once per tile and reused.
-        constexpr bool kHold = C::MT == 1;
-        constexpr int HM = kHold ? C::MT : 1, HK = kHold ? C::KS : 1;
-        bf16x8 pop[HM][HK], yop[HM][HK];
-        if constexpr (kHold) {
+        auto store = [&](int buf) __attribute__((always_inline)) {
+            uint16_t* Kd = reinterpret_cast<uint16_t*>(smem + C::OFF_K + buf * C::TILE);
+            uint16_t* Vd = reinterpret_cast<uint16_t*>(smem + C::OFF_V + buf * C::TILE);
 #pragma unroll
-            for (int kk = 0; kk < C::KS; ++kk) {
-                const int prow = w * MW + l32;
-                pop[0][kk] = lds_b128(Ps, swz<D>(prow, 2 * kk + hl));
-                yop[0][kk] = lds_b128(Ys, swz<D>(prow, 2 * kk + hl));
-            }
-        }
-        for (int ts = t0; ts < t1; ts += 32) {
-            __syncthreads();  // previous tile's K, V, lse, D consumed
-#pragma unroll
-            for (int c = 0; c < NCH; ++c) {
+            for (int c = 0; c < C::NCH; ++c) {
                 const int idx = tid + c * C::THREADS;
                 if (idx < C::LD_CHUNKS) {
                     const int tok = idx / C::KCH, ch = idx % C::KCH;
-                    *reinterpret_cast<uint4*>(Ks + swz<D>(tok, ch)) = kreg[c];
-                    *reinterpret_cast<uint4*>(Vs + swz<D>(tok, ch)) = vreg[c];
+                    *reinterpret_cast<u32x4*>(Kd + swz<D>(tok, ch)) = kreg[c];
+                    *reinterpret_cast<u32x4*>(Vd + swz<D>(tok, ch)) = vreg[c];
                 }
             }
             if (tid < 32) {
-                nls[tid] = lse_r;
-                Ds[tid] = d_r;
+                reinterpret_cast<float*>(smem + C::OFF_L)[buf * 32 + tid] = lse_r;
+                reinterpret_cast<float*>(smem + C::OFF_D)[buf * 32 + tid] = d_r;
             }
-            __syncthreads();
-            if (ts + 32 < t1) fetch(ts + 32);
+        };
+
+        fetch(t0);
+        // With one prototype tile per wave, this wave's rows of P and dY are B
+        // operands held in registers for the whole segment (each K / V operand is
+        // then used once); with more, K and V operands are read once per tile and
+        // reused, and P and dY are read from the LDS slices.
+        constexpr int HK = kHold ? C::KS : 1;
+        bf16x8 pop[HK], yop[HK];
+        if constexpr (kHold) {
+            const int prow = w * MW + l32;
+#pragma unroll
+            for (int kk = 0; kk < C::KS; ++kk) {
+                pop[kk] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(Pg + prow * D + 16 * kk + 8 * hl));
+                yop[kk] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(Yg + prow * D + 16 * kk + 8 * hl));
+            }
+        }
+        __syncthreads();  // the previous segment is done with every LDS buffer
+        if constexpr (!kHold) {
+            for (int i = tid; i < C::MP * C::KCH; i += C::THREADS) {
+                const int r = i / C::KCH, c = i % C::KCH;
+                if (h != cur_h) *reinterpret_cast<u32x4*>(Ps + swz<D>(r, c)) = reinterpret_cast<const u32x4*>(Pg)[i];
+                *reinterpret_cast<u32x4*>(Ys + swz<D>(r, c)) = reinterpret_cast<const u32x4*>(Yg)[i];
+            }
+        }
+        cur_h = h;
+        store(0);
+        __syncthreads();
+
+        f32x16 acc[C::MT][C::JT];
+#pragma unroll
+        for (int mt = 0; mt < C::MT; ++mt)
+#pragma unroll
+            for (int jt = 0; jt < C::JT; ++jt)
+#pragma unroll
+                for (int r = 0; r < 16; ++r) acc[mt][jt][r] = 0.f;
+
+        int buf = 0;
+        for (int ts = t0; ts < t1; ts += 32, buf ^= 1) {
+            const bool more = ts + 32 < t1;
+            if (more) fetch(ts + 32);
+            const uint16_t* Ks = reinterpret_cast<const uint16_t*>(smem + C::OFF_K + buf * C::TILE);
+            const uint16_t* Vs = reinterpret_cast<const uint16_t*>(smem + C::OFF_V + buf * C::TILE);
+            const float* nls = reinterpret_cast<const float*>(smem + C::OFF_L) + buf * 32;
+            const float* Ds = reinterpret_cast<const float*>(smem + C::OFF_D) + buf * 32;
 
             constexpr int OK = kHold ? 1 : C::KS;
             bf16x8 kop[OK], vop[OK];
@@ -458,8 +485,8 @@ __global__ __launch_bounds__(NW * 64, 1) void bwd_proto_kernel(ProtoArgs a) {
 #pragma unroll
                 for (int kk = 0; kk < C::KS; ++kk) {
                     if constexpr (kHold) {
-                        s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(lds_b128(Ks, swz<D>(l32, 2 * kk + hl)), pop[0][kk], s, 0, 0, 0);
-                        da = __builtin_amdgcn_mfma_f32_32x32x16_bf16(lds_b128(Vs, swz<D>(l32, 2 * kk + hl)), yop[0][kk], da, 0, 0, 0);
+                        s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(lds_b128(Ks, swz<D>(l32, 2 * kk + hl)), pop[kk], s, 0, 0, 0);
+                        da = __builtin_amdgcn_mfma_f32_32x32x16_bf16(lds_b128(Vs, swz<D>(l32, 2 * kk + hl)), yop[kk], da, 0, 0, 0);
                     } else {
                         s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kop[kk], lds_b128(Ps, swz<D>(prow, 2 * kk + hl)), s, 0, 0, 0);
                         da = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vop[kk], lds_b128(Ys, swz<D>(prow, 2 * kk + hl)), da, 0, 0, 0);
@@ -486,6 +513,10 @@ __global__ __launch_bounds__(NW * 64, 1) void bwd_proto_kernel(ProtoArgs a) {
                     acc[mt][jt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(dso[mt][1], k1v, acc[mt][jt], 0, 0, 0);
                 }
             }
+            // the next tile goes to the other buffer, whose readers (the previous
+            // tile) passed the barrier at the end of the previous iteration
+            if (more) store(buf ^ 1);
+            __syncthreads();
         }
         // partial of this segment for this part's prototype rows
         float* out = a.partials + k * MD + (int64_t)part * C::MP * D;

@@ -157,7 +157,7 @@ __global__ __launch_bounds__(NW * 64, 1) void fwd_fused_kernel(FusedFwdArgs a) {
     const int l32 = lane & 31;
     const int hl = lane >> 5;  // half of the wave
 
-    const int64_t range = blockIdx.x;
+    const int64_t range = xcd_range(blockIdx.x, gridDim.x);
     const int64_t k0 = a.wg_start[range];
     const int64_t k1 = a.wg_start[range + 1];
     if (k0 < 0 || k1 < k0 || k1 > a.max_items) return;  // malformed offsets: nothing safe to do

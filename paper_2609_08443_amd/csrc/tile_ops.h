@@ -54,6 +54,17 @@ __device__ inline uint4 scale8(uint4 v, float f) {
     return r;
 }
 
+// Work-list range of workgroup b out of n.  The dispatcher deals workgroups to
+// the 8 XCDs round-robin (b % 8), each with its own L2; this gives the
+// workgroups of one XCD consecutive ranges (same head, mostly the same users), so
+// the prototype and dY blocks they stream are shared in that L2.  XCD x takes
+// ranges [x*q + min(x, n%8), ...) with q = n/8, one more when x < n%8: a
+// bijection of [0, n).
+__device__ inline int64_t xcd_range(int64_t b, int64_t n) {
+    const int64_t q = n / 8, rem = n % 8, x = b % 8, i = b / 8;
+    return x * q + (x < rem ? x : rem) + i;
+}
+
 __device__ inline int perm16(int t) { return (t & ~12) | ((t & 4) << 1) | ((t & 8) >> 1); }
 
 // row of a C tile held by register r of lane-half hl
@@ -65,16 +76,30 @@ __device__ inline int srow(int r, int hl) { return 8 * (r >> 2) + 4 * hl + (r & 
 // and the transposing 8-byte reads of lds_tr_tokens touch each bank once per 16
 // lanes; a plain row layout costs two passes per read.
 template <int COLS>
-__device__ inline int swz(int r, int c) {
+__device__ inline int swz_x(int r) {
     if constexpr (COLS == 32) {
-        return r * 32 + ((c ^ ((r >> 2) & 3)) << 3);
+        return (r >> 2) & 3;
     } else if constexpr (COLS == 64) {
-        return r * 64 + ((c ^ ((r & 6) | ((r >> 3) & 1))) << 3);
+        return (r & 6) | ((r >> 3) & 1);
     } else {
         static_assert(COLS == 128, "tile width");
-        return r * 128 + ((c ^ (((r & 3) << 1) | ((r & 4) << 1) | ((r >> 3) & 1))) << 3);
+        return ((r & 3) << 1) | ((r & 4) << 1) | ((r >> 3) & 1);
     }
 }
+template <int COLS>
+__device__ inline int swz(int r, int c) {
+    return r * COLS + ((c ^ swz_x<COLS>(r)) << 3);
+}
+
+// Direct global -> LDS copy of 16 bytes per lane (global_load_lds_dwordx4): lane l
+// of the wave writes LDS bytes [16 l, 16 l + 16) after `lds_base` (wave-uniform).
+// Completion is tracked by vmcnt; wait for it before the barrier that publishes
+// the data.
+__device__ inline void load_lds16(const void* src, void* lds_base) {
+    __builtin_amdgcn_global_load_lds((const void __attribute__((address_space(1)))*)(src),
+                                     (void __attribute__((address_space(3)))*)(lds_base), 16, 0, 0);
+}
+__device__ inline void wait_vmem() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
 
 __device__ inline bf16x8 lds_b128(const uint16_t* base, int off) {
     return __builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4*>(base + off));
