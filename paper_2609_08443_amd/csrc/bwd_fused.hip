@@ -52,29 +52,61 @@ __device__ inline float xhalf_sum(float v) {
 // ------------------------------------------------------------------ prep
 // dY[b,h] = sum_r dsketch[b,r,h] (fp32) written as bf16 row-major Ymj[b,h,m,j]
 // and transposed Yjm[b,h,j,p] with p = perm16(m); P -> Pjm[h,j,p] likewise.
-__global__ __launch_bounds__(256) void prep_kernel(const float* __restrict__ ds, int64_t B,
-                                                   int32_t R, int32_t H, int32_t M, int32_t D,
+// One workgroup per 32-prototype block: the rows are summed and converted with
+// 16-byte accesses, staged in LDS, and the transposed block is written as 64-byte
+// rows.  Workgroups [0, B*H*M/32) take dY blocks, the next H*M/32 take P blocks.
+template <int D>
+__global__ __launch_bounds__(256) void prep_kernel(const float* __restrict__ ds, int64_t B, int32_t R,
+                                                   int32_t H, int32_t M,
                                                    const uint16_t* __restrict__ P,
                                                    uint16_t* __restrict__ Ymj,
                                                    uint16_t* __restrict__ Yjm,
                                                    uint16_t* __restrict__ Pjm) {
+    constexpr int KCH = D / 8;                       // 16-byte bf16 chunks per row
+    constexpr int NCH = 32 * KCH;                    // chunks per block
+    __shared__ __attribute__((aligned(16))) uint16_t tile[32 * D];
+    const int tid = threadIdx.x;
     const int64_t MD = (int64_t)M * D;
-    const int64_t nY = B * H * MD;
-    const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
-    if (i < nY) {
-        const int64_t bh = i / MD, rest = i % MD;
-        const int64_t b = bh / H, h = bh % H;
-        const int m = (int)(rest / D), j = (int)(rest % D);
-        float s = 0.f;
-        for (int r = 0; r < R; ++r) s += ds[((b * R + r) * H + h) * MD + rest];
-        const uint16_t v = to_bf16(s);
-        Ymj[i] = v;
-        Yjm[bh * MD + (int64_t)j * M + perm16(m)] = v;
-    } else if (i < nY + (int64_t)H * MD) {
-        const int64_t k = i - nY;
-        const int64_t h = k / MD, rest = k % MD;
-        const int m = (int)(rest / D), j = (int)(rest % D);
-        Pjm[h * MD + (int64_t)j * M + perm16(m)] = P[k];
+    const int64_t nb = M / 32;
+    const int64_t blk = blockIdx.x;
+    const bool is_y = blk < B * H * nb;
+    const int64_t pair = is_y ? blk / nb : (blk - B * H * nb) / nb;   // b*H + h, or h
+    const int mb = (int)((is_y ? blk : blk - B * H * nb) % nb);
+    if (!is_y && pair >= H) return;
+    uint16_t* rowdst = is_y ? Ymj + pair * MD : nullptr;
+    uint16_t* trdst = (is_y ? Yjm : Pjm) + pair * MD;
+    for (int i = tid; i < NCH; i += 256) {
+        const int r = i / KCH, c = i % KCH;
+        const int64_t off = (int64_t)(mb * 32 + r) * D + c * 8;
+        u32x4 v;
+        if (is_y) {
+            const int64_t b = pair / H, h = pair % H;
+            float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+            for (int rr = 0; rr < R; ++rr) {
+                const float4* src = reinterpret_cast<const float4*>(ds + ((b * R + rr) * H + h) * MD + off);
+                const float4 x0 = src[0], x1 = src[1];
+                acc[0] += x0.x; acc[1] += x0.y; acc[2] += x0.z; acc[3] += x0.w;
+                acc[4] += x1.x; acc[5] += x1.y; acc[6] += x1.z; acc[7] += x1.w;
+            }
+            v = (u32x4){pack_bf16x2(acc[0], acc[1]), pack_bf16x2(acc[2], acc[3]),
+                        pack_bf16x2(acc[4], acc[5]), pack_bf16x2(acc[6], acc[7])};
+            *reinterpret_cast<u32x4*>(rowdst + off) = v;
+        } else {
+            v = *reinterpret_cast<const u32x4*>(P + pair * MD + off);
+        }
+        *reinterpret_cast<u32x4*>(tile + r * D + c * 8) = v;
+    }
+    __syncthreads();
+    // transposed: row j, columns p = 0..31 of this block, p = perm16(m)
+    for (int i = tid; i < NCH; i += 256) {
+        const int j = i / 4, c = i % 4;
+        uint32_t w[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            const int m0 = perm16(8 * c + 2 * e), m1 = perm16(8 * c + 2 * e + 1);
+            w[e] = (uint32_t)tile[m0 * D + j] | ((uint32_t)tile[m1 * D + j] << 16);
+        }
+        *reinterpret_cast<u32x4*>(trdst + (int64_t)j * M + mb * 32 + c * 8) = (u32x4){w[0], w[1], w[2], w[3]};
     }
 }
 
@@ -349,7 +381,9 @@ struct ProtoArgs {
     const int32_t* wg_start;
     int64_t max_items;
     int64_t T;
+    int64_t n_ranges;
     int32_t B, H, M;
+    int32_t parts;    // M / MP
     float scale;
     float* partials;  // [max_items][M][D]
 };
@@ -364,8 +398,15 @@ __global__ __launch_bounds__(NW * 64, 1) void bwd_proto_kernel(ProtoArgs a) {
     const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
     const int l32 = lane & 31, hl = lane >> 5;
 
-    const int64_t range = xcd_range(blockIdx.x, gridDim.x);
-    const int part = blockIdx.y;          // prototypes [part*MP, (part+1)*MP)
+    // Workgroup -> (range, part): the XCD of workgroup L is L % 8; on each XCD the
+    // parts of one range are dispatched back to back (their K and V reads share
+    // that XCD's L2) and the ranges are consecutive (see xcd_range).
+    const int64_t xcd = blockIdx.x % 8, jx = blockIdx.x / 8;
+    const int part = (int)(jx % a.parts);          // prototypes [part*MP, (part+1)*MP)
+    const int64_t ix = jx / a.parts;
+    const int64_t q8 = a.n_ranges / 8, r8 = a.n_ranges % 8;
+    if (ix >= q8 + (xcd < r8 ? 1 : 0)) return;     // this XCD has fewer ranges
+    const int64_t range = xcd * q8 + (xcd < r8 ? xcd : r8) + ix;
     const int64_t k0 = a.wg_start[range], k1 = a.wg_start[range + 1];
     if (k0 < 0 || k1 < k0 || k1 > a.max_items) return;
     const float ks2 = a.scale * kLog2e;
@@ -574,8 +615,11 @@ hipError_t launch_proto(const ProtoArgs& a, int64_t n_ranges, hipStream_t stream
     hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
                                        hipFuncAttributeMaxDynamicSharedMemorySize, C::LDS);
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(kern, dim3((unsigned)n_ranges, (unsigned)(a.M / C::MP)), dim3(C::THREADS),
-                       C::LDS, stream, a);
+    ProtoArgs b = a;
+    b.n_ranges = n_ranges;
+    b.parts = a.M / C::MP;
+    const int64_t per_xcd = (n_ranges + 7) / 8;
+    hipLaunchKernelGGL(kern, dim3((unsigned)(8 * per_xcd * b.parts)), dim3(C::THREADS), C::LDS, stream, b);
     return hipGetLastError();
 }
 
@@ -603,9 +647,13 @@ hipError_t launch_fused_bwd(const FusedBwdArgs& f, hipStream_t stream) {
     // dY (R summed) and P in the layouts the contractions read
     {
         ProfScope ps("bwd_prep", stream);
-        const int64_t n = f.B * f.H * MD + (int64_t)f.H * MD;
-        hipLaunchKernelGGL(prep_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, stream,
-                           f.dsketch, f.B, f.R, f.H, f.M, f.d, f.P, f.Ymj, f.Yjm, f.Pjm);
+        const int64_t nblocks = (f.B * f.H + f.H) * (f.M / 32);
+        if (f.d == 64)
+            hipLaunchKernelGGL(prep_kernel<64>, dim3((unsigned)nblocks), dim3(256), 0, stream,
+                               f.dsketch, f.B, f.R, f.H, f.M, f.P, f.Ymj, f.Yjm, f.Pjm);
+        else
+            hipLaunchKernelGGL(prep_kernel<128>, dim3((unsigned)nblocks), dim3(256), 0, stream,
+                               f.dsketch, f.B, f.R, f.H, f.M, f.P, f.Ymj, f.Yjm, f.Pjm);
         hipError_t e = hipGetLastError();
         if (e != hipSuccess) return e;
     }
