@@ -7,7 +7,8 @@ only marshals numpy arrays.
 
 Functions follow SequenceO1 section 3.1 (affinities S, prototype-wise softmax
 A, sketch A X), Appendix B steps 1-3, and the chain-rule backward stated in the
-header of ``sa_oracle.c``.
+header of ``sa_oracle.c``; ``fwd_tokenwise`` is the token-wise normalised
+alternative of the appendix on prototype-wise normalisation.
 """
 from __future__ import annotations
 
@@ -46,6 +47,10 @@ def _load():
     lib.sa_oracle_weights.argtypes = [_f32p, _f32p, c.c_int64, c.c_int32, c.c_int32,
                                       c.c_int32, c.c_double, _f64p, c.c_void_p]
     lib.sa_oracle_weights.restype = c.c_int
+    lib.sa_oracle_fwd_tokenwise.argtypes = [_f32p, _f32p, _f32p, _i64p, c.c_int64, c.c_int32,
+                                            c.c_int32, c.c_int32, c.c_double, _f64p,
+                                            c.c_void_p, c.c_int32]
+    lib.sa_oracle_fwd_tokenwise.restype = c.c_int
     lib.sa_oracle_max_threads.argtypes = []
     lib.sa_oracle_max_threads.restype = c.c_int
     _lib = lib
@@ -123,3 +128,23 @@ def weights(K, P, scale=None):
     if rc != 0:
         raise ValueError(f"sa_oracle_weights failed ({rc})")
     return A, lse
+
+
+def fwd_tokenwise(K, V, P, offsets, scale=None, nthreads: int = 0, want_lse: bool = True):
+    """Token-wise normalised forward (softmax over each user's tokens per prototype).
+
+    Returns (sketch [B,H,M,d] fp64, lse_m [B,H,M] fp64 or None; -inf for empty users).
+    """
+    lib = _load()
+    T, H, M, d = _dims(K, P)
+    offsets = np.ascontiguousarray(offsets, dtype=np.int64)
+    B = offsets.shape[0] - 1
+    if scale is None:
+        scale = 1.0 / np.sqrt(d)
+    sketch = np.empty((B, H, M, d), np.float64)
+    lse = np.full((B, H, M), np.nan, np.float64) if want_lse else None
+    rc = lib.sa_oracle_fwd_tokenwise(_f32(K), _f32(V), _f32(P), offsets, B, H, M, d, float(scale),
+                                     sketch, lse.ctypes.data if want_lse else None, int(nthreads))
+    if rc != 0:
+        raise ValueError(f"sa_oracle_fwd_tokenwise failed ({rc})")
+    return sketch, lse

@@ -34,6 +34,17 @@
  * Heads are independent SA instances, each with its own P[h] (the paper's SA is
  * single-head; H = 1 is exactly the paper).  An empty user (L_b = 0) has a zero
  * sketch.
+ *
+ * Token-wise ("vanilla") normalisation, the alternative the paper compares SA
+ * against (Appendix "Why prototype-wise normalization"; Table 1 baseline):
+ * the weights are normalised over the tokens of a user for each prototype,
+ * p(i | j) instead of p(j | i):
+ *   for every user b, head h, prototype m:
+ *     s_t        = scale * K[t,h] . P[h,m]            (t over the user's tokens)
+ *     w_t        = exp(s_t) / sum_t' exp(s_t')
+ *     sketch[b,h,m,:] = sum_t w_t V[t,h,:]
+ *     lse_m[b,h,m]    = log sum_t exp(s_t)              (-inf for an empty user)
+ * evaluated in two passes: the maximum over tokens, then the shifted sums.
  */
 #include <math.h>
 #include <stdint.h>
@@ -158,6 +169,74 @@ int sa_oracle_fwd(const float* K, const float* V, const float* P,
         }
         free(s);
         free(a);
+    }
+    return err;
+}
+
+/*
+ * Token-wise normalised forward.  sketch: [B,H,M,d] (overwritten); lse_m:
+ * [B,H,M] or NULL.  Two passes over the user's tokens per (user, head): the
+ * per-prototype maximum of the logits, then exp(s - max) summed into the
+ * normaliser and, weighted, into the sketch rows.
+ */
+int sa_oracle_fwd_tokenwise(const float* K, const float* V, const float* P,
+                            const int64_t* offsets, int64_t B, int32_t H, int32_t M,
+                            int32_t d, double scale, double* sketch, double* lse_m,
+                            int32_t nthreads) {
+    if (B < 0 || H < 1 || M < 1 || d < 1) return ORACLE_EINVAL;
+    if (check_offsets(offsets, B)) return ORACLE_EINVAL;
+    set_threads(nthreads);
+    const int64_t npairs = B * (int64_t)H;
+    int err = ORACLE_OK;
+#pragma omp parallel
+    {
+        double* s = (double*)malloc(sizeof(double) * (size_t)M);
+        double* mu = (double*)malloc(sizeof(double) * (size_t)M);
+        double* z = (double*)malloc(sizeof(double) * (size_t)M);
+        if (!s || !mu || !z) {
+#pragma omp atomic write
+            err = ORACLE_ENOMEM;
+        }
+#pragma omp for schedule(dynamic, 1)
+        for (int64_t p = 0; p < npairs; ++p) {
+            if (!s || !mu || !z) continue;
+            const int64_t b = p / H;
+            const int32_t h = (int32_t)(p % H);
+            const float* Ph = P + (int64_t)h * M * d;
+            double* out = sketch + p * (int64_t)M * d;
+            memset(out, 0, sizeof(double) * (size_t)M * (size_t)d);
+            for (int32_t m = 0; m < M; ++m) {
+                mu[m] = -INFINITY;
+                z[m] = 0.0;
+            }
+            /* pass 1: max over the user's tokens, per prototype */
+            for (int64_t t = offsets[b]; t < offsets[b + 1]; ++t) {
+                logits(K + (t * H + h) * (int64_t)d, Ph, M, d, scale, s);
+                for (int32_t m = 0; m < M; ++m)
+                    if (s[m] > mu[m]) mu[m] = s[m];
+            }
+            /* pass 2: shifted exponentials into the normaliser and the sketch */
+            for (int64_t t = offsets[b]; t < offsets[b + 1]; ++t) {
+                const float* Vt = V + (t * H + h) * (int64_t)d;
+                logits(K + (t * H + h) * (int64_t)d, Ph, M, d, scale, s);
+                for (int32_t m = 0; m < M; ++m) {
+                    const double e = exp(s[m] - mu[m]);
+                    z[m] += e;
+                    double* row = out + (int64_t)m * d;
+                    for (int32_t j = 0; j < d; ++j) row[j] += e * (double)Vt[j];
+                }
+            }
+            for (int32_t m = 0; m < M; ++m) {
+                if (z[m] > 0.0) {
+                    double* row = out + (int64_t)m * d;
+                    for (int32_t j = 0; j < d; ++j) row[j] /= z[m];
+                }
+                if (lse_m) lse_m[p * M + m] = z[m] > 0.0 ? mu[m] + log(z[m]) : -INFINITY;
+            }
+        }
+        free(s);
+        free(mu);
+        free(z);
     }
     return err;
 }
