@@ -161,6 +161,8 @@ def main(argv=None) -> int:
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="c5", choices=sorted(WORKLOADS))
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-tokenwise", action="store_true",
+                    help="skip the timing of the token-wise normalised variant")
     ap.add_argument("--cpu-tokens", type=int, default=300000,
                     help="tokens of the CPU-baseline sample (shortest users first)")
     ap.add_argument("--copy-calibration", action="store_true",
@@ -254,6 +256,40 @@ def main(argv=None) -> int:
                 "algorithmic_flops_per_launch": fl, "algorithmic_bytes_per_launch": by,
                 "executed_mfma_tflops": fl_exec / (avg_ms * 1e-3) / 1e12 if fl_exec else None}
 
+    # token-wise normalised variant (the paper's comparison normalisation), timed on
+    # the same batch after the step; not part of the step
+    tokenwise = None
+    if w.dtype == "bf16" and not args.no_tokenwise:
+        sk_tw = torch.empty((B, H, M, d), dtype=torch.float32, device="cuda")
+        lse_tw = torch.empty((B, H, M), dtype=torch.float32, device="cuda")
+        ws_tw = torch.empty(max(sa.tokenwise_workspace_size(B, T, H, M, d, code), 1), dtype=torch.uint8,
+                            device="cuda")
+
+        def tw():
+            sa.sketch_fwd_tokenwise(dev["K"], dev["V"], dev["P"], dev["offsets"], w.scale, sketch=sk_tw,
+                                    lse_m=lse_tw, workspace=ws_tw)
+        for _ in range(args.warmup):
+            tw()
+        torch.cuda.synchronize()
+        sa.kernel_times()
+        sa.profile_enable(True)
+        t0 = torch.cuda.Event(enable_timing=True)
+        t1 = torch.cuda.Event(enable_timing=True)
+        t0.record(stream)
+        for _ in range(args.steps):
+            tw()
+        t1.record(stream)
+        torch.cuda.synchronize()
+        sa.profile_enable(False)
+        ktw = sa.kernel_times()
+        tw_ms = t0.elapsed_time(t1) / args.steps
+        main_ms = ktw["tokenwise_fwd"][1] / ktw["tokenwise_fwd"][0] if "tokenwise_fwd" in ktw else None
+        tokenwise = {"tokens_per_s": T / (tw_ms * 1e-3), "ms": tw_ms,
+                     "kernels": {n: {"launches": c, "avg_ms": tot / c} for n, (c, tot) in ktw.items()},
+                     "mfma_util": fwd_algorithmic_flops(w) / (tw_ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS,
+                     "kernel_mfma_frac": (fwd_algorithmic_flops(w) / (main_ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS
+                                          if main_ms else None)}
+
     out = {
         "metric": METRIC,
         "value": T / (ms_step * 1e-3),
@@ -277,6 +313,7 @@ def main(argv=None) -> int:
         "wall_s_timed": wall,
         "kernels": kernels,
         "roofline": roof,
+        "tokenwise_fwd": tokenwise,
         "cpu_baseline": None,
     }
     if not args.no_cpu_baseline:

@@ -113,6 +113,36 @@ sa_status sa_sketch_fwd(const void* K, const void* V, const void* P,
                         float* sketch, float* lse, void* workspace,
                         size_t workspace_bytes, void* stream);
 
+/* Bytes of workspace that sa_sketch_fwd_tokenwise needs for this shape. */
+size_t sa_sketch_fwd_tokenwise_workspace_size(int64_t B, int64_t T, int32_t H,
+                                              int32_t M, int32_t d, sa_dtype dtype);
+
+/*
+ * Forward of the token-wise normalised variant: the normalisation the paper
+ * compares SA's prototype-wise one with (appendix on prototype-wise
+ * normalisation; Table 1 baseline).  For each user b, head h and prototype m
+ * the weights are normalised over the user's tokens:
+ *
+ *   s_t            = scale * K[t,h] . P[h,m]           t over the user's tokens
+ *   sketch[b,h,m]  = sum_t exp(s_t) V[t,h] / sum_t exp(s_t)
+ *   lse_m[b,h,m]   = log sum_t exp(s_t)                  (-inf for an empty user)
+ *
+ * i.e. attention with the prototypes as queries over each user's tokens.
+ * Arguments, layouts, supported shapes and error behaviour are those of
+ * sa_sketch_fwd except:
+ *   lse_m     output [B,H,M] fp32 per-prototype log-sum-exp, or NULL
+ * An empty user gets a zero sketch (and lse_m = -inf).  bf16 with d in {64,128}
+ * and M a multiple of 128 runs the matrix-core kernel (online softmax over token
+ * tiles, users cut across ranges merged by log-sum-exp); other shapes and
+ * SA_FP32 run a plain fp32 path.
+ */
+sa_status sa_sketch_fwd_tokenwise(const void* K, const void* V, const void* P,
+                                  const int64_t* offsets, int64_t B, int64_t T,
+                                  int32_t H, int32_t M, int32_t d, float scale,
+                                  sa_dtype dtype, float* sketch, float* lse_m,
+                                  void* workspace, size_t workspace_bytes,
+                                  void* stream);
+
 /* Bytes of workspace that sa_sketch_bwd needs for this shape. */
 size_t sa_sketch_bwd_workspace_size(int64_t B, int64_t T, int32_t H, int32_t M,
                                     int32_t d, sa_dtype dtype, int32_t R);

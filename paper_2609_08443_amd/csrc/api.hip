@@ -157,6 +157,44 @@ FwdPlan plan_fwd(int64_t B, int64_t T, int32_t H, int32_t M, int32_t d, sa_dtype
     return p;
 }
 
+// ---------------------------------------------------------------- token-wise plan
+struct TwPlan {
+    bool fused = false;
+    int64_t C = 0, n_ranges = 0, max_items = 0;
+    size_t off_nitems = 0, off_wgstart = 0, off_pairstart = 0, off_items = 0, off_partials = 0,
+           off_stats = 0, total = 0;
+};
+
+TwPlan plan_tokenwise(int64_t B, int64_t T, int32_t H, int32_t M, int32_t d, sa_dtype dtype) {
+    TwPlan p;
+    p.fused = dtype == SA_BF16 && sa::tokenwise_fused_supported(M, d);
+    size_t off = 0;
+    auto carve = [&](size_t bytes) {
+        const size_t o = off;
+        off = align_up(off + bytes, 256);
+        return o;
+    };
+    if (p.fused) {
+        // one range per CU; each range runs M / (prototypes per workgroup) workgroups
+        const int64_t HT = (int64_t)H * T;
+        const int64_t target = device_cus();
+        int64_t C = (HT + target - 1) / target;
+        C = (C + sa::kTileTokens - 1) / sa::kTileTokens * sa::kTileTokens;
+        if (C < sa::kTileTokens) C = sa::kTileTokens;
+        p.C = C;
+        p.n_ranges = (HT + C - 1) / C;
+        p.max_items = p.n_ranges + (int64_t)H * B;
+        p.off_nitems = carve(sizeof(int64_t));
+        p.off_wgstart = carve(sizeof(int32_t) * (p.n_ranges + 1));
+        p.off_pairstart = carve(sizeof(int32_t) * ((int64_t)H * B + 1));
+        p.off_items = carve(sizeof(int32_t) * sa::IT_WORDS * p.max_items);
+        p.off_partials = carve(sizeof(float) * (size_t)p.max_items * M * d);
+        p.off_stats = carve(sizeof(float) * (size_t)p.max_items * M * 2);
+    }
+    p.total = off;
+    return p;
+}
+
 // ---------------------------------------------------------------- backward plan
 struct BwdPlan {
     bool fused = false;
@@ -328,6 +366,74 @@ sa_status sa_sketch_fwd(const void* K, const void* V, const void* P, const int64
                                    sketch, lse_out, stream);
     }
     if (e != hipSuccess) return hip_fail(e, "fp32 forward launch");
+    return SA_OK;
+}
+
+size_t sa_sketch_fwd_tokenwise_workspace_size(int64_t B, int64_t T, int32_t H, int32_t M,
+                                              int32_t d, sa_dtype dtype) {
+    if (check_common(B, T, H, M, d, 1.0f, dtype) != SA_OK) return 0;
+    return plan_tokenwise(B, T, H, M, d, dtype).total;
+}
+
+sa_status sa_sketch_fwd_tokenwise(const void* K, const void* V, const void* P,
+                                  const int64_t* offsets, int64_t B, int64_t T, int32_t H,
+                                  int32_t M, int32_t d, float scale, sa_dtype dtype, float* sketch,
+                                  float* lse_m, void* workspace, size_t workspace_bytes,
+                                  void* stream_) {
+    g_last_error[0] = 0;
+    sa_status st = check_common(B, T, H, M, d, scale, dtype);
+    if (st != SA_OK) return st;
+    if (B == 0) return SA_OK;
+    if (!offsets || !sketch || !P || (T > 0 && (!K || !V)))
+        return fail(SA_ERR_INVALID_ARG, "null pointer argument");
+    if (!aligned16(K) || !aligned16(V) || !aligned16(P) || !aligned16(sketch) ||
+        !aligned16(lse_m))
+        return fail(SA_ERR_INVALID_ARG, "K, V, P, sketch and lse_m must be 16-byte aligned");
+    hipStream_t stream = reinterpret_cast<hipStream_t>(stream_);
+    const TwPlan plan = plan_tokenwise(B, T, H, M, d, dtype);
+    if (plan.total > 0 && (!workspace || workspace_bytes < plan.total))
+        return fail(SA_ERR_WORKSPACE, "workspace of %zu bytes needed, %zu given", plan.total,
+                    workspace ? workspace_bytes : (size_t)0);
+    if (debug_validate()) {
+        st = validate_offsets(offsets, B, T, stream);
+        if (st != SA_OK) return st;
+    }
+    hipError_t e;
+    if (plan.fused) {
+        uint8_t* ws = reinterpret_cast<uint8_t*>(workspace);
+        int32_t* items = reinterpret_cast<int32_t*>(ws + plan.off_items);
+        int32_t* wg_start = reinterpret_cast<int32_t*>(ws + plan.off_wgstart);
+        int32_t* pair_start = reinterpret_cast<int32_t*>(ws + plan.off_pairstart);
+        int64_t* n_items = reinterpret_cast<int64_t*>(ws + plan.off_nitems);
+        float* partials = reinterpret_cast<float*>(ws + plan.off_partials);
+        float* stats = reinterpret_cast<float*>(ws + plan.off_stats);
+        {
+            sa::ProfScope ps("worklist", stream);
+            e = sa::launch_worklist(offsets, B, T, H, plan.C, plan.n_ranges, items,
+                                    plan.max_items, wg_start, pair_start, n_items, stream);
+        }
+        if (e != hipSuccess) return hip_fail(e, "work list launch");
+        {
+            sa::ProfScope ps("tokenwise_fwd", stream);
+            e = sa::launch_tokenwise_fused(items, wg_start, plan.n_ranges, plan.max_items, K, V, P,
+                                           B, T, H, M, d, scale, sketch, lse_m, partials, stats,
+                                           stream);
+        }
+        if (e != hipSuccess) return hip_fail(e, "token-wise forward launch");
+        {
+            sa::ProfScope ps("tokenwise_merge", stream);
+            e = sa::launch_tokenwise_merge(pair_start, B, H, M, d, plan.max_items, partials, stats,
+                                           sketch, lse_m, stream);
+        }
+        if (e != hipSuccess) return hip_fail(e, "token-wise merge launch");
+        return SA_OK;
+    }
+    {
+        sa::ProfScope ps("tokenwise_plain", stream);
+        e = sa::launch_tokenwise_generic(K, V, P, offsets, B, H, M, d, scale, dtype == SA_BF16,
+                                         sketch, lse_m, stream);
+    }
+    if (e != hipSuccess) return hip_fail(e, "token-wise plain launch");
     return SA_OK;
 }
 

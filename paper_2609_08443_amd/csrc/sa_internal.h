@@ -104,6 +104,20 @@ int32_t fused_bwd_part(int32_t M, int32_t d);
 int32_t fused_bwd_ranges_per_cu();
 hipError_t launch_fused_bwd(const FusedBwdArgs& a, hipStream_t stream);
 
+// Token-wise normalised forward (sa_sketch_fwd_tokenwise).
+bool tokenwise_fused_supported(int32_t M, int32_t d);
+hipError_t launch_tokenwise_fused(const int32_t* items, const int32_t* wg_start, int64_t n_ranges,
+                                  int64_t max_items, const void* K, const void* V, const void* P,
+                                  int64_t B, int64_t T, int32_t H, int32_t M, int32_t d, float scale,
+                                  float* sketch, float* lse_m, float* partials, float* stats,
+                                  hipStream_t stream);
+hipError_t launch_tokenwise_merge(const int32_t* pair_start, int64_t B, int32_t H, int32_t M, int32_t d,
+                                  int64_t max_items, const float* partials, const float* stats,
+                                  float* sketch, float* lse_m, hipStream_t stream);
+hipError_t launch_tokenwise_generic(const void* K, const void* V, const void* P, const int64_t* offsets,
+                                    int64_t B, int32_t H, int32_t M, int32_t d, float scale, bool bf16,
+                                    float* sketch, float* lse_m, hipStream_t stream);
+
 // Plain fp32-arithmetic path (fp32 or bf16 inputs).
 hipError_t launch_generic_fwd(const void* K, const void* V, const void* P,
                               const int64_t* offsets, int64_t B, int64_t T, int32_t H,

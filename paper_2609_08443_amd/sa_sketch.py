@@ -22,6 +22,7 @@ ITEM_WORDS = 8
 
 EXPORTS = ("sa_sketch_fwd_workspace_size", "sa_sketch_fwd", "sa_sketch_bwd_workspace_size",
            "sa_sketch_bwd", "sa_build_worklist", "sa_sketch_fwd_chunk_tokens",
+           "sa_sketch_fwd_tokenwise_workspace_size", "sa_sketch_fwd_tokenwise",
            "sa_profile_enable", "sa_kernel_times", "sa_status_string", "sa_last_error")
 
 
@@ -57,6 +58,11 @@ def lib() -> ctypes.CDLL:
     L.sa_sketch_bwd.argtypes = [vp, vp, vp, vp, i64, i64, i32, i32, i32, f32, c.c_int, vp, i32,
                                 vp, vp, vp, vp, vp, sz, vp]
     L.sa_sketch_bwd.restype = c.c_int
+    L.sa_sketch_fwd_tokenwise_workspace_size.argtypes = [i64, i64, i32, i32, i32, c.c_int]
+    L.sa_sketch_fwd_tokenwise_workspace_size.restype = sz
+    L.sa_sketch_fwd_tokenwise.argtypes = [vp, vp, vp, vp, i64, i64, i32, i32, i32, f32, c.c_int,
+                                          vp, vp, vp, sz, vp]
+    L.sa_sketch_fwd_tokenwise.restype = c.c_int
     L.sa_build_worklist.argtypes = [vp, i64, i64, i32, i64, vp, i64, vp, vp]
     L.sa_build_worklist.restype = c.c_int
     L.sa_status_string.argtypes = [c.c_int]
@@ -158,6 +164,41 @@ def sketch_fwd(K, V, P, offsets, scale: Optional[float] = None, sketch=None, lse
                              _stream_handle(stream))
     _check(rc)
     return sketch, lse
+
+
+def tokenwise_workspace_size(B, T, H, M, d, dtype_code) -> int:
+    return int(lib().sa_sketch_fwd_tokenwise_workspace_size(B, T, H, M, d, dtype_code))
+
+
+def sketch_fwd_tokenwise(K, V, P, offsets, scale: Optional[float] = None, sketch=None, lse_m=None,
+                         want_lse: bool = True, workspace=None, stream=None):
+    """sa_sketch_fwd_tokenwise on torch tensors (weights normalised over each user's
+    tokens per prototype).  Returns (sketch [B,H,M,d] fp32, lse_m [B,H,M] or None)."""
+    import torch
+    T, H, d = K.shape
+    M = P.shape[1]
+    B = offsets.shape[0] - 1
+    dev = K.device
+    code = _dtype_code(K)
+    _require(K, "K", (T, H, d), K.dtype, dev)
+    _require(V, "V", (T, H, d), K.dtype, dev)
+    _require(P, "P", (H, M, d), K.dtype, dev)
+    _require(offsets, "offsets", (B + 1,), torch.int64, dev)
+    if scale is None:
+        scale = 1.0 / math.sqrt(d)
+    if sketch is None:
+        sketch = torch.empty((B, H, M, d), dtype=torch.float32, device=dev)
+    _require(sketch, "sketch", (B, H, M, d), torch.float32, dev)
+    if lse_m is None and want_lse:
+        lse_m = torch.empty((B, H, M), dtype=torch.float32, device=dev)
+    if lse_m is not None:
+        _require(lse_m, "lse_m", (B, H, M), torch.float32, dev)
+    ws, nbytes = _workspace(tokenwise_workspace_size(B, T, H, M, d, code), dev, workspace)
+    rc = lib().sa_sketch_fwd_tokenwise(_ptr(K), _ptr(V), _ptr(P), _ptr(offsets), B, T, H, M, d,
+                                       float(scale), code, _ptr(sketch), _ptr(lse_m), _ptr(ws),
+                                       nbytes, _stream_handle(stream))
+    _check(rc)
+    return sketch, lse_m
 
 
 def sketch_bwd(K, V, P, offsets, dsketch, lse, scale: Optional[float] = None, dK=None,
