@@ -8,7 +8,9 @@ only marshals numpy arrays.
 Functions follow SequenceO1 section 3.1 (affinities S, prototype-wise softmax
 A, sketch A X), Appendix B steps 1-3, and the chain-rule backward stated in the
 header of ``sa_oracle.c``; ``fwd_tokenwise`` is the token-wise normalised
-alternative of the appendix on prototype-wise normalisation.
+alternative of the appendix on prototype-wise normalisation.  ``oracle.layer``
+holds the SA layer with its projections (Appendix G.3: Q = P W_Q, K = X W_K,
+V = X) in fp64 numpy.
 """
 from __future__ import annotations
 
