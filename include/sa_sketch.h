@@ -171,6 +171,64 @@ sa_status sa_sketch_bwd(const void* K, const void* V, const void* P,
                         float* dK, float* dV, float* dP, void* workspace,
                         size_t workspace_bytes, void* stream);
 
+/* Bytes of workspace that sa_layer_fwd needs for this shape. */
+size_t sa_layer_fwd_workspace_size(int64_t B, int64_t T, int32_t H, int32_t M,
+                                   int32_t d, sa_dtype dtype);
+
+/*
+ * Forward of one SA layer with its projections (Appendix G.3; section 3.1):
+ *
+ *   Q = P W_Q,  K = X W_K,  S = scale Q K^T,  A = softmax over prototypes,
+ *   sketch = A X      (the history X itself is aggregated, as in section 3.1)
+ *
+ * per user and per head (heads are independent SA instances with their own
+ * P[h], W_Q[h], W_K[h]; H = 1 is the paper's single-head SA).  The key
+ * projection is folded into the prototypes, S = scale (P W_Q W_K^T) X^T (the
+ * reordering the paper uses for single-query STCA, Appendix G.2): no key tensor
+ * is formed and X is read once.  In bf16 mode P' = P W_Q W_K^T is computed with
+ * fp32 accumulation and rounded once to bf16.
+ *
+ *   X         [T,H,d] history, dtype
+ *   P         [H,M,d] prototypes P^(0), dtype
+ *   Wq, Wk    [H,d,d] row-major, K[t,h,j] = sum_i X[t,h,i] Wk[h,i,j]; dtype
+ *   sketch    output [B,H,M,d] fp32; lse output [T,H] fp32 or NULL (as sa_sketch_fwd)
+ *
+ * Offsets, sizes, supported shapes, errors, ownership and streams are those of
+ * sa_sketch_fwd; the workspace is required (at least the per-head products).
+ */
+sa_status sa_layer_fwd(const void* X, const void* P, const void* Wq, const void* Wk,
+                       const int64_t* offsets, int64_t B, int64_t T, int32_t H, int32_t M,
+                       int32_t d, float scale, sa_dtype dtype, float* sketch, float* lse,
+                       void* workspace, size_t workspace_bytes, void* stream);
+
+/* Bytes of workspace that sa_layer_bwd needs for this shape. */
+size_t sa_layer_bwd_workspace_size(int64_t B, int64_t T, int32_t H, int32_t M,
+                                   int32_t d, sa_dtype dtype, int32_t R);
+
+/*
+ * Backward of sa_layer_fwd, by the chain rule (dY = sum over the R target
+ * instances, section 4.2):
+ *
+ *   dX  = A^T dY + dK W_K^T         (X is both the value and the key input)
+ *   dW_K = sum over users of X^T dK,  dK = scale dS^T Q
+ *   dQ  = scale sum over users of dS K,  dW_Q = P^T dQ,  dP = dQ W_Q^T
+ *
+ * with dS the prototype-softmax gradient of sa_sketch_bwd.  Computed as the
+ * sketching backward with K = V = X and prototypes P' = Q W_K^T, which yields
+ * dX = dV + scale dS P' per token and dP', followed by dW_K = dP'^T Q,
+ * dQ = dP' W_K, dW_Q = P^T dQ and dP = dQ W_Q^T per head.
+ *
+ *   lse             the lse written by sa_layer_fwd for the same inputs (required)
+ *   dsketch         [B,R,H,M,d] fp32
+ *   dX              output [T,H,d] fp32, overwritten
+ *   dP              output [H,M,d] fp32; dWq, dWk outputs [H,d,d] fp32; overwritten
+ */
+sa_status sa_layer_bwd(const void* X, const void* P, const void* Wq, const void* Wk,
+                       const int64_t* offsets, int64_t B, int64_t T, int32_t H, int32_t M,
+                       int32_t d, float scale, sa_dtype dtype, const float* dsketch, int32_t R,
+                       const float* lse, float* dX, float* dP, float* dWq, float* dWk,
+                       void* workspace, size_t workspace_bytes, void* stream);
+
 /*
  * Work list used by the fused forward, exposed for exact testing.
  *

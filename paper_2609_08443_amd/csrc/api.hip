@@ -244,6 +244,183 @@ BwdPlan plan_bwd(int64_t B, int64_t T, int32_t H, int32_t M, int32_t d, sa_dtype
     return p;
 }
 
+// ---------------------------------------------------------------- SA layer plan
+// [Q fp32 | P' = Q W_K^T in the input dtype | (bwd) dP' fp32 | dQ fp32 |
+//  (bwd, plain path) dK, dV fp32 | workspace of the sketching call]
+struct LayerPlan {
+    size_t off_q = 0, off_pp = 0, off_dpp = 0, off_dq = 0, off_dk = 0, off_dv = 0, off_base = 0;
+    size_t total = 0;
+};
+
+LayerPlan plan_layer(int64_t T, int32_t H, int32_t M, int32_t d, sa_dtype dtype, bool bwd,
+                     bool plain_bwd, size_t base_bytes) {
+    LayerPlan p;
+    size_t off = 0;
+    auto carve = [&](size_t bytes) {
+        const size_t o = off;
+        off = align_up(off + bytes, 256);
+        return o;
+    };
+    const size_t hmd = (size_t)H * M * d;
+    p.off_q = carve(sizeof(float) * hmd);
+    p.off_pp = carve((dtype == SA_BF16 ? 2 : 4) * hmd);
+    if (bwd) {
+        p.off_dpp = carve(sizeof(float) * hmd);
+        p.off_dq = carve(sizeof(float) * hmd);
+        if (plain_bwd) {
+            p.off_dk = carve(sizeof(float) * (size_t)T * H * d);
+            p.off_dv = carve(sizeof(float) * (size_t)T * H * d);
+        }
+    }
+    p.off_base = carve(base_bytes);
+    p.total = off;
+    return p;
+}
+
+// Q = P W_Q (fp32) and P' = Q W_K^T (input dtype), per head
+sa_status layer_prototypes(const void* P, const void* Wq, const void* Wk, int32_t H, int32_t M,
+                           int32_t d, sa_dtype dtype, float* Q, void* Pp, hipStream_t stream) {
+    const bool bf = dtype == SA_BF16;
+    const int64_t md = (int64_t)M * d, dd = (int64_t)d * d;
+    sa::ProfScope ps("layer_proto_proj", stream);
+    hipError_t e = sa::launch_small_gemm({P, bf, md, d, 1}, {Wq, bf, dd, d, 1}, Q, false, H, M, d, d,
+                                         stream);
+    if (e == hipSuccess)
+        e = sa::launch_small_gemm({Q, false, md, d, 1}, {Wk, bf, dd, 1, d}, Pp, bf, H, M, d, d, stream);
+    if (e != hipSuccess) return hip_fail(e, "prototype projection launch");
+    return SA_OK;
+}
+
+// forward on a checked plan and workspace (shared by sa_sketch_fwd and sa_layer_fwd)
+sa_status run_fwd(const void* K, const void* V, const void* P, const int64_t* offsets, int64_t B,
+                  int64_t T, int32_t H, int32_t M, int32_t d, float scale, sa_dtype dtype,
+                  float* sketch, float* lse, uint8_t* ws, const FwdPlan& plan, hipStream_t stream) {
+    hipError_t e;
+    if (plan.fused) {
+        int32_t* items = reinterpret_cast<int32_t*>(ws + plan.off_items);
+        int32_t* wg_start = reinterpret_cast<int32_t*>(ws + plan.off_wgstart);
+        int32_t* pair_start = reinterpret_cast<int32_t*>(ws + plan.off_pairstart);
+        int64_t* n_items = reinterpret_cast<int64_t*>(ws + plan.off_nitems);
+        float* partials = reinterpret_cast<float*>(ws + plan.off_partials);
+        {
+            sa::ProfScope ps("worklist", stream);
+            e = sa::launch_worklist(offsets, B, T, H, plan.C, plan.n_ranges, items,
+                                    plan.max_items, wg_start, pair_start, n_items, stream);
+        }
+        if (e != hipSuccess) return hip_fail(e, "work list launch");
+        sa::FusedFwdArgs a;
+        a.K = reinterpret_cast<const uint16_t*>(K);
+        a.V = reinterpret_cast<const uint16_t*>(V);
+        a.P = reinterpret_cast<const uint16_t*>(P);
+        a.items = items;
+        a.wg_start = wg_start;
+        a.n_ranges = plan.n_ranges;
+        a.max_items = plan.max_items;
+        a.T = T;
+        a.B = (int32_t)B;
+        a.H = H;
+        a.M = M;
+        a.d = d;
+        a.scale = scale;
+        a.sketch = sketch;
+        a.lse = lse;
+        a.partials = partials;
+        {
+            sa::ProfScope ps("fused_fwd", stream);
+            e = sa::launch_fused_fwd(a, stream);
+        }
+        if (e != hipSuccess) return hip_fail(e, "fused forward launch");
+        {
+            sa::ProfScope ps("splitL_merge", stream);
+            e = sa::launch_merge(pair_start, B, H, plan.max_items, partials, (int64_t)M * d,
+                                 sketch, stream);
+        }
+        if (e != hipSuccess) return hip_fail(e, "split-L merge launch");
+        return SA_OK;
+    }
+    float* lse_out = lse ? lse : reinterpret_cast<float*>(ws + plan.off_lse);
+    {
+        sa::ProfScope ps("plain_fwd", stream);
+        e = sa::launch_generic_fwd(K, V, P, offsets, B, T, H, M, d, scale, dtype == SA_BF16,
+                                   sketch, lse_out, stream);
+    }
+    if (e != hipSuccess) return hip_fail(e, "fp32 forward launch");
+    return SA_OK;
+}
+
+
+// backward on a checked plan and workspace.  With dX non-null, K and V are the
+// same tensor X and the gradient w.r.t. it, dX = dK + dV, is written instead of
+// dK and dV (the plain path still needs dK and dV as scratch).
+sa_status run_bwd(const void* K, const void* V, const void* P, const int64_t* offsets, int64_t B,
+                  int64_t T, int32_t H, int32_t M, int32_t d, float scale, sa_dtype dtype,
+                  const float* dsketch, int32_t R, const float* lse, float* dK, float* dV,
+                  float* dP, float* dX, uint8_t* ws, const BwdPlan& plan, hipStream_t stream) {
+    float* dY = reinterpret_cast<float*>(ws + plan.off_dY);
+    float* Dbuf = reinterpret_cast<float*>(ws + plan.off_D);
+    float* part = reinterpret_cast<float*>(ws + plan.off_part);
+    hipError_t e;
+    if (plan.fused) {
+        sa::FusedBwdArgs f;
+        f.K = reinterpret_cast<const uint16_t*>(K);
+        f.V = reinterpret_cast<const uint16_t*>(V);
+        f.P = reinterpret_cast<const uint16_t*>(P);
+        f.dsketch = dsketch;
+        f.lse = lse;
+        f.items = reinterpret_cast<int32_t*>(ws + plan.off_items);
+        f.wg_start = reinterpret_cast<int32_t*>(ws + plan.off_wgstart);
+        f.pair_start = reinterpret_cast<int32_t*>(ws + plan.off_pairstart);
+        f.n_ranges = plan.n_ranges;
+        f.max_items = plan.max_items;
+        f.B = B;
+        f.T = T;
+        f.H = H;
+        f.M = M;
+        f.d = d;
+        f.R = R;
+        f.scale = scale;
+        f.Ymj = reinterpret_cast<uint16_t*>(ws + plan.off_ymj);
+        f.Yjm = reinterpret_cast<uint16_t*>(ws + plan.off_yjm);
+        f.Pjm = reinterpret_cast<uint16_t*>(ws + plan.off_pjm);
+        f.Dbuf = Dbuf;
+        f.partials = part;
+        f.dK = dK;
+        f.dV = dV;
+        f.dP = dP;
+        f.dX = dX;
+        {
+            sa::ProfScope ps("worklist", stream);
+            e = sa::launch_worklist(offsets, B, T, H, plan.C, plan.n_ranges,
+                                    const_cast<int32_t*>(f.items), plan.max_items,
+                                    const_cast<int32_t*>(f.wg_start),
+                                    const_cast<int32_t*>(f.pair_start),
+                                    reinterpret_cast<int64_t*>(ws + plan.off_nitems), stream);
+        }
+        if (e != hipSuccess) return hip_fail(e, "work list launch");
+        e = sa::launch_fused_bwd(f, stream);
+        if (e != hipSuccess) return hip_fail(e, "fused backward launch");
+        return SA_OK;
+    }
+    {
+        sa::ProfScope ps("dY_reduce", stream);
+        e = sa::launch_dy_reduce(dsketch, B, R, H, (int64_t)M * d, dY, stream);
+    }
+    if (e != hipSuccess) return hip_fail(e, "dY reduce launch");
+    {
+        sa::ProfScope ps("plain_bwd", stream);
+        e = sa::launch_generic_bwd(K, V, P, offsets, B, T, H, M, d, scale, dtype == SA_BF16, dY,
+                                   lse, Dbuf, dK, dV, dP, part, plan.n_chunks, stream);
+    }
+    if (e != hipSuccess) return hip_fail(e, "backward launch");
+    if (dX) {
+        sa::ProfScope ps("dX_sum", stream);
+        e = sa::launch_add(dK, dV, dX, T * H * d, stream);
+        if (e != hipSuccess) return hip_fail(e, "dX sum launch");
+    }
+    return SA_OK;
+}
+
+
 }  // namespace
 
 namespace sa {
@@ -315,58 +492,8 @@ sa_status sa_sketch_fwd(const void* K, const void* V, const void* P, const int64
         st = validate_offsets(offsets, B, T, stream);
         if (st != SA_OK) return st;
     }
-    uint8_t* ws = reinterpret_cast<uint8_t*>(workspace);
-    hipError_t e;
-    if (plan.fused) {
-        int32_t* items = reinterpret_cast<int32_t*>(ws + plan.off_items);
-        int32_t* wg_start = reinterpret_cast<int32_t*>(ws + plan.off_wgstart);
-        int32_t* pair_start = reinterpret_cast<int32_t*>(ws + plan.off_pairstart);
-        int64_t* n_items = reinterpret_cast<int64_t*>(ws + plan.off_nitems);
-        float* partials = reinterpret_cast<float*>(ws + plan.off_partials);
-        {
-            sa::ProfScope ps("worklist", stream);
-            e = sa::launch_worklist(offsets, B, T, H, plan.C, plan.n_ranges, items,
-                                    plan.max_items, wg_start, pair_start, n_items, stream);
-        }
-        if (e != hipSuccess) return hip_fail(e, "work list launch");
-        sa::FusedFwdArgs a;
-        a.K = reinterpret_cast<const uint16_t*>(K);
-        a.V = reinterpret_cast<const uint16_t*>(V);
-        a.P = reinterpret_cast<const uint16_t*>(P);
-        a.items = items;
-        a.wg_start = wg_start;
-        a.n_ranges = plan.n_ranges;
-        a.max_items = plan.max_items;
-        a.T = T;
-        a.B = (int32_t)B;
-        a.H = H;
-        a.M = M;
-        a.d = d;
-        a.scale = scale;
-        a.sketch = sketch;
-        a.lse = lse;
-        a.partials = partials;
-        {
-            sa::ProfScope ps("fused_fwd", stream);
-            e = sa::launch_fused_fwd(a, stream);
-        }
-        if (e != hipSuccess) return hip_fail(e, "fused forward launch");
-        {
-            sa::ProfScope ps("splitL_merge", stream);
-            e = sa::launch_merge(pair_start, B, H, plan.max_items, partials, (int64_t)M * d,
-                                 sketch, stream);
-        }
-        if (e != hipSuccess) return hip_fail(e, "split-L merge launch");
-        return SA_OK;
-    }
-    float* lse_out = lse ? lse : reinterpret_cast<float*>(ws + plan.off_lse);
-    {
-        sa::ProfScope ps("plain_fwd", stream);
-        e = sa::launch_generic_fwd(K, V, P, offsets, B, T, H, M, d, scale, dtype == SA_BF16,
-                                   sketch, lse_out, stream);
-    }
-    if (e != hipSuccess) return hip_fail(e, "fp32 forward launch");
-    return SA_OK;
+    return run_fwd(K, V, P, offsets, B, T, H, M, d, scale, dtype, sketch, lse,
+                   reinterpret_cast<uint8_t*>(workspace), plan, stream);
 }
 
 size_t sa_sketch_fwd_tokenwise_workspace_size(int64_t B, int64_t T, int32_t H, int32_t M,
@@ -467,62 +594,106 @@ sa_status sa_sketch_bwd(const void* K, const void* V, const void* P, const int64
         st = validate_offsets(offsets, B, T, stream);
         if (st != SA_OK) return st;
     }
+    return run_bwd(K, V, P, offsets, B, T, H, M, d, scale, dtype, dsketch, R, lse, dK, dV, dP,
+                   nullptr, reinterpret_cast<uint8_t*>(workspace), plan, stream);
+}
+
+size_t sa_layer_fwd_workspace_size(int64_t B, int64_t T, int32_t H, int32_t M, int32_t d,
+                                   sa_dtype dtype) {
+    if (check_common(B, T, H, M, d, 1.0f, dtype) != SA_OK) return 0;
+    return plan_layer(T, H, M, d, dtype, false, false, plan_fwd(B, T, H, M, d, dtype, true).total)
+        .total;
+}
+
+sa_status sa_layer_fwd(const void* X, const void* P, const void* Wq, const void* Wk,
+                       const int64_t* offsets, int64_t B, int64_t T, int32_t H, int32_t M,
+                       int32_t d, float scale, sa_dtype dtype, float* sketch, float* lse,
+                       void* workspace, size_t workspace_bytes, void* stream_) {
+    g_last_error[0] = 0;
+    sa_status st = check_common(B, T, H, M, d, scale, dtype);
+    if (st != SA_OK) return st;
+    if (B == 0) return SA_OK;
+    if (!offsets || !sketch || !P || !Wq || !Wk || (T > 0 && !X))
+        return fail(SA_ERR_INVALID_ARG, "null pointer argument");
+    if (!aligned16(X) || !aligned16(P) || !aligned16(Wq) || !aligned16(Wk) || !aligned16(sketch) ||
+        !aligned16(lse))
+        return fail(SA_ERR_INVALID_ARG, "X, P, W_Q, W_K, sketch and lse must be 16-byte aligned");
+    hipStream_t stream = reinterpret_cast<hipStream_t>(stream_);
+    const FwdPlan base = plan_fwd(B, T, H, M, d, dtype, lse == nullptr);
+    const LayerPlan plan = plan_layer(T, H, M, d, dtype, false, false, base.total);
+    if (!workspace || workspace_bytes < plan.total)
+        return fail(SA_ERR_WORKSPACE, "workspace of %zu bytes needed, %zu given", plan.total,
+                    workspace ? workspace_bytes : (size_t)0);
+    if (debug_validate()) {
+        st = validate_offsets(offsets, B, T, stream);
+        if (st != SA_OK) return st;
+    }
     uint8_t* ws = reinterpret_cast<uint8_t*>(workspace);
-    float* dY = reinterpret_cast<float*>(ws + plan.off_dY);
-    float* Dbuf = reinterpret_cast<float*>(ws + plan.off_D);
-    float* part = reinterpret_cast<float*>(ws + plan.off_part);
-    hipError_t e;
-    if (plan.fused) {
-        sa::FusedBwdArgs f;
-        f.K = reinterpret_cast<const uint16_t*>(K);
-        f.V = reinterpret_cast<const uint16_t*>(V);
-        f.P = reinterpret_cast<const uint16_t*>(P);
-        f.dsketch = dsketch;
-        f.lse = lse;
-        f.items = reinterpret_cast<int32_t*>(ws + plan.off_items);
-        f.wg_start = reinterpret_cast<int32_t*>(ws + plan.off_wgstart);
-        f.pair_start = reinterpret_cast<int32_t*>(ws + plan.off_pairstart);
-        f.n_ranges = plan.n_ranges;
-        f.max_items = plan.max_items;
-        f.B = B;
-        f.T = T;
-        f.H = H;
-        f.M = M;
-        f.d = d;
-        f.R = R;
-        f.scale = scale;
-        f.Ymj = reinterpret_cast<uint16_t*>(ws + plan.off_ymj);
-        f.Yjm = reinterpret_cast<uint16_t*>(ws + plan.off_yjm);
-        f.Pjm = reinterpret_cast<uint16_t*>(ws + plan.off_pjm);
-        f.Dbuf = Dbuf;
-        f.partials = part;
-        f.dK = dK;
-        f.dV = dV;
-        f.dP = dP;
-        {
-            sa::ProfScope ps("worklist", stream);
-            e = sa::launch_worklist(offsets, B, T, H, plan.C, plan.n_ranges,
-                                    const_cast<int32_t*>(f.items), plan.max_items,
-                                    const_cast<int32_t*>(f.wg_start),
-                                    const_cast<int32_t*>(f.pair_start),
-                                    reinterpret_cast<int64_t*>(ws + plan.off_nitems), stream);
-        }
-        if (e != hipSuccess) return hip_fail(e, "work list launch");
-        e = sa::launch_fused_bwd(f, stream);
-        if (e != hipSuccess) return hip_fail(e, "fused backward launch");
-        return SA_OK;
+    float* Q = reinterpret_cast<float*>(ws + plan.off_q);
+    void* Pp = ws + plan.off_pp;
+    st = layer_prototypes(P, Wq, Wk, H, M, d, dtype, Q, Pp, stream);
+    if (st != SA_OK) return st;
+    return run_fwd(X, X, Pp, offsets, B, T, H, M, d, scale, dtype, sketch, lse, ws + plan.off_base,
+                   base, stream);
+}
+
+size_t sa_layer_bwd_workspace_size(int64_t B, int64_t T, int32_t H, int32_t M, int32_t d,
+                                   sa_dtype dtype, int32_t R) {
+    if (check_common(B, T, H, M, d, 1.0f, dtype) != SA_OK || R < 1) return 0;
+    const BwdPlan base = plan_bwd(B, T, H, M, d, dtype);
+    return plan_layer(T, H, M, d, dtype, true, !base.fused, base.total).total;
+}
+
+sa_status sa_layer_bwd(const void* X, const void* P, const void* Wq, const void* Wk,
+                       const int64_t* offsets, int64_t B, int64_t T, int32_t H, int32_t M,
+                       int32_t d, float scale, sa_dtype dtype, const float* dsketch, int32_t R,
+                       const float* lse, float* dX, float* dP, float* dWq, float* dWk,
+                       void* workspace, size_t workspace_bytes, void* stream_) {
+    g_last_error[0] = 0;
+    sa_status st = check_common(B, T, H, M, d, scale, dtype);
+    if (st != SA_OK) return st;
+    if (R < 1) return fail(SA_ERR_INVALID_ARG, "R must be >= 1 (got %d)", R);
+    if (!offsets || !P || !Wq || !Wk || !dP || !dWq || !dWk || (B > 0 && !dsketch) ||
+        (T > 0 && (!X || !lse || !dX)))
+        return fail(SA_ERR_INVALID_ARG, "null pointer argument");
+    if (!aligned16(X) || !aligned16(P) || !aligned16(Wq) || !aligned16(Wk) || !aligned16(dsketch) ||
+        !aligned16(lse) || !aligned16(dX) || !aligned16(dP) || !aligned16(dWq) || !aligned16(dWk))
+        return fail(SA_ERR_INVALID_ARG, "tensor arguments must be 16-byte aligned");
+    hipStream_t stream = reinterpret_cast<hipStream_t>(stream_);
+    const BwdPlan base = plan_bwd(B, T, H, M, d, dtype);
+    const LayerPlan plan = plan_layer(T, H, M, d, dtype, true, !base.fused, base.total);
+    if (!workspace || workspace_bytes < plan.total)
+        return fail(SA_ERR_WORKSPACE, "workspace of %zu bytes needed, %zu given", plan.total,
+                    workspace ? workspace_bytes : (size_t)0);
+    if (debug_validate() && B > 0) {
+        st = validate_offsets(offsets, B, T, stream);
+        if (st != SA_OK) return st;
     }
-    {
-        sa::ProfScope ps("dY_reduce", stream);
-        e = sa::launch_dy_reduce(dsketch, B, R, H, (int64_t)M * d, dY, stream);
-    }
-    if (e != hipSuccess) return hip_fail(e, "dY reduce launch");
-    {
-        sa::ProfScope ps("plain_bwd", stream);
-        e = sa::launch_generic_bwd(K, V, P, offsets, B, T, H, M, d, scale, dtype == SA_BF16, dY,
-                                   lse, Dbuf, dK, dV, dP, part, plan.n_chunks, stream);
-    }
-    if (e != hipSuccess) return hip_fail(e, "backward launch");
+    uint8_t* ws = reinterpret_cast<uint8_t*>(workspace);
+    float* Q = reinterpret_cast<float*>(ws + plan.off_q);
+    void* Pp = ws + plan.off_pp;
+    float* dPp = reinterpret_cast<float*>(ws + plan.off_dpp);
+    float* dQ = reinterpret_cast<float*>(ws + plan.off_dq);
+    st = layer_prototypes(P, Wq, Wk, H, M, d, dtype, Q, Pp, stream);
+    if (st != SA_OK) return st;
+    float* dKs = base.fused ? nullptr : reinterpret_cast<float*>(ws + plan.off_dk);
+    float* dVs = base.fused ? nullptr : reinterpret_cast<float*>(ws + plan.off_dv);
+    st = run_bwd(X, X, Pp, offsets, B, T, H, M, d, scale, dtype, dsketch, R, lse, dKs, dVs, dPp, dX,
+                 ws + plan.off_base, base, stream);
+    if (st != SA_OK) return st;
+    // dW_K = dP'^T Q, dQ = dP' W_K, dW_Q = P^T dQ, dP = dQ W_Q^T
+    const bool bf = dtype == SA_BF16;
+    const int64_t md = (int64_t)M * d, dd = (int64_t)d * d;
+    sa::ProfScope ps("layer_proj_grads", stream);
+    hipError_t e = sa::launch_small_gemm({dPp, false, md, 1, d}, {Q, false, md, d, 1}, dWk, false, H, d,
+                                         d, M, stream);
+    if (e == hipSuccess)
+        e = sa::launch_small_gemm({dPp, false, md, d, 1}, {Wk, bf, dd, d, 1}, dQ, false, H, M, d, d, stream);
+    if (e == hipSuccess)
+        e = sa::launch_small_gemm({P, bf, md, 1, d}, {dQ, false, md, d, 1}, dWq, false, H, d, d, M, stream);
+    if (e == hipSuccess)
+        e = sa::launch_small_gemm({dQ, false, md, d, 1}, {Wq, bf, dd, 1, d}, dP, false, H, M, d, d, stream);
+    if (e != hipSuccess) return hip_fail(e, "projection gradient launch");
     return SA_OK;
 }
 

@@ -111,6 +111,8 @@ __global__ __launch_bounds__(256) void prep_kernel(const float* __restrict__ ds,
 }
 
 // ------------------------------------------------------------------ token side
+constexpr int kTokWaves = 8;   // waves of the token-side kernel: two per SIMD
+
 template <int D, int NW_>
 struct TokCfg {
     static constexpr int NW = NW_;
@@ -142,10 +144,15 @@ struct TokArgs {
     float scale;
     float* dK;
     float* dV;
+    float* dX;      // XV: dX = dV + dK (K and V are the same tensor X)
     float* Dbuf;
 };
 
-template <int D, int NW>
+// XV: K and V are one tensor X (the SA layer aggregates its own history and its
+// key projection is folded into P).  X is loaded once, and the second sweep keeps
+// accumulating into the dV registers with scale folded into dS, so the kernel
+// writes dX = dV + dK once.
+template <int D, int NW, bool XV>
 __global__ __launch_bounds__(NW * 64, 8 / NW) void bwd_token_kernel(TokArgs a) {
     using C = TokCfg<D, NW>;
     extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
@@ -187,7 +194,7 @@ __global__ __launch_bounds__(NW * 64, 8 / NW) void bwd_token_kernel(TokArgs a) {
 #pragma unroll
                 for (int kk = 0; kk < C::KS; ++kk) {
                     uint4 x = *reinterpret_cast<const uint4*>(kr + 16 * kk + 8 * hl);
-                    uint4 y = *reinterpret_cast<const uint4*>(vr + 16 * kk + 8 * hl);
+                    uint4 y = XV ? x : *reinterpret_cast<const uint4*>(vr + 16 * kk + 8 * hl);
                     if (!tv) x = y = make_uint4(0, 0, 0, 0);
                     kb[kk] = __builtin_bit_cast(bf16x8, x);
                     vb[kk] = __builtin_bit_cast(bf16x8, y);
@@ -277,23 +284,27 @@ __global__ __launch_bounds__(NW * 64, 8 / NW) void bwd_token_kernel(TokArgs a) {
             }
             // write dV now (frees its registers)
             if (tv) {
-                float* out = a.dV + ((int64_t)tok * a.H + h) * D;
-                // registers 4g..4g+3 hold 4 consecutive columns: 16-byte stores
+                if constexpr (!XV) {
+                    float* out = a.dV + ((int64_t)tok * a.H + h) * D;
+                    // registers 4g..4g+3 hold 4 consecutive columns: 16-byte stores
 #pragma unroll
-                for (int jt = 0; jt < C::JT; ++jt)
+                    for (int jt = 0; jt < C::JT; ++jt)
 #pragma unroll
-                    for (int g = 0; g < 4; ++g)
-                        *reinterpret_cast<float4*>(out + jt * 32 + 8 * g + 4 * hl) =
-                            make_float4(dvt[jt][4 * g], dvt[jt][4 * g + 1], dvt[jt][4 * g + 2], dvt[jt][4 * g + 3]);
+                        for (int g = 0; g < 4; ++g)
+                            *reinterpret_cast<float4*>(out + jt * 32 + 8 * g + 4 * hl) =
+                                make_float4(dvt[jt][4 * g], dvt[jt][4 * g + 1], dvt[jt][4 * g + 2], dvt[jt][4 * g + 3]);
+                }
                 if (hl == 0) a.Dbuf[(int64_t)tok * a.H + h] = Dt;
             }
 
             // ---------------- sweep 2: dK^T[j, t] = scale sum_m P[m, j] dS[t, m]
+            // (XV: continues from dV^T, with scale folded into the weights)
             f32x16 dkt[C::JT];
 #pragma unroll
             for (int jt = 0; jt < C::JT; ++jt)
 #pragma unroll
-                for (int r = 0; r < 16; ++r) dkt[jt][r] = 0.f;
+                for (int r = 0; r < 16; ++r) dkt[jt][r] = XV ? dvt[jt][r] : 0.f;
+            const float nl2 = XV ? nl + __log2f(a.scale) : nl;
             fetch(0, 1, 0);
             wait_vmem();
             __syncthreads();
@@ -314,7 +325,7 @@ __global__ __launch_bounds__(NW * 64, 8 / NW) void bwd_token_kernel(TokArgs a) {
                 float e[16];
 #pragma unroll
                 for (int r = 0; r < 16; ++r) {
-                    const float A = __builtin_amdgcn_exp2f(__builtin_fmaf(s[r], ks2, nl));
+                    const float A = __builtin_amdgcn_exp2f(__builtin_fmaf(s[r], ks2, nl2));
                     e[r] = A * (da[r] - Dt);
                 }
                 const bf16x8 d0 = pack8(e), d1 = pack8(e + 8);
@@ -330,14 +341,15 @@ __global__ __launch_bounds__(NW * 64, 8 / NW) void bwd_token_kernel(TokArgs a) {
                 __syncthreads();
             }
             if (tv) {
-                float* out = a.dK + ((int64_t)tok * a.H + h) * D;
+                float* out = (XV ? a.dX : a.dK) + ((int64_t)tok * a.H + h) * D;
+                const float f = XV ? 1.0f : a.scale;
 #pragma unroll
                 for (int jt = 0; jt < C::JT; ++jt)
 #pragma unroll
                     for (int g = 0; g < 4; ++g)
                         *reinterpret_cast<float4*>(out + jt * 32 + 8 * g + 4 * hl) =
-                            make_float4(a.scale * dkt[jt][4 * g], a.scale * dkt[jt][4 * g + 1],
-                                        a.scale * dkt[jt][4 * g + 2], a.scale * dkt[jt][4 * g + 3]);
+                            make_float4(f * dkt[jt][4 * g], f * dkt[jt][4 * g + 1],
+                                        f * dkt[jt][4 * g + 2], f * dkt[jt][4 * g + 3]);
             }
         }
     }
@@ -388,7 +400,8 @@ struct ProtoArgs {
     float* partials;  // [max_items][M][D]
 };
 
-template <int D, int MW, int NW>
+// XV: K and V are one tensor (one tile load serves both operands).
+template <int D, int MW, int NW, bool XV>
 __global__ __launch_bounds__(NW * 64, 1) void bwd_proto_kernel(ProtoArgs a) {
     using C = ProtoCfg<D, MW, NW>;
     constexpr bool kHold = C::HOLD;
@@ -434,7 +447,7 @@ __global__ __launch_bounds__(NW * 64, 1) void bwd_proto_kernel(ProtoArgs a) {
                 if (idx < C::LD_CHUNKS && ts + tok < t1) {
                     const uint32_t off = (uint32_t)tok * row_stride + (uint32_t)(ch * 8);
                     kv = *reinterpret_cast<const u32x4*>(a.K + tb + off);
-                    vv = *reinterpret_cast<const u32x4*>(a.V + tb + off);
+                    if constexpr (!XV) vv = *reinterpret_cast<const u32x4*>(a.V + tb + off);
                 }
                 kreg[c] = kv;
                 vreg[c] = vv;
@@ -454,7 +467,7 @@ __global__ __launch_bounds__(NW * 64, 1) void bwd_proto_kernel(ProtoArgs a) {
                 if (idx < C::LD_CHUNKS) {
                     const int tok = idx / C::KCH, ch = idx % C::KCH;
                     *reinterpret_cast<u32x4*>(Kd + swz<D>(tok, ch)) = kreg[c];
-                    *reinterpret_cast<u32x4*>(Vd + swz<D>(tok, ch)) = vreg[c];
+                    if constexpr (!XV) *reinterpret_cast<u32x4*>(Vd + swz<D>(tok, ch)) = vreg[c];
                 }
             }
             if (tid < 32) {
@@ -503,7 +516,7 @@ __global__ __launch_bounds__(NW * 64, 1) void bwd_proto_kernel(ProtoArgs a) {
             const bool more = ts + 32 < t1;
             if (more) fetch(ts + 32);
             const uint16_t* Ks = reinterpret_cast<const uint16_t*>(smem + C::OFF_K + buf * C::TILE);
-            const uint16_t* Vs = reinterpret_cast<const uint16_t*>(smem + C::OFF_V + buf * C::TILE);
+            const uint16_t* Vs = XV ? Ks : reinterpret_cast<const uint16_t*>(smem + C::OFF_V + buf * C::TILE);
             const float* nls = reinterpret_cast<const float*>(smem + C::OFF_L) + buf * 32;
             const float* Ds = reinterpret_cast<const float*>(smem + C::OFF_D) + buf * 32;
 
@@ -597,10 +610,10 @@ __global__ __launch_bounds__(256) void dp_sum_kernel(const int32_t* __restrict__
     *reinterpret_cast<float4*>(dP + i) = acc;
 }
 
-template <int D, int NW>
+template <int D, int NW, bool XV>
 hipError_t launch_token(const TokArgs& a, int64_t n_ranges, hipStream_t stream) {
     using C = TokCfg<D, NW>;
-    auto kern = bwd_token_kernel<D, NW>;
+    auto kern = bwd_token_kernel<D, NW, XV>;
     hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
                                        hipFuncAttributeMaxDynamicSharedMemorySize, C::LDS);
     if (e != hipSuccess) return e;
@@ -608,10 +621,10 @@ hipError_t launch_token(const TokArgs& a, int64_t n_ranges, hipStream_t stream) 
     return hipGetLastError();
 }
 
-template <int D, int MW, int NW>
-hipError_t launch_proto(const ProtoArgs& a, int64_t n_ranges, hipStream_t stream) {
+template <int D, int MW, int NW, bool XV>
+hipError_t launch_proto_t(const ProtoArgs& a, int64_t n_ranges, hipStream_t stream) {
     using C = ProtoCfg<D, MW, NW>;
-    auto kern = bwd_proto_kernel<D, MW, NW>;
+    auto kern = bwd_proto_kernel<D, MW, NW, XV>;
     hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
                                        hipFuncAttributeMaxDynamicSharedMemorySize, C::LDS);
     if (e != hipSuccess) return e;
@@ -623,10 +636,19 @@ hipError_t launch_proto(const ProtoArgs& a, int64_t n_ranges, hipStream_t stream
     return hipGetLastError();
 }
 
-}  // namespace
+template <int D, int MW, int NW>
+hipError_t launch_proto(const ProtoArgs& a, bool xv, int64_t n_ranges, hipStream_t stream) {
+    return xv ? launch_proto_t<D, MW, NW, true>(a, n_ranges, stream)
+              : launch_proto_t<D, MW, NW, false>(a, n_ranges, stream);
+}
 
-// waves of the token-side kernel: two per SIMD, one workgroup per CU
-constexpr int kTokWaves = 8;
+template <int D>
+hipError_t launch_token_d(const TokArgs& a, bool xv, int64_t n_ranges, hipStream_t stream) {
+    return xv ? launch_token<D, kTokWaves, true>(a, n_ranges, stream)
+              : launch_token<D, kTokWaves, false>(a, n_ranges, stream);
+}
+
+}  // namespace
 
 int32_t fused_bwd_ranges_per_cu() { return 8 / kTokWaves; }
 
@@ -662,12 +684,13 @@ hipError_t launch_fused_bwd(const FusedBwdArgs& f, hipStream_t stream) {
         t.K = f.K; t.V = f.V; t.P = f.P; t.Pjm = f.Pjm; t.Ymj = f.Ymj; t.Yjm = f.Yjm;
         t.lse = f.lse; t.items = f.items; t.wg_start = f.wg_start; t.max_items = f.max_items;
         t.T = f.T; t.B = (int32_t)f.B; t.H = f.H; t.M = f.M; t.scale = f.scale;
-        t.dK = f.dK; t.dV = f.dV; t.Dbuf = f.Dbuf;
+        t.dK = f.dK; t.dV = f.dV; t.dX = f.dX; t.Dbuf = f.Dbuf;
+        const bool xv = f.dX != nullptr;
         hipError_t e;
         {
             ProfScope ps("bwd_token", stream);
-            e = f.d == 64 ? launch_token<64, kTokWaves>(t, f.n_ranges, stream)
-                          : launch_token<128, kTokWaves>(t, f.n_ranges, stream);
+            e = f.d == 64 ? launch_token_d<64>(t, xv, f.n_ranges, stream)
+                          : launch_token_d<128>(t, xv, f.n_ranges, stream);
         }
         if (e != hipSuccess) return e;
         ProtoArgs p;
@@ -678,12 +701,12 @@ hipError_t launch_fused_bwd(const FusedBwdArgs& f, hipStream_t stream) {
         ProfScope ps("bwd_proto", stream);
         // eight waves (two per SIMD) when the part has at least 32 prototypes per wave
         if (f.d == 64) {
-            e = mp == 128 ? launch_proto<64, 32, 4>(p, f.n_ranges, stream)
-              : mp == 256 ? launch_proto<64, 32, 8>(p, f.n_ranges, stream)
-                          : launch_proto<64, 64, 8>(p, f.n_ranges, stream);
+            e = mp == 128 ? launch_proto<64, 32, 4>(p, xv, f.n_ranges, stream)
+              : mp == 256 ? launch_proto<64, 32, 8>(p, xv, f.n_ranges, stream)
+                          : launch_proto<64, 64, 8>(p, xv, f.n_ranges, stream);
         } else {
-            e = mp == 128 ? launch_proto<128, 32, 4>(p, f.n_ranges, stream)
-                          : launch_proto<128, 32, 8>(p, f.n_ranges, stream);
+            e = mp == 128 ? launch_proto<128, 32, 4>(p, xv, f.n_ranges, stream)
+                          : launch_proto<128, 32, 8>(p, xv, f.n_ranges, stream);
         }
         if (e != hipSuccess) return e;
     }

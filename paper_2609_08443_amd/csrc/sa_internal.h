@@ -97,6 +97,10 @@ struct FusedBwdArgs {
     float* dK;
     float* dV;
     float* dP;
+    // When non-null, K and V are the same tensor X (the SA layer, whose value
+    // is its history and whose key projection is absorbed into P): the token
+    // side writes dX = dV + dK here instead of dK and dV.
+    float* dX;
 };
 bool fused_bwd_supported(int32_t M, int32_t d);
 int32_t fused_bwd_part(int32_t M, int32_t d);
@@ -117,6 +121,20 @@ hipError_t launch_tokenwise_merge(const int32_t* pair_start, int64_t B, int32_t 
 hipError_t launch_tokenwise_generic(const void* K, const void* V, const void* P, const int64_t* offsets,
                                     int64_t B, int32_t H, int32_t M, int32_t d, float scale, bool bf16,
                                     float* sketch, float* lse_m, hipStream_t stream);
+
+// Small batched product for the SA layer's projections (fp32 accumulation):
+// C[h][r][c] = sum_k A[h](r, k) B[h](k, c), r < R, c < N, k < Kd, C row-major
+// [R][N] per head, bf16 (rounded) or fp32.  Operand element (i, j) of head h
+// sits at p[h * s_h + i * s_0 + j * s_1], so a transpose is a swap of strides.
+struct MatView {
+    const void* p;
+    bool bf16;
+    int64_t s_h, s_0, s_1;
+};
+hipError_t launch_small_gemm(const MatView& a, const MatView& b, void* c, bool c_bf16, int32_t H, int32_t R,
+                             int32_t N, int32_t Kd, hipStream_t stream);
+// out = a + b elementwise (n fp32 values, n a multiple of 4, 16-byte aligned)
+hipError_t launch_add(const float* a, const float* b, float* out, int64_t n, hipStream_t stream);
 
 // Plain fp32-arithmetic path (fp32 or bf16 inputs).
 hipError_t launch_generic_fwd(const void* K, const void* V, const void* P,

@@ -23,6 +23,8 @@ ITEM_WORDS = 8
 EXPORTS = ("sa_sketch_fwd_workspace_size", "sa_sketch_fwd", "sa_sketch_bwd_workspace_size",
            "sa_sketch_bwd", "sa_build_worklist", "sa_sketch_fwd_chunk_tokens",
            "sa_sketch_fwd_tokenwise_workspace_size", "sa_sketch_fwd_tokenwise",
+           "sa_layer_fwd_workspace_size", "sa_layer_fwd", "sa_layer_bwd_workspace_size",
+           "sa_layer_bwd",
            "sa_profile_enable", "sa_kernel_times", "sa_status_string", "sa_last_error")
 
 
@@ -63,6 +65,16 @@ def lib() -> ctypes.CDLL:
     L.sa_sketch_fwd_tokenwise.argtypes = [vp, vp, vp, vp, i64, i64, i32, i32, i32, f32, c.c_int,
                                           vp, vp, vp, sz, vp]
     L.sa_sketch_fwd_tokenwise.restype = c.c_int
+    L.sa_layer_fwd_workspace_size.argtypes = [i64, i64, i32, i32, i32, c.c_int]
+    L.sa_layer_fwd_workspace_size.restype = sz
+    L.sa_layer_fwd.argtypes = [vp, vp, vp, vp, vp, i64, i64, i32, i32, i32, f32, c.c_int, vp, vp,
+                               vp, sz, vp]
+    L.sa_layer_fwd.restype = c.c_int
+    L.sa_layer_bwd_workspace_size.argtypes = [i64, i64, i32, i32, i32, c.c_int, i32]
+    L.sa_layer_bwd_workspace_size.restype = sz
+    L.sa_layer_bwd.argtypes = [vp, vp, vp, vp, vp, i64, i64, i32, i32, i32, f32, c.c_int, vp, i32,
+                               vp, vp, vp, vp, vp, vp, sz, vp]
+    L.sa_layer_bwd.restype = c.c_int
     L.sa_build_worklist.argtypes = [vp, i64, i64, i32, i64, vp, i64, vp, vp]
     L.sa_build_worklist.restype = c.c_int
     L.sa_status_string.argtypes = [c.c_int]
@@ -231,6 +243,73 @@ def sketch_bwd(K, V, P, offsets, dsketch, lse, scale: Optional[float] = None, dK
                              _ptr(dP), _ptr(ws), nbytes, _stream_handle(stream))
     _check(rc)
     return dK, dV, dP
+
+
+def layer_fwd_workspace_size(B, T, H, M, d, dtype_code) -> int:
+    return int(lib().sa_layer_fwd_workspace_size(B, T, H, M, d, dtype_code))
+
+
+def layer_bwd_workspace_size(B, T, H, M, d, dtype_code, R) -> int:
+    return int(lib().sa_layer_bwd_workspace_size(B, T, H, M, d, dtype_code, R))
+
+
+def _layer_inputs(X, P, Wq, Wk, offsets):
+    import torch
+    T, H, d = X.shape
+    M = P.shape[1]
+    B = offsets.shape[0] - 1
+    dev = X.device
+    _require(X, "X", (T, H, d), X.dtype, dev)
+    _require(P, "P", (H, M, d), X.dtype, dev)
+    _require(Wq, "Wq", (H, d, d), X.dtype, dev)
+    _require(Wk, "Wk", (H, d, d), X.dtype, dev)
+    _require(offsets, "offsets", (B + 1,), torch.int64, dev)
+    return B, T, H, M, d, dev, _dtype_code(X)
+
+
+def layer_fwd(X, P, Wq, Wk, offsets, scale: Optional[float] = None, sketch=None, lse=None,
+              want_lse: bool = True, workspace=None, stream=None):
+    """sa_layer_fwd on torch tensors: one SA layer with its projections (K = X W_K,
+    Q = P W_Q, the history X aggregated).  Returns (sketch [B,H,M,d] fp32, lse [T,H] or None)."""
+    import torch
+    B, T, H, M, d, dev, code = _layer_inputs(X, P, Wq, Wk, offsets)
+    if scale is None:
+        scale = 1.0 / math.sqrt(d)
+    if sketch is None:
+        sketch = torch.empty((B, H, M, d), dtype=torch.float32, device=dev)
+    _require(sketch, "sketch", (B, H, M, d), torch.float32, dev)
+    if lse is None and want_lse:
+        lse = torch.empty((T, H), dtype=torch.float32, device=dev)
+    if lse is not None:
+        _require(lse, "lse", (T, H), torch.float32, dev)
+    ws, nbytes = _workspace(layer_fwd_workspace_size(B, T, H, M, d, code), dev, workspace)
+    rc = lib().sa_layer_fwd(_ptr(X), _ptr(P), _ptr(Wq), _ptr(Wk), _ptr(offsets), B, T, H, M, d,
+                            float(scale), code, _ptr(sketch), _ptr(lse), _ptr(ws), nbytes,
+                            _stream_handle(stream))
+    _check(rc)
+    return sketch, lse
+
+
+def layer_bwd(X, P, Wq, Wk, offsets, dsketch, lse, scale: Optional[float] = None, workspace=None,
+              stream=None) -> Tuple:
+    """sa_layer_bwd on torch tensors.  dsketch: [B,R,H,M,d].  Returns (dX, dP, dWq, dWk), fp32."""
+    import torch
+    B, T, H, M, d, dev, code = _layer_inputs(X, P, Wq, Wk, offsets)
+    R = dsketch.shape[1]
+    _require(dsketch, "dsketch", (B, R, H, M, d), torch.float32, dev)
+    _require(lse, "lse", (T, H), torch.float32, dev)
+    if scale is None:
+        scale = 1.0 / math.sqrt(d)
+    dX = torch.empty((T, H, d), dtype=torch.float32, device=dev)
+    dP = torch.empty((H, M, d), dtype=torch.float32, device=dev)
+    dWq = torch.empty((H, d, d), dtype=torch.float32, device=dev)
+    dWk = torch.empty((H, d, d), dtype=torch.float32, device=dev)
+    ws, nbytes = _workspace(layer_bwd_workspace_size(B, T, H, M, d, code, R), dev, workspace)
+    rc = lib().sa_layer_bwd(_ptr(X), _ptr(P), _ptr(Wq), _ptr(Wk), _ptr(offsets), B, T, H, M, d,
+                            float(scale), code, _ptr(dsketch), R, _ptr(lse), _ptr(dX), _ptr(dP),
+                            _ptr(dWq), _ptr(dWk), _ptr(ws), nbytes, _stream_handle(stream))
+    _check(rc)
+    return dX, dP, dWq, dWk
 
 
 def profile_enable(on: bool = True) -> None:

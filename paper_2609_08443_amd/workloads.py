@@ -26,6 +26,10 @@ Tensor layouts (token-major, packed, no padding):
   P        [H, M, d]     shared by all users
   offsets  [B + 1] int64 CSR offsets, offsets[0] = 0, offsets[B] = T
   dsketch  [B, R, H, M, d] fp32
+
+For the SA layer with its projections the history X is the V stream and the
+projections W_Q, W_K [H, d, d] ~ N(0, 1/d), so that K = X W_K and Q = P W_Q have
+the statistics of the K and P above.
 """
 
 from __future__ import annotations
@@ -39,6 +43,7 @@ import numpy as np
 
 # tensor ids of the per-(seed, tensor, user) streams
 TID_LENGTHS, TID_K, TID_V, TID_P, TID_DSKETCH = 0, 1, 2, 3, 4
+TID_WQ, TID_WK = 5, 6
 
 BASE_SEED = 8443
 
@@ -181,6 +186,27 @@ def host_prototypes(w: Workload) -> np.ndarray:
                    w.dtype)
 
 
+def host_projections(w: Workload) -> dict:
+    """W_Q, W_K [H, d, d] of the SA layer (exact bf16 values in bf16 mode)."""
+    sd = 1.0 / math.sqrt(w.d)
+    return {"Wq": _finish(_normal(w.seed, TID_WQ, 0, (w.H, w.d, w.d), sd), w.dtype),
+            "Wk": _finish(_normal(w.seed, TID_WK, 0, (w.H, w.d, w.d), sd), w.dtype)}
+
+
+def device_projections(w: Workload, device="cuda") -> dict:
+    """W_Q, W_K on the device (torch Philox, as device_tensors)."""
+    import torch
+
+    tdt = torch.bfloat16 if w.dtype == "bf16" else torch.float32
+    g = torch.Generator(device=device)
+    out = {}
+    for name, tid in (("Wq", TID_WQ), ("Wk", TID_WK)):
+        g.manual_seed(_torch_seed(w.seed, tid, 0))
+        out[name] = (torch.randn((w.H, w.d, w.d), generator=g, device=device, dtype=torch.float32)
+                     / math.sqrt(w.d)).to(tdt)
+    return out
+
+
 def host_dsketch_user(w: Workload, b: int) -> np.ndarray:
     return _normal(w.seed, TID_DSKETCH, b, (w.R, w.H, w.M, w.d))
 
@@ -273,7 +299,7 @@ def to_device(host: dict, dtype: str, device="cuda") -> dict:
 
     out = {}
     for k, v in host.items():
-        if k in ("K", "V", "P") and dtype == "bf16":
+        if k in ("K", "V", "X", "P", "Wq", "Wk") and dtype == "bf16":
             bits = f32_to_bf16_bits(v).view(np.int16)
             out[k] = torch.from_numpy(bits.copy()).to(device).view(torch.bfloat16)
         else:

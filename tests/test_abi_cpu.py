@@ -106,3 +106,46 @@ def test_reference_worklist_covers_every_token_once(offsets, T, H, C):
     assert len(items) <= n_ranges + H * (len(offsets) - 1)
     for (b, h, t0, t1, r, split, first, _) in items:
         assert t1 > t0 and r * C <= h * T + t0 and h * T + t1 <= (r + 1) * C
+
+
+def test_layer_fwd_rejects_bad_arguments():
+    L = sa.lib()
+    p = 1 << 12
+    args = dict(X=p, P=p, Wq=p, Wk=p, off=p, B=2, T=10, H=1, M=128, d=64, scale=0.125, dtype=0,
+                sketch=p, lse=NULL, ws=NULL, wsb=0)
+
+    def call(**kw):
+        a = dict(args, **kw)
+        return L.sa_layer_fwd(a["X"], a["P"], a["Wq"], a["Wk"], a["off"], a["B"], a["T"], a["H"],
+                              a["M"], a["d"], a["scale"], a["dtype"], a["sketch"], a["lse"], a["ws"],
+                              a["wsb"], None)
+    for name in ("X", "P", "Wq", "Wk", "off", "sketch"):
+        assert call(**{name: NULL}) == 1, name
+    assert call(Wk=p + 2) == 1
+    assert call(d=96) == 2
+    assert call(B=0, X=NULL, P=NULL) == 0
+    need = sa.layer_fwd_workspace_size(2, 10, 1, 128, 64, 0)
+    # at least Q (fp32) and P' (bf16) on top of the sketching workspace
+    assert need >= sa.fwd_workspace_size(2, 10, 1, 128, 64, 0) + 128 * 64 * 6
+    assert call() == 3
+    assert call(ws=1 << 20, wsb=need - 1) == 3
+
+
+def test_layer_bwd_rejects_bad_arguments():
+    L = sa.lib()
+    p = 1 << 12
+    args = dict(X=p, P=p, Wq=p, Wk=p, off=p, B=2, T=10, H=1, M=128, d=64, scale=0.125, dtype=0,
+                ds=p, R=1, lse=p, dX=p, dP=p, dWq=p, dWk=p, ws=NULL, wsb=0)
+
+    def call(**kw):
+        a = dict(args, **kw)
+        return L.sa_layer_bwd(a["X"], a["P"], a["Wq"], a["Wk"], a["off"], a["B"], a["T"], a["H"],
+                              a["M"], a["d"], a["scale"], a["dtype"], a["ds"], a["R"], a["lse"],
+                              a["dX"], a["dP"], a["dWq"], a["dWk"], a["ws"], a["wsb"], None)
+    assert call(R=0) == 1
+    for name in ("X", "P", "Wq", "Wk", "ds", "lse", "dX", "dP", "dWq", "dWk"):
+        assert call(**{name: NULL}) == 1, name
+    assert call(dWq=p + 4) == 1
+    assert call(d=80) == 2
+    assert call() == 3
+    assert sa.layer_bwd_workspace_size(2, 10, 1, 128, 64, 0, 1) > sa.bwd_workspace_size(2, 10, 1, 128, 64, 0, 1)
