@@ -161,8 +161,8 @@ def main(argv=None) -> int:
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="c5", choices=sorted(WORKLOADS))
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--no-tokenwise", action="store_true",
-                    help="skip the timing of the token-wise normalised variant")
+    ap.add_argument("--no-variants", action="store_true",
+                    help="skip the timings of the token-wise variant and of the SA layer")
     ap.add_argument("--cpu-tokens", type=int, default=300000,
                     help="tokens of the CPU-baseline sample (shortest users first)")
     ap.add_argument("--copy-calibration", action="store_true",
@@ -256,10 +256,30 @@ def main(argv=None) -> int:
                 "algorithmic_flops_per_launch": fl, "algorithmic_bytes_per_launch": by,
                 "executed_mfma_tflops": fl_exec / (avg_ms * 1e-3) / 1e12 if fl_exec else None}
 
+    def timed(fn):
+        """ms per call of fn over the timed steps, and the library's per-kernel times."""
+        for _ in range(args.warmup):
+            fn()
+        torch.cuda.synchronize()
+        sa.kernel_times()
+        sa.profile_enable(True)
+        t0 = torch.cuda.Event(enable_timing=True)
+        t1 = torch.cuda.Event(enable_timing=True)
+        t0.record(stream)
+        for _ in range(args.steps):
+            fn()
+        t1.record(stream)
+        torch.cuda.synchronize()
+        sa.profile_enable(False)
+        return t0.elapsed_time(t1) / args.steps, sa.kernel_times()
+
+    def kernel_dict(kd):
+        return {n: {"launches": c, "avg_ms": tot / c} for n, (c, tot) in kd.items()}
+
     # token-wise normalised variant (the paper's comparison normalisation), timed on
     # the same batch after the step; not part of the step
     tokenwise = None
-    if w.dtype == "bf16" and not args.no_tokenwise:
+    if w.dtype == "bf16" and not args.no_variants:
         sk_tw = torch.empty((B, H, M, d), dtype=torch.float32, device="cuda")
         lse_tw = torch.empty((B, H, M), dtype=torch.float32, device="cuda")
         ws_tw = torch.empty(max(sa.tokenwise_workspace_size(B, T, H, M, d, code), 1), dtype=torch.uint8,
@@ -268,27 +288,36 @@ def main(argv=None) -> int:
         def tw():
             sa.sketch_fwd_tokenwise(dev["K"], dev["V"], dev["P"], dev["offsets"], w.scale, sketch=sk_tw,
                                     lse_m=lse_tw, workspace=ws_tw)
-        for _ in range(args.warmup):
-            tw()
-        torch.cuda.synchronize()
-        sa.kernel_times()
-        sa.profile_enable(True)
-        t0 = torch.cuda.Event(enable_timing=True)
-        t1 = torch.cuda.Event(enable_timing=True)
-        t0.record(stream)
-        for _ in range(args.steps):
-            tw()
-        t1.record(stream)
-        torch.cuda.synchronize()
-        sa.profile_enable(False)
-        ktw = sa.kernel_times()
-        tw_ms = t0.elapsed_time(t1) / args.steps
+        tw_ms, ktw = timed(tw)
+        del sk_tw, lse_tw, ws_tw
         main_ms = ktw["tokenwise_fwd"][1] / ktw["tokenwise_fwd"][0] if "tokenwise_fwd" in ktw else None
-        tokenwise = {"tokens_per_s": T / (tw_ms * 1e-3), "ms": tw_ms,
-                     "kernels": {n: {"launches": c, "avg_ms": tot / c} for n, (c, tot) in ktw.items()},
+        tokenwise = {"tokens_per_s": T / (tw_ms * 1e-3), "ms": tw_ms, "kernels": kernel_dict(ktw),
                      "mfma_util": fwd_algorithmic_flops(w) / (tw_ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS,
                      "kernel_mfma_frac": (fwd_algorithmic_flops(w) / (main_ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS
                                           if main_ms else None)}
+
+    # SA layer with its projections (K = X W_K, Q = P W_Q, X aggregated) on the same
+    # batch, X = the V tensor: fwd (+ bwd) per step; not part of the step
+    layer = None
+    if not args.no_variants:
+        proj = wl.device_projections(w, "cuda")
+        X = dev["V"]
+        ws_lf = torch.empty(max(sa.layer_fwd_workspace_size(B, T, H, M, d, code), 1), dtype=torch.uint8,
+                            device="cuda")
+        if w.bwd:
+            ws_lb = torch.empty(max(sa.layer_bwd_workspace_size(B, T, H, M, d, code, R), 1),
+                                dtype=torch.uint8, device="cuda")
+
+        def lay():
+            sa.layer_fwd(X, dev["P"], proj["Wq"], proj["Wk"], dev["offsets"], w.scale, sketch=sketch,
+                         lse=lse, workspace=ws_lf)
+            if w.bwd:
+                sa.layer_bwd(X, dev["P"], proj["Wq"], proj["Wk"], dev["offsets"], dev["dsketch"], lse,
+                             w.scale, workspace=ws_lb)
+        ly_ms, kly = timed(lay)
+        layer = {"tokens_per_s": T / (ly_ms * 1e-3), "ms": ly_ms, "kernels": kernel_dict(kly),
+                 "step": "sa_layer_fwd + sa_layer_bwd" if w.bwd else "sa_layer_fwd",
+                 "mfma_util": flops_step / (ly_ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS}
 
     out = {
         "metric": METRIC,
@@ -314,6 +343,7 @@ def main(argv=None) -> int:
         "kernels": kernels,
         "roofline": roof,
         "tokenwise_fwd": tokenwise,
+        "layer": layer,
         "cpu_baseline": None,
     }
     if not args.no_cpu_baseline:

@@ -44,30 +44,47 @@ __device__ inline void store_el<uint16_t>(uint16_t* p, int64_t i, float v) { p[i
 // C[h][r][c] = sum_k A[h](r, k) B[h](k, c) for r < R, c < N, k < Kd, with
 // A(r, k) = A[h * a_h + r * a_r + k * a_k] and B(k, c) = B[h * b_h + k * b_k + c * b_c];
 // C row-major [R][N] per head.  A 32 x 32 output tile per workgroup of 256
-// threads; k advances in slabs of 32 staged in LDS.
+// threads; k advances in slabs of 32 staged in LDS, the next slab's loads in
+// flight (registers) while the current one is used.  Consecutive lanes walk the
+// unit-stride index of each operand so that its loads coalesce.
 template <typename TA, typename TB, typename TC>
 __global__ __launch_bounds__(256) void small_gemm_kernel(const TA* __restrict__ A, int64_t a_h, int64_t a_r,
                                                          int64_t a_k, const TB* __restrict__ Bm, int64_t b_h,
                                                          int64_t b_k, int64_t b_c, TC* __restrict__ C,
                                                          int32_t R, int32_t N, int32_t Kd) {
-    __shared__ float As[32][33];
-    __shared__ float Bs[32][33];
+    __shared__ float As[32][33];   // [r][k]
+    __shared__ float Bs[32][33];   // [k][c]
     const int tid = threadIdx.x, tx = tid & 31, ty = tid >> 5;
     const int r0 = blockIdx.x * 32, c0 = blockIdx.y * 32;
     const int64_t h = blockIdx.z;
     const TA* Ah = A + h * a_h;
     const TB* Bh = Bm + h * b_h;
+    const bool a_rows_fast = a_r == 1 && a_k != 1;   // lanes along r
+    const bool b_k_fast = b_k == 1 && b_c != 1;      // lanes along k
+    float ra[4], rb[4];
+    auto fetch = [&](int k0) {
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const int u = ty + 8 * i;
+            const int ar = a_rows_fast ? tx : u, ak = a_rows_fast ? u : tx;
+            const int r = r0 + ar, k = k0 + ak;
+            ra[i] = (r < R && k < Kd) ? load_el(Ah, (int64_t)r * a_r + (int64_t)k * a_k) : 0.f;
+            const int bk = b_k_fast ? tx : u, bc = b_k_fast ? u : tx;
+            const int kb = k0 + bk, c = c0 + bc;
+            rb[i] = (kb < Kd && c < N) ? load_el(Bh, (int64_t)kb * b_k + (int64_t)c * b_c) : 0.f;
+        }
+    };
     float acc[4] = {0.f, 0.f, 0.f, 0.f};
+    fetch(0);
     for (int k0 = 0; k0 < Kd; k0 += 32) {
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-            const int rr = ty + 8 * i;   // tile row (A) or tile k (B)
-            const int r = r0 + rr, k = k0 + tx;
-            As[rr][tx] = (r < R && k < Kd) ? load_el(Ah, (int64_t)r * a_r + (int64_t)k * a_k) : 0.f;
-            const int kb = k0 + rr, c = c0 + tx;
-            Bs[rr][tx] = (kb < Kd && c < N) ? load_el(Bh, (int64_t)kb * b_k + (int64_t)c * b_c) : 0.f;
+            const int u = ty + 8 * i;
+            if (a_rows_fast) As[tx][u] = ra[i]; else As[u][tx] = ra[i];
+            if (b_k_fast) Bs[tx][u] = rb[i]; else Bs[u][tx] = rb[i];
         }
         __syncthreads();
+        if (k0 + 32 < Kd) fetch(k0 + 32);
 #pragma unroll 8
         for (int kk = 0; kk < 32; ++kk) {
             const float b = Bs[kk][tx];
