@@ -44,6 +44,24 @@ using namespace tile;
 __device__ inline void prio_up(const bf16x8& a) { asm volatile("s_setprio 1" :: "v"(a)); }
 __device__ inline void prio_down(f32x16& a) { asm volatile("s_setprio 0" : "+v"(a)); }
 
+// Scheduling groups (sched_group_barrier masks: 0x008 MFMA, 0x002 VALU, 0x100
+// LDS read).  N copies of {one MFMA, R LDS reads, V VALU instructions}: the
+// MFMAs of one chain alternate with the independent VALU work of the previous
+// block, and the operand reads run ahead of the MFMAs that take them.
+template <int N, int R, int V>
+__device__ inline void sched_mfma_ds_valu() {
+    if constexpr (N > 0) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+        if constexpr (R > 0) __builtin_amdgcn_sched_group_barrier(0x100, R, 0);
+        if constexpr (V > 0) __builtin_amdgcn_sched_group_barrier(0x002, V, 0);
+        sched_mfma_ds_valu<N - 1, R, V>();
+    }
+}
+template <int R>
+__device__ inline void sched_ds() {
+    __builtin_amdgcn_sched_group_barrier(0x100, R, 0);
+}
+
 __device__ inline float xhalf_sum(float v) {
     const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
     return __uint_as_float(r[0]) + __uint_as_float(r[1]);
@@ -122,9 +140,15 @@ struct TokCfg {
     static constexpr int JT = D / 32;
     static constexpr int KCH = D / 8;                  // 16-byte chunks per row
     static constexpr int BLK = 32 * D;                 // bf16 elements of one 32-row block
-    // LDS: two buffers of {Pmj, Pjm, Ymj, Yjm} prototype blocks
+    // LDS: three stages of {Pmj, Pjm, Ymj, Yjm} prototype blocks (block mb + 1 is
+    // resident while mb is consumed and mb + 2 is in flight)
     static constexpr int BUF = 4 * BLK;
-    static constexpr int LDS = 2 * BUF * 2;
+    static constexpr int STAGES = 3;
+    // per wave: one [32 tokens][32 columns] fp32 slice of an output, rows padded
+    static constexpr int ROWF = 36;
+    static constexpr int STG_FLOATS = 32 * ROWF;
+    static constexpr int OFF_STG = STAGES * BUF * 2;   // bytes
+    static constexpr int LDS = OFF_STG + NW * STG_FLOATS * 4;
     static constexpr int CHUNKS = BLK / 8;             // 16-byte chunks of one block
 };
 
@@ -159,199 +183,295 @@ __global__ __launch_bounds__(NW * 64, 8 / NW) void bwd_token_kernel(TokArgs a) {
     uint16_t* lds = reinterpret_cast<uint16_t*>(smem);
     const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
     const int l32 = lane & 31, hl = lane >> 5;
+    float* stg = reinterpret_cast<float*>(smem + C::OFF_STG) + w * C::STG_FLOATS;
 
     const int64_t range = xcd_range(blockIdx.x, gridDim.x);
     const int64_t k0 = a.wg_start[range], k1 = a.wg_start[range + 1];
     if (k0 < 0 || k1 < k0 || k1 > a.max_items) return;
     const float ks2 = a.scale * kLog2e;
-    const int nblk = a.M / 32;
+    const int nblk = a.M / 32;   // >= 4
     const int64_t MD = (int64_t)a.M * D;
 
-    // The workgroup's first token block is shortened by (range % 4) quarter blocks:
-    // workgroups then reach their HBM phases (K/V loads, dV/dK stores) at staggered
-    // times, overlapping other workgroups' matrix work, instead of all at once.
-    int first_cut = (int)(range % 4) * (C::TB / 4);
-    for (int64_t k = k0; k < k1; ++k) {
-        const int32_t* it = a.items + k * IT_WORDS;
-        const int b = it[IT_B], h = it[IT_H], t0 = it[IT_T0], t1 = it[IT_T1];
-        if (b < 0 || b >= a.B || h < 0 || h >= a.H || t0 < 0 || t1 < t0 || t1 > a.T) continue;
-        const uint16_t* Pmj_g = a.P + (int64_t)h * MD;
-        const uint16_t* Pjm_g = a.Pjm + (int64_t)h * MD;
-        const uint16_t* Ymj_g = a.Ymj + ((int64_t)b * a.H + h) * MD;
-        const uint16_t* Yjm_g = a.Yjm + ((int64_t)b * a.H + h) * MD;
+    // Token blocks of the workgroup's segments, in order.  The first one is
+    // shortened by (range % 4) quarter blocks, so that workgroups reach their HBM
+    // phases (K/V loads, dV/dK stores) at staggered times.
+    struct Blk {
+        int64_t k;
+        int b, h, t1, tb, te;
+    };
+    auto first_from = [&](int64_t k, int cut, Blk& o) -> bool {
+        for (; k < k1; ++k) {
+            const int32_t* it = a.items + k * IT_WORDS;
+            const int b = it[IT_B], h = it[IT_H], t0 = it[IT_T0], t1 = it[IT_T1];
+            if (b < 0 || b >= a.B || h < 0 || h >= a.H || t0 < 0 || t1 <= t0 || t1 > a.T) continue;
+            o.k = k; o.b = b; o.h = h; o.t1 = t1; o.tb = t0;
+            o.te = t0 + C::TB - cut < t1 ? t0 + C::TB - cut : t1;
+            return true;
+        }
+        return false;
+    };
+    auto next_of = [&](const Blk& c, Blk& o) -> bool {
+        if (c.te < c.t1) {
+            o = c;
+            o.tb = c.te;
+            o.te = c.te + C::TB < c.t1 ? c.te + C::TB : c.t1;
+            return true;
+        }
+        return first_from(c.k + 1, 0, o);
+    };
 
-        for (int tb = t0, te = t0; tb < t1; tb = te) {
-            te = tb + C::TB - first_cut;
-            first_cut = 0;
-            if (te > t1) te = t1;
-            const int tok = tb + 32 * w + l32;   // this lane's token (column of S^T)
-            const bool tv = tok < te;
-            // K and V as B operands: lane (hl, t) holds 8 consecutive j of its token
-            bf16x8 kb[C::KS], vb[C::KS];
-            {
-                const uint16_t* kr = a.K + ((int64_t)(tv ? tok : t0) * a.H + h) * D;
-                const uint16_t* vr = a.V + ((int64_t)(tv ? tok : t0) * a.H + h) * D;
+    // K as B operands (lane (hl, t) holds 8 consecutive j of its token) and the
+    // lane's -lse * log2(e), for block c
+    bf16x8 kb[C::KS], vb[C::KS];
+    float nl = 0.f;
+    auto load_k = [&](const Blk& c) __attribute__((always_inline)) {
+        const int tok = c.tb + 32 * w + l32;
+        const bool tv = tok < c.te;
+        const int64_t row = ((int64_t)(tv ? tok : c.tb) * a.H + c.h) * D;
 #pragma unroll
-                for (int kk = 0; kk < C::KS; ++kk) {
-                    uint4 x = *reinterpret_cast<const uint4*>(kr + 16 * kk + 8 * hl);
-                    uint4 y = XV ? x : *reinterpret_cast<const uint4*>(vr + 16 * kk + 8 * hl);
-                    if (!tv) x = y = make_uint4(0, 0, 0, 0);
-                    kb[kk] = __builtin_bit_cast(bf16x8, x);
-                    vb[kk] = __builtin_bit_cast(bf16x8, y);
-                }
+        for (int kk = 0; kk < C::KS; ++kk) {
+            uint4 x = *reinterpret_cast<const uint4*>(a.K + row + 16 * kk + 8 * hl);
+            if (!tv) x = make_uint4(0, 0, 0, 0);
+            kb[kk] = __builtin_bit_cast(bf16x8, x);
+        }
+        nl = tv ? -a.lse[(int64_t)tok * a.H + c.h] * kLog2e : 0.f;
+    };
+
+    // Prototype block mb of the matrices a sweep reads, straight into LDS buffer
+    // `buf` (sweep 0: Pmj, Yjm; sweep 1: Pmj, Pjm, Ymj).  Lane l of a wave fetches
+    // the global chunk that belongs at LDS chunk position p = 64 q + l of the
+    // swizzled layout (the XOR swizzle is its own inverse).
+    auto fetch = [&](const Blk& c, int mb, int sweep, int buf) __attribute__((always_inline)) {
+        const uint16_t* Pmj_g = a.P + (int64_t)c.h * MD;
+        const uint16_t* Pjm_g = a.Pjm + (int64_t)c.h * MD;
+        const uint16_t* Ymj_g = a.Ymj + ((int64_t)c.b * a.H + c.h) * MD;
+        const uint16_t* Yjm_g = a.Yjm + ((int64_t)c.b * a.H + c.h) * MD;
+        uint16_t* L = lds + buf * C::BUF;
+        constexpr int NQ = C::CHUNKS / 64;   // wave-loads per matrix block
+        for (int q = w; q < NQ; q += NW) {
+            const int p = q * 64 + lane;
+            {   // row-major [32 prototypes][D]: Pmj, and Ymj in sweep 1
+                const int r = p / C::KCH, cc = (p % C::KCH) ^ swz_x<D>(r);
+                const int64_t src = (int64_t)(mb * 32 + r) * D + cc * 8;
+                load_lds16(Pmj_g + src, L + q * 512);
+                if (sweep == 1) load_lds16(Ymj_g + src, L + 2 * C::BLK + q * 512);
             }
-            const float nl = tv ? -a.lse[(int64_t)tok * a.H + h] * kLog2e : 0.f;
+            {   // [D][32 prototypes], prototype index permuted: Yjm or Pjm
+                const int j = p / 4, cc = (p % 4) ^ swz_x<32>(j);
+                const int64_t srcj = (int64_t)j * a.M + mb * 32 + cc * 8;
+                load_lds16((sweep == 1 ? Pjm_g : Yjm_g) + srcj, L + (sweep == 1 ? C::BLK : 3 * C::BLK) + q * 512);
+            }
+        }
+    };
+    // S^T tile of a prototype block (rows = its 32 prototypes, cols = tokens)
+    auto st_tile = [&](const uint16_t* L) {
+        f32x16 s;
+#pragma unroll
+        for (int r = 0; r < 16; ++r) s[r] = 0.f;
+#pragma unroll
+        for (int kk = 0; kk < C::KS; ++kk)
+            s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(lds_b128(L, swz<D>(l32, 2 * kk + hl)), kb[kk], s, 0, 0, 0);
+        return s;
+    };
+    // f * acc (this wave's 32 tokens of the block, columns j = 32 jt + srow(r, hl))
+    // into the rows of `out`.  The C layout holds 16-byte pieces of 32 token rows
+    // per store; each 32-column slice goes through this wave's LDS area so that
+    // every store instruction writes whole 128-byte lines of 8 tokens.
+    auto store_rows = [&](const f32x16 (&acc)[C::JT], float* out, float f, int tb, int te, int h)
+        __attribute__((always_inline)) {
+#pragma unroll
+        for (int jt = 0; jt < C::JT; ++jt) {
+#pragma unroll
+            for (int g = 0; g < 4; ++g)
+                *reinterpret_cast<float4*>(stg + l32 * C::ROWF + 8 * g + 4 * hl) =
+                    make_float4(f * acc[jt][4 * g], f * acc[jt][4 * g + 1], f * acc[jt][4 * g + 2],
+                                f * acc[jt][4 * g + 3]);
+            asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");   // the wave's own area
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                const int t = 8 * q + (lane >> 3), cc = 4 * (lane & 7);
+                const float4 v = *reinterpret_cast<const float4*>(stg + t * C::ROWF + cc);
+                const int tk = tb + 32 * w + t;
+                if (tk < te) *reinterpret_cast<float4*>(out + ((int64_t)tk * a.H + h) * D + jt * 32 + cc) = v;
+            }
+            asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");   // reads done before the next slice
+        }
+    };
 
-            // prototype block mb of the requested matrices straight into LDS buffer
-            // `buf` (sweep 0: Pmj, Yjm; sweep 1: Pmj, Pjm, Ymj).  Lane l of a wave
-            // fetches the global chunk that belongs at LDS chunk position p = 64 q + l
-            // of the swizzled layout (the XOR swizzle is its own inverse).
-            auto fetch = [&](int mb, int sweep, int buf) __attribute__((always_inline)) {
-                uint16_t* L = lds + buf * C::BUF;
-                constexpr int NQ = C::CHUNKS / 64;   // wave-loads per matrix block
-                for (int q = w; q < NQ; q += NW) {
-                    const int p = q * 64 + lane;
-                    {   // row-major [32 prototypes][D]: Pmj, and Ymj in sweep 1
-                        const int r = p / C::KCH, c = (p % C::KCH) ^ swz_x<D>(r);
-                        const int64_t src = (int64_t)(mb * 32 + r) * D + c * 8;
-                        load_lds16(Pmj_g + src, L + q * 512);
-                        if (sweep == 1) load_lds16(Ymj_g + src, L + 2 * C::BLK + q * 512);
-                    }
-                    {   // [D][32 prototypes], prototype index permuted: Yjm or Pjm
-                        const int j = p / 4, c = (p % 4) ^ swz_x<32>(j);
-                        const int64_t srcj = (int64_t)j * a.M + mb * 32 + c * 8;
-                        load_lds16((sweep == 1 ? Pjm_g : Yjm_g) + srcj, L + (sweep == 1 ? C::BLK : 3 * C::BLK) + q * 512);
-                    }
-                }
-            };
-            // S^T tile of block mb (rows = the block's 32 prototypes, cols = tokens)
-            auto st_tile = [&](const uint16_t* L) {
-                f32x16 s;
-#pragma unroll
-                for (int r = 0; r < 16; ++r) s[r] = 0.f;
-#pragma unroll
-                for (int kk = 0; kk < C::KS; ++kk)
-                    s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(lds_b128(L, swz<D>(l32, 2 * kk + hl)), kb[kk], s, 0, 0, 0);
-                return s;
-            };
+    Blk cur;
+    if (!first_from(k0, (int)(range % 4) * (C::TB / 4), cur)) return;
+    load_k(cur);
+    fetch(cur, 0, 0, 0);
+    fetch(cur, 1, 0, 1);
+    wait_vmem();
+    __syncthreads();
 
-            // ---------------- sweep 1: dV^T[j, t] = sum_m dY[m, j] A[t, m]
-            f32x16 dvt[C::JT];
+    // Per block: a stream of 2 nblk stages (sweep 1's prototype blocks, then sweep
+    // 2's) through three LDS buffers; at the block's entry its K and stages 0 and
+    // 1 are resident.
+    while (true) {
+        const int tb = cur.tb, te = cur.te, h = cur.h;
+        const int tok = tb + 32 * w + l32;   // this lane's token (column of S^T)
+        const bool tv = tok < te;
+
+        // ---------------- sweep 1: dV^T[j, t] = sum_m dY[m, j] A[t, m]
+        // The S^T tile of block mb + 1 is issued before the exponentials of block
+        // mb, so the matrix core works through them while the VALU runs; the
+        // scheduling groups interleave the two instruction streams.
+        f32x16 dvt[C::JT];
 #pragma unroll
-            for (int jt = 0; jt < C::JT; ++jt)
+        for (int jt = 0; jt < C::JT; ++jt)
 #pragma unroll
-                for (int r = 0; r < 16; ++r) dvt[jt][r] = 0.f;
-            __syncthreads();  // previous users of the buffers are done
-            fetch(0, 0, 0);
-            wait_vmem();
+            for (int r = 0; r < 16; ++r) dvt[jt][r] = 0.f;
+        f32x16 s_next = st_tile(lds);
+        for (int mb = 0, bc = 0; mb < nblk; ++mb, bc = bc == 2 ? 0 : bc + 1) {
+            const int bn = bc == 2 ? 0 : bc + 1, bnn = bn == 2 ? 0 : bn + 1;
+            const uint16_t* L = lds + bc * C::BUF;
+            if (mb + 2 < nblk) fetch(cur, mb + 2, 0, bnn);
+            else fetch(cur, mb + 2 - nblk, 1, bnn);
+            const f32x16 s = s_next;
+            s_next = st_tile(lds + (mb + 1 < nblk ? bn : bc) * C::BUF);   // last block: unused
+            float e[16];
+#pragma unroll
+            for (int r = 0; r < 16; ++r) e[r] = __builtin_amdgcn_exp2f(__builtin_fmaf(s[r], ks2, nl));
+            const bf16x8 ab0 = pack8(e), ab1 = pack8(e + 8);
+#pragma unroll
+            for (int jt = 0; jt < C::JT; ++jt) {
+                const uint16_t* Y = L + 3 * C::BLK;
+                dvt[jt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(lds_b128(Y, swz<32>(jt * 32 + l32, 0 + hl)), ab0, dvt[jt], 0, 0, 0);
+                dvt[jt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(lds_b128(Y, swz<32>(jt * 32 + l32, 2 + hl)), ab1, dvt[jt], 0, 0, 0);
+            }
+            // S^T(mb + 1) with the exponentials of mb, then dV(mb)
+            sched_ds<2>();
+            sched_mfma_ds_valu<C::KS, 1, 40 / C::KS>();
+            sched_mfma_ds_valu<2 * C::JT, 1, 0>();
+            wait_vmem();   // stage mb + 2 has landed in LDS
             __syncthreads();
-            for (int mb = 0; mb < nblk; ++mb) {
-                const uint16_t* L = lds + (mb & 1) * C::BUF;
-                if (mb + 1 < nblk) fetch(mb + 1, 0, (mb + 1) & 1);
-                prio_up(kb[0]);
-                f32x16 s = st_tile(L);
-                prio_down(s);
-                float e[16];
+        }
 #pragma unroll
-                for (int r = 0; r < 16; ++r) e[r] = __builtin_amdgcn_exp2f(__builtin_fmaf(s[r], ks2, nl));
-                const bf16x8 ab0 = pack8(e), ab1 = pack8(e + 8);
-                prio_up(ab1);
-#pragma unroll
-                for (int jt = 0; jt < C::JT; ++jt) {
-                    const uint16_t* Y = L + 3 * C::BLK;
-                    dvt[jt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(lds_b128(Y, swz<32>(jt * 32 + l32, 0 + hl)), ab0, dvt[jt], 0, 0, 0);
-                    dvt[jt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(lds_b128(Y, swz<32>(jt * 32 + l32, 2 + hl)), ab1, dvt[jt], 0, 0, 0);
-                }
-                prio_down(dvt[C::JT - 1]);
-                wait_vmem();   // block mb + 1 has landed in LDS
-                __syncthreads();
+        for (int kk = 0; kk < C::KS; ++kk) {
+            if constexpr (XV) {
+                vb[kk] = kb[kk];
+            } else {
+                const int64_t row = ((int64_t)(tv ? tok : tb) * a.H + h) * D;
+                uint4 y = *reinterpret_cast<const uint4*>(a.V + row + 16 * kk + 8 * hl);
+                if (!tv) y = make_uint4(0, 0, 0, 0);
+                vb[kk] = __builtin_bit_cast(bf16x8, y);
             }
-            // D_t = <V_t, dV_t>: this lane holds dV[t, j] for j = jt*32 + srow(r, hl)
-            float Dt = 0.f;
-            {
-                const uint16_t* vr = a.V + ((int64_t)(tv ? tok : t0) * a.H + h) * D;
+        }
+        // D_t = <V_t, dV_t>.  This lane holds dV[t, j] for j = 32 jt + 8 g + 4 hl + e
+        // (e < 4) and V[t, j] for j = 16 kk + 8 hl + 0..7.  Swapping dwords 0-1
+        // of the upper half with dwords 2-3 of the lower half gives both halves
+        // V at j = 16 kk + 4 hl + 0..3 (dwords 0-1) and 16 kk + 8 + 4 hl + 0..3
+        // (dwords 2-3): with kk = 2 jt + g / 2, the columns of dV registers 4 g..4 g + 3.
+        float Dt = 0.f;
 #pragma unroll
-                for (int jt = 0; jt < C::JT; ++jt)
+        for (int kk = 0; kk < C::KS; ++kk) {
+            const u32x4 v = __builtin_bit_cast(u32x4, vb[kk]);
+            const auto p0 = __builtin_amdgcn_permlane32_swap(v[0], v[2], false, false);
+            const auto p1 = __builtin_amdgcn_permlane32_swap(v[1], v[3], false, false);
+            const uint32_t q[2][2] = {{p0[0], p1[0]}, {p0[1], p1[1]}};
 #pragma unroll
-                    for (int g = 0; g < 4; ++g) {
-                        const uint2 v4 = *reinterpret_cast<const uint2*>(vr + jt * 32 + 8 * g + 4 * hl);
-                        Dt = __builtin_fmaf(bf16_lo(v4.x), dvt[jt][4 * g + 0], Dt);
-                        Dt = __builtin_fmaf(bf16_hi(v4.x), dvt[jt][4 * g + 1], Dt);
-                        Dt = __builtin_fmaf(bf16_lo(v4.y), dvt[jt][4 * g + 2], Dt);
-                        Dt = __builtin_fmaf(bf16_hi(v4.y), dvt[jt][4 * g + 3], Dt);
-                    }
-                Dt = tv ? xhalf_sum(Dt) : 0.f;
+            for (int sh = 0; sh < 2; ++sh) {
+                const int jt = kk >> 1, g = 2 * (kk & 1) + sh;
+                Dt = __builtin_fmaf(bf16_lo(q[sh][0]), dvt[jt][4 * g + 0], Dt);
+                Dt = __builtin_fmaf(bf16_hi(q[sh][0]), dvt[jt][4 * g + 1], Dt);
+                Dt = __builtin_fmaf(bf16_lo(q[sh][1]), dvt[jt][4 * g + 2], Dt);
+                Dt = __builtin_fmaf(bf16_hi(q[sh][1]), dvt[jt][4 * g + 3], Dt);
             }
-            // write dV now (frees its registers)
-            if (tv) {
-                if constexpr (!XV) {
-                    float* out = a.dV + ((int64_t)tok * a.H + h) * D;
-                    // registers 4g..4g+3 hold 4 consecutive columns: 16-byte stores
-#pragma unroll
-                    for (int jt = 0; jt < C::JT; ++jt)
-#pragma unroll
-                        for (int g = 0; g < 4; ++g)
-                            *reinterpret_cast<float4*>(out + jt * 32 + 8 * g + 4 * hl) =
-                                make_float4(dvt[jt][4 * g], dvt[jt][4 * g + 1], dvt[jt][4 * g + 2], dvt[jt][4 * g + 3]);
-                }
-                if (hl == 0) a.Dbuf[(int64_t)tok * a.H + h] = Dt;
-            }
+        }
+        Dt = tv ? xhalf_sum(Dt) : 0.f;
+        if (tv && hl == 0) a.Dbuf[(int64_t)tok * a.H + h] = Dt;
+        // dV rows now (frees their registers); they drain under sweep 2's first stage
+        if constexpr (!XV) store_rows(dvt, a.dV, 1.0f, tb, te, h);
 
-            // ---------------- sweep 2: dK^T[j, t] = scale sum_m P[m, j] dS[t, m]
-            // (XV: continues from dV^T, with scale folded into the weights)
-            f32x16 dkt[C::JT];
+        // ---------------- sweep 2: dK^T[j, t] = scale sum_m P[m, j] dS[t, m]
+        // (XV: continues from dV^T, with scale folded into the weights)
+        f32x16 dkt[C::JT];
 #pragma unroll
-            for (int jt = 0; jt < C::JT; ++jt)
+        for (int jt = 0; jt < C::JT; ++jt)
 #pragma unroll
-                for (int r = 0; r < 16; ++r) dkt[jt][r] = XV ? dvt[jt][r] : 0.f;
-            const float nl2 = XV ? nl + __log2f(a.scale) : nl;
-            fetch(0, 1, 0);
-            wait_vmem();
-            __syncthreads();
-            for (int mb = 0; mb < nblk; ++mb) {
-                const uint16_t* L = lds + (mb & 1) * C::BUF;
-                if (mb + 1 < nblk) fetch(mb + 1, 1, (mb + 1) & 1);
-                prio_up(kb[0]);
-                f32x16 s = st_tile(L);
-                f32x16 da;
+            for (int r = 0; r < 16; ++r) dkt[jt][r] = XV ? dvt[jt][r] : 0.f;
+        const float nl2 = XV ? nl + __log2f(a.scale) : nl;
+        // sweep 2's block mb is stage nblk + mb: blocks 0 and 1 are resident
+        const int b0 = nblk % 3;
+        // Pipelined form: iteration mb runs the elementwise work of block mb
+        // beside the S^T MFMAs of block mb + 1, then the dK MFMAs of mb beside
+        // the dA MFMAs of mb + 1 (two independent chains).  It holds 16 more
+        // registers than the plain form, which separate K and V operands at
+        // d = 128 do not leave.
+        constexpr bool kPipe2 = XV || D == 64;
+        auto da_tile = [&](const uint16_t* Lb) {
+            f32x16 da;
 #pragma unroll
-                for (int r = 0; r < 16; ++r) da[r] = 0.f;
-                const uint16_t* Ym = L + 2 * C::BLK;
+            for (int r = 0; r < 16; ++r) da[r] = 0.f;
+            const uint16_t* Ym = Lb + 2 * C::BLK;
 #pragma unroll
-                for (int kk = 0; kk < C::KS; ++kk)
-                    da = __builtin_amdgcn_mfma_f32_32x32x16_bf16(lds_b128(Ym, swz<D>(l32, 2 * kk + hl)), vb[kk], da, 0, 0, 0);
-                prio_down(s);
-                prio_down(da);
-                float e[16];
+            for (int kk = 0; kk < C::KS; ++kk)
+                da = __builtin_amdgcn_mfma_f32_32x32x16_bf16(lds_b128(Ym, swz<D>(l32, 2 * kk + hl)), vb[kk], da, 0, 0, 0);
+            return da;
+        };
+        auto dk_acc = [&](const uint16_t* Lb, const f32x16& s, const f32x16& da) __attribute__((always_inline)) {
+            float e[16];
 #pragma unroll
-                for (int r = 0; r < 16; ++r) {
-                    const float A = __builtin_amdgcn_exp2f(__builtin_fmaf(s[r], ks2, nl2));
-                    e[r] = A * (da[r] - Dt);
-                }
-                const bf16x8 d0 = pack8(e), d1 = pack8(e + 8);
-                prio_up(d1);
-                const uint16_t* Pj = L + C::BLK;
+            for (int r = 0; r < 16; ++r) {
+                const float A = __builtin_amdgcn_exp2f(__builtin_fmaf(s[r], ks2, nl2));
+                e[r] = A * (da[r] - Dt);
+            }
+            const bf16x8 d0 = pack8(e), d1 = pack8(e + 8);
+            const uint16_t* Pj = Lb + C::BLK;
 #pragma unroll
-                for (int jt = 0; jt < C::JT; ++jt) {
-                    dkt[jt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(lds_b128(Pj, swz<32>(jt * 32 + l32, 0 + hl)), d0, dkt[jt], 0, 0, 0);
-                    dkt[jt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(lds_b128(Pj, swz<32>(jt * 32 + l32, 2 + hl)), d1, dkt[jt], 0, 0, 0);
-                }
-                prio_down(dkt[C::JT - 1]);
+            for (int jt = 0; jt < C::JT; ++jt) {
+                dkt[jt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(lds_b128(Pj, swz<32>(jt * 32 + l32, 0 + hl)), d0, dkt[jt], 0, 0, 0);
+                dkt[jt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(lds_b128(Pj, swz<32>(jt * 32 + l32, 2 + hl)), d1, dkt[jt], 0, 0, 0);
+            }
+        };
+        if constexpr (kPipe2) {
+            s_next = st_tile(lds + b0 * C::BUF);
+            f32x16 da_next = da_tile(lds + b0 * C::BUF);
+            for (int mb = 0, bc = b0; mb < nblk; ++mb, bc = bc == 2 ? 0 : bc + 1) {
+                const int bn = bc == 2 ? 0 : bc + 1, bnn = bn == 2 ? 0 : bn + 1;
+                const uint16_t* L = lds + bc * C::BUF;
+                if (mb + 2 < nblk) fetch(cur, mb + 2, 1, bnn);
+                const uint16_t* Ln = lds + (mb + 1 < nblk ? bn : bc) * C::BUF;   // last block: unused
+                const f32x16 s = s_next, da = da_next;
+                s_next = st_tile(Ln);
+                dk_acc(L, s, da);
+                da_next = da_tile(Ln);
+                sched_ds<2>();
+                sched_mfma_ds_valu<C::KS, 1, 72 / C::KS>();
+                sched_mfma_ds_valu<C::KS + 2 * C::JT, 1, 0>();
                 wait_vmem();
                 __syncthreads();
             }
-            if (tv) {
-                float* out = (XV ? a.dX : a.dK) + ((int64_t)tok * a.H + h) * D;
-                const float f = XV ? 1.0f : a.scale;
-#pragma unroll
-                for (int jt = 0; jt < C::JT; ++jt)
-#pragma unroll
-                    for (int g = 0; g < 4; ++g)
-                        *reinterpret_cast<float4*>(out + jt * 32 + 8 * g + 4 * hl) =
-                            make_float4(f * dkt[jt][4 * g], f * dkt[jt][4 * g + 1],
-                                        f * dkt[jt][4 * g + 2], f * dkt[jt][4 * g + 3]);
+        } else {
+            for (int mb = 0, bc = b0; mb < nblk; ++mb, bc = bc == 2 ? 0 : bc + 1) {
+                const int bnn = bc == 0 ? 2 : bc - 1;   // (bc + 2) % 3
+                const uint16_t* L = lds + bc * C::BUF;
+                if (mb + 2 < nblk) fetch(cur, mb + 2, 1, bnn);
+                const f32x16 da = da_tile(L);
+                const f32x16 s = st_tile(L);
+                dk_acc(L, s, da);
+                wait_vmem();
+                __syncthreads();
             }
         }
+
+        // The next block's K and its first two stages go out before this block's
+        // dK rows: the wait for them then includes no store, and the stores drain
+        // under the next block's first stage.
+        Blk nxt;
+        const bool more = next_of(cur, nxt);
+        if (more) {
+            load_k(nxt);
+            fetch(nxt, 0, 0, 0);
+            fetch(nxt, 1, 0, 1);
+            wait_vmem();
+            __syncthreads();
+        }
+        store_rows(dkt, XV ? a.dX : a.dK, XV ? 1.0f : a.scale, tb, te, h);
+        if (!more) break;
+        cur = nxt;
     }
 }
 
