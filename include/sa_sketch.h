@@ -229,6 +229,41 @@ sa_status sa_layer_bwd(const void* X, const void* P, const void* Wq, const void*
                        const float* lse, float* dX, float* dP, float* dWq, float* dWk,
                        void* workspace, size_t workspace_bytes, void* stream);
 
+/* Bytes of workspace that sa_block_fwd needs for this shape. */
+size_t sa_block_fwd_workspace_size(int64_t B, int64_t T, int32_t H, int32_t M, int32_t d,
+                                   int32_t n_layers, sa_dtype dtype);
+
+/*
+ * Forward of stacked SA (section 3.3, stacked refinement) with n_layers layers.
+ * Per user and head, starting from the shared prototypes Xt = P:
+ *
+ *   Xhat = sketch of X with queries Xt W_Q and keys X W_K   (as sa_layer_fwd; per
+ *          user prototypes from the second layer on)
+ *   Xbar = LN1(Xt + Xhat)
+ *   Xt   = LN2(Xbar + FFN(Xbar)),   FFN(x) = (silu(x W1) * (x W3)) W2
+ *
+ * with LN(x) = (x - mean) / sqrt(var + eps) * gamma + beta over the d features
+ * (biased variance) and a SwiGLU FFN of intermediate width 2d without biases.
+ *
+ *   X         [T,H,d] history; P [H,M,d] prototypes (dtype)
+ *   Wq, Wk    [n_layers,H,d,d]; W1, W3 [n_layers,H,d,2d]; W2 [n_layers,H,2d,d] (dtype)
+ *   ln        [n_layers,4,H,d]: gamma1, beta1, gamma2, beta2 (dtype)
+ *   eps       layer-norm epsilon (> 0)
+ *   out       output [B,H,M,d] fp32: the refined sketch
+ *   lse       output [n_layers,T,H] fp32 (each layer's per-token log-sum-exp), or NULL
+ *
+ * A user without tokens has a zero Xhat in every layer, so its output is the
+ * refinement of the prototypes alone.  The sketching steps run on the same
+ * kernels as sa_layer_fwd; the projections and the FFN on a batched fp32
+ * product.  Offsets, sizes, errors, ownership and streams as for sa_sketch_fwd;
+ * n_layers < 1 or a non-positive eps is SA_ERR_INVALID_ARG.
+ */
+sa_status sa_block_fwd(const void* X, const void* P, const void* Wq, const void* Wk, const void* ln,
+                       const void* W1, const void* W3, const void* W2, const int64_t* offsets,
+                       int64_t B, int64_t T, int32_t H, int32_t M, int32_t d, int32_t n_layers,
+                       float scale, float eps, sa_dtype dtype, float* out, float* lse,
+                       void* workspace, size_t workspace_bytes, void* stream);
+
 /*
  * Work list used by the fused forward, exposed for exact testing.
  *

@@ -291,10 +291,44 @@ sa_status layer_prototypes(const void* P, const void* Wq, const void* Wk, int32_
     return SA_OK;
 }
 
+// ---------------------------------------------------------------- stacked block plan
+// [state | Q | P' (input dtype) | Xhat (also the FFN output) | Xbar | gate | up |
+//  lse scratch | workspace of the sketching call]; state, Q, P', Xhat, Xbar are
+// [B,H,M,d] fp32 (P' in the input dtype), gate and up [B,H,M,2d] fp32.
+struct BlockPlan {
+    FwdPlan base;
+    size_t off_state = 0, off_q = 0, off_pp = 0, off_xhat = 0, off_xbar = 0, off_g = 0, off_u = 0, off_lse = 0,
+           off_base = 0, total = 0;
+};
+
+BlockPlan plan_block(int64_t B, int64_t T, int32_t H, int32_t M, int32_t d, sa_dtype dtype) {
+    BlockPlan p;
+    p.base = plan_fwd(B, T, H, M, d, dtype, false);
+    size_t off = 0;
+    auto carve = [&](size_t bytes) {
+        const size_t o = off;
+        off = align_up(off + bytes, 256);
+        return o;
+    };
+    const size_t rows = (size_t)B * H * M;
+    p.off_state = carve(sizeof(float) * rows * d);
+    p.off_q = carve(sizeof(float) * rows * d);
+    p.off_pp = carve((dtype == SA_BF16 ? 2 : 4) * rows * d);
+    p.off_xhat = carve(sizeof(float) * rows * d);
+    p.off_xbar = carve(sizeof(float) * rows * d);
+    p.off_g = carve(sizeof(float) * rows * 2 * d);
+    p.off_u = carve(sizeof(float) * rows * 2 * d);
+    p.off_lse = carve(sizeof(float) * (size_t)T * H);
+    p.off_base = carve(p.base.total);
+    p.total = off;
+    return p;
+}
+
 // forward on a checked plan and workspace (shared by sa_sketch_fwd and sa_layer_fwd)
 sa_status run_fwd(const void* K, const void* V, const void* P, const int64_t* offsets, int64_t B,
                   int64_t T, int32_t H, int32_t M, int32_t d, float scale, sa_dtype dtype,
-                  float* sketch, float* lse, uint8_t* ws, const FwdPlan& plan, hipStream_t stream) {
+                  float* sketch, float* lse, uint8_t* ws, const FwdPlan& plan, hipStream_t stream,
+                  bool p_user) {
     hipError_t e;
     if (plan.fused) {
         int32_t* items = reinterpret_cast<int32_t*>(ws + plan.off_items);
@@ -325,6 +359,7 @@ sa_status run_fwd(const void* K, const void* V, const void* P, const int64_t* of
         a.sketch = sketch;
         a.lse = lse;
         a.partials = partials;
+        a.p_user = p_user;
         {
             sa::ProfScope ps("fused_fwd", stream);
             e = sa::launch_fused_fwd(a, stream);
@@ -342,7 +377,7 @@ sa_status run_fwd(const void* K, const void* V, const void* P, const int64_t* of
     {
         sa::ProfScope ps("plain_fwd", stream);
         e = sa::launch_generic_fwd(K, V, P, offsets, B, T, H, M, d, scale, dtype == SA_BF16,
-                                   sketch, lse_out, stream);
+                                   sketch, lse_out, stream, p_user);
     }
     if (e != hipSuccess) return hip_fail(e, "fp32 forward launch");
     return SA_OK;
@@ -493,7 +528,7 @@ sa_status sa_sketch_fwd(const void* K, const void* V, const void* P, const int64
         if (st != SA_OK) return st;
     }
     return run_fwd(K, V, P, offsets, B, T, H, M, d, scale, dtype, sketch, lse,
-                   reinterpret_cast<uint8_t*>(workspace), plan, stream);
+                   reinterpret_cast<uint8_t*>(workspace), plan, stream, false);
 }
 
 size_t sa_sketch_fwd_tokenwise_workspace_size(int64_t B, int64_t T, int32_t H, int32_t M,
@@ -634,7 +669,7 @@ sa_status sa_layer_fwd(const void* X, const void* P, const void* Wq, const void*
     st = layer_prototypes(P, Wq, Wk, H, M, d, dtype, Q, Pp, stream);
     if (st != SA_OK) return st;
     return run_fwd(X, X, Pp, offsets, B, T, H, M, d, scale, dtype, sketch, lse, ws + plan.off_base,
-                   base, stream);
+                   base, stream, false);
 }
 
 size_t sa_layer_bwd_workspace_size(int64_t B, int64_t T, int32_t H, int32_t M, int32_t d,
@@ -694,6 +729,99 @@ sa_status sa_layer_bwd(const void* X, const void* P, const void* Wq, const void*
     if (e == hipSuccess)
         e = sa::launch_small_gemm({dQ, false, md, d, 1}, {Wq, bf, dd, 1, d}, dP, false, H, M, d, d, stream);
     if (e != hipSuccess) return hip_fail(e, "projection gradient launch");
+    return SA_OK;
+}
+
+size_t sa_block_fwd_workspace_size(int64_t B, int64_t T, int32_t H, int32_t M, int32_t d,
+                                   int32_t n_layers, sa_dtype dtype) {
+    if (check_common(B, T, H, M, d, 1.0f, dtype) != SA_OK || n_layers < 1) return 0;
+    return plan_block(B, T, H, M, d, dtype).total;
+}
+
+sa_status sa_block_fwd(const void* X, const void* P, const void* Wq, const void* Wk, const void* ln,
+                       const void* W1, const void* W3, const void* W2, const int64_t* offsets, int64_t B,
+                       int64_t T, int32_t H, int32_t M, int32_t d, int32_t n_layers, float scale, float eps,
+                       sa_dtype dtype, float* out, float* lse, void* workspace, size_t workspace_bytes,
+                       void* stream_) {
+    g_last_error[0] = 0;
+    sa_status st = check_common(B, T, H, M, d, scale, dtype);
+    if (st != SA_OK) return st;
+    if (n_layers < 1) return fail(SA_ERR_INVALID_ARG, "n_layers must be >= 1 (got %d)", n_layers);
+    if (!(std::isfinite(eps) && eps > 0.f)) return fail(SA_ERR_INVALID_ARG, "eps must be finite and > 0");
+    if (B == 0) return SA_OK;
+    if (!offsets || !out || !P || !Wq || !Wk || !ln || !W1 || !W3 || !W2 || (T > 0 && !X))
+        return fail(SA_ERR_INVALID_ARG, "null pointer argument");
+    if (!aligned16(X) || !aligned16(P) || !aligned16(Wq) || !aligned16(Wk) || !aligned16(ln) || !aligned16(W1) ||
+        !aligned16(W3) || !aligned16(W2) || !aligned16(out) || !aligned16(lse))
+        return fail(SA_ERR_INVALID_ARG, "tensor arguments must be 16-byte aligned");
+    hipStream_t stream = reinterpret_cast<hipStream_t>(stream_);
+    const BlockPlan plan = plan_block(B, T, H, M, d, dtype);
+    if (!workspace || workspace_bytes < plan.total)
+        return fail(SA_ERR_WORKSPACE, "workspace of %zu bytes needed, %zu given", plan.total,
+                    workspace ? workspace_bytes : (size_t)0);
+    if (debug_validate()) {
+        st = validate_offsets(offsets, B, T, stream);
+        if (st != SA_OK) return st;
+    }
+    uint8_t* ws = reinterpret_cast<uint8_t*>(workspace);
+    float* state = reinterpret_cast<float*>(ws + plan.off_state);
+    float* Q = reinterpret_cast<float*>(ws + plan.off_q);
+    void* Pp = ws + plan.off_pp;
+    float* Xhat = reinterpret_cast<float*>(ws + plan.off_xhat);
+    float* Xbar = reinterpret_cast<float*>(ws + plan.off_xbar);
+    float* G = reinterpret_cast<float*>(ws + plan.off_g);
+    float* U = reinterpret_cast<float*>(ws + plan.off_u);
+    const bool bf = dtype == SA_BF16;
+    const size_t el = bf ? 2 : 4;
+    const int64_t md = (int64_t)M * d, dd = (int64_t)d * d, d2 = 2 * (int64_t)d;
+    const int64_t BH = B * H, rows = BH * M;
+    hipError_t e = hipSuccess;
+    for (int32_t l = 0; l < n_layers; ++l) {
+        const bool first = l == 0;
+        const uint8_t* wq = reinterpret_cast<const uint8_t*>(Wq) + el * (size_t)l * H * dd;
+        const uint8_t* wk = reinterpret_cast<const uint8_t*>(Wk) + el * (size_t)l * H * dd;
+        const uint8_t* w1 = reinterpret_cast<const uint8_t*>(W1) + el * (size_t)l * H * d * d2;
+        const uint8_t* w3 = reinterpret_cast<const uint8_t*>(W3) + el * (size_t)l * H * d * d2;
+        const uint8_t* w2 = reinterpret_cast<const uint8_t*>(W2) + el * (size_t)l * H * d2 * d;
+        auto lnp = [&](int k) {
+            return reinterpret_cast<const uint8_t*>(ln) + el * ((size_t)(l * 4 + k) * H) * d;
+        };
+        // queries of this layer: the shared prototypes first, then each user's state
+        const int64_t nq = first ? H : BH;
+        {
+            sa::ProfScope ps("block_proj", stream);
+            const sa::MatView xt = first ? sa::MatView{P, bf, md, d, 1} : sa::MatView{state, false, md, d, 1};
+            e = sa::launch_small_gemm(xt, {wq, bf, dd, d, 1}, Q, false, (int32_t)nq, M, d, d, stream, H);
+            if (e == hipSuccess)
+                e = sa::launch_small_gemm({Q, false, md, d, 1}, {wk, bf, dd, 1, d}, Pp, bf, (int32_t)nq, M, d, d,
+                                          stream, H);
+            if (e != hipSuccess) return hip_fail(e, "block projection launch");
+        }
+        float* lse_l = lse ? lse + (size_t)l * T * H : reinterpret_cast<float*>(ws + plan.off_lse);
+        st = run_fwd(X, X, Pp, offsets, B, T, H, M, d, scale, dtype, Xhat, lse_l, ws + plan.off_base, plan.base,
+                     stream, !first);
+        if (st != SA_OK) return st;
+        sa::ProfScope ps("block_refine", stream);
+        // Xbar = LN1(Xt + Xhat)
+        e = sa::launch_add_ln(first ? P : state, first && bf, first ? (int64_t)H * M : rows, Xhat, lnp(0), lnp(1),
+                              bf, rows, H, M, d, eps, Xbar, stream);
+        // FFN(Xbar) = (silu(Xbar W1) * (Xbar W3)) W2, into the Xhat buffer
+        if (e == hipSuccess)
+            e = sa::launch_small_gemm({Xbar, false, md, d, 1}, {w1, bf, d * d2, d2, 1}, G, false, (int32_t)BH, M,
+                                      (int32_t)d2, d, stream, H);
+        if (e == hipSuccess)
+            e = sa::launch_small_gemm({Xbar, false, md, d, 1}, {w3, bf, d * d2, d2, 1}, U, false, (int32_t)BH, M,
+                                      (int32_t)d2, d, stream, H);
+        if (e == hipSuccess) e = sa::launch_swiglu_gate(G, U, rows * d2, stream);
+        if (e == hipSuccess)
+            e = sa::launch_small_gemm({G, false, M * d2, d2, 1}, {w2, bf, d2 * d, d, 1}, Xhat, false, (int32_t)BH, M,
+                                      d, (int32_t)d2, stream, H);
+        // Xt' = LN2(Xbar + FFN)
+        if (e == hipSuccess)
+            e = sa::launch_add_ln(Xbar, false, rows, Xhat, lnp(2), lnp(3), bf, rows, H, M, d, eps,
+                                  l == n_layers - 1 ? out : state, stream);
+        if (e != hipSuccess) return hip_fail(e, "block refinement launch");
+    }
     return SA_OK;
 }
 

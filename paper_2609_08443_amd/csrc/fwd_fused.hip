@@ -165,7 +165,7 @@ __global__ __launch_bounds__(NW * 64, 1) void fwd_fused_kernel(FusedFwdArgs a) {
     const float ks2 = a.scale * kLog2e;
     const int64_t MD = (int64_t)C::M * D;
     const uint32_t row_stride = (uint32_t)a.H * D;
-    int cur_h = -1;
+    int64_t cur_p = -1;   // prototype block in LDS: head, or (user, head) with per-user P
     float pmax = 0.f;  // max_m |P[h, m]| of the loaded head
 
     for (int64_t k = k0; k < k1; ++k) {
@@ -178,8 +178,9 @@ __global__ __launch_bounds__(NW * 64, 1) void fwd_fused_kernel(FusedFwdArgs a) {
         if (b < 0 || b >= a.B || h < 0 || h >= a.H || t0 < 0 || t1 < t0 || t1 > a.T) continue;
 
         // ---- prototypes of head h into LDS, with max_m |P_m|
-        if (h != cur_h) {
-            const uint4* src = reinterpret_cast<const uint4*>(a.P + (int64_t)h * C::M * D);
+        const int64_t pkey = a.p_user ? (int64_t)b * a.H + h : h;
+        if (pkey != cur_p) {
+            const uint4* src = reinterpret_cast<const uint4*>(a.P + pkey * C::M * D);
             float nmax = 0.f;
             for (int i = tid; i < C::M * C::KCH; i += C::THREADS) {
                 const int r = i / C::KCH, c = i % C::KCH;
@@ -195,7 +196,7 @@ __global__ __launch_bounds__(NW * 64, 1) void fwd_fused_kernel(FusedFwdArgs a) {
 #pragma unroll
             for (int ww = 1; ww < NW; ++ww) m2 = fmaxf(m2, pnorm[ww]);
             pmax = __builtin_sqrtf(m2);
-            cur_h = h;
+            cur_p = pkey;
         }
         // shift bound of token t = cb * |K_t|
         const float cb = a.scale * pmax * kBoundMargin;

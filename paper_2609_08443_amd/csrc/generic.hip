@@ -48,24 +48,32 @@ __device__ inline float wave_sum(float v) {
 }
 
 // ---------------------------------------------------------------- forward
-// one thread per (t, h): lse = log sum_m exp(scale * <K_t, P_m>)
+// one thread per (t, h): lse = log sum_m exp(scale * <K_t, P_m>).  With per-user
+// prototypes (p_user) P is [B, H, M, d] and the token's user selects its block.
 template <bool BF16, int D>
 __global__ __launch_bounds__(256) void lse_kernel(const void* __restrict__ K,
-                                                  const void* __restrict__ P, int64_t T,
-                                                  int32_t H, int32_t M, float scale,
-                                                  float* __restrict__ lse) {
+                                                  const void* __restrict__ P,
+                                                  const int64_t* __restrict__ off, int64_t B,
+                                                  int64_t T, int32_t H, int32_t M, float scale,
+                                                  bool p_user, float* __restrict__ lse) {
     constexpr int d = D;
     const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
     if (i >= T * H) return;
     const int64_t t = i / H;
     const int32_t h = (int32_t)(i % H);
+    int64_t pi = h;
+    if (p_user) {
+        const int64_t b = user_of(off, B, T, t);
+        if (b < 0) return;   // outside every user: no lse row
+        pi = b * H + h;
+    }
     float kr[D];
 #pragma unroll
     for (int j = 0; j < d; ++j) kr[j] = ld<BF16>(K, (t * H + h) * d + j);
     float mu = -INFINITY, z = 0.f;
     for (int m = 0; m < M; ++m) {
         float s = 0.f;
-        const int64_t pb = ((int64_t)h * M + m) * d;
+        const int64_t pb = (pi * M + m) * d;
 #pragma unroll
         for (int j = 0; j < d; ++j) s = __builtin_fmaf(kr[j], ld<BF16>(P, pb + j), s);
         s *= scale;
@@ -86,7 +94,7 @@ __global__ __launch_bounds__(256) void agg_kernel(const void* __restrict__ K,
                                                   const void* __restrict__ P,
                                                   const int64_t* __restrict__ off, int64_t B,
                                                   int64_t T, int32_t H, int32_t M,
-                                                  float scale, const float* __restrict__ lse,
+                                                  float scale, bool p_user, const float* __restrict__ lse,
                                                   float* __restrict__ sketch) {
     constexpr int d = D;
     const int64_t pair = blockIdx.x;  // b*H + h
@@ -99,7 +107,7 @@ __global__ __launch_bounds__(256) void agg_kernel(const void* __restrict__ K,
     const bool mv = m < M;
     float pr[dq], acc[dq];
     for (int c = 0; c < dq; ++c) {
-        pr[c] = mv ? ld<BF16>(P, ((int64_t)h * M + m) * d + jb + c) : 0.f;
+        pr[c] = mv ? ld<BF16>(P, ((p_user ? pair : (int64_t)h) * M + m) * d + jb + c) : 0.f;
         acc[c] = 0.f;
     }
     const int64_t t0 = clampT(off[b], T), t1 = clampT(off[b + 1], T);
@@ -270,17 +278,17 @@ __global__ __launch_bounds__(256) void dp_reduce_kernel(const float* __restrict_
 
 template <bool BF16, int D>
 hipError_t fwd_impl(const void* K, const void* V, const void* P, const int64_t* off, int64_t B,
-                    int64_t T, int32_t H, int32_t M, int32_t d, float scale, float* sketch,
+                    int64_t T, int32_t H, int32_t M, int32_t d, float scale, bool p_user, float* sketch,
                     float* lse, hipStream_t stream) {
     if (T * H > 0) {
         hipLaunchKernelGGL((lse_kernel<BF16, D>), dim3((unsigned)((T * H + 255) / 256)), dim3(256), 0,
-                           stream, K, P, T, H, M, scale, lse);
+                           stream, K, P, off, B, T, H, M, scale, p_user, lse);
         hipError_t e = hipGetLastError();
         if (e != hipSuccess) return e;
     }
     if (B * H > 0) {
         hipLaunchKernelGGL((agg_kernel<BF16, D>), dim3((unsigned)(B * H), (unsigned)((M + 63) / 64)),
-                           dim3(256), 0, stream, K, V, P, off, B, T, H, M, scale, lse, sketch);
+                           dim3(256), 0, stream, K, V, P, off, B, T, H, M, scale, p_user, lse, sketch);
         return hipGetLastError();
     }
     return hipSuccess;
@@ -319,13 +327,11 @@ hipError_t bwd_impl(const void* K, const void* V, const void* P, const int64_t* 
 
 hipError_t launch_generic_fwd(const void* K, const void* V, const void* P, const int64_t* off,
                               int64_t B, int64_t T, int32_t H, int32_t M, int32_t d, float scale,
-                              bool bf16, float* sketch, float* lse_out, hipStream_t stream) {
-    if (d == 64)
-        return bf16 ? fwd_impl<true, 64>(K, V, P, off, B, T, H, M, d, scale, sketch, lse_out, stream)
-                    : fwd_impl<false, 64>(K, V, P, off, B, T, H, M, d, scale, sketch, lse_out, stream);
-    if (d == 128)
-        return bf16 ? fwd_impl<true, 128>(K, V, P, off, B, T, H, M, d, scale, sketch, lse_out, stream)
-                    : fwd_impl<false, 128>(K, V, P, off, B, T, H, M, d, scale, sketch, lse_out, stream);
+                              bool bf16, float* sketch, float* lse_out, hipStream_t stream, bool p_user) {
+#define SA_FWD(BF, DD) fwd_impl<BF, DD>(K, V, P, off, B, T, H, M, d, scale, p_user, sketch, lse_out, stream)
+    if (d == 64) return bf16 ? SA_FWD(true, 64) : SA_FWD(false, 64);
+    if (d == 128) return bf16 ? SA_FWD(true, 128) : SA_FWD(false, 128);
+#undef SA_FWD
     return hipErrorInvalidValue;
 }
 

@@ -41,63 +41,82 @@ __device__ inline void store_el<float>(float* p, int64_t i, float v) { p[i] = v;
 template <>
 __device__ inline void store_el<uint16_t>(uint16_t* p, int64_t i, float v) { p[i] = tile::to_bf16(v); }
 
-// C[h][r][c] = sum_k A[h](r, k) B[h](k, c) for r < R, c < N, k < Kd, with
-// A(r, k) = A[h * a_h + r * a_r + k * a_k] and B(k, c) = B[h * b_h + k * b_k + c * b_c];
-// C row-major [R][N] per head.  A 32 x 32 output tile per workgroup of 256
-// threads; k advances in slabs of 32 staged in LDS, the next slab's loads in
-// flight (registers) while the current one is used.  Consecutive lanes walk the
-// unit-stride index of each operand so that its loads coalesce.
+// C[z][r][c] = sum_k A[z](r, k) B[z % b_mod](k, c) for r < R, c < N, k < Kd, with
+// A(r, k) = A[z * a_h + r * a_r + k * a_k] and B(k, c) = B[z' * b_h + k * b_k + c * b_c];
+// C row-major [R][N] per batch z.  A 64 x 64 output tile per workgroup of 256
+// threads, 4 x 4 outputs per thread; k advances in slabs of 16 staged in LDS
+// (k-major, so each k step is two 16-byte LDS reads for 16 FMAs), the next
+// slab's loads in flight while the current one is used.  Consecutive lanes walk
+// the unit-stride index of each operand so that its loads coalesce.
 template <typename TA, typename TB, typename TC>
 __global__ __launch_bounds__(256) void small_gemm_kernel(const TA* __restrict__ A, int64_t a_h, int64_t a_r,
                                                          int64_t a_k, const TB* __restrict__ Bm, int64_t b_h,
-                                                         int64_t b_k, int64_t b_c, TC* __restrict__ C,
-                                                         int32_t R, int32_t N, int32_t Kd) {
-    __shared__ float As[32][33];   // [r][k]
-    __shared__ float Bs[32][33];   // [k][c]
-    const int tid = threadIdx.x, tx = tid & 31, ty = tid >> 5;
-    const int r0 = blockIdx.x * 32, c0 = blockIdx.y * 32;
-    const int64_t h = blockIdx.z;
-    const TA* Ah = A + h * a_h;
-    const TB* Bh = Bm + h * b_h;
-    const bool a_rows_fast = a_r == 1 && a_k != 1;   // lanes along r
-    const bool b_k_fast = b_k == 1 && b_c != 1;      // lanes along k
+                                                         int64_t b_k, int64_t b_c, int32_t b_mod,
+                                                         TC* __restrict__ C, int32_t R, int32_t N, int32_t Kd) {
+    constexpr int TR = 64, TC_ = 64, TK = 16, PAD = 4;
+    __shared__ __attribute__((aligned(16))) float As[TK][TR + PAD];   // [k][r]
+    __shared__ __attribute__((aligned(16))) float Bs[TK][TC_ + PAD];  // [k][c]
+    const int tid = threadIdx.x, tx = tid & 15, ty = tid >> 4;
+    const int r0 = blockIdx.x * TR, c0 = blockIdx.y * TC_;
+    const int64_t z = blockIdx.z;
+    const TA* Az = A + z * a_h;
+    const TB* Bz = Bm + (z % b_mod) * b_h;
+    const bool a_rows_fast = a_r == 1 && a_k != 1;   // lanes along r, else along k
+    const bool b_k_fast = b_k == 1 && b_c != 1;      // lanes along k, else along c
     float ra[4], rb[4];
     auto fetch = [&](int k0) {
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-            const int u = ty + 8 * i;
-            const int ar = a_rows_fast ? tx : u, ak = a_rows_fast ? u : tx;
+            const int ar = a_rows_fast ? tid & 63 : (tid >> 4) + 16 * i;
+            const int ak = a_rows_fast ? (tid >> 6) + 4 * i : tid & 15;
             const int r = r0 + ar, k = k0 + ak;
-            ra[i] = (r < R && k < Kd) ? load_el(Ah, (int64_t)r * a_r + (int64_t)k * a_k) : 0.f;
-            const int bk = b_k_fast ? tx : u, bc = b_k_fast ? u : tx;
+            ra[i] = (r < R && k < Kd) ? load_el(Az, (int64_t)r * a_r + (int64_t)k * a_k) : 0.f;
+            const int bk = b_k_fast ? tid & 15 : (tid >> 6) + 4 * i;
+            const int bc = b_k_fast ? (tid >> 4) + 16 * i : tid & 63;
             const int kb = k0 + bk, c = c0 + bc;
-            rb[i] = (kb < Kd && c < N) ? load_el(Bh, (int64_t)kb * b_k + (int64_t)c * b_c) : 0.f;
+            rb[i] = (kb < Kd && c < N) ? load_el(Bz, (int64_t)kb * b_k + (int64_t)c * b_c) : 0.f;
         }
     };
-    float acc[4] = {0.f, 0.f, 0.f, 0.f};
+    float acc[4][4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) acc[i][j] = 0.f;
     fetch(0);
-    for (int k0 = 0; k0 < Kd; k0 += 32) {
+    for (int k0 = 0; k0 < Kd; k0 += TK) {
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-            const int u = ty + 8 * i;
-            if (a_rows_fast) As[tx][u] = ra[i]; else As[u][tx] = ra[i];
-            if (b_k_fast) Bs[tx][u] = rb[i]; else Bs[u][tx] = rb[i];
+            const int ar = a_rows_fast ? tid & 63 : (tid >> 4) + 16 * i;
+            const int ak = a_rows_fast ? (tid >> 6) + 4 * i : tid & 15;
+            As[ak][ar] = ra[i];
+            const int bk = b_k_fast ? tid & 15 : (tid >> 6) + 4 * i;
+            const int bc = b_k_fast ? (tid >> 4) + 16 * i : tid & 63;
+            Bs[bk][bc] = rb[i];
         }
         __syncthreads();
-        if (k0 + 32 < Kd) fetch(k0 + 32);
-#pragma unroll 8
-        for (int kk = 0; kk < 32; ++kk) {
-            const float b = Bs[kk][tx];
+        if (k0 + TK < Kd) fetch(k0 + TK);
 #pragma unroll
-            for (int i = 0; i < 4; ++i) acc[i] = __builtin_fmaf(As[ty + 8 * i][kk], b, acc[i]);
+        for (int kk = 0; kk < TK; ++kk) {
+            const float4 av = *reinterpret_cast<const float4*>(&As[kk][ty * 4]);
+            const float4 bv = *reinterpret_cast<const float4*>(&Bs[kk][tx * 4]);
+            const float a4[4] = {av.x, av.y, av.z, av.w}, b4[4] = {bv.x, bv.y, bv.z, bv.w};
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+#pragma unroll
+                for (int j = 0; j < 4; ++j) acc[i][j] = __builtin_fmaf(a4[i], b4[j], acc[i][j]);
         }
         __syncthreads();
     }
-    TC* Ch = C + h * (int64_t)R * N;
+    TC* Cz = C + z * (int64_t)R * N;
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-        const int r = r0 + ty + 8 * i, c = c0 + tx;
-        if (r < R && c < N) store_el(Ch, (int64_t)r * N + c, acc[i]);
+        const int r = r0 + ty * 4 + i;
+        if (r >= R) continue;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            const int c = c0 + tx * 4 + j;
+            if (c < N) store_el(Cz, (int64_t)r * N + c, acc[i][j]);
+        }
     }
 }
 
@@ -111,32 +130,30 @@ __global__ __launch_bounds__(256) void add_kernel(const float* __restrict__ a, c
 }
 
 template <typename TA, typename TB, typename TC>
-hipError_t gemm_t(const MatView& a, const MatView& b, void* c, int32_t H, int32_t R, int32_t N, int32_t Kd,
-                  hipStream_t stream) {
-    const dim3 grid((unsigned)((R + 31) / 32), (unsigned)((N + 31) / 32), (unsigned)H);
+hipError_t gemm_t(const MatView& a, const MatView& b, int32_t b_mod, void* c, int32_t H, int32_t R, int32_t N,
+                  int32_t Kd, hipStream_t stream) {
+    const dim3 grid((unsigned)((R + 63) / 64), (unsigned)((N + 63) / 64), (unsigned)H);
     hipLaunchKernelGGL((small_gemm_kernel<TA, TB, TC>), grid, dim3(256), 0, stream,
                        reinterpret_cast<const TA*>(a.p), a.s_h, a.s_0, a.s_1,
-                       reinterpret_cast<const TB*>(b.p), b.s_h, b.s_0, b.s_1, reinterpret_cast<TC*>(c), R,
-                       N, Kd);
+                       reinterpret_cast<const TB*>(b.p), b.s_h, b.s_0, b.s_1, b_mod, reinterpret_cast<TC*>(c),
+                       R, N, Kd);
     return hipGetLastError();
 }
 
 }  // namespace
 
 hipError_t launch_small_gemm(const MatView& a, const MatView& b, void* c, bool c_bf16, int32_t H, int32_t R,
-                             int32_t N, int32_t Kd, hipStream_t stream) {
+                             int32_t N, int32_t Kd, hipStream_t stream, int32_t b_mod) {
     if (H <= 0 || R <= 0 || N <= 0) return hipSuccess;
-    if (a.bf16 && b.bf16)
-        return c_bf16 ? gemm_t<uint16_t, uint16_t, uint16_t>(a, b, c, H, R, N, Kd, stream)
-                      : gemm_t<uint16_t, uint16_t, float>(a, b, c, H, R, N, Kd, stream);
-    if (a.bf16)
-        return c_bf16 ? gemm_t<uint16_t, float, uint16_t>(a, b, c, H, R, N, Kd, stream)
-                      : gemm_t<uint16_t, float, float>(a, b, c, H, R, N, Kd, stream);
-    if (b.bf16)
-        return c_bf16 ? gemm_t<float, uint16_t, uint16_t>(a, b, c, H, R, N, Kd, stream)
-                      : gemm_t<float, uint16_t, float>(a, b, c, H, R, N, Kd, stream);
-    return c_bf16 ? gemm_t<float, float, uint16_t>(a, b, c, H, R, N, Kd, stream)
-                  : gemm_t<float, float, float>(a, b, c, H, R, N, Kd, stream);
+    if (b_mod <= 0) b_mod = H;
+#define SA_GEMM(TA, TB) \
+    return c_bf16 ? gemm_t<TA, TB, uint16_t>(a, b, b_mod, c, H, R, N, Kd, stream) \
+                  : gemm_t<TA, TB, float>(a, b, b_mod, c, H, R, N, Kd, stream)
+    if (a.bf16 && b.bf16) SA_GEMM(uint16_t, uint16_t);
+    if (a.bf16) SA_GEMM(uint16_t, float);
+    if (b.bf16) SA_GEMM(float, uint16_t);
+    SA_GEMM(float, float);
+#undef SA_GEMM
 }
 
 hipError_t launch_add(const float* a, const float* b, float* out, int64_t n, hipStream_t stream) {

@@ -67,6 +67,7 @@ struct FusedFwdArgs {
     float* sketch;
     float* lse;
     float* partials;
+    bool p_user;   // P is [B,H,M,d], one prototype block per user (stacked layers)
 };
 bool fused_fwd_supported(int32_t M, int32_t d);
 size_t fused_fwd_lds_bytes(int32_t M, int32_t d);
@@ -122,17 +123,28 @@ hipError_t launch_tokenwise_generic(const void* K, const void* V, const void* P,
                                     int64_t B, int32_t H, int32_t M, int32_t d, float scale, bool bf16,
                                     float* sketch, float* lse_m, hipStream_t stream);
 
-// Small batched product for the SA layer's projections (fp32 accumulation):
-// C[h][r][c] = sum_k A[h](r, k) B[h](k, c), r < R, c < N, k < Kd, C row-major
-// [R][N] per head, bf16 (rounded) or fp32.  Operand element (i, j) of head h
-// sits at p[h * s_h + i * s_0 + j * s_1], so a transpose is a swap of strides.
+// Batched product for the projections and the FFN of the SA layers (fp32
+// accumulation): C[z][r][c] = sum_k A[z](r, k) B[z % b_mod](k, c), r < R, c < N,
+// k < Kd, z < H batches, C row-major [R][N] per batch, bf16 (rounded) or fp32.
+// Operand element (i, j) of batch z sits at p[z * s_h + i * s_0 + j * s_1], so a
+// transpose is a swap of strides; b_mod <= 0 means b_mod = H (one B per batch).
 struct MatView {
     const void* p;
     bool bf16;
     int64_t s_h, s_0, s_1;
 };
 hipError_t launch_small_gemm(const MatView& a, const MatView& b, void* c, bool c_bf16, int32_t H, int32_t R,
-                             int32_t N, int32_t Kd, hipStream_t stream);
+                             int32_t N, int32_t Kd, hipStream_t stream, int32_t b_mod = 0);
+// Stacked-SA refinement (block.hip).  add_ln: one row of d features per
+// (user, head, prototype): out[r] = LN(x[r mod x_rows] + y[r]) * gamma[h] + beta[h],
+// h = (r / M) % H; x fp32 or bf16 (the shared prototypes broadcast over users
+// when x_rows = H * M), y fp32, gamma / beta [H][d] in the parameter dtype.
+hipError_t launch_add_ln(const void* x, bool x_bf16, int64_t x_rows, const float* y, const void* gamma,
+                         const void* beta, bool p_bf16, int64_t rows, int32_t H, int32_t M, int32_t d, float eps,
+                         float* out, hipStream_t stream);
+// g = silu(g) * u elementwise (n fp32 values, n a multiple of 4)
+hipError_t launch_swiglu_gate(float* g, const float* u, int64_t n, hipStream_t stream);
+
 // out = a + b elementwise (n fp32 values, n a multiple of 4, 16-byte aligned)
 hipError_t launch_add(const float* a, const float* b, float* out, int64_t n, hipStream_t stream);
 
@@ -140,7 +152,7 @@ hipError_t launch_add(const float* a, const float* b, float* out, int64_t n, hip
 hipError_t launch_generic_fwd(const void* K, const void* V, const void* P,
                               const int64_t* offsets, int64_t B, int64_t T, int32_t H,
                               int32_t M, int32_t d, float scale, bool bf16, float* sketch,
-                              float* lse_out, hipStream_t stream);
+                              float* lse_out, hipStream_t stream, bool p_user = false);
 
 // dY[b,h] = sum_r dsketch[b,r,h]  (fp32, [B,H,M,d])
 hipError_t launch_dy_reduce(const float* dsketch, int64_t B, int32_t R, int32_t H, int64_t MD,

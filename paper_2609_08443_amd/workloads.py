@@ -44,6 +44,7 @@ import numpy as np
 # tensor ids of the per-(seed, tensor, user) streams
 TID_LENGTHS, TID_K, TID_V, TID_P, TID_DSKETCH = 0, 1, 2, 3, 4
 TID_WQ, TID_WK = 5, 6
+TID_BLOCK = 7   # stacked-block parameters: 7 + 10 * layer + kind
 
 BASE_SEED = 8443
 
@@ -207,6 +208,50 @@ def device_projections(w: Workload, device="cuda") -> dict:
     return out
 
 
+def _block_shapes(w: Workload, L: int):
+    d = w.d
+    return {"Wq": ((L, w.H, d, d), 1.0 / math.sqrt(d)), "Wk": ((L, w.H, d, d), 1.0 / math.sqrt(d)),
+            "W1": ((L, w.H, d, 2 * d), 1.0 / math.sqrt(d)), "W3": ((L, w.H, d, 2 * d), 1.0 / math.sqrt(d)),
+            "W2": ((L, w.H, 2 * d, d), 1.0 / math.sqrt(2 * d)), "ln": ((L, 4, w.H, d), 0.1)}
+
+
+def _ln_from_noise(x: np.ndarray) -> np.ndarray:
+    """Gains 1 + noise (slots 0, 2), biases = noise (slots 1, 3)."""
+    x = x.copy()
+    x[:, 0] += 1.0
+    x[:, 2] += 1.0
+    return x
+
+
+def host_block_params(w: Workload, L: int) -> dict:
+    """Stacked-block parameters for L layers (exact bf16 values in bf16 mode):
+    projections ~ N(0, 1/fan_in), norm gains 1 + N(0, 0.01), biases N(0, 0.01)."""
+    out = {}
+    for k, (name, (shape, sd)) in enumerate(_block_shapes(w, L).items()):
+        x = _normal(w.seed, TID_BLOCK + k, 0, shape, sd)
+        if name == "ln":
+            x = _ln_from_noise(x)
+        out[name] = _finish(x, w.dtype)
+    return out
+
+
+def device_block_params(w: Workload, L: int, device="cuda") -> dict:
+    """host_block_params' distributions, drawn on the device (torch Philox)."""
+    import torch
+
+    tdt = torch.bfloat16 if w.dtype == "bf16" else torch.float32
+    g = torch.Generator(device=device)
+    out = {}
+    for k, (name, (shape, sd)) in enumerate(_block_shapes(w, L).items()):
+        g.manual_seed(_torch_seed(w.seed, TID_BLOCK + k, 0))
+        x = torch.randn(shape, generator=g, device=device, dtype=torch.float32) * sd
+        if name == "ln":
+            x[:, 0] += 1.0
+            x[:, 2] += 1.0
+        out[name] = x.to(tdt)
+    return out
+
+
 def host_dsketch_user(w: Workload, b: int) -> np.ndarray:
     return _normal(w.seed, TID_DSKETCH, b, (w.R, w.H, w.M, w.d))
 
@@ -299,7 +344,7 @@ def to_device(host: dict, dtype: str, device="cuda") -> dict:
 
     out = {}
     for k, v in host.items():
-        if k in ("K", "V", "X", "P", "Wq", "Wk") and dtype == "bf16":
+        if k in ("K", "V", "X", "P", "Wq", "Wk", "W1", "W2", "W3", "ln") and dtype == "bf16":
             bits = f32_to_bf16_bits(v).view(np.int16)
             out[k] = torch.from_numpy(bits.copy()).to(device).view(torch.bfloat16)
         else:

@@ -149,3 +149,24 @@ def test_layer_bwd_rejects_bad_arguments():
     assert call(d=80) == 2
     assert call() == 3
     assert sa.layer_bwd_workspace_size(2, 10, 1, 128, 64, 0, 1) > sa.bwd_workspace_size(2, 10, 1, 128, 64, 0, 1)
+
+
+def test_block_fwd_rejects_bad_arguments():
+    L = sa.lib()
+    p = 1 << 12
+    args = dict(X=p, P=p, Wq=p, Wk=p, ln=p, W1=p, W3=p, W2=p, off=p, B=2, T=10, H=1, M=128, d=64, n=2,
+                scale=0.125, eps=1e-5, dtype=0, out=p, lse=NULL, ws=NULL, wsb=0)
+
+    def call(**kw):
+        a = dict(args, **kw)
+        return L.sa_block_fwd(a["X"], a["P"], a["Wq"], a["Wk"], a["ln"], a["W1"], a["W3"], a["W2"], a["off"],
+                              a["B"], a["T"], a["H"], a["M"], a["d"], a["n"], a["scale"], a["eps"], a["dtype"],
+                              a["out"], a["lse"], a["ws"], a["wsb"], None)
+    for name in ("X", "P", "Wq", "Wk", "ln", "W1", "W3", "W2", "off", "out"):
+        assert call(**{name: NULL}) == 1, name
+    assert call(n=0) == 1
+    assert call(eps=0.0) == 1 and call(eps=float("nan")) == 1
+    assert call(W2=p + 2) == 1
+    assert call(d=96) == 2
+    assert call() == 3
+    assert sa.block_fwd_workspace_size(2, 10, 1, 128, 64, 2, 0) > sa.fwd_workspace_size(2, 10, 1, 128, 64, 0)

@@ -1,0 +1,102 @@
+"""GPU parity of stacked SA (sa_block_fwd: per layer the sketch with the
+current state as queries, residual + LN, SwiGLU FFN + residual + LN; section
+3.3) against the fp64 numpy block oracle, through the C ABI.
+
+Output tolerance: normwise max relative error per (user, head) slice <= 2e-2
+(bf16) / 1e-4 (fp32), as for the other paths.  The first layer's lse keeps the
+sketching step's absolute bounds (1e-3 bf16, 1e-5 fp32).  Later layers' logits
+come from per-user queries computed from the refined state and rounded to
+bf16 once (P' = state W_Q W_K^T); their lse bound is 5e-3 in bf16 (about four
+times the first layer's, for logits of unit scale and a relative rounding of
+2^-9 in P') and 1e-4 in fp32.
+"""
+import numpy as np
+import pytest
+
+from oracle import block as oblock
+from paper_2609_08443_amd import workloads as wl
+
+torch = pytest.importorskip("torch")
+pytestmark = pytest.mark.gpu
+
+TOL = {"bf16": 2e-2, "fp32": 1e-4}
+LSE0 = {"bf16": 1e-3, "fp32": 1e-5}
+LSE1 = {"bf16": 5e-3, "fp32": 1e-4}
+
+
+@pytest.fixture(scope="module")
+def sa():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from paper_2609_08443_amd import sa_sketch
+    sa_sketch.lib()
+    return sa_sketch
+
+
+def normwise(gpu, ref, axes):
+    err = np.abs(gpu.astype(np.float64) - ref).max(axis=axes)
+    den = np.abs(ref).max(axis=axes)
+    return err / np.maximum(den, 1e-30)
+
+
+NAMES = ("Wq", "Wk", "ln", "W1", "W3", "W2")
+
+
+def run(sa, lengths, H, M, d, L, dtype, seed):
+    w = wl.custom(lengths, H, M, d, dtype, seed=seed)
+    host = wl.host_tensors(w)
+    host.update(wl.host_block_params(w, L))
+    host["X"] = host.pop("V")
+    del host["K"]
+    dev = wl.to_device(host, dtype)
+    print(f"block case lengths={lengths} H={H} M={M} d={d} L={L} {dtype}", flush=True)
+    out, lse = sa.block_fwd(dev["X"], dev["P"], *[dev[k] for k in NAMES], dev["offsets"], w.scale,
+                            want_lse=True)
+    torch.cuda.synchronize()
+    ref, rlse = oblock.block_fwd(host["X"], host["P"], *[host[k] for k in NAMES], host["offsets"],
+                                 scale=w.scale)
+    return w, out.cpu().numpy(), lse.cpu().numpy(), ref, rlse
+
+
+def check(w, out, lse, ref, rlse, dtype):
+    e = normwise(out, ref, (2, 3))
+    assert np.all(e <= TOL[dtype]), ("out", e.max())
+    if w.T:
+        assert np.abs(lse[0] - rlse[0]).max() <= LSE0[dtype], ("lse0", np.abs(lse[0] - rlse[0]).max())
+        for l in range(1, lse.shape[0]):
+            assert np.abs(lse[l] - rlse[l]).max() <= LSE1[dtype], ("lse", l, np.abs(lse[l] - rlse[l]).max())
+
+
+FUSED = [
+    ([37, 0, 70, 1, 5], 2, 128, 64, 2),
+    ([300, 17, 64], 2, 512, 128, 2),
+    ([96, 31, 200], 1, 256, 64, 3),
+    ([2000, 3, 513], 4, 512, 128, 2),
+]
+
+
+@pytest.mark.parametrize("lengths,H,M,d,L", FUSED)
+def test_block_fused_matches_oracle(sa, lengths, H, M, d, L):
+    check(*run(sa, lengths, H, M, d, L, "bf16", seed=13 * sum(lengths) + M + d + L), "bf16")
+
+
+PLAIN = [
+    ([40, 0, 77], 2, 64, 64, 2, "fp32"),
+    ([50, 9], 1, 200, 128, 2, "fp32"),
+    ([33, 64], 2, 64, 64, 2, "bf16"),
+]
+
+
+@pytest.mark.parametrize("lengths,H,M,d,L,dtype", PLAIN)
+def test_block_plain_matches_oracle(sa, lengths, H, M, d, L, dtype):
+    check(*run(sa, lengths, H, M, d, L, dtype, seed=17 * sum(lengths) + M + d), dtype)
+
+
+def test_block_empty_users_and_determinism(sa):
+    # users without tokens get the refinement of the prototypes alone: equal rows
+    w, out, lse, ref, rlse = run(sa, [0, 120, 0], 2, 128, 64, 2, "bf16", seed=31)
+    np.testing.assert_array_equal(out[0], out[2])
+    check(w, out, lse, ref, rlse, "bf16")
+    _, out2, lse2, _, _ = run(sa, [0, 120, 0], 2, 128, 64, 2, "bf16", seed=31)
+    np.testing.assert_array_equal(out, out2)
+    np.testing.assert_array_equal(lse, lse2)
