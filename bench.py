@@ -319,6 +319,23 @@ def main(argv=None) -> int:
                  "step": "sa_layer_fwd + sa_layer_bwd" if w.bwd else "sa_layer_fwd",
                  "mfma_util": flops_step / (ly_ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS}
 
+    # stacked SA forward (N_sa = 2 layers, the paper's deployed depth) on the same
+    # batch, X = the V tensor; not part of the step
+    block = None
+    if not args.no_variants:
+        n_layers = 2
+        bp = wl.device_block_params(w, n_layers, "cuda")
+        ws_bl = torch.empty(max(sa.block_fwd_workspace_size(B, T, H, M, d, n_layers, code), 1),
+                            dtype=torch.uint8, device="cuda")
+        out_bl = torch.empty((B, H, M, d), dtype=torch.float32, device="cuda")
+
+        def blk():
+            sa.block_fwd(dev["V"], dev["P"], bp["Wq"], bp["Wk"], bp["ln"], bp["W1"], bp["W3"], bp["W2"],
+                         dev["offsets"], w.scale, out=out_bl, workspace=ws_bl)
+        bl_ms, kbl = timed(blk)
+        block = {"tokens_per_s": T / (bl_ms * 1e-3), "ms": bl_ms, "n_layers": n_layers,
+                 "kernels": kernel_dict(kbl), "step": "sa_block_fwd"}
+
     out = {
         "metric": METRIC,
         "value": T / (ms_step * 1e-3),
@@ -344,6 +361,7 @@ def main(argv=None) -> int:
         "roofline": roof,
         "tokenwise_fwd": tokenwise,
         "layer": layer,
+        "block_fwd": block,
         "cpu_baseline": None,
     }
     if not args.no_cpu_baseline:
