@@ -264,6 +264,38 @@ sa_status sa_block_fwd(const void* X, const void* P, const void* Wq, const void*
                        float scale, float eps, sa_dtype dtype, float* out, float* lse,
                        void* workspace, size_t workspace_bytes, void* stream);
 
+/* Bytes of workspace that sa_block_bwd needs for this shape. */
+size_t sa_block_bwd_workspace_size(int64_t B, int64_t T, int32_t H, int32_t M, int32_t d,
+                                   int32_t n_layers, sa_dtype dtype);
+
+/*
+ * Backward of sa_block_fwd (section 3.3) by the chain rule: the gradients of
+ * <dout, out> with respect to every input.  The forward is replayed first,
+ * keeping each layer's intermediates in the workspace; then, from the last
+ * layer down: the second norm, the FFN (dW2 = Z^T dY2, the gate
+ * silu'(g) = s (1 + g (1 - s)), dW1 = Xbar^T dG, dW3 = Xbar^T dU), the first
+ * norm, the sketch (the sketching backward with dsketch = the gradient of Xhat,
+ * one target instance, per-user prototypes from the second layer on) and the two
+ * projections.  The first layer's state gradient is the prototypes' gradient,
+ * summed over users; weight gradients are summed over users in user order.
+ *
+ *   dout      [B,H,M,d] fp32, the gradient of out
+ *   dX        output [T,H,d] fp32;  dP output [H,M,d] fp32
+ *   dWq, dWk  outputs [n_layers,H,d,d];  dW1, dW3 [n_layers,H,d,2d];  dW2 [n_layers,H,2d,d]
+ *   dln       output [n_layers,4,H,d] (gamma1, beta1, gamma2, beta2)
+ *
+ * All outputs fp32 and overwritten.  Results are deterministic (fixed
+ * summation orders).  Other arguments, errors, ownership and streams as for
+ * sa_block_fwd; B = 0 is SA_ERR_INVALID_ARG here (no gradients to write) and
+ * more than 65535 users SA_ERR_UNSUPPORTED.
+ */
+sa_status sa_block_bwd(const void* X, const void* P, const void* Wq, const void* Wk, const void* ln,
+                       const void* W1, const void* W3, const void* W2, const int64_t* offsets,
+                       int64_t B, int64_t T, int32_t H, int32_t M, int32_t d, int32_t n_layers,
+                       float scale, float eps, sa_dtype dtype, const float* dout, float* dX,
+                       float* dP, float* dWq, float* dWk, float* dln, float* dW1, float* dW3,
+                       float* dW2, void* workspace, size_t workspace_bytes, void* stream);
+
 /*
  * Work list used by the fused forward, exposed for exact testing.
  *

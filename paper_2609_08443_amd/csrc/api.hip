@@ -2,6 +2,7 @@
 // launch plans, workspace carving and kernel launches on the caller's stream.
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
@@ -205,7 +206,8 @@ struct BwdPlan {
            off_yjm = 0, off_pjm = 0, total = 0;
 };
 
-BwdPlan plan_bwd(int64_t B, int64_t T, int32_t H, int32_t M, int32_t d, sa_dtype dtype) {
+BwdPlan plan_bwd(int64_t B, int64_t T, int32_t H, int32_t M, int32_t d, sa_dtype dtype,
+                 bool p_user = false) {
     BwdPlan p;
     p.fused = dtype == SA_BF16 && sa::fused_bwd_supported(M, d);
     size_t off = 0;
@@ -231,7 +233,7 @@ BwdPlan plan_bwd(int64_t B, int64_t T, int32_t H, int32_t M, int32_t d, sa_dtype
         p.off_items = carve(sizeof(int32_t) * sa::IT_WORDS * p.max_items);
         p.off_ymj = carve(sizeof(uint16_t) * (size_t)B * H * M * d);
         p.off_yjm = carve(sizeof(uint16_t) * (size_t)B * H * M * d);
-        p.off_pjm = carve(sizeof(uint16_t) * (size_t)H * M * d);
+        p.off_pjm = carve(sizeof(uint16_t) * (size_t)(p_user ? B * H : H) * M * d);
         p.off_D = carve(sizeof(float) * (size_t)T * H);
         p.off_part = carve(sizeof(float) * (size_t)p.max_items * M * d);
     } else {
@@ -324,6 +326,148 @@ BlockPlan plan_block(int64_t B, int64_t T, int32_t H, int32_t M, int32_t d, sa_d
     return p;
 }
 
+// ---------------------------------------------------------------- stacked block backward plan
+// Per layer l a region [state_l (l >= 1) | Q_l | P'_l | lse_l | Y1_l | Xbar_l | G_l | U_l | Y2_l]
+// holding the forward's intermediates (Y1 = Xt + Xhat, Y2 = Xbar + FFN: the
+// inputs of the two norms), then the backward's scratch, then one region
+// shared by the sketching forward and backward calls.
+struct BlockBwdPlan {
+    FwdPlan fwd;
+    BwdPlan bshared, buser;
+    size_t l_state = 0, l_q = 0, l_pp = 0, l_lse = 0, l_y1 = 0, l_xbar = 0, l_g = 0, l_u = 0, l_y2 = 0,
+           l_stride = 0;
+    size_t off_layers = 0, off_xhat = 0, off_z = 0, off_du = 0, off_dy2 = 0, off_dy1 = 0, off_dpp = 0,
+           off_dq = 0, off_stats = 0, off_colpart = 0, off_wpart = 0, off_dxl = 0, off_dk = 0, off_dv = 0,
+           off_out = 0, off_base = 0, total = 0;
+    int64_t nch = 1;
+};
+
+BlockBwdPlan plan_block_bwd(int64_t B, int64_t T, int32_t H, int32_t M, int32_t d, int32_t L, sa_dtype dtype) {
+    BlockBwdPlan p;
+    p.fwd = plan_fwd(B, T, H, M, d, dtype, false);
+    p.bshared = plan_bwd(B, T, H, M, d, dtype, false);
+    p.buser = plan_bwd(B, T, H, M, d, dtype, true);
+    size_t off = 0;
+    auto carve = [&](size_t bytes) {
+        const size_t o = off;
+        off = align_up(off + bytes, 256);
+        return o;
+    };
+    const size_t rd = (size_t)B * H * M * d, f = sizeof(float);
+    p.l_state = carve(f * rd);
+    p.l_q = carve(f * rd);
+    p.l_pp = carve((dtype == SA_BF16 ? 2 : 4) * rd);
+    p.l_lse = carve(f * (size_t)T * H);
+    p.l_y1 = carve(f * rd);
+    p.l_xbar = carve(f * rd);
+    p.l_g = carve(f * 2 * rd);
+    p.l_u = carve(f * 2 * rd);
+    p.l_y2 = carve(f * rd);
+    p.l_stride = off;
+    off = 0;
+    p.off_layers = carve(p.l_stride * (size_t)L);
+    p.off_xhat = carve(f * rd);
+    p.off_z = carve(f * 2 * rd);
+    p.off_du = carve(f * 2 * rd);
+    p.off_dy2 = carve(f * rd);
+    p.off_dy1 = carve(f * rd);
+    p.off_dpp = carve(f * rd);
+    p.off_dq = carve(f * rd);
+    p.off_stats = carve(sizeof(float) * 2 * (size_t)B * H * M);
+    // column-sum chunks of the norms' gamma / beta gradients: about 1024 workgroups
+    p.nch = std::max<int64_t>(1, std::min<int64_t>(B * M, (1024 + H - 1) / H));
+    p.off_colpart = carve(f * (size_t)p.nch * H * 2 * d);
+    p.off_wpart = carve(f * (size_t)B * H * 2 * d * d);
+    p.off_dxl = carve(L > 1 ? f * (size_t)T * H * d : 0);
+    if (!p.bshared.fused) {
+        p.off_dk = carve(f * (size_t)T * H * d);
+        p.off_dv = carve(f * (size_t)T * H * d);
+    }
+    p.off_out = carve(f * rd);
+    p.off_base = carve(std::max({p.fwd.total, p.bshared.total, p.buser.total}));
+    p.total = off;
+    return p;
+}
+
+// parameters of the stacked block, sliced per layer
+struct BlockParams {
+    const void *Wq, *Wk, *ln, *W1, *W3, *W2;
+    int32_t H, d;
+    size_t el;
+    const void* at(const void* base, size_t per_layer, int32_t l) const {
+        return reinterpret_cast<const uint8_t*>(base) + el * per_layer * (size_t)l;
+    }
+    const void* wq(int32_t l) const { return at(Wq, (size_t)H * d * d, l); }
+    const void* wk(int32_t l) const { return at(Wk, (size_t)H * d * d, l); }
+    const void* w1(int32_t l) const { return at(W1, (size_t)H * d * 2 * d, l); }
+    const void* w3(int32_t l) const { return at(W3, (size_t)H * d * 2 * d, l); }
+    const void* w2(int32_t l) const { return at(W2, (size_t)H * 2 * d * d, l); }
+    // k = 0: gamma1, 1: beta1, 2: gamma2, 3: beta2
+    const void* ln_(int32_t l, int k) const { return at(ln, (size_t)H * d, 4 * l + k); }
+};
+
+// Buffers of one layer of the stacked forward.  xt is the layer's state: the
+// shared prototypes (input dtype, H * M rows) for the first layer, else fp32
+// [B,H,M,d].  Y1, Y2 and Z may be null: without Z the gate is applied to G in place.
+struct BlockLayerIo {
+    const void* xt;
+    bool first;
+    float *Q, *lse, *Xhat, *Y1, *Xbar, *G, *U, *Z, *Y2, *out;
+    void* Pp;
+};
+
+sa_status run_fwd(const void* K, const void* V, const void* P, const int64_t* offsets, int64_t B,
+                  int64_t T, int32_t H, int32_t M, int32_t d, float scale, sa_dtype dtype,
+                  float* sketch, float* lse, uint8_t* ws, const FwdPlan& plan, hipStream_t stream,
+                  bool p_user);
+
+sa_status block_layer_fwd(const void* X, const int64_t* offsets, int64_t B, int64_t T, int32_t H, int32_t M,
+                          int32_t d, int32_t l, float scale, float eps, sa_dtype dtype, const BlockParams& w,
+                          const BlockLayerIo& io, uint8_t* base_ws, const FwdPlan& base, hipStream_t stream) {
+    const bool bf = dtype == SA_BF16;
+    const int64_t md = (int64_t)M * d, dd = (int64_t)d * d, d2 = 2 * (int64_t)d;
+    const int64_t BH = B * H, rows = BH * M;
+    // queries of this layer: the shared prototypes first, then each user's state
+    const int64_t nq = io.first ? H : BH;
+    hipError_t e;
+    {
+        sa::ProfScope ps("block_proj", stream);
+        const sa::MatView xt{io.xt, io.first && bf, md, d, 1};
+        e = sa::launch_small_gemm(xt, {w.wq(l), bf, dd, d, 1}, io.Q, false, (int32_t)nq, M, d, d, stream, H);
+        if (e == hipSuccess)
+            e = sa::launch_small_gemm({io.Q, false, md, d, 1}, {w.wk(l), bf, dd, 1, d}, io.Pp, bf, (int32_t)nq, M,
+                                      d, d, stream, H);
+        if (e != hipSuccess) return hip_fail(e, "block projection launch");
+    }
+    sa_status st = run_fwd(X, X, io.Pp, offsets, B, T, H, M, d, scale, dtype, io.Xhat, io.lse, base_ws, base,
+                           stream, !io.first);
+    if (st != SA_OK) return st;
+    sa::ProfScope ps("block_refine", stream);
+    // Xbar = LN1(Xt + Xhat)
+    e = sa::launch_add_ln(io.xt, io.first && bf, io.first ? (int64_t)H * M : rows, io.Xhat, w.ln_(l, 0),
+                          w.ln_(l, 1), bf, rows, H, M, d, eps, io.Xbar, stream, io.Y1);
+    // FFN(Xbar) = (silu(Xbar W1) * (Xbar W3)) W2, into the Xhat buffer
+    if (e == hipSuccess)
+        e = sa::launch_small_gemm({io.Xbar, false, md, d, 1}, {w.w1(l), bf, d * d2, d2, 1}, io.G, false,
+                                  (int32_t)BH, M, (int32_t)d2, d, stream, H);
+    if (e == hipSuccess)
+        e = sa::launch_small_gemm({io.Xbar, false, md, d, 1}, {w.w3(l), bf, d * d2, d2, 1}, io.U, false,
+                                  (int32_t)BH, M, (int32_t)d2, d, stream, H);
+    float* Z = io.Z ? io.Z : io.G;
+    if (e == hipSuccess)
+        e = io.Z ? sa::launch_swiglu_fwd(io.G, io.U, io.Z, rows * d2, stream)
+                 : sa::launch_swiglu_gate(io.G, io.U, rows * d2, stream);
+    if (e == hipSuccess)
+        e = sa::launch_small_gemm({Z, false, M * d2, d2, 1}, {w.w2(l), bf, d2 * d, d, 1}, io.Xhat, false,
+                                  (int32_t)BH, M, d, (int32_t)d2, stream, H);
+    // Xt' = LN2(Xbar + FFN)
+    if (e == hipSuccess)
+        e = sa::launch_add_ln(io.Xbar, false, rows, io.Xhat, w.ln_(l, 2), w.ln_(l, 3), bf, rows, H, M, d, eps,
+                              io.out, stream, io.Y2);
+    if (e != hipSuccess) return hip_fail(e, "block refinement launch");
+    return SA_OK;
+}
+
 // forward on a checked plan and workspace (shared by sa_sketch_fwd and sa_layer_fwd)
 sa_status run_fwd(const void* K, const void* V, const void* P, const int64_t* offsets, int64_t B,
                   int64_t T, int32_t H, int32_t M, int32_t d, float scale, sa_dtype dtype,
@@ -390,7 +534,8 @@ sa_status run_fwd(const void* K, const void* V, const void* P, const int64_t* of
 sa_status run_bwd(const void* K, const void* V, const void* P, const int64_t* offsets, int64_t B,
                   int64_t T, int32_t H, int32_t M, int32_t d, float scale, sa_dtype dtype,
                   const float* dsketch, int32_t R, const float* lse, float* dK, float* dV,
-                  float* dP, float* dX, uint8_t* ws, const BwdPlan& plan, hipStream_t stream) {
+                  float* dP, float* dX, uint8_t* ws, const BwdPlan& plan, hipStream_t stream,
+                  bool p_user = false) {
     float* dY = reinterpret_cast<float*>(ws + plan.off_dY);
     float* Dbuf = reinterpret_cast<float*>(ws + plan.off_D);
     float* part = reinterpret_cast<float*>(ws + plan.off_part);
@@ -423,6 +568,7 @@ sa_status run_bwd(const void* K, const void* V, const void* P, const int64_t* of
         f.dV = dV;
         f.dP = dP;
         f.dX = dX;
+        f.p_user = p_user;
         {
             sa::ProfScope ps("worklist", stream);
             e = sa::launch_worklist(offsets, B, T, H, plan.C, plan.n_ranges,
@@ -444,7 +590,7 @@ sa_status run_bwd(const void* K, const void* V, const void* P, const int64_t* of
     {
         sa::ProfScope ps("plain_bwd", stream);
         e = sa::launch_generic_bwd(K, V, P, offsets, B, T, H, M, d, scale, dtype == SA_BF16, dY,
-                                   lse, Dbuf, dK, dV, dP, part, plan.n_chunks, stream);
+                                   lse, Dbuf, dK, dV, dP, part, plan.n_chunks, stream, p_user);
     }
     if (e != hipSuccess) return hip_fail(e, "backward launch");
     if (dX) {
@@ -765,62 +911,198 @@ sa_status sa_block_fwd(const void* X, const void* P, const void* Wq, const void*
     }
     uint8_t* ws = reinterpret_cast<uint8_t*>(workspace);
     float* state = reinterpret_cast<float*>(ws + plan.off_state);
-    float* Q = reinterpret_cast<float*>(ws + plan.off_q);
-    void* Pp = ws + plan.off_pp;
-    float* Xhat = reinterpret_cast<float*>(ws + plan.off_xhat);
-    float* Xbar = reinterpret_cast<float*>(ws + plan.off_xbar);
-    float* G = reinterpret_cast<float*>(ws + plan.off_g);
-    float* U = reinterpret_cast<float*>(ws + plan.off_u);
+    const BlockParams w{Wq, Wk, ln, W1, W3, W2, H, d, (size_t)(dtype == SA_BF16 ? 2 : 4)};
+    for (int32_t l = 0; l < n_layers; ++l) {
+        BlockLayerIo io{};
+        io.first = l == 0;
+        io.xt = io.first ? P : state;
+        io.Q = reinterpret_cast<float*>(ws + plan.off_q);
+        io.Pp = ws + plan.off_pp;
+        io.lse = lse ? lse + (size_t)l * T * H : reinterpret_cast<float*>(ws + plan.off_lse);
+        io.Xhat = reinterpret_cast<float*>(ws + plan.off_xhat);
+        io.Xbar = reinterpret_cast<float*>(ws + plan.off_xbar);
+        io.G = reinterpret_cast<float*>(ws + plan.off_g);
+        io.U = reinterpret_cast<float*>(ws + plan.off_u);
+        io.out = l == n_layers - 1 ? out : state;
+        st = block_layer_fwd(X, offsets, B, T, H, M, d, l, scale, eps, dtype, w, io, ws + plan.off_base, plan.base,
+                             stream);
+        if (st != SA_OK) return st;
+    }
+    return SA_OK;
+}
+
+size_t sa_block_bwd_workspace_size(int64_t B, int64_t T, int32_t H, int32_t M, int32_t d,
+                                   int32_t n_layers, sa_dtype dtype) {
+    if (check_common(B, T, H, M, d, 1.0f, dtype) != SA_OK || n_layers < 1) return 0;
+    return plan_block_bwd(B, T, H, M, d, n_layers, dtype).total;
+}
+
+sa_status sa_block_bwd(const void* X, const void* P, const void* Wq, const void* Wk, const void* ln,
+                       const void* W1, const void* W3, const void* W2, const int64_t* offsets, int64_t B,
+                       int64_t T, int32_t H, int32_t M, int32_t d, int32_t n_layers, float scale, float eps,
+                       sa_dtype dtype, const float* dout, float* dX, float* dP, float* dWq, float* dWk,
+                       float* dln, float* dW1, float* dW3, float* dW2, void* workspace, size_t workspace_bytes,
+                       void* stream_) {
+    g_last_error[0] = 0;
+    sa_status st = check_common(B, T, H, M, d, scale, dtype);
+    if (st != SA_OK) return st;
+    if (n_layers < 1) return fail(SA_ERR_INVALID_ARG, "n_layers must be >= 1 (got %d)", n_layers);
+    if (!(std::isfinite(eps) && eps > 0.f)) return fail(SA_ERR_INVALID_ARG, "eps must be finite and > 0");
+    if (B < 1) return fail(SA_ERR_INVALID_ARG, "B must be >= 1 for the backward (got %lld)", (long long)B);
+    if (B > 65535) return fail(SA_ERR_UNSUPPORTED, "more than 65535 users");
+    if (!offsets || !P || !Wq || !Wk || !ln || !W1 || !W3 || !W2 || !dout || !dP || !dWq || !dWk || !dln ||
+        !dW1 || !dW3 || !dW2 || (T > 0 && (!X || !dX)))
+        return fail(SA_ERR_INVALID_ARG, "null pointer argument");
+    if (!aligned16(X) || !aligned16(P) || !aligned16(Wq) || !aligned16(Wk) || !aligned16(ln) || !aligned16(W1) ||
+        !aligned16(W3) || !aligned16(W2) || !aligned16(dout) || !aligned16(dX) || !aligned16(dP) ||
+        !aligned16(dWq) || !aligned16(dWk) || !aligned16(dln) || !aligned16(dW1) || !aligned16(dW3) ||
+        !aligned16(dW2))
+        return fail(SA_ERR_INVALID_ARG, "tensor arguments must be 16-byte aligned");
+    hipStream_t stream = reinterpret_cast<hipStream_t>(stream_);
+    const BlockBwdPlan plan = plan_block_bwd(B, T, H, M, d, n_layers, dtype);
+    if (!workspace || workspace_bytes < plan.total)
+        return fail(SA_ERR_WORKSPACE, "workspace of %zu bytes needed, %zu given", plan.total,
+                    workspace ? workspace_bytes : (size_t)0);
+    if (debug_validate()) {
+        st = validate_offsets(offsets, B, T, stream);
+        if (st != SA_OK) return st;
+    }
+    uint8_t* ws = reinterpret_cast<uint8_t*>(workspace);
+    auto F = [&](size_t o) { return reinterpret_cast<float*>(ws + o); };
+    const BlockParams w{Wq, Wk, ln, W1, W3, W2, H, d, (size_t)(dtype == SA_BF16 ? 2 : 4)};
     const bool bf = dtype == SA_BF16;
-    const size_t el = bf ? 2 : 4;
     const int64_t md = (int64_t)M * d, dd = (int64_t)d * d, d2 = 2 * (int64_t)d;
     const int64_t BH = B * H, rows = BH * M;
-    hipError_t e = hipSuccess;
+    auto layer_io = [&](int32_t l) {
+        uint8_t* r = ws + plan.off_layers + plan.l_stride * (size_t)l;
+        BlockLayerIo io{};
+        io.first = l == 0;
+        io.xt = io.first ? P : reinterpret_cast<const void*>(r + plan.l_state);
+        io.Q = reinterpret_cast<float*>(r + plan.l_q);
+        io.Pp = r + plan.l_pp;
+        io.lse = reinterpret_cast<float*>(r + plan.l_lse);
+        io.Y1 = reinterpret_cast<float*>(r + plan.l_y1);
+        io.Xbar = reinterpret_cast<float*>(r + plan.l_xbar);
+        io.G = reinterpret_cast<float*>(r + plan.l_g);
+        io.U = reinterpret_cast<float*>(r + plan.l_u);
+        io.Y2 = reinterpret_cast<float*>(r + plan.l_y2);
+        io.Xhat = F(plan.off_xhat);
+        io.Z = F(plan.off_z);
+        // the state of the next layer, or (last layer) a scratch output
+        io.out = l + 1 < n_layers
+                     ? reinterpret_cast<float*>(ws + plan.off_layers + plan.l_stride * (size_t)(l + 1) + plan.l_state)
+                     : F(plan.off_out);
+        return io;
+    };
+    // forward replay keeping every layer's intermediates
     for (int32_t l = 0; l < n_layers; ++l) {
-        const bool first = l == 0;
-        const uint8_t* wq = reinterpret_cast<const uint8_t*>(Wq) + el * (size_t)l * H * dd;
-        const uint8_t* wk = reinterpret_cast<const uint8_t*>(Wk) + el * (size_t)l * H * dd;
-        const uint8_t* w1 = reinterpret_cast<const uint8_t*>(W1) + el * (size_t)l * H * d * d2;
-        const uint8_t* w3 = reinterpret_cast<const uint8_t*>(W3) + el * (size_t)l * H * d * d2;
-        const uint8_t* w2 = reinterpret_cast<const uint8_t*>(W2) + el * (size_t)l * H * d2 * d;
-        auto lnp = [&](int k) {
-            return reinterpret_cast<const uint8_t*>(ln) + el * ((size_t)(l * 4 + k) * H) * d;
-        };
-        // queries of this layer: the shared prototypes first, then each user's state
-        const int64_t nq = first ? H : BH;
-        {
-            sa::ProfScope ps("block_proj", stream);
-            const sa::MatView xt = first ? sa::MatView{P, bf, md, d, 1} : sa::MatView{state, false, md, d, 1};
-            e = sa::launch_small_gemm(xt, {wq, bf, dd, d, 1}, Q, false, (int32_t)nq, M, d, d, stream, H);
-            if (e == hipSuccess)
-                e = sa::launch_small_gemm({Q, false, md, d, 1}, {wk, bf, dd, 1, d}, Pp, bf, (int32_t)nq, M, d, d,
-                                          stream, H);
-            if (e != hipSuccess) return hip_fail(e, "block projection launch");
-        }
-        float* lse_l = lse ? lse + (size_t)l * T * H : reinterpret_cast<float*>(ws + plan.off_lse);
-        st = run_fwd(X, X, Pp, offsets, B, T, H, M, d, scale, dtype, Xhat, lse_l, ws + plan.off_base, plan.base,
-                     stream, !first);
+        st = block_layer_fwd(X, offsets, B, T, H, M, d, l, scale, eps, dtype, w, layer_io(l), ws + plan.off_base,
+                             plan.fwd, stream);
         if (st != SA_OK) return st;
-        sa::ProfScope ps("block_refine", stream);
-        // Xbar = LN1(Xt + Xhat)
-        e = sa::launch_add_ln(first ? P : state, first && bf, first ? (int64_t)H * M : rows, Xhat, lnp(0), lnp(1),
-                              bf, rows, H, M, d, eps, Xbar, stream);
-        // FFN(Xbar) = (silu(Xbar W1) * (Xbar W3)) W2, into the Xhat buffer
+    }
+    float* Zb = F(plan.off_z);     // Z, then dZ, then dG
+    float* dU = F(plan.off_du);
+    float* dY2 = F(plan.off_dy2);
+    float* dY1 = F(plan.off_dy1);  // the state gradient of the layer below
+    float* dXbar = F(plan.off_xhat);
+    float* dPp = F(plan.off_dpp);
+    float* dQ = F(plan.off_dq);
+    float* wpart = F(plan.off_wpart);
+    float2* stats = reinterpret_cast<float2*>(ws + plan.off_stats);
+    float* colpart = F(plan.off_colpart);
+    const float* dXt = dout;
+    hipError_t e = hipSuccess;
+    for (int32_t l = n_layers - 1; l >= 0; --l) {
+        const BlockLayerIo io = layer_io(l);
+        const int64_t nq = io.first ? H : BH;
+        float* dlnl = dln + (size_t)4 * l * H * d;
+        {
+            sa::ProfScope ps("block_refine_bwd", stream);
+            // LN2: dY2, dgamma2, dbeta2
+            e = sa::launch_ln_bwd(dXt, nullptr, io.Y2, w.ln_(l, 2), bf, B, H, M, d, eps, dY2, stats, colpart,
+                                  plan.nch, dlnl + 2 * (size_t)H * d, (int64_t)H * d, stream);
+            // dW2 = sum over users of Z^T dY2, dZ = dY2 W2^T
+            if (e == hipSuccess) e = sa::launch_swiglu_fwd(io.G, io.U, Zb, rows * d2, stream);
+            if (e == hipSuccess)
+                e = sa::launch_small_gemm({Zb, false, M * d2, 1, d2}, {dY2, false, md, d, 1}, wpart, false,
+                                          (int32_t)BH, (int32_t)d2, d, M, stream);
+            if (e == hipSuccess)
+                e = sa::launch_sum_users(wpart, B, H, d2 * d, dW2 + (size_t)l * H * d2 * d, stream);
+            if (e == hipSuccess)
+                e = sa::launch_small_gemm({dY2, false, md, d, 1}, {w.w2(l), bf, d2 * d, 1, d}, Zb, false,
+                                          (int32_t)BH, M, (int32_t)d2, d, stream, H);
+            // through the gate: dG (over dZ), dU
+            if (e == hipSuccess) e = sa::launch_swiglu_bwd(Zb, io.G, io.U, dU, rows * d2, stream);
+            // dW1 = sum Xbar^T dG, dW3 = sum Xbar^T dU
+            if (e == hipSuccess)
+                e = sa::launch_small_gemm({io.Xbar, false, md, 1, d}, {Zb, false, M * d2, d2, 1}, wpart, false,
+                                          (int32_t)BH, d, (int32_t)d2, M, stream);
+            if (e == hipSuccess)
+                e = sa::launch_sum_users(wpart, B, H, d * d2, dW1 + (size_t)l * H * d * d2, stream);
+            if (e == hipSuccess)
+                e = sa::launch_small_gemm({io.Xbar, false, md, 1, d}, {dU, false, M * d2, d2, 1}, wpart, false,
+                                          (int32_t)BH, d, (int32_t)d2, M, stream);
+            if (e == hipSuccess)
+                e = sa::launch_sum_users(wpart, B, H, d * d2, dW3 + (size_t)l * H * d * d2, stream);
+            // dXbar = dY2 + dG W1^T + dU W3^T (dY2 enters through the norm's second input)
+            if (e == hipSuccess)
+                e = sa::launch_small_gemm({Zb, false, M * d2, d2, 1}, {w.w1(l), bf, d * d2, 1, d2}, dXbar, false,
+                                          (int32_t)BH, M, d, (int32_t)d2, stream, H);
+            if (e == hipSuccess)
+                e = sa::launch_small_gemm({dU, false, M * d2, d2, 1}, {w.w3(l), bf, d * d2, 1, d2}, dXbar, false,
+                                          (int32_t)BH, M, d, (int32_t)d2, stream, H, true);
+            // LN1: dY1 = gradient of Xt + Xhat
+            if (e == hipSuccess)
+                e = sa::launch_ln_bwd(dXbar, dY2, io.Y1, w.ln_(l, 0), bf, B, H, M, d, eps, dY1, stats, colpart,
+                                      plan.nch, dlnl, (int64_t)H * d, stream);
+            if (e != hipSuccess) return hip_fail(e, "block refinement backward launch");
+        }
+        // the sketch (dsketch = dY1, one target instance): dX of this layer and dP'
+        float* dXl = l == n_layers - 1 ? dX : F(plan.off_dxl);
+        if (T > 0) {
+            float* dKs = plan.bshared.fused ? nullptr : F(plan.off_dk);
+            float* dVs = plan.bshared.fused ? nullptr : F(plan.off_dv);
+            st = run_bwd(X, X, io.Pp, offsets, B, T, H, M, d, scale, dtype, dY1, 1, io.lse, dKs, dVs, dPp, dXl,
+                         ws + plan.off_base, io.first ? plan.bshared : plan.buser, stream, !io.first);
+            if (st != SA_OK) return st;
+            if (dXl != dX) {
+                sa::ProfScope ps("dX_sum", stream);
+                e = sa::launch_add(dX, dXl, dX, T * H * d, stream);
+                if (e != hipSuccess) return hip_fail(e, "dX sum launch");
+            }
+        } else {
+            e = sa::launch_fill(dPp, nq * md, 0.f, stream);
+            if (e != hipSuccess) return hip_fail(e, "fill launch");
+        }
+        sa::ProfScope ps("block_proj_grads", stream);
+        // P' = Q W_K^T, Q = Xt W_Q:  dW_K = sum dP'^T Q, dQ = dP' W_K, dW_Q = sum Xt^T dQ,
+        // and the state gradient dXt = dY1 + dQ W_Q^T
+        float* dwk = dWk + (size_t)l * H * dd;
+        float* dwq = dWq + (size_t)l * H * dd;
+        e = sa::launch_small_gemm({dPp, false, md, 1, d}, {io.Q, false, md, d, 1}, io.first ? dwk : wpart, false,
+                                  (int32_t)nq, d, d, M, stream);
+        if (e == hipSuccess && !io.first) e = sa::launch_sum_users(wpart, B, H, dd, dwk, stream);
         if (e == hipSuccess)
-            e = sa::launch_small_gemm({Xbar, false, md, d, 1}, {w1, bf, d * d2, d2, 1}, G, false, (int32_t)BH, M,
-                                      (int32_t)d2, d, stream, H);
+            e = sa::launch_small_gemm({dPp, false, md, d, 1}, {w.wk(l), bf, dd, d, 1}, dQ, false, (int32_t)nq, M, d,
+                                      d, stream, H);
         if (e == hipSuccess)
-            e = sa::launch_small_gemm({Xbar, false, md, d, 1}, {w3, bf, d * d2, d2, 1}, U, false, (int32_t)BH, M,
-                                      (int32_t)d2, d, stream, H);
-        if (e == hipSuccess) e = sa::launch_swiglu_gate(G, U, rows * d2, stream);
-        if (e == hipSuccess)
-            e = sa::launch_small_gemm({G, false, M * d2, d2, 1}, {w2, bf, d2 * d, d, 1}, Xhat, false, (int32_t)BH, M,
-                                      d, (int32_t)d2, stream, H);
-        // Xt' = LN2(Xbar + FFN)
-        if (e == hipSuccess)
-            e = sa::launch_add_ln(Xbar, false, rows, Xhat, lnp(2), lnp(3), bf, rows, H, M, d, eps,
-                                  l == n_layers - 1 ? out : state, stream);
-        if (e != hipSuccess) return hip_fail(e, "block refinement launch");
+            e = sa::launch_small_gemm({io.xt, io.first && bf, md, 1, d}, {dQ, false, md, d, 1},
+                                      io.first ? dwq : wpart, false, (int32_t)nq, d, d, M, stream);
+        if (e == hipSuccess && !io.first) e = sa::launch_sum_users(wpart, B, H, dd, dwq, stream);
+        if (e == hipSuccess) {
+            if (io.first) {
+                // the shared prototypes: dP = sum over users of dY1, plus dQ W_Q^T
+                e = sa::launch_sum_users(dY1, B, H, md, dP, stream);
+                if (e == hipSuccess)
+                    e = sa::launch_small_gemm({dQ, false, md, d, 1}, {w.wq(l), bf, dd, 1, d}, dP, false, H, M, d, d,
+                                              stream, H, true);
+            } else {
+                e = sa::launch_small_gemm({dQ, false, md, d, 1}, {w.wq(l), bf, dd, 1, d}, dY1, false, (int32_t)BH,
+                                          M, d, d, stream, H, true);
+            }
+        }
+        if (e != hipSuccess) return hip_fail(e, "block projection gradient launch");
+        dXt = dY1;
     }
     return SA_OK;
 }

@@ -33,7 +33,8 @@ template <int D, bool XBF16, bool PBF16>
 __global__ __launch_bounds__(256) void add_ln_kernel(const void* __restrict__ x, int64_t x_rows,
                                                      const float* __restrict__ y, const void* __restrict__ gamma,
                                                      const void* __restrict__ beta, int64_t rows, int32_t H,
-                                                     int32_t M, float eps, float* __restrict__ out) {
+                                                     int32_t M, float eps, float* __restrict__ out,
+                                                     float* __restrict__ sum_out) {
     constexpr int E = D / 64;   // features per lane
     const int64_t r = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
     if (r >= rows) return;
@@ -46,6 +47,7 @@ __global__ __launch_bounds__(256) void add_ln_kernel(const void* __restrict__ x,
     for (int e = 0; e < E; ++e) {
         const int j = lane + 64 * e;
         v[e] = ldv<XBF16>(x, xr * D + j) + y[r * D + j];
+        if (sum_out) sum_out[r * D + j] = v[e];
         s += v[e];
     }
     const float mean = wave_sum(s) * (1.0f / D);
@@ -77,14 +79,136 @@ __global__ __launch_bounds__(256) void swiglu_gate_kernel(float* __restrict__ g,
     reinterpret_cast<float4*>(g)[i] = a;
 }
 
+// z = silu(g) * u (g, u kept for the backward)
+__global__ __launch_bounds__(256) void swiglu_fwd_kernel(const float* __restrict__ g, const float* __restrict__ u,
+                                                         float* __restrict__ z, int64_t n) {
+    const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    if (i >= n) return;
+    const float a = g[i];
+    z[i] = a / (1.0f + __expf(-a)) * u[i];
+}
+
+// Backward of z = silu(g) * u: dg = dz u s (1 + g (1 - s)), du = dz g s, s = sigmoid(g).
+// dg overwrites dz.
+__global__ __launch_bounds__(256) void swiglu_bwd_kernel(float* __restrict__ dz_dg, const float* __restrict__ g,
+                                                         const float* __restrict__ u, float* __restrict__ du,
+                                                         int64_t n) {
+    const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    if (i >= n) return;
+    const float a = g[i], dz = dz_dg[i];
+    const float sg = 1.0f / (1.0f + __expf(-a));
+    dz_dg[i] = dz * u[i] * sg * (1.0f + a * (1.0f - sg));
+    du[i] = dz * a * sg;
+}
+
+// Backward of out = LN(y) * gamma + beta per row (one wave per row):
+// dx = rstd (g - mean(g) - xh mean(g xh)), g = (dy1 + dy2) gamma, xh = (y - mean) rstd.
+// dy2 may be null.  Writes (mean, rstd) per row for the gamma / beta reduction.
+template <int D, bool PBF16>
+__global__ __launch_bounds__(256) void ln_bwd_kernel(const float* __restrict__ dy1, const float* __restrict__ dy2,
+                                                     const float* __restrict__ y, const void* __restrict__ gamma,
+                                                     int64_t rows, int32_t H, int32_t M, float eps,
+                                                     float* __restrict__ dx, float2* __restrict__ stats) {
+    constexpr int E = D / 64;
+    const int64_t r = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+    if (r >= rows) return;
+    const int lane = threadIdx.x & 63;
+    const int64_t h = (r / M) % H;
+    float v[E], gv[E];
+    float s = 0.f;
+#pragma unroll
+    for (int e = 0; e < E; ++e) {
+        v[e] = y[r * D + lane + 64 * e];
+        s += v[e];
+    }
+    const float mean = wave_sum(s) * (1.0f / D);
+    float q = 0.f;
+#pragma unroll
+    for (int e = 0; e < E; ++e) {
+        v[e] -= mean;
+        q = __builtin_fmaf(v[e], v[e], q);
+    }
+    const float rstd = 1.0f / __builtin_sqrtf(wave_sum(q) * (1.0f / D) + eps);
+    float sg = 0.f, sgx = 0.f;
+#pragma unroll
+    for (int e = 0; e < E; ++e) {
+        const int j = lane + 64 * e;
+        float d = dy1[r * D + j];
+        if (dy2) d += dy2[r * D + j];
+        v[e] *= rstd;   // xh
+        gv[e] = d * ldv<PBF16>(gamma, h * D + j);
+        sg += gv[e];
+        sgx = __builtin_fmaf(gv[e], v[e], sgx);
+    }
+    const float mg = wave_sum(sg) * (1.0f / D), mgx = wave_sum(sgx) * (1.0f / D);
+#pragma unroll
+    for (int e = 0; e < E; ++e) dx[r * D + lane + 64 * e] = rstd * (gv[e] - mg - v[e] * mgx);
+    if (lane == 0) stats[r] = make_float2(mean, rstd);
+}
+
+// Column sums for gamma / beta of one layer norm: part[c][h][0][j] = sum over the
+// chunk c of head h's rows of (dy1 + dy2) * xh, part[c][h][1][j] of (dy1 + dy2).
+// Rows of head h: (b * H + h) * M + m; a chunk covers CH consecutive (b, m).
+template <int D>
+__global__ __launch_bounds__(256) void ln_colsum_kernel(const float* __restrict__ dy1, const float* __restrict__ dy2,
+                                                        const float* __restrict__ y, const float2* __restrict__ stats,
+                                                        int64_t B, int32_t H, int32_t M, int64_t CH,
+                                                        float* __restrict__ part) {
+    const int j = blockIdx.y * 256 + threadIdx.x;
+    if (j >= D) return;
+    const int64_t h = blockIdx.z, c = blockIdx.x;
+    const int64_t n = B * M;
+    const int64_t i0 = c * CH, i1 = i0 + CH < n ? i0 + CH : n;
+    float sx = 0.f, s1 = 0.f;
+    for (int64_t i = i0; i < i1; ++i) {
+        const int64_t r = (i / M * H + h) * M + i % M;
+        float d = dy1[r * D + j];
+        if (dy2) d += dy2[r * D + j];
+        const float2 st = stats[r];
+        sx = __builtin_fmaf(d, (y[r * D + j] - st.x) * st.y, sx);
+        s1 += d;
+    }
+    float* o = part + ((c * H + h) * 2) * D;
+    o[j] = sx;
+    o[D + j] = s1;
+}
+
+// out[h][k][j] = sum over chunks, in order, of part[c][h][k][j]; out has a
+// stride of ostride floats between k = 0 (gamma) and k = 1 (beta)
+__global__ __launch_bounds__(256) void ln_chunk_sum_kernel(const float* __restrict__ part, int64_t nch, int32_t H,
+                                                           int32_t D, float* __restrict__ out, int64_t ostride) {
+    const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    if (i >= (int64_t)H * 2 * D) return;
+    const int64_t h = i / (2 * D), k = (i / D) % 2, j = i % D;
+    float s = 0.f;
+    for (int64_t c = 0; c < nch; ++c) s += part[((c * H + h) * 2 + k) * D + j];
+    out[k * ostride + h * D + j] = s;
+}
+
+__global__ __launch_bounds__(256) void fill_kernel(float* __restrict__ p, int64_t n, float v) {
+    const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    if (i < n) p[i] = v;
+}
+
+// out[h][i] = sum over users b, in order, of part[b * H + h][i]  (n values per block)
+__global__ __launch_bounds__(256) void sum_users_kernel(const float* __restrict__ part, int64_t B, int32_t H,
+                                                        int64_t n, float* __restrict__ out) {
+    const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    if (i >= (int64_t)H * n) return;
+    const int64_t h = i / n, k = i % n;
+    float s = 0.f;
+    for (int64_t b = 0; b < B; ++b) s += part[(b * H + h) * n + k];
+    out[i] = s;
+}
+
 template <int D>
 hipError_t add_ln_d(const void* x, bool x_bf16, int64_t x_rows, const float* y, const void* gamma,
                     const void* beta, bool p_bf16, int64_t rows, int32_t H, int32_t M, float eps, float* out,
-                    hipStream_t stream) {
+                    float* sum_out, hipStream_t stream) {
     const dim3 grid((unsigned)((rows + 3) / 4));
 #define SA_LN(XB, PB)                                                                                      \
     hipLaunchKernelGGL((add_ln_kernel<D, XB, PB>), grid, dim3(256), 0, stream, x, x_rows, y, gamma, beta, \
-                       rows, H, M, eps, out)
+                       rows, H, M, eps, out, sum_out)
     if (x_bf16) {
         if (p_bf16) SA_LN(true, true); else SA_LN(true, false);
     } else {
@@ -98,11 +222,69 @@ hipError_t add_ln_d(const void* x, bool x_bf16, int64_t x_rows, const float* y, 
 
 hipError_t launch_add_ln(const void* x, bool x_bf16, int64_t x_rows, const float* y, const void* gamma,
                          const void* beta, bool p_bf16, int64_t rows, int32_t H, int32_t M, int32_t d, float eps,
-                         float* out, hipStream_t stream) {
+                         float* out, hipStream_t stream, float* sum_out) {
     if (rows <= 0) return hipSuccess;
-    if (d == 64) return add_ln_d<64>(x, x_bf16, x_rows, y, gamma, beta, p_bf16, rows, H, M, eps, out, stream);
-    if (d == 128) return add_ln_d<128>(x, x_bf16, x_rows, y, gamma, beta, p_bf16, rows, H, M, eps, out, stream);
+    if (d == 64)
+        return add_ln_d<64>(x, x_bf16, x_rows, y, gamma, beta, p_bf16, rows, H, M, eps, out, sum_out, stream);
+    if (d == 128)
+        return add_ln_d<128>(x, x_bf16, x_rows, y, gamma, beta, p_bf16, rows, H, M, eps, out, sum_out, stream);
     return hipErrorInvalidValue;
+}
+
+hipError_t launch_swiglu_fwd(const float* g, const float* u, float* z, int64_t n, hipStream_t stream) {
+    if (n <= 0) return hipSuccess;
+    hipLaunchKernelGGL(swiglu_fwd_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, stream, g, u, z, n);
+    return hipGetLastError();
+}
+
+hipError_t launch_swiglu_bwd(float* dz_dg, const float* g, const float* u, float* du, int64_t n,
+                             hipStream_t stream) {
+    if (n <= 0) return hipSuccess;
+    hipLaunchKernelGGL(swiglu_bwd_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, stream, dz_dg, g, u,
+                       du, n);
+    return hipGetLastError();
+}
+
+hipError_t launch_ln_bwd(const float* dy1, const float* dy2, const float* y, const void* gamma, bool p_bf16,
+                         int64_t B, int32_t H, int32_t M, int32_t d, float eps, float* dx, float2* stats,
+                         float* colpart, int64_t nch, float* dgamma_dbeta, int64_t ostride, hipStream_t stream) {
+    const int64_t rows = B * H * M;
+    if (rows <= 0) return hipSuccess;
+    const dim3 grid((unsigned)((rows + 3) / 4));
+    const int64_t n = B * M, CH = (n + nch - 1) / nch;
+#define SA_COL(DD)                                                                                            \
+    hipLaunchKernelGGL(ln_colsum_kernel<DD>, dim3((unsigned)nch, 1, (unsigned)H), dim3(256), 0, stream, dy1, \
+                       dy2, y, stats, B, H, M, CH, colpart)
+#define SA_LNB(DD, PB)                                                                                    \
+    hipLaunchKernelGGL((ln_bwd_kernel<DD, PB>), grid, dim3(256), 0, stream, dy1, dy2, y, gamma, rows, H, M, \
+                       eps, dx, stats)
+    // rows first: the column sums read their statistics
+    if (d == 64) { if (p_bf16) SA_LNB(64, true); else SA_LNB(64, false); }
+    else { if (p_bf16) SA_LNB(128, true); else SA_LNB(128, false); }
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    if (d == 64) SA_COL(64); else SA_COL(128);
+#undef SA_COL
+#undef SA_LNB
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    const int64_t m = (int64_t)H * 2 * d;
+    hipLaunchKernelGGL(ln_chunk_sum_kernel, dim3((unsigned)((m + 255) / 256)), dim3(256), 0, stream, colpart, nch, H,
+                       d, dgamma_dbeta, ostride);
+    return hipGetLastError();
+}
+
+hipError_t launch_fill(float* p, int64_t n, float v, hipStream_t stream) {
+    if (n <= 0) return hipSuccess;
+    hipLaunchKernelGGL(fill_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, stream, p, n, v);
+    return hipGetLastError();
+}
+
+hipError_t launch_sum_users(const float* part, int64_t B, int32_t H, int64_t n, float* out, hipStream_t stream) {
+    const int64_t m = (int64_t)H * n;
+    if (m <= 0) return hipSuccess;
+    hipLaunchKernelGGL(sum_users_kernel, dim3((unsigned)((m + 255) / 256)), dim3(256), 0, stream, part, B, H, n, out);
+    return hipGetLastError();
 }
 
 hipError_t launch_swiglu_gate(float* g, const float* u, int64_t n, hipStream_t stream) {

@@ -72,10 +72,11 @@ __device__ inline float xhalf_sum(float v) {
 // and transposed Yjm[b,h,j,p] with p = perm16(m); P -> Pjm[h,j,p] likewise.
 // One workgroup per 32-prototype block: the rows are summed and converted with
 // 16-byte accesses, staged in LDS, and the transposed block is written as 64-byte
-// rows.  Workgroups [0, B*H*M/32) take dY blocks, the next H*M/32 take P blocks.
+// rows.  Workgroups [0, B*H*M/32) take dY blocks, the next n_p*M/32 take P blocks
+// (n_p = H shared prototype blocks, or B*H with one block per user and head).
 template <int D>
 __global__ __launch_bounds__(256) void prep_kernel(const float* __restrict__ ds, int64_t B, int32_t R,
-                                                   int32_t H, int32_t M,
+                                                   int32_t H, int32_t M, int64_t n_p,
                                                    const uint16_t* __restrict__ P,
                                                    uint16_t* __restrict__ Ymj,
                                                    uint16_t* __restrict__ Yjm,
@@ -90,7 +91,7 @@ __global__ __launch_bounds__(256) void prep_kernel(const float* __restrict__ ds,
     const bool is_y = blk < B * H * nb;
     const int64_t pair = is_y ? blk / nb : (blk - B * H * nb) / nb;   // b*H + h, or h
     const int mb = (int)((is_y ? blk : blk - B * H * nb) % nb);
-    if (!is_y && pair >= H) return;
+    if (!is_y && pair >= n_p) return;
     uint16_t* rowdst = is_y ? Ymj + pair * MD : nullptr;
     uint16_t* trdst = (is_y ? Yjm : Pjm) + pair * MD;
     for (int i = tid; i < NCH; i += 256) {
@@ -170,6 +171,7 @@ struct TokArgs {
     float* dV;
     float* dX;      // XV: dX = dV + dK (K and V are the same tensor X)
     float* Dbuf;
+    bool p_user;    // P, Pjm hold one block per (user, head)
 };
 
 // XV: K and V are one tensor X (the SA layer aggregates its own history and its
@@ -242,8 +244,9 @@ __global__ __launch_bounds__(NW * 64, 8 / NW) void bwd_token_kernel(TokArgs a) {
     // the global chunk that belongs at LDS chunk position p = 64 q + l of the
     // swizzled layout (the XOR swizzle is its own inverse).
     auto fetch = [&](const Blk& c, int mb, int sweep, int buf) __attribute__((always_inline)) {
-        const uint16_t* Pmj_g = a.P + (int64_t)c.h * MD;
-        const uint16_t* Pjm_g = a.Pjm + (int64_t)c.h * MD;
+        const int64_t pkey = a.p_user ? (int64_t)c.b * a.H + c.h : c.h;
+        const uint16_t* Pmj_g = a.P + pkey * MD;
+        const uint16_t* Pjm_g = a.Pjm + pkey * MD;
         const uint16_t* Ymj_g = a.Ymj + ((int64_t)c.b * a.H + c.h) * MD;
         const uint16_t* Yjm_g = a.Yjm + ((int64_t)c.b * a.H + c.h) * MD;
         uint16_t* L = lds + buf * C::BUF;
@@ -518,6 +521,7 @@ struct ProtoArgs {
     int32_t parts;    // M / MP
     float scale;
     float* partials;  // [max_items][M][D]
+    bool p_user;      // P holds one block per (user, head)
 };
 
 // XV: K and V are one tensor (one tile load serves both operands).
@@ -545,13 +549,14 @@ __global__ __launch_bounds__(NW * 64, 1) void bwd_proto_kernel(ProtoArgs a) {
     const float ks2 = a.scale * kLog2e;
     const int64_t MD = (int64_t)a.M * D;
     const uint32_t row_stride = (uint32_t)a.H * D;
-    int cur_h = -1;
+    int64_t cur_p = -1;
 
     for (int64_t k = k0; k < k1; ++k) {
         const int32_t* it = a.items + k * IT_WORDS;
         const int b = it[IT_B], h = it[IT_H], t0 = it[IT_T0], t1 = it[IT_T1];
         if (b < 0 || b >= a.B || h < 0 || h >= a.H || t0 < 0 || t1 < t0 || t1 > a.T) continue;
-        const uint16_t* Pg = a.P + (int64_t)h * MD + (int64_t)part * C::MP * D;
+        const int64_t pkey = a.p_user ? (int64_t)b * a.H + h : h;
+        const uint16_t* Pg = a.P + pkey * MD + (int64_t)part * C::MP * D;
         const uint16_t* Yg = a.Ymj + ((int64_t)b * a.H + h) * MD + (int64_t)part * C::MP * D;
 
         // token tiles: global -> registers one tile ahead, registers -> LDS buffer
@@ -615,11 +620,11 @@ __global__ __launch_bounds__(NW * 64, 1) void bwd_proto_kernel(ProtoArgs a) {
         if constexpr (!kHold) {
             for (int i = tid; i < C::MP * C::KCH; i += C::THREADS) {
                 const int r = i / C::KCH, c = i % C::KCH;
-                if (h != cur_h) *reinterpret_cast<u32x4*>(Ps + swz<D>(r, c)) = reinterpret_cast<const u32x4*>(Pg)[i];
+                if (pkey != cur_p) *reinterpret_cast<u32x4*>(Ps + swz<D>(r, c)) = reinterpret_cast<const u32x4*>(Pg)[i];
                 *reinterpret_cast<u32x4*>(Ys + swz<D>(r, c)) = reinterpret_cast<const u32x4*>(Yg)[i];
             }
         }
-        cur_h = h;
+        cur_p = pkey;
         store(0);
         __syncthreads();
 
@@ -730,6 +735,31 @@ __global__ __launch_bounds__(256) void dp_sum_kernel(const int32_t* __restrict__
     *reinterpret_cast<float4*>(dP + i) = acc;
 }
 
+// dP[b,h] = sum of the partials of the segments of pair (b, h), in segment order
+// (per-user prototypes); zero for a pair without tokens
+__global__ __launch_bounds__(256) void dp_pair_sum_kernel(const int32_t* __restrict__ pair_start, int64_t B,
+                                                          int32_t H, int64_t max_items,
+                                                          const float* __restrict__ partials, int64_t MD,
+                                                          float* __restrict__ dP) {
+    const int64_t i = ((int64_t)blockIdx.x * 256 + threadIdx.x) * 4;
+    if (i >= B * H * MD) return;
+    const int64_t bh = i / MD, rest = i % MD;
+    const int64_t b = bh / H, h = bh % H;
+    const int64_t pr = h * B + b;   // head-major pair order of the work list
+    int64_t s0 = pair_start[pr], s1 = pair_start[pr + 1];
+    s0 = s0 < 0 ? 0 : (s0 > max_items ? max_items : s0);
+    s1 = s1 < s0 ? s0 : (s1 > max_items ? max_items : s1);
+    float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+    for (int64_t k = s0; k < s1; ++k) {
+        const float4 v = *reinterpret_cast<const float4*>(partials + k * MD + rest);
+        acc.x += v.x;
+        acc.y += v.y;
+        acc.z += v.z;
+        acc.w += v.w;
+    }
+    *reinterpret_cast<float4*>(dP + i) = acc;
+}
+
 template <int D, int NW, bool XV>
 hipError_t launch_token(const TokArgs& a, int64_t n_ranges, hipStream_t stream) {
     using C = TokCfg<D, NW>;
@@ -789,13 +819,14 @@ hipError_t launch_fused_bwd(const FusedBwdArgs& f, hipStream_t stream) {
     // dY (R summed) and P in the layouts the contractions read
     {
         ProfScope ps("bwd_prep", stream);
-        const int64_t nblocks = (f.B * f.H + f.H) * (f.M / 32);
+        const int64_t n_p = f.p_user ? f.B * f.H : f.H;
+        const int64_t nblocks = (f.B * f.H + n_p) * (f.M / 32);
         if (f.d == 64)
             hipLaunchKernelGGL(prep_kernel<64>, dim3((unsigned)nblocks), dim3(256), 0, stream,
-                               f.dsketch, f.B, f.R, f.H, f.M, f.P, f.Ymj, f.Yjm, f.Pjm);
+                               f.dsketch, f.B, f.R, f.H, f.M, n_p, f.P, f.Ymj, f.Yjm, f.Pjm);
         else
             hipLaunchKernelGGL(prep_kernel<128>, dim3((unsigned)nblocks), dim3(256), 0, stream,
-                               f.dsketch, f.B, f.R, f.H, f.M, f.P, f.Ymj, f.Yjm, f.Pjm);
+                               f.dsketch, f.B, f.R, f.H, f.M, n_p, f.P, f.Ymj, f.Yjm, f.Pjm);
         hipError_t e = hipGetLastError();
         if (e != hipSuccess) return e;
     }
@@ -804,7 +835,7 @@ hipError_t launch_fused_bwd(const FusedBwdArgs& f, hipStream_t stream) {
         t.K = f.K; t.V = f.V; t.P = f.P; t.Pjm = f.Pjm; t.Ymj = f.Ymj; t.Yjm = f.Yjm;
         t.lse = f.lse; t.items = f.items; t.wg_start = f.wg_start; t.max_items = f.max_items;
         t.T = f.T; t.B = (int32_t)f.B; t.H = f.H; t.M = f.M; t.scale = f.scale;
-        t.dK = f.dK; t.dV = f.dV; t.dX = f.dX; t.Dbuf = f.Dbuf;
+        t.dK = f.dK; t.dV = f.dV; t.dX = f.dX; t.Dbuf = f.Dbuf; t.p_user = f.p_user;
         const bool xv = f.dX != nullptr;
         hipError_t e;
         {
@@ -817,6 +848,7 @@ hipError_t launch_fused_bwd(const FusedBwdArgs& f, hipStream_t stream) {
         p.K = f.K; p.V = f.V; p.P = f.P; p.Ymj = f.Ymj; p.lse = f.lse; p.Dbuf = f.Dbuf;
         p.items = f.items; p.wg_start = f.wg_start; p.max_items = f.max_items; p.T = f.T;
         p.B = (int32_t)f.B; p.H = f.H; p.M = f.M; p.scale = f.scale; p.partials = f.partials;
+        p.p_user = f.p_user;
         const int mp = fused_bwd_part(f.M, f.d);
         ProfScope ps("bwd_proto", stream);
         // eight waves (two per SIMD) when the part has at least 32 prototypes per wave
@@ -830,10 +862,16 @@ hipError_t launch_fused_bwd(const FusedBwdArgs& f, hipStream_t stream) {
         }
         if (e != hipSuccess) return e;
     }
-    const int64_t n = (int64_t)f.H * MD / 4;
     ProfScope ps("bwd_dp_sum", stream);
-    hipLaunchKernelGGL(dp_sum_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, stream,
-                       f.pair_start, f.B, f.H, f.max_items, f.partials, MD, f.dP);
+    if (f.p_user) {
+        const int64_t n = f.B * f.H * MD / 4;
+        hipLaunchKernelGGL(dp_pair_sum_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, stream,
+                           f.pair_start, f.B, f.H, f.max_items, f.partials, MD, f.dP);
+    } else {
+        const int64_t n = (int64_t)f.H * MD / 4;
+        hipLaunchKernelGGL(dp_sum_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, stream,
+                           f.pair_start, f.B, f.H, f.max_items, f.partials, MD, f.dP);
+    }
     return hipGetLastError();
 }
 

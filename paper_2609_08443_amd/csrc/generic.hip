@@ -11,6 +11,8 @@
 // section 4.2 is done first): per token, D_t = sum_m A g, dV_t = sum_m A dY_m,
 // dS = A (g - D_t), dK_t = scale sum_m dS P_m with g_m = V_t . dY_m; then
 // dP[h,m] = scale sum_t dS[t,m] K_t over token chunks, summed in chunk order.
+// With per-user prototypes (P, dP [B,H,M,d]) each user's tokens form one chunk
+// and write their dP block directly.
 #include "sa_internal.h"
 
 namespace sa {
@@ -147,7 +149,7 @@ __global__ __launch_bounds__(256) void bwd_token_kernel(
     const void* __restrict__ K, const void* __restrict__ V, const void* __restrict__ P,
     const int64_t* __restrict__ off, int64_t B, int64_t T, int32_t H, int32_t M,
     float scale, const float* __restrict__ dY, const float* __restrict__ lse,
-    float* __restrict__ Dbuf, float* __restrict__ dK, float* __restrict__ dV) {
+    float* __restrict__ Dbuf, float* __restrict__ dK, float* __restrict__ dV, bool p_user) {
     extern __shared__ float sm[];
     const int lane = threadIdx.x & 63;
     const int w = threadIdx.x >> 6;
@@ -176,9 +178,10 @@ __global__ __launch_bounds__(256) void bwd_token_kernel(
     }
     const float l = lse[i];
     const float* dYb = dY + ((b * H + h) * (int64_t)M) * d;
+    const int64_t pkey = p_user ? b * H + h : h;
     float Dacc = 0.f;
     for (int m = 0; m < M; ++m) {
-        const int64_t pb = ((int64_t)h * M + m) * d;
+        const int64_t pb = (pkey * M + m) * d;
         float s = 0.f, g = 0.f;
         for (int c = 0; c < jpl; ++c) {
             s = __builtin_fmaf(kr[c], ld<BF16>(P, pb + lane + 64 * c), s);
@@ -196,7 +199,7 @@ __global__ __launch_bounds__(256) void bwd_token_kernel(
     }
     for (int m = 0; m < M; ++m) {
         const float dS = aw[m] * (gw[m] - Dacc);
-        const int64_t pb = ((int64_t)h * M + m) * d;
+        const int64_t pb = (pkey * M + m) * d;
         for (int c = 0; c < jpl; ++c) dk[c] = __builtin_fmaf(dS, ld<BF16>(P, pb + lane + 64 * c), dk[c]);
     }
     for (int c = 0; c < jpl; ++c) {
@@ -206,13 +209,14 @@ __global__ __launch_bounds__(256) void bwd_token_kernel(
     if (lane == 0) Dbuf[i] = Dacc;
 }
 
-// grid = (H * ceil(M/64), n_chunks); block = 64 prototypes x 4 column quarters
+// grid = (H * ceil(M/64), n_chunks, or B with per-user prototypes); block = 64
+// prototypes x 4 column quarters
 template <bool BF16, int D>
 __global__ __launch_bounds__(256) void bwd_dp_kernel(
     const void* __restrict__ K, const void* __restrict__ V, const void* __restrict__ P,
     const int64_t* __restrict__ off, int64_t B, int64_t T, int32_t H, int32_t M,
     float scale, const float* __restrict__ dY, const float* __restrict__ lse,
-    const float* __restrict__ Dbuf, int64_t chunk, float* __restrict__ part) {
+    const float* __restrict__ Dbuf, int64_t chunk, bool p_user, float* __restrict__ part) {
     const int mblocks = (M + 63) / 64;
     const int32_t h = blockIdx.x / mblocks;
     const int mb = blockIdx.x % mblocks;
@@ -222,14 +226,22 @@ __global__ __launch_bounds__(256) void bwd_dp_kernel(
     constexpr int d = D;
     constexpr int dq = D / 4;
     const int jb = jq * dq;
+    const int64_t pkey = p_user ? (int64_t)blockIdx.y * H + h : h;
     float pr[dq], yr[dq], acc[dq];
     for (int c = 0; c < dq; ++c) {
-        pr[c] = mv ? ld<BF16>(P, ((int64_t)h * M + m) * d + jb + c) : 0.f;
+        pr[c] = mv ? ld<BF16>(P, (pkey * M + m) * d + jb + c) : 0.f;
         acc[c] = 0.f;
         yr[c] = 0.f;
     }
-    const int64_t ta = (int64_t)blockIdx.y * chunk;
-    const int64_t tb = ta + chunk < T ? ta + chunk : T;
+    int64_t ta, tb;
+    if (p_user) {
+        ta = clampT(off[blockIdx.y], T);
+        tb = clampT(off[blockIdx.y + 1], T);
+        if (tb < ta) tb = ta;
+    } else {
+        ta = (int64_t)blockIdx.y * chunk;
+        tb = ta + chunk < T ? ta + chunk : T;
+    }
     int64_t cur_b = -2, bend = -1;
     for (int64_t t = ta; t < tb; ++t) {
         if (t >= bend || cur_b < 0) {
@@ -261,7 +273,8 @@ __global__ __launch_bounds__(256) void bwd_dp_kernel(
         for (int c = 0; c < dq; ++c) acc[c] = __builtin_fmaf(dS, ld<BF16>(K, base + c), acc[c]);
     }
     if (mv) {
-        float* out = part + (((int64_t)blockIdx.y * H + h) * M + m) * d + jb;
+        // per-user prototypes: pkey = blockIdx.y * H + h, the user's dP block
+        float* out = part + ((p_user ? pkey : (int64_t)blockIdx.y * H + h) * M + m) * d + jb;
         for (int c = 0; c < dq; ++c) out[c] = scale * acc[c];
     }
 }
@@ -298,7 +311,7 @@ template <bool BF16, int D>
 hipError_t bwd_impl(const void* K, const void* V, const void* P, const int64_t* off, int64_t B,
                     int64_t T, int32_t H, int32_t M, int32_t d, float scale, const float* dY,
                     const float* lse, float* Dbuf, float* dK, float* dV, float* dP, float* part,
-                    int32_t n_chunks, hipStream_t stream) {
+                    int32_t n_chunks, bool p_user, hipStream_t stream) {
     hipError_t e;
     if (T * H > 0) {
         const size_t lds = (size_t)4 * 2 * M * sizeof(float);
@@ -307,14 +320,21 @@ hipError_t bwd_impl(const void* K, const void* V, const void* P, const int64_t* 
                                 hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
         if (e != hipSuccess) return e;
         hipLaunchKernelGGL(kern, dim3((unsigned)((T * H + 3) / 4)), dim3(256), lds, stream, K, V,
-                           P, off, B, T, H, M, scale, dY, lse, Dbuf, dK, dV);
+                           P, off, B, T, H, M, scale, dY, lse, Dbuf, dK, dV, p_user);
         e = hipGetLastError();
         if (e != hipSuccess) return e;
     }
     const int64_t chunk = T > 0 ? (T + n_chunks - 1) / n_chunks : 1;
+    if (p_user) {
+        if (B <= 0) return hipSuccess;
+        hipLaunchKernelGGL((bwd_dp_kernel<BF16, D>), dim3((unsigned)(H * ((M + 63) / 64)), (unsigned)B),
+                           dim3(256), 0, stream, K, V, P, off, B, T, H, M, scale, dY, lse, Dbuf, chunk, true,
+                           dP);
+        return hipGetLastError();
+    }
     hipLaunchKernelGGL((bwd_dp_kernel<BF16, D>),
                        dim3((unsigned)(H * ((M + 63) / 64)), (unsigned)n_chunks), dim3(256), 0,
-                       stream, K, V, P, off, B, T, H, M, scale, dY, lse, Dbuf, chunk, part);
+                       stream, K, V, P, off, B, T, H, M, scale, dY, lse, Dbuf, chunk, false, part);
     e = hipGetLastError();
     if (e != hipSuccess) return e;
     const int64_t n = (int64_t)H * M * d;
@@ -358,8 +378,8 @@ hipError_t launch_generic_bwd(const void* K, const void* V, const void* P, const
                               int64_t B, int64_t T, int32_t H, int32_t M, int32_t d, float scale,
                               bool bf16, const float* dY, const float* lse, float* Dbuf,
                               float* dK, float* dV, float* dP, float* part, int32_t n_chunks,
-                              hipStream_t stream) {
-#define SA_BWD(BF, DD) bwd_impl<BF, DD>(K, V, P, off, B, T, H, M, d, scale, dY, lse, Dbuf, dK, dV, dP, part, n_chunks, stream)
+                              hipStream_t stream, bool p_user) {
+#define SA_BWD(BF, DD) bwd_impl<BF, DD>(K, V, P, off, B, T, H, M, d, scale, dY, lse, Dbuf, dK, dV, dP, part, n_chunks, p_user, stream)
     if (d == 64) return bf16 ? SA_BWD(true, 64) : SA_BWD(false, 64);
     if (d == 128) return bf16 ? SA_BWD(true, 128) : SA_BWD(false, 128);
 #undef SA_BWD

@@ -43,7 +43,7 @@ __device__ inline void store_el<uint16_t>(uint16_t* p, int64_t i, float v) { p[i
 
 // C[z][r][c] = sum_k A[z](r, k) B[z % b_mod](k, c) for r < R, c < N, k < Kd, with
 // A(r, k) = A[z * a_h + r * a_r + k * a_k] and B(k, c) = B[z' * b_h + k * b_k + c * b_c];
-// C row-major [R][N] per batch z.  A 64 x 64 output tile per workgroup of 256
+// C row-major [R][N] per batch z (with accumulate, C += instead of C =).  A 64 x 64 output tile per workgroup of 256
 // threads, 4 x 4 outputs per thread; k advances in slabs of 16 staged in LDS
 // (k-major, so each k step is two 16-byte LDS reads for 16 FMAs), the next
 // slab's loads in flight while the current one is used.  Consecutive lanes walk
@@ -52,7 +52,8 @@ template <typename TA, typename TB, typename TC>
 __global__ __launch_bounds__(256) void small_gemm_kernel(const TA* __restrict__ A, int64_t a_h, int64_t a_r,
                                                          int64_t a_k, const TB* __restrict__ Bm, int64_t b_h,
                                                          int64_t b_k, int64_t b_c, int32_t b_mod,
-                                                         TC* __restrict__ C, int32_t R, int32_t N, int32_t Kd) {
+                                                         TC* __restrict__ C, int32_t R, int32_t N, int32_t Kd,
+                                                         bool accumulate) {
     constexpr int TR = 64, TC_ = 64, TK = 16, PAD = 4;
     __shared__ __attribute__((aligned(16))) float As[TK][TR + PAD];   // [k][r]
     __shared__ __attribute__((aligned(16))) float Bs[TK][TC_ + PAD];  // [k][c]
@@ -115,7 +116,9 @@ __global__ __launch_bounds__(256) void small_gemm_kernel(const TA* __restrict__ 
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
             const int c = c0 + tx * 4 + j;
-            if (c < N) store_el(Cz, (int64_t)r * N + c, acc[i][j]);
+            if (c >= N) continue;
+            const int64_t o = (int64_t)r * N + c;
+            store_el(Cz, o, accumulate ? acc[i][j] + load_el(Cz, o) : acc[i][j]);
         }
     }
 }
@@ -131,24 +134,24 @@ __global__ __launch_bounds__(256) void add_kernel(const float* __restrict__ a, c
 
 template <typename TA, typename TB, typename TC>
 hipError_t gemm_t(const MatView& a, const MatView& b, int32_t b_mod, void* c, int32_t H, int32_t R, int32_t N,
-                  int32_t Kd, hipStream_t stream) {
+                  int32_t Kd, bool accumulate, hipStream_t stream) {
     const dim3 grid((unsigned)((R + 63) / 64), (unsigned)((N + 63) / 64), (unsigned)H);
     hipLaunchKernelGGL((small_gemm_kernel<TA, TB, TC>), grid, dim3(256), 0, stream,
                        reinterpret_cast<const TA*>(a.p), a.s_h, a.s_0, a.s_1,
                        reinterpret_cast<const TB*>(b.p), b.s_h, b.s_0, b.s_1, b_mod, reinterpret_cast<TC*>(c),
-                       R, N, Kd);
+                       R, N, Kd, accumulate);
     return hipGetLastError();
 }
 
 }  // namespace
 
 hipError_t launch_small_gemm(const MatView& a, const MatView& b, void* c, bool c_bf16, int32_t H, int32_t R,
-                             int32_t N, int32_t Kd, hipStream_t stream, int32_t b_mod) {
+                             int32_t N, int32_t Kd, hipStream_t stream, int32_t b_mod, bool accumulate) {
     if (H <= 0 || R <= 0 || N <= 0) return hipSuccess;
     if (b_mod <= 0) b_mod = H;
 #define SA_GEMM(TA, TB) \
-    return c_bf16 ? gemm_t<TA, TB, uint16_t>(a, b, b_mod, c, H, R, N, Kd, stream) \
-                  : gemm_t<TA, TB, float>(a, b, b_mod, c, H, R, N, Kd, stream)
+    return c_bf16 ? gemm_t<TA, TB, uint16_t>(a, b, b_mod, c, H, R, N, Kd, accumulate, stream) \
+                  : gemm_t<TA, TB, float>(a, b, b_mod, c, H, R, N, Kd, accumulate, stream)
     if (a.bf16 && b.bf16) SA_GEMM(uint16_t, uint16_t);
     if (a.bf16) SA_GEMM(uint16_t, float);
     if (b.bf16) SA_GEMM(float, uint16_t);

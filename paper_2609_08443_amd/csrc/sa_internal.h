@@ -102,6 +102,9 @@ struct FusedBwdArgs {
     // is its history and whose key projection is absorbed into P): the token
     // side writes dX = dV + dK here instead of dK and dV.
     float* dX;
+    // P (and Pjm) hold one prototype block per (user, head) and dP is [B,H,M,d],
+    // each pair's gradient (stacked layers after the first)
+    bool p_user;
 };
 bool fused_bwd_supported(int32_t M, int32_t d);
 int32_t fused_bwd_part(int32_t M, int32_t d);
@@ -128,22 +131,43 @@ hipError_t launch_tokenwise_generic(const void* K, const void* V, const void* P,
 // k < Kd, z < H batches, C row-major [R][N] per batch, bf16 (rounded) or fp32.
 // Operand element (i, j) of batch z sits at p[z * s_h + i * s_0 + j * s_1], so a
 // transpose is a swap of strides; b_mod <= 0 means b_mod = H (one B per batch).
+// With accumulate the product is added to C's values.
 struct MatView {
     const void* p;
     bool bf16;
     int64_t s_h, s_0, s_1;
 };
 hipError_t launch_small_gemm(const MatView& a, const MatView& b, void* c, bool c_bf16, int32_t H, int32_t R,
-                             int32_t N, int32_t Kd, hipStream_t stream, int32_t b_mod = 0);
+                             int32_t N, int32_t Kd, hipStream_t stream, int32_t b_mod = 0,
+                             bool accumulate = false);
 // Stacked-SA refinement (block.hip).  add_ln: one row of d features per
 // (user, head, prototype): out[r] = LN(x[r mod x_rows] + y[r]) * gamma[h] + beta[h],
 // h = (r / M) % H; x fp32 or bf16 (the shared prototypes broadcast over users
 // when x_rows = H * M), y fp32, gamma / beta [H][d] in the parameter dtype.
+// With sum_out non-null the pre-norm sum x + y is also written there.
 hipError_t launch_add_ln(const void* x, bool x_bf16, int64_t x_rows, const float* y, const void* gamma,
                          const void* beta, bool p_bf16, int64_t rows, int32_t H, int32_t M, int32_t d, float eps,
-                         float* out, hipStream_t stream);
+                         float* out, hipStream_t stream, float* sum_out = nullptr);
 // g = silu(g) * u elementwise (n fp32 values, n a multiple of 4)
 hipError_t launch_swiglu_gate(float* g, const float* u, int64_t n, hipStream_t stream);
+// z = silu(g) * u, keeping g and u
+hipError_t launch_swiglu_fwd(const float* g, const float* u, float* z, int64_t n, hipStream_t stream);
+// backward of z = silu(g) * u: dz_dg holds dz on entry and dg on exit; du written
+hipError_t launch_swiglu_bwd(float* dz_dg, const float* g, const float* u, float* du, int64_t n,
+                             hipStream_t stream);
+// Backward of out = LN(y) * gamma[h] + beta[h] over the B * H * M rows of [B,H,M,d]
+// (fp32): with dout = dy1 + dy2 (dy2 may be null), writes dx (aliasing neither),
+// the per-row (mean, rstd) into stats [rows], and the gamma / beta gradients,
+// [H][d] each, to dgamma_dbeta and dgamma_dbeta + ostride.  The column sums run
+// over nch chunks of the (user, prototype) rows of each head into colpart
+// [nch][H][2][d], then over the chunks in order (deterministic).
+hipError_t launch_ln_bwd(const float* dy1, const float* dy2, const float* y, const void* gamma, bool p_bf16,
+                         int64_t B, int32_t H, int32_t M, int32_t d, float eps, float* dx, float2* stats,
+                         float* colpart, int64_t nch, float* dgamma_dbeta, int64_t ostride, hipStream_t stream);
+// p[i] = v for i < n (fp32)
+hipError_t launch_fill(float* p, int64_t n, float v, hipStream_t stream);
+// out[h][i] = sum over b, in order, of part[b * H + h][i], i < n (fp32)
+hipError_t launch_sum_users(const float* part, int64_t B, int32_t H, int64_t n, float* out, hipStream_t stream);
 
 // out = a + b elementwise (n fp32 values, n a multiple of 4, 16-byte aligned)
 hipError_t launch_add(const float* a, const float* b, float* out, int64_t n, hipStream_t stream);
@@ -162,7 +186,8 @@ hipError_t launch_generic_bwd(const void* K, const void* V, const void* P,
                               const int64_t* offsets, int64_t B, int64_t T, int32_t H,
                               int32_t M, int32_t d, float scale, bool bf16, const float* dY,
                               const float* lse, float* Dbuf, float* dK, float* dV, float* dP,
-                              float* dp_partials, int32_t n_chunks, hipStream_t stream);
+                              float* dp_partials, int32_t n_chunks, hipStream_t stream,
+                              bool p_user = false);
 
 // number of token chunks the generic dP kernel uses (sizes its partial buffer)
 int32_t generic_dp_chunks(int64_t T, int32_t H, int32_t M);

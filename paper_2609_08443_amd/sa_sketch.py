@@ -25,6 +25,7 @@ EXPORTS = ("sa_sketch_fwd_workspace_size", "sa_sketch_fwd", "sa_sketch_bwd_works
            "sa_sketch_fwd_tokenwise_workspace_size", "sa_sketch_fwd_tokenwise",
            "sa_layer_fwd_workspace_size", "sa_layer_fwd", "sa_layer_bwd_workspace_size",
            "sa_layer_bwd", "sa_block_fwd_workspace_size", "sa_block_fwd",
+           "sa_block_bwd_workspace_size", "sa_block_bwd",
            "sa_profile_enable", "sa_kernel_times", "sa_status_string", "sa_last_error")
 
 
@@ -80,6 +81,11 @@ def lib() -> ctypes.CDLL:
     L.sa_block_fwd.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp, vp, i64, i64, i32, i32, i32, i32, f32, f32,
                                c.c_int, vp, vp, vp, sz, vp]
     L.sa_block_fwd.restype = c.c_int
+    L.sa_block_bwd_workspace_size.argtypes = [i64, i64, i32, i32, i32, i32, c.c_int]
+    L.sa_block_bwd_workspace_size.restype = sz
+    L.sa_block_bwd.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp, vp, i64, i64, i32, i32, i32, i32, f32, f32,
+                               c.c_int, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
+    L.sa_block_bwd.restype = c.c_int
     L.sa_build_worklist.argtypes = [vp, i64, i64, i32, i64, vp, i64, vp, vp]
     L.sa_build_worklist.restype = c.c_int
     L.sa_status_string.argtypes = [c.c_int]
@@ -354,6 +360,50 @@ def block_fwd(X, P, Wq, Wk, ln, W1, W3, W2, offsets, scale: Optional[float] = No
                             _ptr(lse), _ptr(ws), nbytes, _stream_handle(stream))
     _check(rc)
     return out, lse
+
+
+def block_bwd_workspace_size(B, T, H, M, d, n_layers, dtype_code) -> int:
+    return int(lib().sa_block_bwd_workspace_size(B, T, H, M, d, n_layers, dtype_code))
+
+
+def block_bwd(X, P, Wq, Wk, ln, W1, W3, W2, offsets, dout, scale: Optional[float] = None, eps: float = 1e-5,
+              workspace=None, stream=None):
+    """sa_block_bwd on torch tensors: gradients of <dout, block_fwd(...)>.
+    Returns a dict of fp32 tensors dX, dP, dWq, dWk, dln, dW1, dW3, dW2 (shapes of
+    the inputs)."""
+    import torch
+    T, H, d = X.shape
+    M = P.shape[1]
+    B = offsets.shape[0] - 1
+    L = Wq.shape[0]
+    dev = X.device
+    code = _dtype_code(X)
+    dt = X.dtype
+    _require(X, "X", (T, H, d), dt, dev)
+    _require(P, "P", (H, M, d), dt, dev)
+    _require(Wq, "Wq", (L, H, d, d), dt, dev)
+    _require(Wk, "Wk", (L, H, d, d), dt, dev)
+    _require(ln, "ln", (L, 4, H, d), dt, dev)
+    _require(W1, "W1", (L, H, d, 2 * d), dt, dev)
+    _require(W3, "W3", (L, H, d, 2 * d), dt, dev)
+    _require(W2, "W2", (L, H, 2 * d, d), dt, dev)
+    _require(offsets, "offsets", (B + 1,), torch.int64, dev)
+    _require(dout, "dout", (B, H, M, d), torch.float32, dev)
+    if scale is None:
+        scale = 1.0 / math.sqrt(d)
+    f32 = dict(dtype=torch.float32, device=dev)
+    g = {"dX": torch.empty((T, H, d), **f32), "dP": torch.empty((H, M, d), **f32),
+         "dWq": torch.empty((L, H, d, d), **f32), "dWk": torch.empty((L, H, d, d), **f32),
+         "dln": torch.empty((L, 4, H, d), **f32), "dW1": torch.empty((L, H, d, 2 * d), **f32),
+         "dW3": torch.empty((L, H, d, 2 * d), **f32), "dW2": torch.empty((L, H, 2 * d, d), **f32)}
+    ws, nbytes = _workspace(block_bwd_workspace_size(B, T, H, M, d, L, code), dev, workspace)
+    rc = lib().sa_block_bwd(_ptr(X), _ptr(P), _ptr(Wq), _ptr(Wk), _ptr(ln), _ptr(W1), _ptr(W3), _ptr(W2),
+                            _ptr(offsets), B, T, H, M, d, L, float(scale), float(eps), code, _ptr(dout),
+                            _ptr(g["dX"]), _ptr(g["dP"]), _ptr(g["dWq"]), _ptr(g["dWk"]), _ptr(g["dln"]),
+                            _ptr(g["dW1"]), _ptr(g["dW3"]), _ptr(g["dW2"]), _ptr(ws), nbytes,
+                            _stream_handle(stream))
+    _check(rc)
+    return g
 
 
 def profile_enable(on: bool = True) -> None:

@@ -100,3 +100,84 @@ def test_block_empty_users_and_determinism(sa):
     _, out2, lse2, _, _ = run(sa, [0, 120, 0], 2, 128, 64, 2, "bf16", seed=31)
     np.testing.assert_array_equal(out, out2)
     np.testing.assert_array_equal(lse, lse2)
+
+
+# ------------------------------------------------------------------ backward
+# sa_block_bwd against the block oracle's chain rule (itself pinned by torch
+# autograd and finite differences).  Same bars as the forward: normwise max
+# relative error <= 2e-2 (bf16) / 1e-4 (fp32) per (user, head) slice for dX,
+# per head for dP and per (layer, head) for each weight and norm gradient.
+GNAMES = ("dWq", "dWk", "dln", "dW1", "dW3", "dW2")
+
+
+def run_bwd(sa, lengths, H, M, d, L, dtype, seed):
+    w = wl.custom(lengths, H, M, d, dtype, seed=seed, R=1, bwd=True)
+    host = wl.host_tensors(w)
+    host.update(wl.host_block_params(w, L))
+    host["X"] = host.pop("V")
+    del host["K"]
+    dout = np.ascontiguousarray(host.pop("dsketch")[:, 0])
+    dev = wl.to_device(host, dtype)
+    print(f"block bwd case lengths={lengths} H={H} M={M} d={d} L={L} {dtype}", flush=True)
+    g = sa.block_bwd(dev["X"], dev["P"], *[dev[k] for k in NAMES], dev["offsets"],
+                     torch.tensor(dout, dtype=torch.float32, device="cuda"), w.scale)
+    torch.cuda.synchronize()
+    ref = oblock.block_bwd(host["X"], host["P"], *[host[k] for k in NAMES], host["offsets"], dout,
+                           scale=w.scale)
+    return w, host, {k: v.cpu().numpy() for k, v in g.items()}, ref
+
+
+def check_bwd(w, host, g, ref, dtype):
+    tol = TOL[dtype]
+    off = host["offsets"]
+    for b in range(w.B):
+        if off[b + 1] == off[b]:
+            continue
+        eb = normwise(g["dX"][off[b]:off[b + 1]], ref["dX"][off[b]:off[b + 1]], (0, 2))
+        assert np.all(eb <= tol), ("dX", b, eb.max())
+    eh = normwise(g["dP"], ref["dP"], (1, 2))
+    assert np.all(eh <= tol), ("dP", eh.max())
+    for name in GNAMES:
+        axes = (3,) if name == "dln" else (2, 3)   # dln: per (layer, parameter, head)
+        e = normwise(g[name], ref[name], axes)
+        assert np.all(e <= tol), (name, e.max())
+
+
+BWD_FUSED = [
+    ([37, 0, 70, 1, 5], 2, 128, 64, 2),
+    ([300, 17, 64], 2, 512, 128, 2),
+    ([96, 31, 200], 1, 256, 64, 3),
+]
+
+
+@pytest.mark.parametrize("lengths,H,M,d,L", BWD_FUSED)
+def test_block_bwd_fused_matches_oracle(sa, lengths, H, M, d, L):
+    check_bwd(*run_bwd(sa, lengths, H, M, d, L, "bf16", seed=19 * sum(lengths) + M + d + L), "bf16")
+
+
+BWD_PLAIN = [
+    ([40, 0, 77], 2, 64, 64, 2, "fp32"),
+    ([50, 9], 1, 200, 128, 1, "fp32"),
+    ([33, 64], 2, 64, 64, 2, "bf16"),
+]
+
+
+@pytest.mark.parametrize("lengths,H,M,d,L,dtype", BWD_PLAIN)
+def test_block_bwd_plain_matches_oracle(sa, lengths, H, M, d, L, dtype):
+    check_bwd(*run_bwd(sa, lengths, H, M, d, L, dtype, seed=23 * sum(lengths) + M + d), dtype)
+
+
+def test_block_bwd_all_users_empty(sa):
+    # no tokens at all: every sketch is zero, the gradients flow through the
+    # refinement of the prototypes only (dW_Q, dW_K vanish)
+    w, host, g, ref = run_bwd(sa, [0, 0], 2, 128, 64, 2, "bf16", seed=37)
+    assert g["dX"].shape == (0, 2, 64)
+    assert np.count_nonzero(g["dWq"]) == 0 and np.count_nonzero(g["dWk"]) == 0
+    check_bwd(w, host, g, ref, "bf16")
+
+
+def test_block_bwd_deterministic(sa):
+    _, _, g1, _ = run_bwd(sa, [500, 0, 77, 260], 2, 256, 128, 2, "bf16", seed=41)
+    _, _, g2, _ = run_bwd(sa, [500, 0, 77, 260], 2, 256, 128, 2, "bf16", seed=41)
+    for k in g1:
+        np.testing.assert_array_equal(g1[k], g2[k], err_msg=k)
