@@ -319,8 +319,9 @@ def main(argv=None) -> int:
                  "step": "sa_layer_fwd + sa_layer_bwd" if w.bwd else "sa_layer_fwd",
                  "mfma_util": flops_step / (ly_ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS}
 
-    # stacked SA forward (N_sa = 2 layers, the paper's deployed depth) on the same
-    # batch, X = the V tensor; not part of the step
+    # stacked SA (N_sa = 2 layers, the paper's deployed depth) on the same batch,
+    # X = the V tensor: the forward alone, then forward + backward (the backward
+    # replays the forward itself); not part of the step
     block = None
     if not args.no_variants:
         n_layers = 2
@@ -335,6 +336,21 @@ def main(argv=None) -> int:
         bl_ms, kbl = timed(blk)
         block = {"tokens_per_s": T / (bl_ms * 1e-3), "ms": bl_ms, "n_layers": n_layers,
                  "kernels": kernel_dict(kbl), "step": "sa_block_fwd"}
+        if w.bwd:
+            del ws_bl
+            ws_bb = torch.empty(max(sa.block_bwd_workspace_size(B, T, H, M, d, n_layers, code), 1),
+                                dtype=torch.uint8, device="cuda")
+            dout = dev["dsketch"][:, 0].contiguous()
+
+            def blk_train():
+                sa.block_fwd(dev["V"], dev["P"], bp["Wq"], bp["Wk"], bp["ln"], bp["W1"], bp["W3"], bp["W2"],
+                             dev["offsets"], w.scale, out=out_bl, workspace=ws_bb)
+                sa.block_bwd(dev["V"], dev["P"], bp["Wq"], bp["Wk"], bp["ln"], bp["W1"], bp["W3"], bp["W2"],
+                             dev["offsets"], dout, w.scale, workspace=ws_bb)
+            bt_ms, kbt = timed(blk_train)
+            block["train_step"] = {"tokens_per_s": T / (bt_ms * 1e-3), "ms": bt_ms, "kernels": kernel_dict(kbt),
+                                   "step": "sa_block_fwd + sa_block_bwd", "workspace_bytes": ws_bb.numel()}
+            del ws_bb
 
     out = {
         "metric": METRIC,
