@@ -10,7 +10,8 @@ A, sketch A X), Appendix B steps 1-3, and the chain-rule backward stated in the
 header of ``sa_oracle.c``; ``fwd_tokenwise`` is the token-wise normalised
 alternative of the appendix on prototype-wise normalisation.  ``oracle.layer``
 holds the SA layer with its projections (Appendix G.3: Q = P W_Q, K = X W_K,
-V = X) in fp64 numpy.
+V = X) in fp64 numpy; ``oracle.block`` the stacked SA block (section 3.3) and
+``oracle.stca`` the reordered single-query STCA over the sketch (Appendix G.2).
 """
 from __future__ import annotations
 
