@@ -296,6 +296,70 @@ sa_status sa_block_bwd(const void* X, const void* P, const void* Wq, const void*
                        float* dP, float* dWq, float* dWk, float* dln, float* dW1, float* dW3,
                        float* dW2, void* workspace, size_t workspace_bytes, void* stream);
 
+/* Bytes of workspace that sa_stca_fwd needs for this shape. */
+size_t sa_stca_fwd_workspace_size(int64_t B, int32_t R, int32_t k, int32_t D, int32_t h,
+                                  sa_dtype dtype);
+
+/*
+ * Single-query target-to-history cross attention over the adapted sketch, in
+ * the reordered form of Appendix G.2 (STCA of section 2.1, applied over the
+ * sketch in section 3.4).  Each of the B users has a sketch Xs [k, D] and R
+ * targets (its MRLB group, section 4.2), each with one query q [D].  Per
+ * target and head i (h heads of width d_h = D / h; W^(i) = columns
+ * i*d_h .. (i+1)*d_h - 1 of W_Q, W_K, W_V):
+ *
+ *   u     = (q W_Q^(i)) W_K^(i)T
+ *   alpha = softmax over the k sketch rows of scale * u Xs^T
+ *   o^(i) = (alpha Xs) W_V^(i)
+ *
+ * which equals softmax(scale (q W_Q^(i))(Xs W_K^(i))^T)(Xs W_V^(i)) without the
+ * length-k projections.  The output projection and the FFNs of a full STCA
+ * layer are separate products.
+ *
+ *   Xs          [B,k,D] adapted sketches (dtype)
+ *   q           [B,R,D] target queries (dtype)
+ *   Wq, Wk, Wv  [D,D] (dtype), row = input feature
+ *   scale       normally 1/sqrt(D/h), finite and > 0
+ *   out         output [B,R,D] fp32: the heads' o^(i) side by side
+ *   lse         output [B,R,h] fp32 log-sum-exp of the scaled logits, or NULL
+ *
+ * bf16 mode runs the products on the matrix cores with bf16 intermediates
+ * (queries, logits' softmax weights, aggregates) and fp32 accumulation; fp32
+ * mode keeps every value in fp32.  D must be a multiple of h; B = 0 is a no-op.
+ * Errors, ownership and streams as for sa_sketch_fwd.
+ */
+sa_status sa_stca_fwd(const void* Xs, const void* q, const void* Wq, const void* Wk, const void* Wv,
+                      int64_t B, int32_t R, int32_t k, int32_t D, int32_t h, float scale,
+                      sa_dtype dtype, float* out, float* lse, void* workspace,
+                      size_t workspace_bytes, void* stream);
+
+/* Bytes of workspace that sa_stca_bwd needs for this shape. */
+size_t sa_stca_bwd_workspace_size(int64_t B, int32_t R, int32_t k, int32_t D, int32_t h,
+                                  sa_dtype dtype);
+
+/*
+ * Backward of sa_stca_fwd by the chain rule: gradients of <dout, out>.  The
+ * forward is replayed in the workspace; then, with c = alpha Xs:
+ * dc = do^(i) W_V^(i)T and dW_V^(i) = sum c^T do^(i); dalpha = dc Xs^T;
+ * ds = scale alpha (dalpha - <alpha, dalpha>); dXs = sum alpha^T dc + ds^T u;
+ * du = ds Xs; with p = q W_Q^(i): dp = du W_K^(i), dW_K^(i) = sum du^T p,
+ * dq = dp W_Q^T (summed over heads), dW_Q = sum q^T dp.  Sums run over every
+ * user and target.
+ *
+ *   dout                    [B,R,D] fp32
+ *   dXs                     output [B,k,D] fp32
+ *   dq                      output [B,R,D] fp32
+ *   dWq, dWk, dWv           outputs [D,D] fp32
+ *
+ * All outputs are overwritten.  B = 0 is SA_ERR_INVALID_ARG (nothing to write);
+ * other arguments as for sa_stca_fwd.
+ */
+sa_status sa_stca_bwd(const void* Xs, const void* q, const void* Wq, const void* Wk, const void* Wv,
+                      int64_t B, int32_t R, int32_t k, int32_t D, int32_t h, float scale,
+                      sa_dtype dtype, const float* dout, float* dXs, float* dq, float* dWq,
+                      float* dWk, float* dWv, void* workspace, size_t workspace_bytes,
+                      void* stream);
+
 /*
  * Work list used by the fused forward, exposed for exact testing.
  *

@@ -468,6 +468,98 @@ sa_status block_layer_fwd(const void* X, const int64_t* offsets, int64_t B, int6
     return SA_OK;
 }
 
+// ---------------------------------------------------------------- STCA over the sketch
+// [Qp | U | S (fp32) | alpha | C | lse (fp32) | (bwd) dout in the operand dtype | dC |
+//  dalpha (fp32) | ds | dU | dQp]; operand buffers in the input dtype.  Per user b,
+// target r and head i: Qp = q W_Q [B,R,D]; U = per-head (Qp W_K^T) [B,R,h,D]; S =
+// scale U Xs^T [B,R h,k]; alpha = softmax rows; C = alpha Xs [B,R,h,D].
+struct StcaPlan {
+    size_t off_qp = 0, off_u = 0, off_s = 0, off_al = 0, off_c = 0, off_lse = 0, off_dob = 0, off_dc = 0,
+           off_da = 0, off_ds = 0, off_du = 0, off_dqp = 0, total = 0;
+};
+
+StcaPlan plan_stca(int64_t B, int32_t R, int32_t k, int32_t D, int32_t h, sa_dtype dtype, bool bwd) {
+    StcaPlan p;
+    size_t off = 0;
+    auto carve = [&](size_t bytes) {
+        const size_t o = off;
+        off = align_up(off + bytes, 256);
+        return o;
+    };
+    const size_t el = dtype == SA_BF16 ? 2 : 4;
+    const size_t BR = (size_t)B * R, rows = BR * h;
+    p.off_qp = carve(el * BR * D);
+    p.off_u = carve(el * rows * D);
+    p.off_s = carve(4 * rows * k);
+    p.off_al = carve(el * rows * k);
+    p.off_c = carve(el * rows * D);
+    p.off_lse = carve(4 * rows);
+    if (bwd) {
+        p.off_dob = carve(dtype == SA_BF16 ? el * BR * D : 0);
+        p.off_dc = carve(el * rows * D);
+        p.off_da = carve(4 * rows * k);
+        p.off_ds = carve(el * rows * k);
+        p.off_du = carve(el * rows * D);
+        p.off_dqp = carve(el * BR * D);
+    }
+    p.total = off;
+    return p;
+}
+
+sa_status check_stca(int64_t B, int32_t R, int32_t k, int32_t D, int32_t h, float scale, sa_dtype dtype) {
+    if (dtype != SA_BF16 && dtype != SA_FP32) return fail(SA_ERR_INVALID_ARG, "unknown dtype %d", (int)dtype);
+    if (B < 0 || R < 1 || k < 1 || D < 1 || h < 1)
+        return fail(SA_ERR_INVALID_ARG, "bad sizes B=%lld R=%d k=%d D=%d h=%d", (long long)B, R, k, D, h);
+    if (D % h != 0) return fail(SA_ERR_INVALID_ARG, "D=%d is not a multiple of h=%d", D, h);
+    if (!(std::isfinite(scale) && scale > 0.f)) return fail(SA_ERR_INVALID_ARG, "scale must be finite and > 0");
+    if (B > 65535 || B * R * (int64_t)h >= (int64_t(1) << 31) || (int64_t)R * h * k >= (int64_t(1) << 31))
+        return fail(SA_ERR_UNSUPPORTED, "sizes beyond the supported range");
+    return SA_OK;
+}
+
+sa_status stca_forward(const void* Xs, const void* q, const void* Wq, const void* Wk, const void* Wv, int64_t B,
+                       int32_t R, int32_t k, int32_t D, int32_t h, float scale, sa_dtype dtype, float* out,
+                       float* lse, uint8_t* ws, const StcaPlan& p, hipStream_t stream) {
+    const bool bf = dtype == SA_BF16;
+    const int32_t BR = (int32_t)(B * R), dh = D / h, Rh = R * h;
+    const int64_t kD = (int64_t)k * D, RhD = (int64_t)Rh * D, Rhk = (int64_t)Rh * k;
+    void* Qp = ws + p.off_qp;
+    void* U = ws + p.off_u;
+    float* S = reinterpret_cast<float*>(ws + p.off_s);
+    void* Al = ws + p.off_al;
+    void* Cc = ws + p.off_c;
+    hipError_t e;
+    {
+        sa::ProfScope ps("stca_query_proj", stream);
+        // Qp = q W_Q;  U[., i] = Qp[., head i] W_K^(i)T
+        e = sa::launch_gemm({q, bf, 0, D, 1, Wq, bf, 0, D, 1, Qp, bf, 0, D, BR, D, D, 1, 1.f, false}, stream);
+        if (e == hipSuccess)
+            e = sa::launch_gemm({Qp, bf, dh, D, 1, Wk, bf, dh, 1, D, U, bf, D, (int64_t)h * D, BR, D, dh, h, 1.f,
+                                 false}, stream);
+    }
+    if (e == hipSuccess) {
+        sa::ProfScope ps("stca_logits", stream);   // S = scale U Xs^T per user
+        e = sa::launch_gemm({U, bf, RhD, D, 1, Xs, bf, kD, 1, D, S, false, Rhk, k, Rh, k, D, (int32_t)B, scale, false},
+                            stream);
+    }
+    if (e == hipSuccess) {
+        sa::ProfScope ps("stca_softmax", stream);
+        e = sa::launch_stca_softmax(S, (int64_t)BR * h, k, bf, Al, lse, stream);
+    }
+    if (e == hipSuccess) {
+        sa::ProfScope ps("stca_aggregate", stream);   // C = alpha Xs per user
+        e = sa::launch_gemm({Al, bf, Rhk, k, 1, Xs, bf, kD, D, 1, Cc, bf, RhD, D, Rh, D, k, (int32_t)B, 1.f, false},
+                            stream);
+    }
+    if (e == hipSuccess && out) {
+        sa::ProfScope ps("stca_value_proj", stream);   // out[., head i] = C[., i] W_V^(i)
+        e = sa::launch_gemm({Cc, bf, D, (int64_t)h * D, 1, Wv, bf, dh, D, 1, out, false, dh, D, BR, dh, D, h, 1.f,
+                             false}, stream);
+    }
+    if (e != hipSuccess) return hip_fail(e, "STCA forward launch");
+    return SA_OK;
+}
+
 // forward on a checked plan and workspace (shared by sa_sketch_fwd and sa_layer_fwd)
 sa_status run_fwd(const void* K, const void* V, const void* P, const int64_t* offsets, int64_t B,
                   int64_t T, int32_t H, int32_t M, int32_t d, float scale, sa_dtype dtype,
@@ -1104,6 +1196,125 @@ sa_status sa_block_bwd(const void* X, const void* P, const void* Wq, const void*
         if (e != hipSuccess) return hip_fail(e, "block projection gradient launch");
         dXt = dY1;
     }
+    return SA_OK;
+}
+
+size_t sa_stca_fwd_workspace_size(int64_t B, int32_t R, int32_t k, int32_t D, int32_t h, sa_dtype dtype) {
+    if (check_stca(B, R, k, D, h, 1.0f, dtype) != SA_OK) return 0;
+    return plan_stca(B, R, k, D, h, dtype, false).total;
+}
+
+sa_status sa_stca_fwd(const void* Xs, const void* q, const void* Wq, const void* Wk, const void* Wv, int64_t B,
+                      int32_t R, int32_t k, int32_t D, int32_t h, float scale, sa_dtype dtype, float* out, float* lse,
+                      void* workspace, size_t workspace_bytes, void* stream_) {
+    g_last_error[0] = 0;
+    sa_status st = check_stca(B, R, k, D, h, scale, dtype);
+    if (st != SA_OK) return st;
+    if (B == 0) return SA_OK;
+    if (!Xs || !q || !Wq || !Wk || !Wv || !out) return fail(SA_ERR_INVALID_ARG, "null pointer argument");
+    if (!aligned16(Xs) || !aligned16(q) || !aligned16(Wq) || !aligned16(Wk) || !aligned16(Wv) || !aligned16(out) ||
+        !aligned16(lse))
+        return fail(SA_ERR_INVALID_ARG, "tensor arguments must be 16-byte aligned");
+    const StcaPlan plan = plan_stca(B, R, k, D, h, dtype, false);
+    if (!workspace || workspace_bytes < plan.total)
+        return fail(SA_ERR_WORKSPACE, "workspace of %zu bytes needed, %zu given", plan.total,
+                    workspace ? workspace_bytes : (size_t)0);
+    uint8_t* ws = reinterpret_cast<uint8_t*>(workspace);
+    return stca_forward(Xs, q, Wq, Wk, Wv, B, R, k, D, h, scale, dtype, out,
+                        lse ? lse : reinterpret_cast<float*>(ws + plan.off_lse), ws, plan,
+                        reinterpret_cast<hipStream_t>(stream_));
+}
+
+size_t sa_stca_bwd_workspace_size(int64_t B, int32_t R, int32_t k, int32_t D, int32_t h, sa_dtype dtype) {
+    if (check_stca(B, R, k, D, h, 1.0f, dtype) != SA_OK) return 0;
+    return plan_stca(B, R, k, D, h, dtype, true).total;
+}
+
+sa_status sa_stca_bwd(const void* Xs, const void* q, const void* Wq, const void* Wk, const void* Wv, int64_t B,
+                      int32_t R, int32_t k, int32_t D, int32_t h, float scale, sa_dtype dtype, const float* dout,
+                      float* dXs, float* dq, float* dWq, float* dWk, float* dWv, void* workspace,
+                      size_t workspace_bytes, void* stream_) {
+    g_last_error[0] = 0;
+    sa_status st = check_stca(B, R, k, D, h, scale, dtype);
+    if (st != SA_OK) return st;
+    if (B < 1) return fail(SA_ERR_INVALID_ARG, "B must be >= 1 for the backward");
+    if (!Xs || !q || !Wq || !Wk || !Wv || !dout || !dXs || !dq || !dWq || !dWk || !dWv)
+        return fail(SA_ERR_INVALID_ARG, "null pointer argument");
+    if (!aligned16(Xs) || !aligned16(q) || !aligned16(Wq) || !aligned16(Wk) || !aligned16(Wv) || !aligned16(dout) ||
+        !aligned16(dXs) || !aligned16(dq) || !aligned16(dWq) || !aligned16(dWk) || !aligned16(dWv))
+        return fail(SA_ERR_INVALID_ARG, "tensor arguments must be 16-byte aligned");
+    const StcaPlan p = plan_stca(B, R, k, D, h, dtype, true);
+    if (!workspace || workspace_bytes < p.total)
+        return fail(SA_ERR_WORKSPACE, "workspace of %zu bytes needed, %zu given", p.total,
+                    workspace ? workspace_bytes : (size_t)0);
+    hipStream_t stream = reinterpret_cast<hipStream_t>(stream_);
+    uint8_t* ws = reinterpret_cast<uint8_t*>(workspace);
+    float* lse = reinterpret_cast<float*>(ws + p.off_lse);
+    // forward replay: Qp, U, S, lse, alpha, C
+    st = stca_forward(Xs, q, Wq, Wk, Wv, B, R, k, D, h, scale, dtype, nullptr, lse, ws, p, stream);
+    if (st != SA_OK) return st;
+    const bool bf = dtype == SA_BF16;
+    const int32_t BR = (int32_t)(B * R), dh = D / h, Rh = R * h;
+    const int64_t kD = (int64_t)k * D, RhD = (int64_t)Rh * D, Rhk = (int64_t)Rh * k, hD = (int64_t)h * D;
+    void* Qp = ws + p.off_qp;
+    void* U = ws + p.off_u;
+    float* S = reinterpret_cast<float*>(ws + p.off_s);
+    void* Al = ws + p.off_al;
+    void* Cc = ws + p.off_c;
+    void* dC = ws + p.off_dc;
+    float* dA = reinterpret_cast<float*>(ws + p.off_da);
+    void* ds = ws + p.off_ds;
+    void* dU = ws + p.off_du;
+    void* dQp = ws + p.off_dqp;
+    const void* dob = dout;
+    hipError_t e = hipSuccess;
+    if (bf) {
+        dob = ws + p.off_dob;
+        e = sa::launch_to_bf16(dout, reinterpret_cast<uint16_t*>(ws + p.off_dob), (int64_t)BR * D, stream);
+    }
+    if (e == hipSuccess) {
+        sa::ProfScope ps("stca_value_grads", stream);
+        // dC[., i] = dout[., head i] W_V^(i)T;  dW_V^(i) = sum over targets of C[., i]^T dout[., head i]
+        e = sa::launch_gemm({dob, bf, dh, D, 1, Wv, bf, dh, 1, D, dC, bf, D, hD, BR, D, dh, h, 1.f, false}, stream);
+        if (e == hipSuccess)
+            e = sa::launch_gemm({Cc, bf, D, 1, hD, dob, bf, dh, D, 1, dWv, false, dh, D, D, dh, BR, h, 1.f, false},
+                                stream);
+    }
+    if (e == hipSuccess) {
+        sa::ProfScope ps("stca_dalpha", stream);   // dalpha = dC Xs^T per user
+        e = sa::launch_gemm({dC, bf, RhD, D, 1, Xs, bf, kD, 1, D, dA, false, Rhk, k, Rh, k, D, (int32_t)B, 1.f, false},
+                            stream);
+    }
+    if (e == hipSuccess) {
+        sa::ProfScope ps("stca_softmax_bwd", stream);
+        e = sa::launch_stca_softmax_bwd(S, lse, dA, (int64_t)BR * h, k, scale, bf, ds, stream);
+    }
+    if (e == hipSuccess) {
+        sa::ProfScope ps("stca_sketch_grads", stream);
+        // dXs = alpha^T dC + (scale ds)^T U per user;  dU = (scale ds) Xs
+        e = sa::launch_gemm({Al, bf, Rhk, 1, k, dC, bf, RhD, D, 1, dXs, false, kD, D, k, D, Rh, (int32_t)B, 1.f, false},
+                            stream);
+        if (e == hipSuccess)
+            e = sa::launch_gemm({ds, bf, Rhk, 1, k, U, bf, RhD, D, 1, dXs, false, kD, D, k, D, Rh, (int32_t)B, 1.f,
+                                 true}, stream);
+        if (e == hipSuccess)
+            e = sa::launch_gemm({ds, bf, Rhk, k, 1, Xs, bf, kD, D, 1, dU, bf, RhD, D, Rh, D, k, (int32_t)B, 1.f, false},
+                                stream);
+    }
+    if (e == hipSuccess) {
+        sa::ProfScope ps("stca_query_grads", stream);
+        // dQp[., head i] = dU[., i] W_K^(i);  dW_K^(i) = sum dU[., i]^T Qp[., head i]
+        e = sa::launch_gemm({dU, bf, D, hD, 1, Wk, bf, dh, D, 1, dQp, bf, dh, D, BR, dh, D, h, 1.f, false}, stream);
+        if (e == hipSuccess)
+            e = sa::launch_gemm({dU, bf, D, 1, hD, Qp, bf, dh, D, 1, dWk, false, dh, D, D, dh, BR, h, 1.f, false},
+                                stream);
+        // dq = dQp W_Q^T;  dW_Q = q^T dQp
+        if (e == hipSuccess)
+            e = sa::launch_gemm({dQp, bf, 0, D, 1, Wq, bf, 0, 1, D, dq, false, 0, D, BR, D, D, 1, 1.f, false}, stream);
+        if (e == hipSuccess)
+            e = sa::launch_gemm({q, bf, 0, 1, D, dQp, bf, 0, D, 1, dWq, false, 0, D, D, D, BR, 1, 1.f, false}, stream);
+    }
+    if (e != hipSuccess) return hip_fail(e, "STCA backward launch");
     return SA_OK;
 }
 

@@ -1,0 +1,231 @@
+// Batched dense products on the matrix cores:
+//
+//   C[z](m, n) = alpha sum_k A[z](m, k) B[z](k, n)   (+ C[z](m, n) when accumulating)
+//
+// with A[z](m, k) = A[z a_z + m a_m + k a_k], B[z](k, n) = B[z b_z + k b_k + n b_n],
+// C[z](m, n) = C[z c_z + m c_m + n].  Each operand is contiguous either along k
+// (a_k = 1, b_k = 1) or along its other index (a_m = 1, b_n = 1), so transposed
+// operands cost nothing at the call site.
+//
+// Tile 128 x 128 x 64 per workgroup of four waves, each wave a 64 x 64 block of
+// 2 x 2 v_mfma_f32_32x32x16_bf16 tiles.  Both operands are staged in LDS as
+// [row][64 k] bf16 (16-byte chunks XOR-swizzled so that operand reads of 32
+// rows are conflict free) in two buffers: the next k slab's global loads are in
+// registers while the current slab is multiplied.  A k-contiguous tile is
+// loaded as 16-byte row pieces; an m- (n-) contiguous tile as 4 k rows x 8
+// columns per thread, transposed in registers into 8 column pieces of 4 k
+// values.  Tiles of one batch run on one XCD so that its operands share that
+// L2.  Products whose shapes or strides do not fit (k not a multiple of 64,
+// unaligned strides, fp32 operands) run on the register-tiled fp32 product of
+// layer.hip.
+#include "sa_internal.h"
+#include "tile_ops.h"
+
+namespace sa {
+
+namespace {
+
+using namespace tile;
+
+constexpr int GBM = 128, GBN = 128, GBK = 64;
+
+struct MgArgs {
+    const uint16_t* A;
+    int64_t a_z, a_m, a_k;
+    const uint16_t* B;
+    int64_t b_z, b_k, b_n;
+    void* C;
+    int64_t c_z, c_m;
+    int32_t M, N, K, tm, tn;
+    float alpha;
+    int32_t accumulate;
+};
+
+// Global -> registers: the [128 rows][64 k] slab at (row0, k0) of an operand whose
+// element (row, k) sits at base[row s_row + k s_k].  KC: s_k = 1 (rows are k
+// runs); otherwise s_row = 1 (k rows are runs of the row index).  Rows at or past
+// nrows read row nrows - 1 (KC) or zeros (not KC; nrows is a multiple of 8).
+template <bool KC>
+__device__ inline void load_slab(const uint16_t* base, int64_t s_row, int64_t s_k, int row0, int nrows, int k0,
+                                 int tid, uint4 (&r)[4]) {
+    if constexpr (KC) {
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const int c = tid + 256 * i, row = row0 + (c >> 3), kc = c & 7;
+            const int rr = row < nrows ? row : nrows - 1;
+            r[i] = *reinterpret_cast<const uint4*>(base + (int64_t)rr * s_row + k0 + 8 * kc);
+        }
+    } else {
+        const int mb = tid & 15, kb = tid >> 4;
+        const int row = row0 + 8 * mb;
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+            r[i] = row < nrows ? *reinterpret_cast<const uint4*>(base + (int64_t)(k0 + 4 * kb + i) * s_k + row)
+                               : make_uint4(0, 0, 0, 0);
+    }
+}
+
+__device__ inline uint32_t u4_at(const uint4& v, int i) {
+    return i == 0 ? v.x : i == 1 ? v.y : i == 2 ? v.z : v.w;
+}
+
+// registers -> LDS slab [128 rows][64 k], swizzled (layout swz<64>)
+template <bool KC>
+__device__ inline void store_slab(uint16_t* lds, const uint4 (&r)[4], int tid) {
+    if constexpr (KC) {
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const int c = tid + 256 * i, row = c >> 3, kc = c & 7;
+            *reinterpret_cast<uint4*>(lds + swz<64>(row, kc)) = r[i];
+        }
+    } else {
+        // r[i] holds columns 8 mb .. 8 mb + 7 of k row 4 kb + i; column j gets the
+        // four k values of this thread, one 8-byte piece
+        const int mb = tid & 15, kb = tid >> 4;
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+            const int dw = j >> 1, sh = 16 * (j & 1);
+            const uint32_t e0 = (u4_at(r[0], dw) >> sh) & 0xffffu, e1 = (u4_at(r[1], dw) >> sh) & 0xffffu;
+            const uint32_t e2 = (u4_at(r[2], dw) >> sh) & 0xffffu, e3 = (u4_at(r[3], dw) >> sh) & 0xffffu;
+            const int row = 8 * mb + j;
+            *reinterpret_cast<uint2*>(lds + swz<64>(row, kb >> 1) + 4 * (kb & 1)) =
+                make_uint2(e0 | (e1 << 16), e2 | (e3 << 16));
+        }
+    }
+}
+
+template <bool A_KC, bool B_KC, bool C_BF16>
+__global__ __launch_bounds__(256, 2) void mfma_gemm_kernel(MgArgs g) {
+    __shared__ __attribute__((aligned(16))) uint16_t As[2][GBM * GBK];
+    __shared__ __attribute__((aligned(16))) uint16_t Bs[2][GBN * GBK];
+    const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, l32 = lane & 31, hl = lane >> 5;
+    const int64_t tiles = (int64_t)g.tm * g.tn;
+    const int64_t id = xcd_range(blockIdx.x, gridDim.x);
+    const int64_t z = id / tiles;
+    const int tt = (int)(id % tiles);
+    const int m0 = (tt / g.tn) * GBM, n0 = (tt % g.tn) * GBN;
+    const uint16_t* Ab = g.A + z * g.a_z;
+    const uint16_t* Bb = g.B + z * g.b_z;
+    const int nk = g.K / GBK;
+
+    uint4 ra[4], rb[4];
+    load_slab<A_KC>(Ab, g.a_m, g.a_k, m0, g.M, 0, tid, ra);
+    load_slab<B_KC>(Bb, g.b_n, g.b_k, n0, g.N, 0, tid, rb);
+    store_slab<A_KC>(As[0], ra, tid);
+    store_slab<B_KC>(Bs[0], rb, tid);
+    __syncthreads();
+
+    f32x16 acc[2][2];
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
+    const int wm = w & 1, wn = w >> 1;
+    for (int kt = 0; kt < nk; ++kt) {
+        const int cur = kt & 1;
+        const bool more = kt + 1 < nk;
+        if (more) {
+            load_slab<A_KC>(Ab, g.a_m, g.a_k, m0, g.M, (kt + 1) * GBK, tid, ra);
+            load_slab<B_KC>(Bb, g.b_n, g.b_k, n0, g.N, (kt + 1) * GBK, tid, rb);
+        }
+        const uint16_t* Ac = As[cur];
+        const uint16_t* Bc = Bs[cur];
+#pragma unroll
+        for (int ks = 0; ks < GBK / 16; ++ks) {
+            const bf16x8 a0 = lds_b128(Ac, swz<64>(wm * 64 + l32, 2 * ks + hl));
+            const bf16x8 a1 = lds_b128(Ac, swz<64>(wm * 64 + 32 + l32, 2 * ks + hl));
+            const bf16x8 b0 = lds_b128(Bc, swz<64>(wn * 64 + l32, 2 * ks + hl));
+            const bf16x8 b1 = lds_b128(Bc, swz<64>(wn * 64 + 32 + l32, 2 * ks + hl));
+            acc[0][0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a0, b0, acc[0][0], 0, 0, 0);
+            acc[0][1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a0, b1, acc[0][1], 0, 0, 0);
+            acc[1][0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1, b0, acc[1][0], 0, 0, 0);
+            acc[1][1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1, b1, acc[1][1], 0, 0, 0);
+        }
+        if (more) {
+            // the other buffer's readers passed the barrier that ended the previous slab
+            store_slab<A_KC>(As[cur ^ 1], ra, tid);
+            store_slab<B_KC>(Bs[cur ^ 1], rb, tid);
+        }
+        __syncthreads();
+    }
+
+    // C layout of a 32 x 32 tile: lane = column, register r = row srow(r, hl)
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j) {
+            const int n = n0 + wn * 64 + 32 * j + l32;
+            if (n >= g.N) continue;
+#pragma unroll
+            for (int r = 0; r < 16; ++r) {
+                const int m = m0 + wm * 64 + 32 * i + srow(r, hl);
+                if (m >= g.M) continue;
+                const int64_t o = z * g.c_z + (int64_t)m * g.c_m + n;
+                float v = g.alpha * acc[i][j][r];
+                if constexpr (C_BF16) {
+                    uint16_t* Cp = reinterpret_cast<uint16_t*>(g.C);
+                    if (g.accumulate) v += __uint_as_float((uint32_t)Cp[o] << 16);
+                    Cp[o] = to_bf16(v);
+                } else {
+                    float* Cp = reinterpret_cast<float*>(g.C);
+                    if (g.accumulate) v += Cp[o];
+                    Cp[o] = v;
+                }
+            }
+        }
+}
+
+template <bool A_KC, bool B_KC>
+hipError_t mgemm_launch(const MgArgs& g, bool c_bf16, int64_t batch, hipStream_t stream) {
+    const int64_t blocks = (int64_t)g.tm * g.tn * batch;
+    if (c_bf16)
+        hipLaunchKernelGGL((mfma_gemm_kernel<A_KC, B_KC, true>), dim3((unsigned)blocks), dim3(256), 0, stream, g);
+    else
+        hipLaunchKernelGGL((mfma_gemm_kernel<A_KC, B_KC, false>), dim3((unsigned)blocks), dim3(256), 0, stream, g);
+    return hipGetLastError();
+}
+
+bool al8(int64_t v) { return v % 8 == 0; }
+bool al16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15) == 0; }
+
+}  // namespace
+
+bool gemm_on_matrix_cores(const GemmDesc& d) {
+    if (!d.a_bf16 || !d.b_bf16 || d.K <= 0 || d.K % GBK != 0 || d.M <= 0 || d.N <= 0) return false;
+    const bool a_kc = d.a_k == 1, b_kc = d.b_k == 1;
+    if (!a_kc && d.a_m != 1) return false;
+    if (!b_kc && d.b_n != 1) return false;
+    // 16-byte pieces: every stride and base on 8 bf16
+    if (!al16(d.A) || !al16(d.B) || !al8(d.a_z) || !al8(d.b_z)) return false;
+    if (!al8(a_kc ? d.a_m : d.a_k) || !al8(b_kc ? d.b_n : d.b_k)) return false;
+    if (!a_kc && d.M % 8 != 0) return false;
+    if (!b_kc && d.N % 8 != 0) return false;
+    const int64_t blocks = (int64_t)((d.M + GBM - 1) / GBM) * ((d.N + GBN - 1) / GBN) * d.batch;
+    return blocks < (int64_t(1) << 31);
+}
+
+hipError_t launch_gemm(const GemmDesc& d, hipStream_t stream) {
+    if (d.batch <= 0 || d.M <= 0 || d.N <= 0) return hipSuccess;
+    if (!gemm_on_matrix_cores(d)) return launch_small_gemm_general(d, stream);
+    MgArgs g;
+    g.A = reinterpret_cast<const uint16_t*>(d.A);
+    g.a_z = d.a_z; g.a_m = d.a_m; g.a_k = d.a_k;
+    g.B = reinterpret_cast<const uint16_t*>(d.B);
+    g.b_z = d.b_z; g.b_k = d.b_k; g.b_n = d.b_n;
+    g.C = d.C;
+    g.c_z = d.c_z; g.c_m = d.c_m;
+    g.M = d.M; g.N = d.N; g.K = d.K;
+    g.tm = (d.M + GBM - 1) / GBM;
+    g.tn = (d.N + GBN - 1) / GBN;
+    g.alpha = d.alpha;
+    g.accumulate = d.accumulate ? 1 : 0;
+    const bool a_kc = d.a_k == 1, b_kc = d.b_k == 1;
+    if (a_kc && b_kc) return mgemm_launch<true, true>(g, d.c_bf16, d.batch, stream);
+    if (a_kc) return mgemm_launch<true, false>(g, d.c_bf16, d.batch, stream);
+    if (b_kc) return mgemm_launch<false, true>(g, d.c_bf16, d.batch, stream);
+    return mgemm_launch<false, false>(g, d.c_bf16, d.batch, stream);
+}
+
+}  // namespace sa

@@ -43,7 +43,7 @@ __device__ inline void store_el<uint16_t>(uint16_t* p, int64_t i, float v) { p[i
 
 // C[z][r][c] = sum_k A[z](r, k) B[z % b_mod](k, c) for r < R, c < N, k < Kd, with
 // A(r, k) = A[z * a_h + r * a_r + k * a_k] and B(k, c) = B[z' * b_h + k * b_k + c * b_c];
-// C row-major [R][N] per batch z (with accumulate, C += instead of C =).  A 64 x 64 output tile per workgroup of 256
+// C[z * c_h + r * c_r + c] (with accumulate, C += alpha A B instead of C = alpha A B).  A 64 x 64 output tile per workgroup of 256
 // threads, 4 x 4 outputs per thread; k advances in slabs of 16 staged in LDS
 // (k-major, so each k step is two 16-byte LDS reads for 16 FMAs), the next
 // slab's loads in flight while the current one is used.  Consecutive lanes walk
@@ -52,8 +52,8 @@ template <typename TA, typename TB, typename TC>
 __global__ __launch_bounds__(256) void small_gemm_kernel(const TA* __restrict__ A, int64_t a_h, int64_t a_r,
                                                          int64_t a_k, const TB* __restrict__ Bm, int64_t b_h,
                                                          int64_t b_k, int64_t b_c, int32_t b_mod,
-                                                         TC* __restrict__ C, int32_t R, int32_t N, int32_t Kd,
-                                                         bool accumulate) {
+                                                         TC* __restrict__ C, int64_t c_h, int64_t c_r, int32_t R,
+                                                         int32_t N, int32_t Kd, float alpha, bool accumulate) {
     constexpr int TR = 64, TC_ = 64, TK = 16, PAD = 4;
     __shared__ __attribute__((aligned(16))) float As[TK][TR + PAD];   // [k][r]
     __shared__ __attribute__((aligned(16))) float Bs[TK][TC_ + PAD];  // [k][c]
@@ -108,7 +108,7 @@ __global__ __launch_bounds__(256) void small_gemm_kernel(const TA* __restrict__ 
         }
         __syncthreads();
     }
-    TC* Cz = C + z * (int64_t)R * N;
+    TC* Cz = C + z * c_h;
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
         const int r = r0 + ty * 4 + i;
@@ -117,8 +117,9 @@ __global__ __launch_bounds__(256) void small_gemm_kernel(const TA* __restrict__ 
         for (int j = 0; j < 4; ++j) {
             const int c = c0 + tx * 4 + j;
             if (c >= N) continue;
-            const int64_t o = (int64_t)r * N + c;
-            store_el(Cz, o, accumulate ? acc[i][j] + load_el(Cz, o) : acc[i][j]);
+            const int64_t o = (int64_t)r * c_r + c;
+            const float v = alpha * acc[i][j];
+            store_el(Cz, o, accumulate ? v + load_el(Cz, o) : v);
         }
     }
 }
@@ -133,30 +134,43 @@ __global__ __launch_bounds__(256) void add_kernel(const float* __restrict__ a, c
 }
 
 template <typename TA, typename TB, typename TC>
-hipError_t gemm_t(const MatView& a, const MatView& b, int32_t b_mod, void* c, int32_t H, int32_t R, int32_t N,
-                  int32_t Kd, bool accumulate, hipStream_t stream) {
+hipError_t gemm_t(const MatView& a, const MatView& b, int32_t b_mod, void* c, int64_t c_h, int64_t c_r, int32_t H,
+                  int32_t R, int32_t N, int32_t Kd, float alpha, bool accumulate, hipStream_t stream) {
     const dim3 grid((unsigned)((R + 63) / 64), (unsigned)((N + 63) / 64), (unsigned)H);
     hipLaunchKernelGGL((small_gemm_kernel<TA, TB, TC>), grid, dim3(256), 0, stream,
                        reinterpret_cast<const TA*>(a.p), a.s_h, a.s_0, a.s_1,
                        reinterpret_cast<const TB*>(b.p), b.s_h, b.s_0, b.s_1, b_mod, reinterpret_cast<TC*>(c),
-                       R, N, Kd, accumulate);
+                       c_h, c_r, R, N, Kd, alpha, accumulate);
     return hipGetLastError();
+}
+
+hipError_t small_gemm_dispatch(const MatView& a, const MatView& b, void* c, bool c_bf16, int64_t c_h, int64_t c_r,
+                               int32_t H, int32_t R, int32_t N, int32_t Kd, int32_t b_mod, float alpha,
+                               bool accumulate, hipStream_t stream) {
+    if (H <= 0 || R <= 0 || N <= 0) return hipSuccess;
+    if (H > 65535) return hipErrorInvalidValue;
+#define SA_GEMM(TA, TB) \
+    return c_bf16 ? gemm_t<TA, TB, uint16_t>(a, b, b_mod, c, c_h, c_r, H, R, N, Kd, alpha, accumulate, stream) \
+                  : gemm_t<TA, TB, float>(a, b, b_mod, c, c_h, c_r, H, R, N, Kd, alpha, accumulate, stream)
+    if (a.bf16 && b.bf16) SA_GEMM(uint16_t, uint16_t);
+    if (a.bf16) SA_GEMM(uint16_t, float);
+    if (b.bf16) SA_GEMM(float, uint16_t);
+    SA_GEMM(float, float);
+#undef SA_GEMM
 }
 
 }  // namespace
 
 hipError_t launch_small_gemm(const MatView& a, const MatView& b, void* c, bool c_bf16, int32_t H, int32_t R,
                              int32_t N, int32_t Kd, hipStream_t stream, int32_t b_mod, bool accumulate) {
-    if (H <= 0 || R <= 0 || N <= 0) return hipSuccess;
     if (b_mod <= 0) b_mod = H;
-#define SA_GEMM(TA, TB) \
-    return c_bf16 ? gemm_t<TA, TB, uint16_t>(a, b, b_mod, c, H, R, N, Kd, accumulate, stream) \
-                  : gemm_t<TA, TB, float>(a, b, b_mod, c, H, R, N, Kd, accumulate, stream)
-    if (a.bf16 && b.bf16) SA_GEMM(uint16_t, uint16_t);
-    if (a.bf16) SA_GEMM(uint16_t, float);
-    if (b.bf16) SA_GEMM(float, uint16_t);
-    SA_GEMM(float, float);
-#undef SA_GEMM
+    return small_gemm_dispatch(a, b, c, c_bf16, (int64_t)R * N, N, H, R, N, Kd, b_mod, 1.0f, accumulate, stream);
+}
+
+hipError_t launch_small_gemm_general(const GemmDesc& d, hipStream_t stream) {
+    return small_gemm_dispatch({d.A, d.a_bf16, d.a_z, d.a_m, d.a_k}, {d.B, d.b_bf16, d.b_z, d.b_k, d.b_n}, d.C,
+                               d.c_bf16, d.c_z, d.c_m, d.batch, d.M, d.N, d.K, d.batch, d.alpha, d.accumulate,
+                               stream);
 }
 
 hipError_t launch_add(const float* a, const float* b, float* out, int64_t n, hipStream_t stream) {

@@ -140,6 +140,39 @@ struct MatView {
 hipError_t launch_small_gemm(const MatView& a, const MatView& b, void* c, bool c_bf16, int32_t H, int32_t R,
                              int32_t N, int32_t Kd, hipStream_t stream, int32_t b_mod = 0,
                              bool accumulate = false);
+// General batched product C[z](m, n) = alpha sum_k A[z](m, k) B[z](k, n) (+ C with
+// accumulate), element (z, m, k) of A at A[z a_z + m a_m + k a_k], (z, k, n) of B at
+// B[z b_z + k b_k + n b_n], (z, m, n) of C at C[z c_z + m c_m + n]; fp32 accumulation.
+// bf16 operands contiguous along k or along m (n), with k a multiple of 64 and
+// 16-byte aligned pieces, run on the matrix cores (gemm.hip); the rest on the
+// register-tiled fp32 product (layer.hip).
+struct GemmDesc {
+    const void* A;
+    bool a_bf16;
+    int64_t a_z, a_m, a_k;
+    const void* B;
+    bool b_bf16;
+    int64_t b_z, b_k, b_n;
+    void* C;
+    bool c_bf16;
+    int64_t c_z, c_m;
+    int32_t M, N, K, batch;
+    float alpha;
+    bool accumulate;
+};
+bool gemm_on_matrix_cores(const GemmDesc& d);
+hipError_t launch_gemm(const GemmDesc& d, hipStream_t stream);
+hipError_t launch_small_gemm_general(const GemmDesc& d, hipStream_t stream);
+
+// Reordered single-query STCA rows (stca.hip), over [rows][k] fp32 logits already
+// scaled: lse and alpha = exp(s - lse) in bf16 or fp32; the backward writes
+// ds = scale alpha (da - <alpha, da>).
+hipError_t launch_stca_softmax(const float* S, int64_t rows, int32_t k, bool bf16, void* alpha, float* lse,
+                               hipStream_t stream);
+hipError_t launch_stca_softmax_bwd(const float* S, const float* lse, const float* dA, int64_t rows, int32_t k,
+                                   float scale, bool bf16, void* ds, hipStream_t stream);
+hipError_t launch_to_bf16(const float* x, uint16_t* y, int64_t n, hipStream_t stream);
+
 // Stacked-SA refinement (block.hip).  add_ln: one row of d features per
 // (user, head, prototype): out[r] = LN(x[r mod x_rows] + y[r]) * gamma[h] + beta[h],
 // h = (r / M) % H; x fp32 or bf16 (the shared prototypes broadcast over users

@@ -1,0 +1,102 @@
+// Row kernels of the reordered single-query STCA over the sketch (Appendix G.2):
+// the softmax over the k sketch rows of each (user, target, head) logit row and
+// its backward.  The products around them run on the batched matrix-core GEMM.
+//
+// Rows are [rows][k] fp32 logits already multiplied by the attention scale.  One
+// wave per row; lanes stride the row so that every access is coalesced.
+#include "sa_internal.h"
+#include "tile_ops.h"
+
+namespace sa {
+
+namespace {
+
+__device__ inline float wave_max(float v) {
+#pragma unroll
+    for (int k = 1; k < 64; k <<= 1) v = fmaxf(v, __shfl_xor(v, k, 64));
+    return v;
+}
+__device__ inline float wave_sum(float v) {
+#pragma unroll
+    for (int k = 1; k < 64; k <<= 1) v += __shfl_xor(v, k, 64);
+    return v;
+}
+
+template <bool BF16>
+__device__ inline void put(void* p, int64_t i, float v) {
+    if constexpr (BF16) reinterpret_cast<uint16_t*>(p)[i] = tile::to_bf16(v);
+    else reinterpret_cast<float*>(p)[i] = v;
+}
+
+// lse = log sum_j exp(s_j); alpha_j = exp(s_j - lse)
+template <bool BF16>
+__global__ __launch_bounds__(256) void stca_softmax_kernel(const float* __restrict__ S, int64_t rows, int32_t k,
+                                                           void* __restrict__ alpha, float* __restrict__ lse) {
+    const int64_t row = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+    if (row >= rows) return;
+    const int lane = threadIdx.x & 63;
+    const float* s = S + row * k;
+    float mx = -INFINITY;
+    for (int j = lane; j < k; j += 64) mx = fmaxf(mx, s[j]);
+    mx = wave_max(mx);
+    float z = 0.f;
+    for (int j = lane; j < k; j += 64) z += __expf(s[j] - mx);
+    const float l = mx + __logf(wave_sum(z));
+    for (int j = lane; j < k; j += 64) put<BF16>(alpha, row * k + j, __expf(s[j] - l));
+    if (lane == 0) lse[row] = l;
+}
+
+// ds_j = scale alpha_j (da_j - sum_i alpha_i da_i), alpha_j = exp(s_j - lse)
+template <bool BF16>
+__global__ __launch_bounds__(256) void stca_softmax_bwd_kernel(const float* __restrict__ S,
+                                                               const float* __restrict__ lse,
+                                                               const float* __restrict__ dA, int64_t rows, int32_t k,
+                                                               float scale, void* __restrict__ ds) {
+    const int64_t row = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+    if (row >= rows) return;
+    const int lane = threadIdx.x & 63;
+    const float* s = S + row * k;
+    const float* da = dA + row * k;
+    const float l = lse[row];
+    float dot = 0.f;
+    for (int j = lane; j < k; j += 64) dot = __builtin_fmaf(__expf(s[j] - l), da[j], dot);
+    dot = wave_sum(dot);
+    for (int j = lane; j < k; j += 64) put<BF16>(ds, row * k + j, scale * __expf(s[j] - l) * (da[j] - dot));
+}
+
+__global__ __launch_bounds__(256) void to_bf16_kernel(const float* __restrict__ x, uint16_t* __restrict__ y,
+                                                      int64_t n) {
+    const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    if (i < n) y[i] = tile::to_bf16(x[i]);
+}
+
+}  // namespace
+
+hipError_t launch_stca_softmax(const float* S, int64_t rows, int32_t k, bool bf16, void* alpha, float* lse,
+                               hipStream_t stream) {
+    if (rows <= 0) return hipSuccess;
+    const dim3 grid((unsigned)((rows + 3) / 4));
+    if (bf16) hipLaunchKernelGGL(stca_softmax_kernel<true>, grid, dim3(256), 0, stream, S, rows, k, alpha, lse);
+    else hipLaunchKernelGGL(stca_softmax_kernel<false>, grid, dim3(256), 0, stream, S, rows, k, alpha, lse);
+    return hipGetLastError();
+}
+
+hipError_t launch_stca_softmax_bwd(const float* S, const float* lse, const float* dA, int64_t rows, int32_t k,
+                                   float scale, bool bf16, void* ds, hipStream_t stream) {
+    if (rows <= 0) return hipSuccess;
+    const dim3 grid((unsigned)((rows + 3) / 4));
+    if (bf16)
+        hipLaunchKernelGGL(stca_softmax_bwd_kernel<true>, grid, dim3(256), 0, stream, S, lse, dA, rows, k, scale, ds);
+    else
+        hipLaunchKernelGGL(stca_softmax_bwd_kernel<false>, grid, dim3(256), 0, stream, S, lse, dA, rows, k, scale,
+                           ds);
+    return hipGetLastError();
+}
+
+hipError_t launch_to_bf16(const float* x, uint16_t* y, int64_t n, hipStream_t stream) {
+    if (n <= 0) return hipSuccess;
+    hipLaunchKernelGGL(to_bf16_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, stream, x, y, n);
+    return hipGetLastError();
+}
+
+}  // namespace sa

@@ -25,7 +25,8 @@ EXPORTS = ("sa_sketch_fwd_workspace_size", "sa_sketch_fwd", "sa_sketch_bwd_works
            "sa_sketch_fwd_tokenwise_workspace_size", "sa_sketch_fwd_tokenwise",
            "sa_layer_fwd_workspace_size", "sa_layer_fwd", "sa_layer_bwd_workspace_size",
            "sa_layer_bwd", "sa_block_fwd_workspace_size", "sa_block_fwd",
-           "sa_block_bwd_workspace_size", "sa_block_bwd",
+           "sa_block_bwd_workspace_size", "sa_block_bwd", "sa_stca_fwd_workspace_size", "sa_stca_fwd",
+           "sa_stca_bwd_workspace_size", "sa_stca_bwd",
            "sa_profile_enable", "sa_kernel_times", "sa_status_string", "sa_last_error")
 
 
@@ -86,6 +87,14 @@ def lib() -> ctypes.CDLL:
     L.sa_block_bwd.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp, vp, i64, i64, i32, i32, i32, i32, f32, f32,
                                c.c_int, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
     L.sa_block_bwd.restype = c.c_int
+    for nm in ("sa_stca_fwd_workspace_size", "sa_stca_bwd_workspace_size"):
+        getattr(L, nm).argtypes = [i64, i32, i32, i32, i32, c.c_int]
+        getattr(L, nm).restype = sz
+    L.sa_stca_fwd.argtypes = [vp, vp, vp, vp, vp, i64, i32, i32, i32, i32, f32, c.c_int, vp, vp, vp, sz, vp]
+    L.sa_stca_fwd.restype = c.c_int
+    L.sa_stca_bwd.argtypes = [vp, vp, vp, vp, vp, i64, i32, i32, i32, i32, f32, c.c_int, vp, vp, vp, vp, vp, vp,
+                              vp, sz, vp]
+    L.sa_stca_bwd.restype = c.c_int
     L.sa_build_worklist.argtypes = [vp, i64, i64, i32, i64, vp, i64, vp, vp]
     L.sa_build_worklist.restype = c.c_int
     L.sa_status_string.argtypes = [c.c_int]
@@ -402,6 +411,61 @@ def block_bwd(X, P, Wq, Wk, ln, W1, W3, W2, offsets, dout, scale: Optional[float
                             _ptr(g["dX"]), _ptr(g["dP"]), _ptr(g["dWq"]), _ptr(g["dWk"]), _ptr(g["dln"]),
                             _ptr(g["dW1"]), _ptr(g["dW3"]), _ptr(g["dW2"]), _ptr(ws), nbytes,
                             _stream_handle(stream))
+    _check(rc)
+    return g
+
+
+def stca_fwd_workspace_size(B, R, k, D, h, dtype_code) -> int:
+    return int(lib().sa_stca_fwd_workspace_size(B, R, k, D, h, dtype_code))
+
+
+def stca_bwd_workspace_size(B, R, k, D, h, dtype_code) -> int:
+    return int(lib().sa_stca_bwd_workspace_size(B, R, k, D, h, dtype_code))
+
+
+def _stca_check(Xs, q, Wq, Wk, Wv):
+    import torch
+    B, k, D = Xs.shape
+    R = q.shape[1]
+    dev, dt = Xs.device, Xs.dtype
+    _require(Xs, "Xs", (B, k, D), dt, dev)
+    _require(q, "q", (B, R, D), dt, dev)
+    for name, W in (("Wq", Wq), ("Wk", Wk), ("Wv", Wv)):
+        _require(W, name, (D, D), dt, dev)
+    return B, R, k, D, dev, _dtype_code(Xs), torch
+
+
+def stca_fwd(Xs, q, Wq, Wk, Wv, h: int, scale: Optional[float] = None, out=None, want_lse: bool = False,
+             workspace=None, stream=None):
+    """sa_stca_fwd on torch tensors: reordered single-query STCA of R targets per user
+    over the user's sketch.  Returns (out [B,R,D] fp32, lse [B,R,h] or None)."""
+    B, R, k, D, dev, code, torch = _stca_check(Xs, q, Wq, Wk, Wv)
+    if scale is None:
+        scale = 1.0 / math.sqrt(D // h)
+    if out is None:
+        out = torch.empty((B, R, D), dtype=torch.float32, device=dev)
+    _require(out, "out", (B, R, D), torch.float32, dev)
+    lse = torch.empty((B, R, h), dtype=torch.float32, device=dev) if want_lse else None
+    ws, nbytes = _workspace(stca_fwd_workspace_size(B, R, k, D, h, code), dev, workspace)
+    rc = lib().sa_stca_fwd(_ptr(Xs), _ptr(q), _ptr(Wq), _ptr(Wk), _ptr(Wv), B, R, k, D, h, float(scale), code,
+                           _ptr(out), _ptr(lse), _ptr(ws), nbytes, _stream_handle(stream))
+    _check(rc)
+    return out, lse
+
+
+def stca_bwd(Xs, q, Wq, Wk, Wv, h: int, dout, scale: Optional[float] = None, workspace=None, stream=None):
+    """sa_stca_bwd on torch tensors: dict of fp32 gradients dXs, dq, dWq, dWk, dWv."""
+    B, R, k, D, dev, code, torch = _stca_check(Xs, q, Wq, Wk, Wv)
+    _require(dout, "dout", (B, R, D), torch.float32, dev)
+    if scale is None:
+        scale = 1.0 / math.sqrt(D // h)
+    f32 = dict(dtype=torch.float32, device=dev)
+    g = {"dXs": torch.empty((B, k, D), **f32), "dq": torch.empty((B, R, D), **f32),
+         "dWq": torch.empty((D, D), **f32), "dWk": torch.empty((D, D), **f32), "dWv": torch.empty((D, D), **f32)}
+    ws, nbytes = _workspace(stca_bwd_workspace_size(B, R, k, D, h, code), dev, workspace)
+    rc = lib().sa_stca_bwd(_ptr(Xs), _ptr(q), _ptr(Wq), _ptr(Wk), _ptr(Wv), B, R, k, D, h, float(scale), code,
+                           _ptr(dout), _ptr(g["dXs"]), _ptr(g["dq"]), _ptr(g["dWq"]), _ptr(g["dWk"]),
+                           _ptr(g["dWv"]), _ptr(ws), nbytes, _stream_handle(stream))
     _check(rc)
     return g
 

@@ -30,6 +30,11 @@ Tensor layouts (token-major, packed, no padding):
 For the SA layer with its projections the history X is the V stream and the
 projections W_Q, W_K [H, d, d] ~ N(0, 1/d), so that K = X W_K and Q = P W_Q have
 the statistics of the K and P above.
+
+For the STCA over the sketch (``host_stca`` / ``device_stca``): adapted sketches
+Xs [B, k, D] ~ N(0, 1), target queries q [B, R, D] ~ N(0, 1), W_Q, W_K, W_V
+[D, D] ~ N(0, 1/D) (so that each head's logits have unit scale at
+scale = 1/sqrt(D/h)) and upstream gradients dout [B, R, D] ~ N(0, 1).
 """
 
 from __future__ import annotations
@@ -44,7 +49,8 @@ import numpy as np
 # tensor ids of the per-(seed, tensor, user) streams
 TID_LENGTHS, TID_K, TID_V, TID_P, TID_DSKETCH = 0, 1, 2, 3, 4
 TID_WQ, TID_WK = 5, 6
-TID_BLOCK = 7   # stacked-block parameters: 7 + 10 * layer + kind
+TID_BLOCK = 7   # stacked-block parameters: 7 + kind
+TID_STCA = 100  # STCA over the sketch: 100 + kind
 
 BASE_SEED = 8443
 
@@ -252,6 +258,38 @@ def device_block_params(w: Workload, L: int, device="cuda") -> dict:
     return out
 
 
+_STCA_KINDS = ("Xs", "q", "Wq", "Wk", "Wv", "dout")
+
+
+def _stca_shapes(B: int, R: int, k: int, D: int):
+    sd = 1.0 / math.sqrt(D)
+    return {"Xs": ((B, k, D), 1.0), "q": ((B, R, D), 1.0), "Wq": ((D, D), sd), "Wk": ((D, D), sd),
+            "Wv": ((D, D), sd), "dout": ((B, R, D), 1.0)}
+
+
+def host_stca(seed: int, B: int, R: int, k: int, D: int, dtype: str = "bf16") -> dict:
+    """STCA inputs on the host (exact bf16 values in bf16 mode; dout stays fp32)."""
+    out = {}
+    for i, (name, (shape, sd)) in enumerate(_stca_shapes(B, R, k, D).items()):
+        x = _normal(seed, TID_STCA + i, 0, shape, sd)
+        out[name] = x if name == "dout" else _finish(x, dtype)
+    return out
+
+
+def device_stca(seed: int, B: int, R: int, k: int, D: int, dtype: str = "bf16", device="cuda") -> dict:
+    """host_stca's distributions drawn on the device (torch Philox)."""
+    import torch
+
+    tdt = torch.bfloat16 if dtype == "bf16" else torch.float32
+    g = torch.Generator(device=device)
+    out = {}
+    for i, (name, (shape, sd)) in enumerate(_stca_shapes(B, R, k, D).items()):
+        g.manual_seed(_torch_seed(seed, TID_STCA + i, 0))
+        x = torch.randn(shape, generator=g, device=device, dtype=torch.float32) * sd
+        out[name] = x if name == "dout" else x.to(tdt)
+    return out
+
+
 def host_dsketch_user(w: Workload, b: int) -> np.ndarray:
     return _normal(w.seed, TID_DSKETCH, b, (w.R, w.H, w.M, w.d))
 
@@ -344,7 +382,7 @@ def to_device(host: dict, dtype: str, device="cuda") -> dict:
 
     out = {}
     for k, v in host.items():
-        if k in ("K", "V", "X", "P", "Wq", "Wk", "W1", "W2", "W3", "ln") and dtype == "bf16":
+        if k in ("K", "V", "X", "P", "Wq", "Wk", "Wv", "W1", "W2", "W3", "ln", "Xs", "q") and dtype == "bf16":
             bits = f32_to_bf16_bits(v).view(np.int16)
             out[k] = torch.from_numpy(bits.copy()).to(device).view(torch.bfloat16)
         else:

@@ -194,3 +194,33 @@ def test_block_bwd_rejects_bad_arguments():
     assert call(d=96) == 2
     assert call() == 3
     assert sa.block_bwd_workspace_size(2, 10, 1, 128, 64, 2, 0) > sa.block_fwd_workspace_size(2, 10, 1, 128, 64, 2, 0)
+
+
+def test_stca_rejects_bad_arguments():
+    L = sa.lib()
+    p = 1 << 12
+    fargs = dict(X=p, q=p, Wq=p, Wk=p, Wv=p, B=2, R=4, k=64, D=128, h=2, scale=0.125, dtype=0, out=p, lse=NULL,
+                 ws=NULL, wsb=0)
+
+    def fwd(**kw):
+        a = dict(fargs, **kw)
+        return L.sa_stca_fwd(a["X"], a["q"], a["Wq"], a["Wk"], a["Wv"], a["B"], a["R"], a["k"], a["D"], a["h"],
+                             a["scale"], a["dtype"], a["out"], a["lse"], a["ws"], a["wsb"], None)
+    for name in ("X", "q", "Wq", "Wk", "Wv", "out"):
+        assert fwd(**{name: NULL}) == 1, name
+    assert fwd(h=3) == 1 and fwd(R=0) == 1 and fwd(k=0) == 1 and fwd(scale=0.0) == 1 and fwd(dtype=7) == 1
+    assert fwd(q=p + 4) == 1
+    assert fwd(B=0) == 0
+    assert fwd() == 3
+    bargs = dict(fargs, dout=p, dX=p, dq=p, dWq=p, dWk=p, dWv=p)
+
+    def bwd(**kw):
+        a = dict(bargs, **kw)
+        return L.sa_stca_bwd(a["X"], a["q"], a["Wq"], a["Wk"], a["Wv"], a["B"], a["R"], a["k"], a["D"], a["h"],
+                             a["scale"], a["dtype"], a["dout"], a["dX"], a["dq"], a["dWq"], a["dWk"], a["dWv"],
+                             a["ws"], a["wsb"], None)
+    for name in ("X", "q", "Wq", "Wk", "Wv", "dout", "dX", "dq", "dWq", "dWk", "dWv"):
+        assert bwd(**{name: NULL}) == 1, name
+    assert bwd(B=0) == 1 and bwd(D=100, h=3) == 1
+    assert bwd() == 3
+    assert sa.stca_bwd_workspace_size(2, 4, 64, 128, 2, 0) > sa.stca_fwd_workspace_size(2, 4, 64, 128, 2, 0) > 0
