@@ -352,6 +352,39 @@ def main(argv=None) -> int:
                                    "step": "sa_block_fwd + sa_block_bwd", "workspace_bytes": ws_bb.numel()}
             del ws_bb
 
+    # reordered single-query STCA over the sketch (the sketch's consumer): the
+    # batch's users, R = 40 targets each (the training-side MRLB group), k = M
+    # sketch rows adapted to D = 1024 with h = 16 heads of 64; not part of the step
+    stca = None
+    if w.dtype == "bf16" and not args.no_variants:
+        Rs, Ds, hs = 40, 1024, 16
+        st = wl.device_stca(w.seed, B, Rs, M, Ds, "bf16")
+        sargs = [st[n] for n in ("Xs", "q", "Wq", "Wk", "Wv")]
+        ws_sf = torch.empty(sa.stca_fwd_workspace_size(B, Rs, M, Ds, hs, code), dtype=torch.uint8, device="cuda")
+        ws_sb = torch.empty(sa.stca_bwd_workspace_size(B, Rs, M, Ds, hs, code), dtype=torch.uint8, device="cuda")
+        out_s = torch.empty((B, Rs, Ds), dtype=torch.float32, device="cuda")
+
+        def stf():
+            sa.stca_fwd(*sargs, h=hs, out=out_s, workspace=ws_sf)
+
+        def stfb():
+            sa.stca_fwd(*sargs, h=hs, out=out_s, workspace=ws_sf)
+            sa.stca_bwd(*sargs, h=hs, dout=st["dout"], workspace=ws_sb)
+        sf_ms, ksf = timed(stf)
+        sb_ms, ksb = timed(stfb)
+        # Appendix G.2: 4 k D h + 6 D^2 per target and layer (forward); the backward
+        # has two products per forward product
+        fl_f = float(B) * Rs * (4.0 * M * Ds * hs + 6.0 * Ds * Ds)
+        stca = {"config": {"B": B, "R": Rs, "k": M, "D": Ds, "h": hs},
+                "fwd_ms": sf_ms, "fwd_bwd_ms": sb_ms,
+                "targets_per_s_fwd": B * Rs / (sf_ms * 1e-3), "targets_per_s_fwd_bwd": B * Rs / (sb_ms * 1e-3),
+                "fwd_tflops": fl_f / (sf_ms * 1e-3) / 1e12,
+                "fwd_bwd_tflops": 3 * fl_f / (sb_ms * 1e-3) / 1e12,
+                "fwd_mfma_util": fl_f / (sf_ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS,
+                "fwd_bwd_mfma_util": 3 * fl_f / (sb_ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS,
+                "kernels_fwd": kernel_dict(ksf), "kernels_fwd_bwd": kernel_dict(ksb)}
+        del st, sargs, ws_sf, ws_sb, out_s
+
     out = {
         "metric": METRIC,
         "value": T / (ms_step * 1e-3),
@@ -378,6 +411,7 @@ def main(argv=None) -> int:
         "tokenwise_fwd": tokenwise,
         "layer": layer,
         "block_fwd": block,
+        "stca": stca,
         "cpu_baseline": None,
     }
     if not args.no_cpu_baseline:

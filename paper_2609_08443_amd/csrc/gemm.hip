@@ -10,11 +10,11 @@
 // Tile 128 x 128 x 64 per workgroup of four waves, each wave a 64 x 64 block of
 // 2 x 2 v_mfma_f32_32x32x16_bf16 tiles.  Both operands are staged in LDS as
 // [row][64 k] bf16 (16-byte chunks XOR-swizzled so that operand reads of 32
-// rows are conflict free) in two buffers: the next k slab's global loads are in
-// registers while the current slab is multiplied.  A k-contiguous tile is
-// loaded as 16-byte row pieces; an m- (n-) contiguous tile as 4 k rows x 8
-// columns per thread, transposed in registers into 8 column pieces of 4 k
-// values.  Tiles of one batch run on one XCD so that its operands share that
+// rows are conflict free) in two buffers; global loads run two k slabs ahead
+// through two register sets, so a load has two slabs of products to land.  A
+// k-contiguous tile is loaded as 16-byte row pieces; an m- (n-) contiguous tile
+// as 4 k rows x 8 columns per thread, transposed in registers into 8 column
+// pieces of 4 k values.  Tiles of one batch run on one XCD so that its operands share that
 // L2.  Products whose shapes or strides do not fit (k not a multiple of 64,
 // unaligned strides, fp32 operands) run on the register-tiled fp32 product of
 // layer.hip.
@@ -41,55 +41,89 @@ struct MgArgs {
     int32_t accumulate;
 };
 
-// Global -> registers: the [128 rows][64 k] slab at (row0, k0) of an operand whose
-// element (row, k) sits at base[row s_row + k s_k].  KC: s_k = 1 (rows are k
-// runs); otherwise s_row = 1 (k rows are runs of the row index).  Rows at or past
-// nrows read row nrows - 1 (KC) or zeros (not KC; nrows is a multiple of 8).
+// One thread's share of a [128 rows][64 k] slab: four 16-byte pieces, named so
+// that they stay in registers.
+struct Slab {
+    uint4 p0, p1, p2, p3;
+};
+
+// Per-thread sources of the four pieces of an operand's slabs: element (row, k)
+// sits at base[row s_row + k s_k].  KC: s_k = 1 (rows are k runs), piece i is
+// row (tid + 256 i) / 8, 16-byte chunk tid % 8; rows at or past nrows read row
+// nrows - 1.  Otherwise s_row = 1: piece i is k row 4 (tid / 16) + i, columns
+// 8 (tid % 16) .. + 7 (nrows is a multiple of 8; columns past it read zeros).
+// Slab kt is the pieces at offset kt * step.
+struct Src {
+    const uint16_t *p0, *p1, *p2, *p3;
+    int64_t step;
+    bool ok;
+};
+
 template <bool KC>
-__device__ inline void load_slab(const uint16_t* base, int64_t s_row, int64_t s_k, int row0, int nrows, int k0,
-                                 int tid, uint4 (&r)[4]) {
+__device__ inline Src make_src(const uint16_t* base, int64_t s_row, int64_t s_k, int row0, int nrows, int tid) {
+    Src s;
     if constexpr (KC) {
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            const int c = tid + 256 * i, row = row0 + (c >> 3), kc = c & 7;
-            const int rr = row < nrows ? row : nrows - 1;
-            r[i] = *reinterpret_cast<const uint4*>(base + (int64_t)rr * s_row + k0 + 8 * kc);
-        }
+        const uint16_t* b = base + 8 * (tid & 7);
+        auto at = [&](int i) {
+            const int row = row0 + ((tid + 256 * i) >> 3);
+            return b + (int64_t)(row < nrows ? row : nrows - 1) * s_row;
+        };
+        s.p0 = at(0);
+        s.p1 = at(1);
+        s.p2 = at(2);
+        s.p3 = at(3);
+        s.step = GBK;
+        s.ok = true;
     } else {
-        const int mb = tid & 15, kb = tid >> 4;
-        const int row = row0 + 8 * mb;
-#pragma unroll
-        for (int i = 0; i < 4; ++i)
-            r[i] = row < nrows ? *reinterpret_cast<const uint4*>(base + (int64_t)(k0 + 4 * kb + i) * s_k + row)
-                               : make_uint4(0, 0, 0, 0);
+        const int row = row0 + 8 * (tid & 15);
+        s.ok = row < nrows;
+        s.p0 = base + (int64_t)(4 * (tid >> 4)) * s_k + (s.ok ? row : 0);
+        s.p1 = s.p0 + s_k;
+        s.p2 = s.p1 + s_k;
+        s.p3 = s.p2 + s_k;
+        s.step = GBK * s_k;
     }
+    return s;
 }
 
-__device__ inline uint32_t u4_at(const uint4& v, int i) {
-    return i == 0 ? v.x : i == 1 ? v.y : i == 2 ? v.z : v.w;
+__device__ inline Slab load_slab(const Src& s, int kt) {
+    const int64_t o = kt * s.step;
+    Slab r;
+    if (s.ok) {
+        r.p0 = *reinterpret_cast<const uint4*>(s.p0 + o);
+        r.p1 = *reinterpret_cast<const uint4*>(s.p1 + o);
+        r.p2 = *reinterpret_cast<const uint4*>(s.p2 + o);
+        r.p3 = *reinterpret_cast<const uint4*>(s.p3 + o);
+    } else {
+        r.p0 = r.p1 = r.p2 = r.p3 = make_uint4(0, 0, 0, 0);
+    }
+    return r;
+}
+
+// bf16 j (0..7) of a 16-byte piece
+__device__ inline uint32_t bf_at(const uint4& v, int j) {
+    const uint32_t w = (j >> 1) == 0 ? v.x : (j >> 1) == 1 ? v.y : (j >> 1) == 2 ? v.z : v.w;
+    return (j & 1) ? w >> 16 : w & 0xffffu;
 }
 
 // registers -> LDS slab [128 rows][64 k], swizzled (layout swz<64>)
 template <bool KC>
-__device__ inline void store_slab(uint16_t* lds, const uint4 (&r)[4], int tid) {
+__device__ inline void store_slab(uint16_t* lds, const Slab& s, int tid) {
     if constexpr (KC) {
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            const int c = tid + 256 * i, row = c >> 3, kc = c & 7;
-            *reinterpret_cast<uint4*>(lds + swz<64>(row, kc)) = r[i];
-        }
+        const int kc = tid & 7;
+        *reinterpret_cast<uint4*>(lds + swz<64>(tid >> 3, kc)) = s.p0;
+        *reinterpret_cast<uint4*>(lds + swz<64>((tid + 256) >> 3, kc)) = s.p1;
+        *reinterpret_cast<uint4*>(lds + swz<64>((tid + 512) >> 3, kc)) = s.p2;
+        *reinterpret_cast<uint4*>(lds + swz<64>((tid + 768) >> 3, kc)) = s.p3;
     } else {
-        // r[i] holds columns 8 mb .. 8 mb + 7 of k row 4 kb + i; column j gets the
-        // four k values of this thread, one 8-byte piece
+        // piece i holds columns 8 mb .. 8 mb + 7 of k row 4 kb + i; column j gets the
+        // thread's four k values as one 8-byte piece
         const int mb = tid & 15, kb = tid >> 4;
 #pragma unroll
         for (int j = 0; j < 8; ++j) {
-            const int dw = j >> 1, sh = 16 * (j & 1);
-            const uint32_t e0 = (u4_at(r[0], dw) >> sh) & 0xffffu, e1 = (u4_at(r[1], dw) >> sh) & 0xffffu;
-            const uint32_t e2 = (u4_at(r[2], dw) >> sh) & 0xffffu, e3 = (u4_at(r[3], dw) >> sh) & 0xffffu;
-            const int row = 8 * mb + j;
-            *reinterpret_cast<uint2*>(lds + swz<64>(row, kb >> 1) + 4 * (kb & 1)) =
-                make_uint2(e0 | (e1 << 16), e2 | (e3 << 16));
+            const uint32_t lo = bf_at(s.p0, j) | (bf_at(s.p1, j) << 16);
+            const uint32_t hi = bf_at(s.p2, j) | (bf_at(s.p3, j) << 16);
+            *reinterpret_cast<uint2*>(lds + swz<64>(8 * mb + j, kb >> 1) + 4 * (kb & 1)) = make_uint2(lo, hi);
         }
     }
 }
@@ -107,13 +141,10 @@ __global__ __launch_bounds__(256, 2) void mfma_gemm_kernel(MgArgs g) {
     const uint16_t* Ab = g.A + z * g.a_z;
     const uint16_t* Bb = g.B + z * g.b_z;
     const int nk = g.K / GBK;
-
-    uint4 ra[4], rb[4];
-    load_slab<A_KC>(Ab, g.a_m, g.a_k, m0, g.M, 0, tid, ra);
-    load_slab<B_KC>(Bb, g.b_n, g.b_k, n0, g.N, 0, tid, rb);
-    store_slab<A_KC>(As[0], ra, tid);
-    store_slab<B_KC>(Bs[0], rb, tid);
-    __syncthreads();
+    const Src sa_ = make_src<A_KC>(Ab, g.a_m, g.a_k, m0, g.M, tid);
+    const Src sb_ = make_src<B_KC>(Bb, g.b_n, g.b_k, n0, g.N, tid);
+    auto lda = [&](int kt) { return load_slab(sa_, kt); };
+    auto ldb = [&](int kt) { return load_slab(sb_, kt); };
 
     f32x16 acc[2][2];
 #pragma unroll
@@ -123,15 +154,9 @@ __global__ __launch_bounds__(256, 2) void mfma_gemm_kernel(MgArgs g) {
 #pragma unroll
             for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
     const int wm = w & 1, wn = w >> 1;
-    for (int kt = 0; kt < nk; ++kt) {
-        const int cur = kt & 1;
-        const bool more = kt + 1 < nk;
-        if (more) {
-            load_slab<A_KC>(Ab, g.a_m, g.a_k, m0, g.M, (kt + 1) * GBK, tid, ra);
-            load_slab<B_KC>(Bb, g.b_n, g.b_k, n0, g.N, (kt + 1) * GBK, tid, rb);
-        }
-        const uint16_t* Ac = As[cur];
-        const uint16_t* Bc = Bs[cur];
+    auto mul = [&](int buf) __attribute__((always_inline)) {
+        const uint16_t* Ac = As[buf];
+        const uint16_t* Bc = Bs[buf];
 #pragma unroll
         for (int ks = 0; ks < GBK / 16; ++ks) {
             const bf16x8 a0 = lds_b128(Ac, swz<64>(wm * 64 + l32, 2 * ks + hl));
@@ -143,12 +168,41 @@ __global__ __launch_bounds__(256, 2) void mfma_gemm_kernel(MgArgs g) {
             acc[1][0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1, b0, acc[1][0], 0, 0, 0);
             acc[1][1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1, b1, acc[1][1], 0, 0, 0);
         }
-        if (more) {
-            // the other buffer's readers passed the barrier that ended the previous slab
-            store_slab<A_KC>(As[cur ^ 1], ra, tid);
-            store_slab<B_KC>(Bs[cur ^ 1], rb, tid);
+    };
+    // LDS writes done, then the barrier; unlike __syncthreads() this does not
+    // wait for the global loads still in flight
+    auto lds_barrier = []() __attribute__((always_inline)) {
+        asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+        __builtin_amdgcn_s_barrier();
+        asm volatile("" ::: "memory");
+    };
+
+    // Slab kt + 1 waits in registers while slab kt is multiplied out of LDS buffer
+    // kt % 2 and slab kt + 2 is loaded: a load has two slabs of products to land.
+    // The buffer a slab is stored into was last read before the previous barrier.
+    Slab an = lda(0), bn = ldb(0);
+    store_slab<A_KC>(As[0], an, tid);
+    store_slab<B_KC>(Bs[0], bn, tid);
+    if (nk > 1) {
+        an = lda(1);
+        bn = ldb(1);
+    }
+    lds_barrier();
+#pragma unroll 2
+    for (int kt = 0; kt < nk; ++kt) {
+        Slab af, bf;
+        if (kt + 2 < nk) {
+            af = lda(kt + 2);
+            bf = ldb(kt + 2);
         }
-        __syncthreads();
+        mul(kt & 1);
+        if (kt + 1 < nk) {
+            store_slab<A_KC>(As[(kt + 1) & 1], an, tid);
+            store_slab<B_KC>(Bs[(kt + 1) & 1], bn, tid);
+        }
+        lds_barrier();
+        an = af;
+        bn = bf;
     }
 
     // C layout of a 32 x 32 tile: lane = column, register r = row srow(r, hl)
