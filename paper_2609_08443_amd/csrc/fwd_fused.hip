@@ -399,7 +399,9 @@ __global__ __launch_bounds__(NW * 64, 1) void fwd_fused_kernel(FusedFwdArgs a) {
 #pragma unroll
             for (int i = 0; i < C::NLD; ++i) vcur[i] = vreg[i];
             if (ti + 2 < ntiles) load_tile(ts + 64);
-            __syncthreads();  // B_v: V' staged, K(i+1) visible
+            // B_v: V' staged, K(i+1) visible; the loads of tile i+2 stay in flight
+            // (they have the aggregation of this tile and the logits of the next)
+            lds_barrier();
 
             // ---- acc[m, j] += E^T . V'
 #pragma unroll

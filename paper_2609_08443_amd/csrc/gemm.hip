@@ -14,7 +14,8 @@
 // through two register sets, so a load has two slabs of products to land.  A
 // k-contiguous tile is loaded as 16-byte row pieces; an m- (n-) contiguous tile
 // as 4 k rows x 8 columns per thread, transposed in registers into 8 column
-// pieces of 4 k values.  Tiles of one batch run on one XCD so that its operands share that
+// pieces of 4 k values (written so that each store instruction meets every
+// LDS bank twice, its minimum).  Tiles of one batch run on one XCD so that its operands share that
 // L2.  Products whose shapes or strides do not fit (k not a multiple of 64,
 // unaligned strides, fp32 operands) run on the register-tiled fp32 product of
 // layer.hip.
@@ -50,8 +51,8 @@ struct Slab {
 // Per-thread sources of the four pieces of an operand's slabs: element (row, k)
 // sits at base[row s_row + k s_k].  KC: s_k = 1 (rows are k runs), piece i is
 // row (tid + 256 i) / 8, 16-byte chunk tid % 8; rows at or past nrows read row
-// nrows - 1.  Otherwise s_row = 1: piece i is k row 4 (tid / 16) + i, columns
-// 8 (tid % 16) .. + 7 (nrows is a multiple of 8; columns past it read zeros).
+// nrows - 1.  Otherwise s_row = 1: piece i is k row 4 (tid % 16) + i, columns
+// 8 (tid / 16) .. + 7 (nrows is a multiple of 8; columns past it read zeros).
 // Slab kt is the pieces at offset kt * step.
 struct Src {
     const uint16_t *p0, *p1, *p2, *p3;
@@ -75,9 +76,9 @@ __device__ inline Src make_src(const uint16_t* base, int64_t s_row, int64_t s_k,
         s.step = GBK;
         s.ok = true;
     } else {
-        const int row = row0 + 8 * (tid & 15);
+        const int row = row0 + 8 * (tid >> 4);
         s.ok = row < nrows;
-        s.p0 = base + (int64_t)(4 * (tid >> 4)) * s_k + (s.ok ? row : 0);
+        s.p0 = base + (int64_t)(4 * (tid & 15)) * s_k + (s.ok ? row : 0);
         s.p1 = s.p0 + s_k;
         s.p2 = s.p1 + s_k;
         s.p3 = s.p2 + s_k;
@@ -100,12 +101,6 @@ __device__ inline Slab load_slab(const Src& s, int kt) {
     return r;
 }
 
-// bf16 j (0..7) of a 16-byte piece
-__device__ inline uint32_t bf_at(const uint4& v, int j) {
-    const uint32_t w = (j >> 1) == 0 ? v.x : (j >> 1) == 1 ? v.y : (j >> 1) == 2 ? v.z : v.w;
-    return (j & 1) ? w >> 16 : w & 0xffffu;
-}
-
 // registers -> LDS slab [128 rows][64 k], swizzled (layout swz<64>)
 template <bool KC>
 __device__ inline void store_slab(uint16_t* lds, const Slab& s, int tid) {
@@ -117,13 +112,22 @@ __device__ inline void store_slab(uint16_t* lds, const Slab& s, int tid) {
         *reinterpret_cast<uint4*>(lds + swz<64>((tid + 768) >> 3, kc)) = s.p3;
     } else {
         // piece i holds columns 8 mb .. 8 mb + 7 of k row 4 kb + i; column j gets the
-        // thread's four k values as one 8-byte piece
-        const int mb = tid & 15, kb = tid >> 4;
+        // thread's four k values as one 8-byte piece.  The 16 k groups of a
+        // half-wave cover every chunk of a row, and the upper half-wave writes
+        // columns in the order j ^ 1 (rows of the other parity), so each write
+        // instruction spreads over all 64 banks.
+        const int kb = tid & 15, mb = tid >> 4, flip = (tid >> 5) & 1;
 #pragma unroll
         for (int j = 0; j < 8; ++j) {
-            const uint32_t lo = bf_at(s.p0, j) | (bf_at(s.p1, j) << 16);
-            const uint32_t hi = bf_at(s.p2, j) | (bf_at(s.p3, j) << 16);
-            *reinterpret_cast<uint2*>(lds + swz<64>(8 * mb + j, kb >> 1) + 4 * (kb & 1)) = make_uint2(lo, hi);
+            const int sh = 16 * ((j & 1) ^ flip);   // column j ^ flip: same dword, other half
+            auto el = [&](const uint4& v) {
+                const uint32_t w = (j >> 1) == 0 ? v.x : (j >> 1) == 1 ? v.y : (j >> 1) == 2 ? v.z : v.w;
+                return (w >> sh) & 0xffffu;
+            };
+            const uint32_t lo = el(s.p0) | (el(s.p1) << 16);
+            const uint32_t hi = el(s.p2) | (el(s.p3) << 16);
+            *reinterpret_cast<uint2*>(lds + swz<64>(8 * mb + (j ^ flip), kb >> 1) + 4 * (kb & 1)) =
+                make_uint2(lo, hi);
         }
     }
 }
@@ -169,17 +173,10 @@ __global__ __launch_bounds__(256, 2) void mfma_gemm_kernel(MgArgs g) {
             acc[1][1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1, b1, acc[1][1], 0, 0, 0);
         }
     };
-    // LDS writes done, then the barrier; unlike __syncthreads() this does not
-    // wait for the global loads still in flight
-    auto lds_barrier = []() __attribute__((always_inline)) {
-        asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
-        __builtin_amdgcn_s_barrier();
-        asm volatile("" ::: "memory");
-    };
-
     // Slab kt + 1 waits in registers while slab kt is multiplied out of LDS buffer
     // kt % 2 and slab kt + 2 is loaded: a load has two slabs of products to land.
-    // The buffer a slab is stored into was last read before the previous barrier.
+    // The buffer a slab is stored into was last read before the previous barrier;
+    // the barriers wait for LDS traffic only, so the loads stay in flight.
     Slab an = lda(0), bn = ldb(0);
     store_slab<A_KC>(As[0], an, tid);
     store_slab<B_KC>(Bs[0], bn, tid);

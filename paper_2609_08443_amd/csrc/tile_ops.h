@@ -101,6 +101,17 @@ __device__ inline void load_lds16(const void* src, void* lds_base) {
 }
 __device__ inline void wait_vmem() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
 
+// Workgroup barrier for LDS traffic only: waits for this wave's LDS operations,
+// then s_barrier.  Unlike __syncthreads(), which also waits for every
+// outstanding global load (vmcnt(0)), loads issued into registers ahead of time
+// stay in flight across it; their uses wait for them as usual.  Not for data
+// that global_load_lds writes into LDS (wait_vmem() first for that).
+__device__ inline void lds_barrier() {
+    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
+}
+
 __device__ inline bf16x8 lds_b128(const uint16_t* base, int off) {
     return __builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4*>(base + off));
 }
