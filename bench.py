@@ -43,14 +43,14 @@ WORKLOADS = {"c1": 1, "c2": 2, "c3": 3, "c4": 4, "c5": 5}
 # Source: profiles/hbm_bytes_c5_ragged100k_fwd_bwd.md
 MEASURED_TRAFFIC = {
     "bwd_token": ("paper_2609_08443_amd/csrc/bwd_fused.hip",
-                  "3a7efaa890bbe826a2ded34b4df97da7c1bfd9faf8d0f687afc9ca2a22d74c5f",
-                  2.181e9 + 2.250e9),
+                  "61cea36a3c6bad741406fd4cddc15cda38376aac07d8d7fd592d84c0faa92db0",
+                  2.179e9 + 2.250e9),
     "bwd_proto": ("paper_2609_08443_amd/csrc/bwd_fused.hip",
-                  "3a7efaa890bbe826a2ded34b4df97da7c1bfd9faf8d0f687afc9ca2a22d74c5f",
+                  "61cea36a3c6bad741406fd4cddc15cda38376aac07d8d7fd592d84c0faa92db0",
                   1.219e9 + 0.100e9),
     "fused_fwd": ("paper_2609_08443_amd/csrc/fwd_fused.hip",
-                  "81e4590139fa386c103d1bf4a49b228eac16704082de79046b7099f92239fed6",
-                  0.834e9 + 0.135e9),
+                  "bf8d1f5560f37af5249df111b3319642b7d7384a61f023ac6b8f44397a436e57",
+                  0.636e9 + 0.135e9),
 }
 
 
