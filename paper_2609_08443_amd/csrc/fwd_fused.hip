@@ -245,16 +245,23 @@ __global__ __launch_bounds__(NW * 64, 1) void fwd_fused_kernel(FusedFwdArgs a) {
             }
         };
         // one 32x32 tile of S for this wave's prototype tile mt
+        // one 32x32 tile of S for this wave's prototype tile mt.  The matrix-core
+        // chain is written out so that the tile lands in VGPRs (the exponentials
+        // read it) while the accumulator stays in AGPRs; the compiler does not
+        // model these instructions, so each waits 2 states after any VALU write
+        // of its operands, and the tile is read 32 states after the last one.
         auto s_tile = [&](const bf16x8* kop, int mt) {
             f32x16 s;
-#pragma unroll
-            for (int r = 0; r < 16; ++r) s[r] = 0.f;
             const int prow = w * MW + mt * 32 + l32;
+            bf16x8 bp[C::KS];
 #pragma unroll
-            for (int kk = 0; kk < C::KS; ++kk) {
-                const bf16x8 bp = lds_b128(Ps, swz<D>(prow, 2 * kk + hl));
-                s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kop[kk], bp, s, 0, 0, 0);
-            }
+            for (int kk = 0; kk < C::KS; ++kk) bp[kk] = lds_b128(Ps, swz<D>(prow, 2 * kk + hl));
+            __builtin_amdgcn_sched_barrier(0);
+            asm("s_nop 1\n\tv_mfma_f32_32x32x16_bf16 %0, %1, %2, 0" : "=&v"(s) : "v"(kop[0]), "v"(bp[0]));
+#pragma unroll
+            for (int kk = 1; kk < C::KS; ++kk)
+                asm("s_nop 1\n\tv_mfma_f32_32x32x16_bf16 %0, %1, %2, %0" : "+v"(s) : "v"(kop[kk]), "v"(bp[kk]));
+            asm volatile("s_nop 15\n\ts_nop 15" : "+v"(s));
             return s;
         };
 
