@@ -320,8 +320,8 @@ def main(argv=None) -> int:
                  "mfma_util": flops_step / (ly_ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS}
 
     # stacked SA (N_sa = 2 layers, the paper's deployed depth) on the same batch,
-    # X = the V tensor: the forward alone, then forward + backward (the backward
-    # replays the forward itself); not part of the step
+    # X = the V tensor: the forward alone, then a training step (forward keeping
+    # its intermediates + backward); not part of the step
     block = None
     if not args.no_variants:
         n_layers = 2
@@ -338,19 +338,24 @@ def main(argv=None) -> int:
                  "kernels": kernel_dict(kbl), "step": "sa_block_fwd"}
         if w.bwd:
             del ws_bl
-            ws_bb = torch.empty(max(sa.block_bwd_workspace_size(B, T, H, M, d, n_layers, code), 1),
+            # training: the forward keeps its intermediates in `saved`, the
+            # backward reads them instead of replaying the forward
+            ws_bb = torch.empty(max(sa.block_bwd_workspace_size(B, T, H, M, d, n_layers, code, True),
+                                    sa.block_fwd_workspace_size(B, T, H, M, d, n_layers, code), 1),
                                 dtype=torch.uint8, device="cuda")
+            saved = sa.block_saved_buffer(dev["V"], dev["P"], bp["Wq"], dev["offsets"])
             dout = dev["dsketch"][:, 0].contiguous()
 
             def blk_train():
                 sa.block_fwd(dev["V"], dev["P"], bp["Wq"], bp["Wk"], bp["ln"], bp["W1"], bp["W3"], bp["W2"],
-                             dev["offsets"], w.scale, out=out_bl, workspace=ws_bb)
+                             dev["offsets"], w.scale, out=out_bl, saved=saved, workspace=ws_bb)
                 sa.block_bwd(dev["V"], dev["P"], bp["Wq"], bp["Wk"], bp["ln"], bp["W1"], bp["W3"], bp["W2"],
-                             dev["offsets"], dout, w.scale, workspace=ws_bb)
+                             dev["offsets"], dout, w.scale, saved=saved, workspace=ws_bb)
             bt_ms, kbt = timed(blk_train)
             block["train_step"] = {"tokens_per_s": T / (bt_ms * 1e-3), "ms": bt_ms, "kernels": kernel_dict(kbt),
-                                   "step": "sa_block_fwd + sa_block_bwd", "workspace_bytes": ws_bb.numel()}
-            del ws_bb
+                                   "step": "sa_block_fwd (saved) + sa_block_bwd",
+                                   "workspace_bytes": ws_bb.numel(), "saved_bytes": saved.numel()}
+            del ws_bb, saved
 
     # reordered single-query STCA over the sketch (the sketch's consumer): the
     # batch's users, R = 40 targets each (the training-side MRLB group), k = M

@@ -251,27 +251,43 @@ size_t sa_block_fwd_workspace_size(int64_t B, int64_t T, int32_t H, int32_t M, i
  *   eps       layer-norm epsilon (> 0)
  *   out       output [B,H,M,d] fp32: the refined sketch
  *   lse       output [n_layers,T,H] fp32 (each layer's per-token log-sum-exp), or NULL
+ *   saved     NULL (inference), or a device buffer of sa_block_saved_size bytes,
+ *             16-byte aligned (training): every layer's intermediates are written
+ *             there for sa_block_bwd, which then skips its replay of the forward.
+ *             Its layout is private to the library; the caller owns it and keeps
+ *             it unchanged between the two calls.
  *
  * A user without tokens has a zero Xhat in every layer, so its output is the
  * refinement of the prototypes alone.  The sketching steps run on the same
  * kernels as sa_layer_fwd; the projections and the FFN on a batched fp32
  * product.  Offsets, sizes, errors, ownership and streams as for sa_sketch_fwd;
- * n_layers < 1 or a non-positive eps is SA_ERR_INVALID_ARG.
+ * n_layers < 1 or a non-positive eps is SA_ERR_INVALID_ARG, a saved buffer too
+ * small or misaligned SA_ERR_WORKSPACE.
  */
 sa_status sa_block_fwd(const void* X, const void* P, const void* Wq, const void* Wk, const void* ln,
                        const void* W1, const void* W3, const void* W2, const int64_t* offsets,
                        int64_t B, int64_t T, int32_t H, int32_t M, int32_t d, int32_t n_layers,
                        float scale, float eps, sa_dtype dtype, float* out, float* lse,
-                       void* workspace, size_t workspace_bytes, void* stream);
+                       void* saved, size_t saved_bytes, void* workspace, size_t workspace_bytes,
+                       void* stream);
 
-/* Bytes of workspace that sa_block_bwd needs for this shape. */
+/* Bytes of the buffer of saved intermediates (sa_block_fwd's `saved`) for this
+ * shape: per layer about (36 + 2 or 4 bytes per element of the dtype) B H M d
+ * bytes plus 4 T H; 0 for invalid sizes. */
+size_t sa_block_saved_size(int64_t B, int64_t T, int32_t H, int32_t M, int32_t d, int32_t n_layers,
+                           sa_dtype dtype);
+
+/* Bytes of workspace that sa_block_bwd needs for this shape; with_saved != 0
+ * when it will be given a saved buffer (then the replay's region is left out). */
 size_t sa_block_bwd_workspace_size(int64_t B, int64_t T, int32_t H, int32_t M, int32_t d,
-                                   int32_t n_layers, sa_dtype dtype);
+                                   int32_t n_layers, sa_dtype dtype, int32_t with_saved);
 
 /*
  * Backward of sa_block_fwd (section 3.3) by the chain rule: the gradients of
- * <dout, out> with respect to every input.  The forward is replayed first,
- * keeping each layer's intermediates in the workspace; then, from the last
+ * <dout, out> with respect to every input.  Each layer's intermediates come
+ * from `saved` when the training forward wrote them there (same inputs, not
+ * changed since); with saved = NULL the forward is replayed first, keeping them
+ * in the workspace.  Both give bit-identical gradients.  Then, from the last
  * layer down: the second norm, the FFN (dW2 = Z^T dY2, the gate
  * silu'(g) = s (1 + g (1 - s)), dW1 = Xbar^T dG, dW3 = Xbar^T dU), the first
  * norm, the sketch (the sketching backward with dsketch = the gradient of Xhat,
@@ -294,7 +310,8 @@ sa_status sa_block_bwd(const void* X, const void* P, const void* Wq, const void*
                        int64_t B, int64_t T, int32_t H, int32_t M, int32_t d, int32_t n_layers,
                        float scale, float eps, sa_dtype dtype, const float* dout, float* dX,
                        float* dP, float* dWq, float* dWk, float* dln, float* dW1, float* dW3,
-                       float* dW2, void* workspace, size_t workspace_bytes, void* stream);
+                       float* dW2, const void* saved, size_t saved_bytes, void* workspace,
+                       size_t workspace_bytes, void* stream);
 
 /* Bytes of workspace that sa_stca_fwd needs for this shape. */
 size_t sa_stca_fwd_workspace_size(int64_t B, int32_t R, int32_t k, int32_t D, int32_t h,

@@ -326,27 +326,18 @@ BlockPlan plan_block(int64_t B, int64_t T, int32_t H, int32_t M, int32_t d, sa_d
     return p;
 }
 
-// ---------------------------------------------------------------- stacked block backward plan
+// ---------------------------------------------------------------- stacked block: saved intermediates
 // Per layer l a region [state_l (l >= 1) | Q_l | P'_l | lse_l | Y1_l | Xbar_l | G_l | U_l | Y2_l]
 // holding the forward's intermediates (Y1 = Xt + Xhat, Y2 = Xbar + FFN: the
-// inputs of the two norms), then the backward's scratch, then one region
-// shared by the sketching forward and backward calls.
-struct BlockBwdPlan {
-    FwdPlan fwd;
-    BwdPlan bshared, buser;
+// inputs of the two norms).  The training forward writes them to the caller's
+// `saved` buffer; without one, the backward replays the forward into its workspace.
+struct BlockSaved {
     size_t l_state = 0, l_q = 0, l_pp = 0, l_lse = 0, l_y1 = 0, l_xbar = 0, l_g = 0, l_u = 0, l_y2 = 0,
            l_stride = 0;
-    size_t off_layers = 0, off_xhat = 0, off_z = 0, off_du = 0, off_dy2 = 0, off_dy1 = 0, off_dpp = 0,
-           off_dq = 0, off_stats = 0, off_colpart = 0, off_wpart = 0, off_dxl = 0, off_dk = 0, off_dv = 0,
-           off_out = 0, off_base = 0, total = 0;
-    int64_t nch = 1;
 };
 
-BlockBwdPlan plan_block_bwd(int64_t B, int64_t T, int32_t H, int32_t M, int32_t d, int32_t L, sa_dtype dtype) {
-    BlockBwdPlan p;
-    p.fwd = plan_fwd(B, T, H, M, d, dtype, false);
-    p.bshared = plan_bwd(B, T, H, M, d, dtype, false);
-    p.buser = plan_bwd(B, T, H, M, d, dtype, true);
+BlockSaved saved_layout(int64_t B, int64_t T, int32_t H, int32_t M, int32_t d, sa_dtype dtype) {
+    BlockSaved p;
     size_t off = 0;
     auto carve = [&](size_t bytes) {
         const size_t o = off;
@@ -364,8 +355,36 @@ BlockBwdPlan plan_block_bwd(int64_t B, int64_t T, int32_t H, int32_t M, int32_t 
     p.l_u = carve(f * 2 * rd);
     p.l_y2 = carve(f * rd);
     p.l_stride = off;
-    off = 0;
-    p.off_layers = carve(p.l_stride * (size_t)L);
+    return p;
+}
+
+// ---------------------------------------------------------------- stacked block backward plan
+// [per-layer intermediates (when no saved buffer is given) | the backward's
+//  scratch | one region shared by the sketching forward and backward calls]
+struct BlockBwdPlan : BlockSaved {
+    FwdPlan fwd;
+    BwdPlan bshared, buser;
+    size_t off_layers = 0, off_xhat = 0, off_z = 0, off_du = 0, off_dy2 = 0, off_dy1 = 0, off_dpp = 0,
+           off_dq = 0, off_stats = 0, off_colpart = 0, off_wpart = 0, off_dxl = 0, off_dk = 0, off_dv = 0,
+           off_out = 0, off_base = 0, total = 0;
+    int64_t nch = 1;
+};
+
+BlockBwdPlan plan_block_bwd(int64_t B, int64_t T, int32_t H, int32_t M, int32_t d, int32_t L, sa_dtype dtype,
+                            bool with_saved) {
+    BlockBwdPlan p;
+    static_cast<BlockSaved&>(p) = saved_layout(B, T, H, M, d, dtype);
+    p.fwd = plan_fwd(B, T, H, M, d, dtype, false);
+    p.bshared = plan_bwd(B, T, H, M, d, dtype, false);
+    p.buser = plan_bwd(B, T, H, M, d, dtype, true);
+    size_t off = 0;
+    auto carve = [&](size_t bytes) {
+        const size_t o = off;
+        off = align_up(off + bytes, 256);
+        return o;
+    };
+    const size_t rd = (size_t)B * H * M * d, f = sizeof(float);
+    p.off_layers = carve(with_saved ? 0 : p.l_stride * (size_t)L);
     p.off_xhat = carve(f * rd);
     p.off_z = carve(f * 2 * rd);
     p.off_du = carve(f * 2 * rd);
@@ -420,6 +439,26 @@ sa_status run_fwd(const void* K, const void* V, const void* P, const int64_t* of
                   int64_t T, int32_t H, int32_t M, int32_t d, float scale, sa_dtype dtype,
                   float* sketch, float* lse, uint8_t* ws, const FwdPlan& plan, hipStream_t stream,
                   bool p_user);
+
+// Layer l's intermediates inside a saved region (layout s, L layers); its state
+// output is the next layer's state, or `last` for the last layer.  Xhat and Z
+// are scratch the caller sets.
+BlockLayerIo saved_io(uint8_t* base, const BlockSaved& s, int32_t l, int32_t L, const void* P, float* last) {
+    uint8_t* r = base + s.l_stride * (size_t)l;
+    BlockLayerIo io{};
+    io.first = l == 0;
+    io.xt = io.first ? P : reinterpret_cast<const void*>(r + s.l_state);
+    io.Q = reinterpret_cast<float*>(r + s.l_q);
+    io.Pp = r + s.l_pp;
+    io.lse = reinterpret_cast<float*>(r + s.l_lse);
+    io.Y1 = reinterpret_cast<float*>(r + s.l_y1);
+    io.Xbar = reinterpret_cast<float*>(r + s.l_xbar);
+    io.G = reinterpret_cast<float*>(r + s.l_g);
+    io.U = reinterpret_cast<float*>(r + s.l_u);
+    io.Y2 = reinterpret_cast<float*>(r + s.l_y2);
+    io.out = l + 1 < L ? reinterpret_cast<float*>(base + s.l_stride * (size_t)(l + 1) + s.l_state) : last;
+    return io;
+}
 
 sa_status block_layer_fwd(const void* X, const int64_t* offsets, int64_t B, int64_t T, int32_t H, int32_t M,
                           int32_t d, int32_t l, float scale, float eps, sa_dtype dtype, const BlockParams& w,
@@ -976,11 +1015,17 @@ size_t sa_block_fwd_workspace_size(int64_t B, int64_t T, int32_t H, int32_t M, i
     return plan_block(B, T, H, M, d, dtype).total;
 }
 
+size_t sa_block_saved_size(int64_t B, int64_t T, int32_t H, int32_t M, int32_t d, int32_t n_layers,
+                           sa_dtype dtype) {
+    if (check_common(B, T, H, M, d, 1.0f, dtype) != SA_OK || n_layers < 1) return 0;
+    return saved_layout(B, T, H, M, d, dtype).l_stride * (size_t)n_layers;
+}
+
 sa_status sa_block_fwd(const void* X, const void* P, const void* Wq, const void* Wk, const void* ln,
                        const void* W1, const void* W3, const void* W2, const int64_t* offsets, int64_t B,
                        int64_t T, int32_t H, int32_t M, int32_t d, int32_t n_layers, float scale, float eps,
-                       sa_dtype dtype, float* out, float* lse, void* workspace, size_t workspace_bytes,
-                       void* stream_) {
+                       sa_dtype dtype, float* out, float* lse, void* saved, size_t saved_bytes, void* workspace,
+                       size_t workspace_bytes, void* stream_) {
     g_last_error[0] = 0;
     sa_status st = check_common(B, T, H, M, d, scale, dtype);
     if (st != SA_OK) return st;
@@ -997,6 +1042,10 @@ sa_status sa_block_fwd(const void* X, const void* P, const void* Wq, const void*
     if (!workspace || workspace_bytes < plan.total)
         return fail(SA_ERR_WORKSPACE, "workspace of %zu bytes needed, %zu given", plan.total,
                     workspace ? workspace_bytes : (size_t)0);
+    const BlockSaved sl = saved_layout(B, T, H, M, d, dtype);
+    if (saved && (saved_bytes < sl.l_stride * (size_t)n_layers || !aligned16(saved)))
+        return fail(SA_ERR_WORKSPACE, "saved buffer of %zu bytes (16-byte aligned) needed, %zu given",
+                    sl.l_stride * (size_t)n_layers, saved_bytes);
     if (debug_validate()) {
         st = validate_offsets(offsets, B, T, stream);
         if (st != SA_OK) return st;
@@ -1004,6 +1053,24 @@ sa_status sa_block_fwd(const void* X, const void* P, const void* Wq, const void*
     uint8_t* ws = reinterpret_cast<uint8_t*>(workspace);
     float* state = reinterpret_cast<float*>(ws + plan.off_state);
     const BlockParams w{Wq, Wk, ln, W1, W3, W2, H, d, (size_t)(dtype == SA_BF16 ? 2 : 4)};
+    if (saved) {
+        // training forward: every layer's intermediates stay in `saved` for the
+        // backward (the gate output goes to scratch so that G is kept)
+        for (int32_t l = 0; l < n_layers; ++l) {
+            BlockLayerIo io = saved_io(reinterpret_cast<uint8_t*>(saved), sl, l, n_layers, P, out);
+            io.Xhat = reinterpret_cast<float*>(ws + plan.off_xhat);
+            io.Z = reinterpret_cast<float*>(ws + plan.off_g);
+            st = block_layer_fwd(X, offsets, B, T, H, M, d, l, scale, eps, dtype, w, io, ws + plan.off_base,
+                                 plan.base, stream);
+            if (st != SA_OK) return st;
+            if (lse && T > 0) {
+                const hipError_t e = hipMemcpyAsync(lse + (size_t)l * T * H, io.lse, sizeof(float) * (size_t)T * H,
+                                                    hipMemcpyDeviceToDevice, stream);
+                if (e != hipSuccess) return hip_fail(e, "lse copy");
+            }
+        }
+        return SA_OK;
+    }
     for (int32_t l = 0; l < n_layers; ++l) {
         BlockLayerIo io{};
         io.first = l == 0;
@@ -1024,17 +1091,17 @@ sa_status sa_block_fwd(const void* X, const void* P, const void* Wq, const void*
 }
 
 size_t sa_block_bwd_workspace_size(int64_t B, int64_t T, int32_t H, int32_t M, int32_t d,
-                                   int32_t n_layers, sa_dtype dtype) {
+                                   int32_t n_layers, sa_dtype dtype, int32_t with_saved) {
     if (check_common(B, T, H, M, d, 1.0f, dtype) != SA_OK || n_layers < 1) return 0;
-    return plan_block_bwd(B, T, H, M, d, n_layers, dtype).total;
+    return plan_block_bwd(B, T, H, M, d, n_layers, dtype, with_saved != 0).total;
 }
 
 sa_status sa_block_bwd(const void* X, const void* P, const void* Wq, const void* Wk, const void* ln,
                        const void* W1, const void* W3, const void* W2, const int64_t* offsets, int64_t B,
                        int64_t T, int32_t H, int32_t M, int32_t d, int32_t n_layers, float scale, float eps,
                        sa_dtype dtype, const float* dout, float* dX, float* dP, float* dWq, float* dWk,
-                       float* dln, float* dW1, float* dW3, float* dW2, void* workspace, size_t workspace_bytes,
-                       void* stream_) {
+                       float* dln, float* dW1, float* dW3, float* dW2, const void* saved, size_t saved_bytes,
+                       void* workspace, size_t workspace_bytes, void* stream_) {
     g_last_error[0] = 0;
     sa_status st = check_common(B, T, H, M, d, scale, dtype);
     if (st != SA_OK) return st;
@@ -1051,10 +1118,13 @@ sa_status sa_block_bwd(const void* X, const void* P, const void* Wq, const void*
         !aligned16(dW2))
         return fail(SA_ERR_INVALID_ARG, "tensor arguments must be 16-byte aligned");
     hipStream_t stream = reinterpret_cast<hipStream_t>(stream_);
-    const BlockBwdPlan plan = plan_block_bwd(B, T, H, M, d, n_layers, dtype);
+    const BlockBwdPlan plan = plan_block_bwd(B, T, H, M, d, n_layers, dtype, saved != nullptr);
     if (!workspace || workspace_bytes < plan.total)
         return fail(SA_ERR_WORKSPACE, "workspace of %zu bytes needed, %zu given", plan.total,
                     workspace ? workspace_bytes : (size_t)0);
+    if (saved && (saved_bytes < plan.l_stride * (size_t)n_layers || !aligned16(saved)))
+        return fail(SA_ERR_WORKSPACE, "saved buffer of %zu bytes (16-byte aligned) needed, %zu given",
+                    plan.l_stride * (size_t)n_layers, saved_bytes);
     if (debug_validate()) {
         st = validate_offsets(offsets, B, T, stream);
         if (st != SA_OK) return st;
@@ -1065,29 +1135,16 @@ sa_status sa_block_bwd(const void* X, const void* P, const void* Wq, const void*
     const bool bf = dtype == SA_BF16;
     const int64_t md = (int64_t)M * d, dd = (int64_t)d * d, d2 = 2 * (int64_t)d;
     const int64_t BH = B * H, rows = BH * M;
+    // the intermediates: the caller's saved buffer (read only), or the workspace
+    uint8_t* layers = saved ? reinterpret_cast<uint8_t*>(const_cast<void*>(saved)) : ws + plan.off_layers;
     auto layer_io = [&](int32_t l) {
-        uint8_t* r = ws + plan.off_layers + plan.l_stride * (size_t)l;
-        BlockLayerIo io{};
-        io.first = l == 0;
-        io.xt = io.first ? P : reinterpret_cast<const void*>(r + plan.l_state);
-        io.Q = reinterpret_cast<float*>(r + plan.l_q);
-        io.Pp = r + plan.l_pp;
-        io.lse = reinterpret_cast<float*>(r + plan.l_lse);
-        io.Y1 = reinterpret_cast<float*>(r + plan.l_y1);
-        io.Xbar = reinterpret_cast<float*>(r + plan.l_xbar);
-        io.G = reinterpret_cast<float*>(r + plan.l_g);
-        io.U = reinterpret_cast<float*>(r + plan.l_u);
-        io.Y2 = reinterpret_cast<float*>(r + plan.l_y2);
+        BlockLayerIo io = saved_io(layers, plan, l, n_layers, P, F(plan.off_out));
         io.Xhat = F(plan.off_xhat);
         io.Z = F(plan.off_z);
-        // the state of the next layer, or (last layer) a scratch output
-        io.out = l + 1 < n_layers
-                     ? reinterpret_cast<float*>(ws + plan.off_layers + plan.l_stride * (size_t)(l + 1) + plan.l_state)
-                     : F(plan.off_out);
         return io;
     };
-    // forward replay keeping every layer's intermediates
-    for (int32_t l = 0; l < n_layers; ++l) {
+    // without a saved buffer: forward replay keeping every layer's intermediates
+    for (int32_t l = 0; !saved && l < n_layers; ++l) {
         st = block_layer_fwd(X, offsets, B, T, H, M, d, l, scale, eps, dtype, w, layer_io(l), ws + plan.off_base,
                              plan.fwd, stream);
         if (st != SA_OK) return st;

@@ -25,7 +25,7 @@ EXPORTS = ("sa_sketch_fwd_workspace_size", "sa_sketch_fwd", "sa_sketch_bwd_works
            "sa_sketch_fwd_tokenwise_workspace_size", "sa_sketch_fwd_tokenwise",
            "sa_layer_fwd_workspace_size", "sa_layer_fwd", "sa_layer_bwd_workspace_size",
            "sa_layer_bwd", "sa_block_fwd_workspace_size", "sa_block_fwd",
-           "sa_block_bwd_workspace_size", "sa_block_bwd", "sa_stca_fwd_workspace_size", "sa_stca_fwd",
+           "sa_block_saved_size", "sa_block_bwd_workspace_size", "sa_block_bwd", "sa_stca_fwd_workspace_size", "sa_stca_fwd",
            "sa_stca_bwd_workspace_size", "sa_stca_bwd",
            "sa_profile_enable", "sa_kernel_times", "sa_status_string", "sa_last_error")
 
@@ -80,12 +80,14 @@ def lib() -> ctypes.CDLL:
     L.sa_block_fwd_workspace_size.argtypes = [i64, i64, i32, i32, i32, i32, c.c_int]
     L.sa_block_fwd_workspace_size.restype = sz
     L.sa_block_fwd.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp, vp, i64, i64, i32, i32, i32, i32, f32, f32,
-                               c.c_int, vp, vp, vp, sz, vp]
+                               c.c_int, vp, vp, vp, sz, vp, sz, vp]
     L.sa_block_fwd.restype = c.c_int
-    L.sa_block_bwd_workspace_size.argtypes = [i64, i64, i32, i32, i32, i32, c.c_int]
+    L.sa_block_saved_size.argtypes = [i64, i64, i32, i32, i32, i32, c.c_int]
+    L.sa_block_saved_size.restype = sz
+    L.sa_block_bwd_workspace_size.argtypes = [i64, i64, i32, i32, i32, i32, c.c_int, i32]
     L.sa_block_bwd_workspace_size.restype = sz
     L.sa_block_bwd.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp, vp, i64, i64, i32, i32, i32, i32, f32, f32,
-                               c.c_int, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
+                               c.c_int, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp, sz, vp]
     L.sa_block_bwd.restype = c.c_int
     for nm in ("sa_stca_fwd_workspace_size", "sa_stca_bwd_workspace_size"):
         getattr(L, nm).argtypes = [i64, i32, i32, i32, i32, c.c_int]
@@ -336,10 +338,33 @@ def block_fwd_workspace_size(B, T, H, M, d, n_layers, dtype_code) -> int:
     return int(lib().sa_block_fwd_workspace_size(B, T, H, M, d, n_layers, dtype_code))
 
 
+def block_saved_size(B, T, H, M, d, n_layers, dtype_code) -> int:
+    return int(lib().sa_block_saved_size(B, T, H, M, d, n_layers, dtype_code))
+
+
+def block_saved_buffer(X, P, Wq, offsets):
+    """A device buffer for the training forward's intermediates (sa_block_fwd's
+    `saved`), sized for these inputs."""
+    import torch
+    T, H, d = X.shape
+    n = block_saved_size(offsets.shape[0] - 1, T, H, P.shape[1], d, Wq.shape[0], _dtype_code(X))
+    return torch.empty(max(n, 1), dtype=torch.uint8, device=X.device)
+
+
+def _saved_arg(saved, nbytes):
+    if saved is None:
+        return None, 0
+    have = saved.numel() * saved.element_size()
+    if have < nbytes:
+        raise SAError(3, f"saved buffer of {nbytes} bytes needed, {have} given")
+    return saved, have
+
+
 def block_fwd(X, P, Wq, Wk, ln, W1, W3, W2, offsets, scale: Optional[float] = None, eps: float = 1e-5,
-              out=None, want_lse: bool = False, workspace=None, stream=None):
+              out=None, want_lse: bool = False, saved=None, workspace=None, stream=None):
     """sa_block_fwd on torch tensors: stacked SA with len(Wq) layers.
-    Returns (out [B,H,M,d] fp32, lse [n_layers,T,H] or None)."""
+    With `saved` (from block_saved_buffer) the intermediates are kept there for
+    block_bwd.  Returns (out [B,H,M,d] fp32, lse [n_layers,T,H] or None)."""
     import torch
     T, H, d = X.shape
     M = P.shape[1]
@@ -364,20 +389,23 @@ def block_fwd(X, P, Wq, Wk, ln, W1, W3, W2, offsets, scale: Optional[float] = No
     _require(out, "out", (B, H, M, d), torch.float32, dev)
     lse = torch.empty((L, T, H), dtype=torch.float32, device=dev) if want_lse else None
     ws, nbytes = _workspace(block_fwd_workspace_size(B, T, H, M, d, L, code), dev, workspace)
+    sv, sbytes = _saved_arg(saved, block_saved_size(B, T, H, M, d, L, code))
     rc = lib().sa_block_fwd(_ptr(X), _ptr(P), _ptr(Wq), _ptr(Wk), _ptr(ln), _ptr(W1), _ptr(W3), _ptr(W2),
                             _ptr(offsets), B, T, H, M, d, L, float(scale), float(eps), code, _ptr(out),
-                            _ptr(lse), _ptr(ws), nbytes, _stream_handle(stream))
+                            _ptr(lse), _ptr(sv), sbytes, _ptr(ws), nbytes, _stream_handle(stream))
     _check(rc)
     return out, lse
 
 
-def block_bwd_workspace_size(B, T, H, M, d, n_layers, dtype_code) -> int:
-    return int(lib().sa_block_bwd_workspace_size(B, T, H, M, d, n_layers, dtype_code))
+def block_bwd_workspace_size(B, T, H, M, d, n_layers, dtype_code, with_saved: bool = False) -> int:
+    return int(lib().sa_block_bwd_workspace_size(B, T, H, M, d, n_layers, dtype_code, int(bool(with_saved))))
 
 
 def block_bwd(X, P, Wq, Wk, ln, W1, W3, W2, offsets, dout, scale: Optional[float] = None, eps: float = 1e-5,
-              workspace=None, stream=None):
+              saved=None, workspace=None, stream=None):
     """sa_block_bwd on torch tensors: gradients of <dout, block_fwd(...)>.
+    `saved`: the buffer a training block_fwd with the same inputs filled (the
+    forward is then not replayed), or None.
     Returns a dict of fp32 tensors dX, dP, dWq, dWk, dln, dW1, dW3, dW2 (shapes of
     the inputs)."""
     import torch
@@ -405,11 +433,12 @@ def block_bwd(X, P, Wq, Wk, ln, W1, W3, W2, offsets, dout, scale: Optional[float
          "dWq": torch.empty((L, H, d, d), **f32), "dWk": torch.empty((L, H, d, d), **f32),
          "dln": torch.empty((L, 4, H, d), **f32), "dW1": torch.empty((L, H, d, 2 * d), **f32),
          "dW3": torch.empty((L, H, d, 2 * d), **f32), "dW2": torch.empty((L, H, 2 * d, d), **f32)}
-    ws, nbytes = _workspace(block_bwd_workspace_size(B, T, H, M, d, L, code), dev, workspace)
+    ws, nbytes = _workspace(block_bwd_workspace_size(B, T, H, M, d, L, code, saved is not None), dev, workspace)
+    sv, sbytes = _saved_arg(saved, block_saved_size(B, T, H, M, d, L, code))
     rc = lib().sa_block_bwd(_ptr(X), _ptr(P), _ptr(Wq), _ptr(Wk), _ptr(ln), _ptr(W1), _ptr(W3), _ptr(W2),
                             _ptr(offsets), B, T, H, M, d, L, float(scale), float(eps), code, _ptr(dout),
                             _ptr(g["dX"]), _ptr(g["dP"]), _ptr(g["dWq"]), _ptr(g["dWk"]), _ptr(g["dln"]),
-                            _ptr(g["dW1"]), _ptr(g["dW3"]), _ptr(g["dW2"]), _ptr(ws), nbytes,
+                            _ptr(g["dW1"]), _ptr(g["dW3"]), _ptr(g["dW2"]), _ptr(sv), sbytes, _ptr(ws), nbytes,
                             _stream_handle(stream))
     _check(rc)
     return g

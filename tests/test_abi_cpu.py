@@ -155,13 +155,13 @@ def test_block_fwd_rejects_bad_arguments():
     L = sa.lib()
     p = 1 << 12
     args = dict(X=p, P=p, Wq=p, Wk=p, ln=p, W1=p, W3=p, W2=p, off=p, B=2, T=10, H=1, M=128, d=64, n=2,
-                scale=0.125, eps=1e-5, dtype=0, out=p, lse=NULL, ws=NULL, wsb=0)
+                scale=0.125, eps=1e-5, dtype=0, out=p, lse=NULL, sv=NULL, svb=0, ws=NULL, wsb=0)
 
     def call(**kw):
         a = dict(args, **kw)
         return L.sa_block_fwd(a["X"], a["P"], a["Wq"], a["Wk"], a["ln"], a["W1"], a["W3"], a["W2"], a["off"],
                               a["B"], a["T"], a["H"], a["M"], a["d"], a["n"], a["scale"], a["eps"], a["dtype"],
-                              a["out"], a["lse"], a["ws"], a["wsb"], None)
+                              a["out"], a["lse"], a["sv"], a["svb"], a["ws"], a["wsb"], None)
     for name in ("X", "P", "Wq", "Wk", "ln", "W1", "W3", "W2", "off", "out"):
         assert call(**{name: NULL}) == 1, name
     assert call(n=0) == 1
@@ -169,6 +169,11 @@ def test_block_fwd_rejects_bad_arguments():
     assert call(W2=p + 2) == 1
     assert call(d=96) == 2
     assert call() == 3
+    # a saved buffer too small or misaligned is rejected before any launch
+    need = sa.block_saved_size(2, 10, 1, 128, 64, 2, 0)
+    assert need > 0 and sa.block_saved_size(2, 10, 1, 128, 64, 0, 0) == 0
+    assert call(ws=p, wsb=1 << 40, sv=p, svb=need - 1) == 3
+    assert call(ws=p, wsb=1 << 40, sv=p + 4, svb=need) == 3
     assert sa.block_fwd_workspace_size(2, 10, 1, 128, 64, 2, 0) > sa.fwd_workspace_size(2, 10, 1, 128, 64, 0)
 
 
@@ -177,14 +182,14 @@ def test_block_bwd_rejects_bad_arguments():
     p = 1 << 12
     args = dict(X=p, P=p, Wq=p, Wk=p, ln=p, W1=p, W3=p, W2=p, off=p, B=2, T=10, H=1, M=128, d=64, n=2,
                 scale=0.125, eps=1e-5, dtype=0, dout=p, dX=p, dP=p, dWq=p, dWk=p, dln=p, dW1=p, dW3=p, dW2=p,
-                ws=NULL, wsb=0)
+                sv=NULL, svb=0, ws=NULL, wsb=0)
 
     def call(**kw):
         a = dict(args, **kw)
         return L.sa_block_bwd(a["X"], a["P"], a["Wq"], a["Wk"], a["ln"], a["W1"], a["W3"], a["W2"], a["off"],
                               a["B"], a["T"], a["H"], a["M"], a["d"], a["n"], a["scale"], a["eps"], a["dtype"],
                               a["dout"], a["dX"], a["dP"], a["dWq"], a["dWk"], a["dln"], a["dW1"], a["dW3"],
-                              a["dW2"], a["ws"], a["wsb"], None)
+                              a["dW2"], a["sv"], a["svb"], a["ws"], a["wsb"], None)
     for name in ("X", "P", "Wq", "Wk", "ln", "W1", "W3", "W2", "off", "dout", "dX", "dP", "dWq", "dWk", "dln",
                  "dW1", "dW3", "dW2"):
         assert call(**{name: NULL}) == 1, name
@@ -193,7 +198,13 @@ def test_block_bwd_rejects_bad_arguments():
     assert call(dW3=p + 8) == 1
     assert call(d=96) == 2
     assert call() == 3
+    need = sa.block_saved_size(2, 10, 1, 128, 64, 2, 0)
+    assert call(ws=p, wsb=1 << 40, sv=p, svb=need - 1) == 3
+    assert call(ws=p, wsb=1 << 40, sv=p + 4, svb=need) == 3
     assert sa.block_bwd_workspace_size(2, 10, 1, 128, 64, 2, 0) > sa.block_fwd_workspace_size(2, 10, 1, 128, 64, 2, 0)
+    # with a saved buffer the replay's per-layer region is left out of the workspace
+    assert (sa.block_bwd_workspace_size(2, 10, 1, 128, 64, 2, 0)
+            - sa.block_bwd_workspace_size(2, 10, 1, 128, 64, 2, 0, True)) == need
 
 
 def test_stca_rejects_bad_arguments():

@@ -181,3 +181,39 @@ def test_block_bwd_deterministic(sa):
     _, _, g2, _ = run_bwd(sa, [500, 0, 77, 260], 2, 256, 128, 2, "bf16", seed=41)
     for k in g1:
         np.testing.assert_array_equal(g1[k], g2[k], err_msg=k)
+
+
+# ------------------------------------------------------------------ training mode
+# The training forward keeps every layer's intermediates in a caller buffer and
+# the backward reads them instead of replaying the forward: the same kernels on
+# the same inputs in the same order, so outputs and gradients are bit-identical
+# to the inference forward and the replaying backward, and the backward leaves
+# the buffer unchanged.
+@pytest.mark.parametrize("lengths,H,M,d,L,dtype", [
+    ([37, 0, 70, 1, 5], 2, 128, 64, 2, "bf16"),
+    ([96, 31, 200], 1, 256, 64, 3, "bf16"),
+    ([40, 0, 77], 2, 64, 64, 2, "fp32"),
+])
+def test_block_saved_matches_replay(sa, lengths, H, M, d, L, dtype):
+    w = wl.custom(lengths, H, M, d, dtype, seed=7 * sum(lengths) + L, R=1, bwd=True)
+    host = wl.host_tensors(w)
+    host.update(wl.host_block_params(w, L))
+    host["X"] = host.pop("V")
+    del host["K"]
+    dout = torch.tensor(np.ascontiguousarray(host.pop("dsketch")[:, 0]), dtype=torch.float32, device="cuda")
+    dev = wl.to_device(host, dtype)
+    args = (dev["X"], dev["P"], *[dev[k] for k in NAMES], dev["offsets"])
+    print(f"block saved case lengths={lengths} H={H} M={M} d={d} L={L} {dtype}", flush=True)
+    out0, lse0 = sa.block_fwd(*args, w.scale, want_lse=True)
+    g0 = sa.block_bwd(*args, dout, w.scale)
+    saved = sa.block_saved_buffer(dev["X"], dev["P"], dev["Wq"], dev["offsets"])
+    out1, lse1 = sa.block_fwd(*args, w.scale, want_lse=True, saved=saved)
+    before = saved.clone()
+    g1 = sa.block_bwd(*args, dout, w.scale, saved=saved)
+    g2 = sa.block_bwd(*args, dout, w.scale, saved=saved)
+    torch.cuda.synchronize()
+    assert torch.equal(out0, out1) and torch.equal(lse0, lse1)
+    assert torch.equal(saved, before)
+    for k in g0:
+        assert torch.equal(g0[k], g1[k]), k
+        assert torch.equal(g1[k], g2[k]), k
