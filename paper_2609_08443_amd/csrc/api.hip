@@ -365,7 +365,7 @@ struct BlockBwdPlan : BlockSaved {
     FwdPlan fwd;
     BwdPlan bshared, buser;
     size_t off_layers = 0, off_xhat = 0, off_z = 0, off_du = 0, off_dy2 = 0, off_dy1 = 0, off_dpp = 0,
-           off_dq = 0, off_stats = 0, off_colpart = 0, off_wpart = 0, off_dxl = 0, off_dk = 0, off_dv = 0,
+           off_dq = 0, off_stats = 0, off_colpart = 0, off_wpart = 0, off_dk = 0, off_dv = 0,
            off_out = 0, off_base = 0, total = 0;
     int64_t nch = 1;
 };
@@ -397,7 +397,6 @@ BlockBwdPlan plan_block_bwd(int64_t B, int64_t T, int32_t H, int32_t M, int32_t 
     p.nch = std::max<int64_t>(1, std::min<int64_t>(B * M, (1024 + H - 1) / H));
     p.off_colpart = carve(f * (size_t)p.nch * H * 2 * d);
     p.off_wpart = carve(f * (size_t)B * H * 2 * d * d);
-    p.off_dxl = carve(L > 1 ? f * (size_t)T * H * d : 0);
     if (!p.bshared.fused) {
         p.off_dk = carve(f * (size_t)T * H * d);
         p.off_dv = carve(f * (size_t)T * H * d);
@@ -660,13 +659,14 @@ sa_status run_fwd(const void* K, const void* V, const void* P, const int64_t* of
 
 
 // backward on a checked plan and workspace.  With dX non-null, K and V are the
-// same tensor X and the gradient w.r.t. it, dX = dK + dV, is written instead of
-// dK and dV (the plain path still needs dK and dV as scratch).
+// same tensor X and the gradient w.r.t. it, dX = dK + dV, is written (added to dX
+// with dx_add) instead of dK and dV (the plain path still needs dK and dV as
+// scratch).
 sa_status run_bwd(const void* K, const void* V, const void* P, const int64_t* offsets, int64_t B,
                   int64_t T, int32_t H, int32_t M, int32_t d, float scale, sa_dtype dtype,
                   const float* dsketch, int32_t R, const float* lse, float* dK, float* dV,
                   float* dP, float* dX, uint8_t* ws, const BwdPlan& plan, hipStream_t stream,
-                  bool p_user = false) {
+                  bool p_user = false, bool dx_add = false) {
     float* dY = reinterpret_cast<float*>(ws + plan.off_dY);
     float* Dbuf = reinterpret_cast<float*>(ws + plan.off_D);
     float* part = reinterpret_cast<float*>(ws + plan.off_part);
@@ -700,6 +700,7 @@ sa_status run_bwd(const void* K, const void* V, const void* P, const int64_t* of
         f.dP = dP;
         f.dX = dX;
         f.p_user = p_user;
+        f.dx_add = dx_add;
         {
             sa::ProfScope ps("worklist", stream);
             e = sa::launch_worklist(offsets, B, T, H, plan.C, plan.n_ranges,
@@ -726,7 +727,8 @@ sa_status run_bwd(const void* K, const void* V, const void* P, const int64_t* of
     if (e != hipSuccess) return hip_fail(e, "backward launch");
     if (dX) {
         sa::ProfScope ps("dX_sum", stream);
-        e = sa::launch_add(dK, dV, dX, T * H * d, stream);
+        e = sa::launch_add(dK, dV, dx_add ? dK : dX, T * H * d, stream);
+        if (e == hipSuccess && dx_add) e = sa::launch_add(dX, dK, dX, T * H * d, stream);
         if (e != hipSuccess) return hip_fail(e, "dX sum launch");
     }
     return SA_OK;
@@ -1206,19 +1208,15 @@ sa_status sa_block_bwd(const void* X, const void* P, const void* Wq, const void*
                                       plan.nch, dlnl, (int64_t)H * d, stream);
             if (e != hipSuccess) return hip_fail(e, "block refinement backward launch");
         }
-        // the sketch (dsketch = dY1, one target instance): dX of this layer and dP'
-        float* dXl = l == n_layers - 1 ? dX : F(plan.off_dxl);
+        // the sketch (dsketch = dY1, one target instance): dX of this layer (the
+        // last layer writes dX, the others add to it) and dP'
         if (T > 0) {
             float* dKs = plan.bshared.fused ? nullptr : F(plan.off_dk);
             float* dVs = plan.bshared.fused ? nullptr : F(plan.off_dv);
-            st = run_bwd(X, X, io.Pp, offsets, B, T, H, M, d, scale, dtype, dY1, 1, io.lse, dKs, dVs, dPp, dXl,
-                         ws + plan.off_base, io.first ? plan.bshared : plan.buser, stream, !io.first);
+            st = run_bwd(X, X, io.Pp, offsets, B, T, H, M, d, scale, dtype, dY1, 1, io.lse, dKs, dVs, dPp, dX,
+                         ws + plan.off_base, io.first ? plan.bshared : plan.buser, stream, !io.first,
+                         l != n_layers - 1);
             if (st != SA_OK) return st;
-            if (dXl != dX) {
-                sa::ProfScope ps("dX_sum", stream);
-                e = sa::launch_add(dX, dXl, dX, T * H * d, stream);
-                if (e != hipSuccess) return hip_fail(e, "dX sum launch");
-            }
         } else {
             e = sa::launch_fill(dPp, nq * md, 0.f, stream);
             if (e != hipSuccess) return hip_fail(e, "fill launch");

@@ -172,6 +172,7 @@ struct TokArgs {
     float* dX;      // XV: dX = dV + dK (K and V are the same tensor X)
     float* Dbuf;
     bool p_user;    // P, Pjm hold one block per (user, head)
+    bool dx_add;    // XV: add to dX instead of overwriting it
 };
 
 // XV: K and V are one tensor X (the SA layer aggregates its own history and its
@@ -280,7 +281,7 @@ __global__ __launch_bounds__(NW * 64, 8 / NW) void bwd_token_kernel(TokArgs a) {
     // into the rows of `out`.  The C layout holds 16-byte pieces of 32 token rows
     // per store; each 32-column slice goes through this wave's LDS area so that
     // every store instruction writes whole 128-byte lines of 8 tokens.
-    auto store_rows = [&](const f32x16 (&acc)[C::JT], float* out, float f, int tb, int te, int h)
+    auto store_rows = [&](const f32x16 (&acc)[C::JT], float* out, float f, int tb, int te, int h, bool add)
         __attribute__((always_inline)) {
 #pragma unroll
         for (int jt = 0; jt < C::JT; ++jt) {
@@ -295,7 +296,15 @@ __global__ __launch_bounds__(NW * 64, 8 / NW) void bwd_token_kernel(TokArgs a) {
                 const int t = 8 * q + (lane >> 3), cc = 4 * (lane & 7);
                 const float4 v = *reinterpret_cast<const float4*>(stg + t * C::ROWF + cc);
                 const int tk = tb + 32 * w + t;
-                if (tk < te) *reinterpret_cast<float4*>(out + ((int64_t)tk * a.H + h) * D + jt * 32 + cc) = v;
+                if (tk < te) {
+                    float4* o = reinterpret_cast<float4*>(out + ((int64_t)tk * a.H + h) * D + jt * 32 + cc);
+                    if (add) {
+                        const float4 u = *o;
+                        *o = make_float4(u.x + v.x, u.y + v.y, u.z + v.z, u.w + v.w);
+                    } else {
+                        *o = v;
+                    }
+                }
             }
             asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");   // reads done before the next slice
         }
@@ -386,7 +395,7 @@ __global__ __launch_bounds__(NW * 64, 8 / NW) void bwd_token_kernel(TokArgs a) {
         Dt = tv ? xhalf_sum(Dt) : 0.f;
         if (tv && hl == 0) a.Dbuf[(int64_t)tok * a.H + h] = Dt;
         // dV rows now (frees their registers); they drain under sweep 2's first stage
-        if constexpr (!XV) store_rows(dvt, a.dV, 1.0f, tb, te, h);
+        if constexpr (!XV) store_rows(dvt, a.dV, 1.0f, tb, te, h, false);
 
         // ---------------- sweep 2: dK^T[j, t] = scale sum_m P[m, j] dS[t, m]
         // (XV: continues from dV^T, with scale folded into the weights)
@@ -472,7 +481,7 @@ __global__ __launch_bounds__(NW * 64, 8 / NW) void bwd_token_kernel(TokArgs a) {
             wait_vmem();
             __syncthreads();
         }
-        store_rows(dkt, XV ? a.dX : a.dK, XV ? 1.0f : a.scale, tb, te, h);
+        store_rows(dkt, XV ? a.dX : a.dK, XV ? 1.0f : a.scale, tb, te, h, XV && a.dx_add);
         if (!more) break;
         cur = nxt;
     }
@@ -835,7 +844,7 @@ hipError_t launch_fused_bwd(const FusedBwdArgs& f, hipStream_t stream) {
         t.K = f.K; t.V = f.V; t.P = f.P; t.Pjm = f.Pjm; t.Ymj = f.Ymj; t.Yjm = f.Yjm;
         t.lse = f.lse; t.items = f.items; t.wg_start = f.wg_start; t.max_items = f.max_items;
         t.T = f.T; t.B = (int32_t)f.B; t.H = f.H; t.M = f.M; t.scale = f.scale;
-        t.dK = f.dK; t.dV = f.dV; t.dX = f.dX; t.Dbuf = f.Dbuf; t.p_user = f.p_user;
+        t.dK = f.dK; t.dV = f.dV; t.dX = f.dX; t.Dbuf = f.Dbuf; t.p_user = f.p_user; t.dx_add = f.dx_add;
         const bool xv = f.dX != nullptr;
         hipError_t e;
         {

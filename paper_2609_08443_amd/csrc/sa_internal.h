@@ -105,6 +105,8 @@ struct FusedBwdArgs {
     // P (and Pjm) hold one prototype block per (user, head) and dP is [B,H,M,d],
     // each pair's gradient (stacked layers after the first)
     bool p_user;
+    // with dX: add the gradient to dX instead of overwriting it
+    bool dx_add = false;
 };
 bool fused_bwd_supported(int32_t M, int32_t d);
 int32_t fused_bwd_part(int32_t M, int32_t d);
