@@ -1,0 +1,128 @@
+"""GPU parity at the full sizes of the paper-shaped configurations, in the launch
+configuration the benchmark times: inputs from the device generator (the same
+seeded streams as the benchmark), the default fused path, one call per pass.
+
+* config 2 (16 users x 10K tokens, H=4, d=64, M=256): every sketch and lse
+  value against the fp64 oracle.
+* config 4 (64 users x 100K tokens, H=8, d=64, M=1024; 13 GB of K and V): the
+  sketches and lse of the first and the last user against the oracle run on
+  those users alone (a user's sketch and its tokens' lse depend only on its own
+  tokens and P), and on every (user, head) the mass identity
+  sum_m sketch[b,h,m,:] = sum_t V[t,h,:] (the weights of a token sum to one),
+  which catches tokens lost, counted twice or leaked across users at full size.
+* config 5 (config 3's ragged batch of 32 users with 1K-100K tokens, H=4,
+  d=128, M=512, plus the backward with R=4): every sketch, lse, dK, dV and dP
+  value against the oracle over the whole batch (about half a minute of host
+  time on 16 threads).
+
+Bounds as in the other parity tests: normwise max relative error <= 2e-2 per
+(user, head) slice (per head for dP), lse absolute error <= 1e-3.
+"""
+import numpy as np
+import pytest
+
+import oracle
+from paper_2609_08443_amd import workloads as wl
+
+torch = pytest.importorskip("torch")
+pytestmark = pytest.mark.gpu
+
+TOL = 2e-2
+LSE_TOL = 1e-3
+
+
+@pytest.fixture(scope="module")
+def sa():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from paper_2609_08443_amd import sa_sketch
+    sa_sketch.lib()
+    return sa_sketch
+
+
+def rel(g, r, axes):
+    err = np.abs(g.astype(np.float64) - r).max(axis=axes)
+    return err / np.maximum(np.abs(r).max(axis=axes), 1e-30)
+
+
+def host_view(dev, keys, s=None, e=None):
+    out = {}
+    for k in keys:
+        t = dev[k] if s is None else dev[k][s:e]
+        out[k] = t.float().cpu().numpy()
+    return out
+
+
+def check_users(w, off, users, sk, lse, ref_sk, ref_lse):
+    """Sketch of each listed user (rows of ref_* in the order of users) and the lse of its tokens."""
+    for i, b in enumerate(users):
+        e = rel(sk[b], ref_sk[i], (1, 2))
+        assert np.all(e <= TOL), ("sketch", b, e.max())
+    lerr = max((np.abs(lse[off[b]:off[b + 1]] - ref_lse[i]).max() for i, b in enumerate(users)
+                if off[b + 1] > off[b]), default=0.0)
+    assert lerr <= LSE_TOL, ("lse", lerr)
+
+
+def test_config2_full_forward(sa):
+    w = wl.config(2)
+    print(f"full-size case {w.name} T={w.T}", flush=True)
+    dev = wl.device_tensors(w, "cuda")
+    sk, lse = sa.sketch_fwd(dev["K"], dev["V"], dev["P"], dev["offsets"], w.scale)
+    torch.cuda.synchronize()
+    h = host_view(dev, ("K", "V", "P"))
+    ref_sk, ref_lse = oracle.fwd(h["K"], h["V"], h["P"], w.offsets, w.scale)
+    e = rel(sk.cpu().numpy(), ref_sk, (2, 3))
+    assert np.all(e <= TOL), e.max()
+    assert np.abs(lse.cpu().numpy() - ref_lse).max() <= LSE_TOL
+
+
+def test_config4_sampled_users_and_mass(sa):
+    w = wl.config(4)
+    print(f"full-size case {w.name} T={w.T}", flush=True)
+    dev = wl.device_tensors(w, "cuda")
+    sk, lse = sa.sketch_fwd(dev["K"], dev["V"], dev["P"], dev["offsets"], w.scale)
+    torch.cuda.synchronize()
+    off = w.offsets
+    # mass identity on every (user, head), from the device tensors in fp64
+    seg = torch.repeat_interleave(torch.arange(w.B, device="cuda"),
+                                  torch.from_numpy(w.lengths).to("cuda"))
+    vsum = torch.zeros((w.B, w.H, w.d), dtype=torch.float64, device="cuda")
+    vsum.index_add_(0, seg, dev["V"].double())
+    msum = sk.double().sum(dim=2)
+    e = ((msum - vsum).abs().amax(dim=2) / vsum.abs().amax(dim=2).clamp_min(1e-30)).cpu().numpy()
+    assert np.all(e <= TOL), ("mass", e.max())
+    # the first and the last user against the oracle, run on those two users alone
+    users = [0, w.B - 1]
+    parts = [host_view(dev, ("K", "V"), int(off[b]), int(off[b + 1])) for b in users]
+    sub = np.zeros(len(users) + 1, np.int64)
+    np.cumsum([off[b + 1] - off[b] for b in users], out=sub[1:])
+    ref_sk, ref_lse = oracle.fwd(np.concatenate([u["K"] for u in parts]),
+                                 np.concatenate([u["V"] for u in parts]),
+                                 dev["P"].float().cpu().numpy(), sub, w.scale)
+    check_users(w, off, users, sk.cpu().numpy(), lse.cpu().numpy(), ref_sk,
+                [ref_lse[sub[i]:sub[i + 1]] for i in range(len(users))])
+
+
+def test_config5_full_forward_and_backward(sa):
+    w = wl.config(5)
+    print(f"full-size case {w.name} T={w.T}", flush=True)
+    dev = wl.device_tensors(w, "cuda")
+    sk, lse = sa.sketch_fwd(dev["K"], dev["V"], dev["P"], dev["offsets"], w.scale)
+    dK, dV, dP = sa.sketch_bwd(dev["K"], dev["V"], dev["P"], dev["offsets"], dev["dsketch"], lse, w.scale)
+    torch.cuda.synchronize()
+    h = host_view(dev, ("K", "V", "P", "dsketch"))
+    off = w.offsets
+    ref_sk, ref_lse = oracle.fwd(h["K"], h["V"], h["P"], off, w.scale)
+    e = rel(sk.cpu().numpy(), ref_sk, (2, 3))
+    assert np.all(e <= TOL), ("sketch", e.max())
+    assert np.abs(lse.cpu().numpy() - ref_lse).max() <= LSE_TOL
+    del ref_sk, ref_lse
+    rK, rV, rP = oracle.bwd(h["K"], h["V"], h["P"], off, h["dsketch"], w.scale)
+    for name, g, r in (("dK", dK, rK), ("dV", dV, rV)):
+        g = g.cpu().numpy()
+        for b in range(w.B):
+            s, t = off[b], off[b + 1]
+            eb = rel(g[s:t], r[s:t], (0, 2))
+            assert np.all(eb <= TOL), (name, b, eb.max())
+    eP = rel(dP.cpu().numpy(), rP, (1, 2))
+    assert np.all(eP <= TOL), ("dP", eP.max())
