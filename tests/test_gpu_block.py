@@ -6,9 +6,14 @@ Output tolerance: normwise max relative error per (user, head) slice <= 2e-2
 (bf16) / 1e-4 (fp32), as for the other paths.  The first layer's lse keeps the
 sketching step's absolute bounds (1e-3 bf16, 1e-5 fp32).  Later layers' logits
 come from per-user queries computed from the refined state and rounded to
-bf16 once (P' = state W_Q W_K^T); their lse bound is 5e-3 in bf16 (about four
-times the first layer's, for logits of unit scale and a relative rounding of
-2^-9 in P') and 1e-4 in fp32.
+bf16 once (P' = state W_Q W_K^T, rows of unit-variance entries after the norm).
+A relative rounding of at most 2^-9 per entry of P' moves a logit
+scale * sum_j X_j P'_j by a sum of d independent terms, with standard deviation
+about 2^-9 / sqrt(3) * scale * sqrt(sum_j X_j^2 P'_j^2) ~ 1.1e-3 for unit-scale
+X and P'; the lse moves by a weighted mean of its logits' errors, so no more.
+The bound 1e-2 in bf16 is about nine of those standard deviations, which
+covers the largest of the ~10^6 token-head values of a full batch with the
+state's own error on top; 1e-4 in fp32.
 """
 import numpy as np
 import pytest
@@ -21,7 +26,7 @@ pytestmark = pytest.mark.gpu
 
 TOL = {"bf16": 2e-2, "fp32": 1e-4}
 LSE0 = {"bf16": 1e-3, "fp32": 1e-5}
-LSE1 = {"bf16": 5e-3, "fp32": 1e-4}
+LSE1 = {"bf16": 1e-2, "fp32": 1e-4}
 
 
 @pytest.fixture(scope="module")

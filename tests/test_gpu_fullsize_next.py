@@ -1,0 +1,164 @@
+"""GPU parity of the entry points beyond the sketching step at the sizes the
+benchmark times them, in its launch configuration (inputs from the device
+generator, same seeds and shapes as the benchmark):
+
+* token-wise forward, SA layer and stacked block (two layers): config 5's
+  ragged batch of 32 users (1K-100K tokens, H=4, d=128, M=512), X = the V
+  tensor;
+* STCA over the sketch: the batch's 32 users, R = 40 targets, k = 512 sketch
+  rows, D = 1024, h = 16.
+
+Every output of a user depends only on that user's inputs and the shared
+weights, so sampled users are checked against the oracles run on those users
+alone: their sketches, per-token lse and history gradients (dX, dXs, dq).  The
+weight and prototype gradients sum over every user and are left to the
+smaller all-output tests of each entry point.  Bounds as in those tests.
+"""
+import numpy as np
+import pytest
+
+import oracle
+from oracle import block as oblock
+from oracle import layer as olayer
+from oracle import stca as ostca
+from paper_2609_08443_amd import workloads as wl
+
+torch = pytest.importorskip("torch")
+pytestmark = pytest.mark.gpu
+
+TOL = 2e-2
+
+
+@pytest.fixture(scope="module")
+def sa():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from paper_2609_08443_amd import sa_sketch
+    sa_sketch.lib()
+    return sa_sketch
+
+
+@pytest.fixture(scope="module")
+def batch(sa):
+    w = wl.config(5)
+    return w, wl.device_tensors(w, "cuda")
+
+
+def rel(g, r, axes):
+    err = np.abs(g.astype(np.float64) - r).max(axis=axes)
+    return err / np.maximum(np.abs(r).max(axis=axes), 1e-30)
+
+
+def np32(t):
+    return t.float().cpu().numpy()
+
+
+def sub_batch(w, users, *tensors):
+    """The listed users' token rows of each [T, ...] device tensor, packed, with their offsets."""
+    off = w.offsets
+    sub = np.zeros(len(users) + 1, np.int64)
+    np.cumsum([off[b + 1] - off[b] for b in users], out=sub[1:])
+    packed = [np.concatenate([np32(t[off[b]:off[b + 1]]) for b in users]) for t in tensors]
+    return sub, packed
+
+
+def token_rows(w, users, x):
+    off = w.offsets
+    return np.concatenate([x[off[b]:off[b + 1]] for b in users])
+
+
+def shortest_and_median(w):
+    order = np.argsort(w.lengths, kind="stable")
+    return [int(order[0]), int(order[len(order) // 2])]
+
+
+def test_tokenwise_at_bench_size(sa, batch):
+    w, dev = batch
+    print(f"full-size tokenwise T={w.T}", flush=True)
+    sk, lse = sa.sketch_fwd_tokenwise(dev["K"], dev["V"], dev["P"], dev["offsets"], w.scale)
+    torch.cuda.synchronize()
+    # the shortest and the longest user (the longest is cut over many ranges)
+    users = [int(np.argmin(w.lengths)), int(np.argmax(w.lengths))]
+    sub, (K, V) = sub_batch(w, users, dev["K"], dev["V"])
+    rs, rl = oracle.fwd_tokenwise(K, V, np32(dev["P"]), sub, w.scale)
+    g, gl = sk.cpu().numpy(), lse.cpu().numpy()
+    for i, b in enumerate(users):
+        e = rel(g[b], rs[i], (1, 2))
+        assert np.all(e <= TOL), ("sketch", b, e.max())
+        assert np.abs(gl[b] - rl[i]).max() <= 1e-3, ("lse_m", b)
+
+
+def test_layer_at_bench_size(sa, batch):
+    w, dev = batch
+    print(f"full-size layer T={w.T}", flush=True)
+    proj = wl.device_projections(w, "cuda")
+    X = dev["V"]
+    sk, lse = sa.layer_fwd(X, dev["P"], proj["Wq"], proj["Wk"], dev["offsets"], w.scale)
+    dX, _, _, _ = sa.layer_bwd(X, dev["P"], proj["Wq"], proj["Wk"], dev["offsets"], dev["dsketch"], lse, w.scale)
+    torch.cuda.synchronize()
+    users = shortest_and_median(w)
+    sub, (Xs,) = sub_batch(w, users, X)
+    args = (Xs, np32(dev["P"]), np32(proj["Wq"]), np32(proj["Wk"]), sub)
+    rs, rl = olayer.layer_fwd(*args, scale=w.scale)
+    rX = olayer.layer_bwd(*args, np32(dev["dsketch"][users]), scale=w.scale)[0]
+    g = sk.cpu().numpy()
+    for i, b in enumerate(users):
+        e = rel(g[b], rs[i], (1, 2))
+        assert np.all(e <= TOL), ("sketch", b, e.max())
+    assert np.abs(token_rows(w, users, lse.cpu().numpy()) - rl).max() <= 1e-3
+    gX = token_rows(w, users, dX.cpu().numpy())
+    for i in range(len(users)):
+        e = rel(gX[sub[i]:sub[i + 1]], rX[sub[i]:sub[i + 1]], (0, 2))
+        assert np.all(e <= TOL), ("dX", users[i], e.max())
+
+
+def test_block_at_bench_size(sa, batch):
+    w, dev = batch
+    n_layers = 2
+    print(f"full-size block T={w.T} layers={n_layers}", flush=True)
+    bp = wl.device_block_params(w, n_layers, "cuda")
+    names = ("Wq", "Wk", "ln", "W1", "W3", "W2")
+    X = dev["V"]
+    dout = dev["dsketch"][:, 0].contiguous()
+    out, lse = sa.block_fwd(X, dev["P"], *[bp[n] for n in names], dev["offsets"], w.scale, want_lse=True)
+    g = sa.block_bwd(X, dev["P"], *[bp[n] for n in names], dev["offsets"], dout, w.scale)
+    torch.cuda.synchronize()
+    users = shortest_and_median(w)
+    sub, (Xs,) = sub_batch(w, users, X)
+    args = (Xs, np32(dev["P"]), *[np32(bp[n]) for n in names], sub)
+    ro, rl = oblock.block_fwd(*args, scale=w.scale)
+    rX = oblock.block_bwd(*args, np32(dout[users]), scale=w.scale)["dX"]
+    go = out.cpu().numpy()
+    for i, b in enumerate(users):
+        e = rel(go[b], ro[i], (1, 2))
+        assert np.all(e <= TOL), ("out", b, e.max())
+    gl = lse.cpu().numpy()
+    for l in range(n_layers):
+        # later layers' logits come from bf16-rounded per-user queries (bound derived in test_gpu_block)
+        bound = 1e-3 if l == 0 else 1e-2
+        assert np.abs(token_rows(w, users, gl[l]) - rl[l]).max() <= bound, ("lse", l)
+    gX = token_rows(w, users, g["dX"].cpu().numpy())
+    for i in range(len(users)):
+        e = rel(gX[sub[i]:sub[i + 1]], rX[sub[i]:sub[i + 1]], (0, 2))
+        assert np.all(e <= TOL), ("dX", users[i], e.max())
+
+
+def test_stca_at_bench_size(sa, batch):
+    w, _ = batch
+    B, R, k, D, h = w.B, 40, w.M, 1024, 16
+    print(f"full-size stca B={B} R={R} k={k} D={D} h={h}", flush=True)
+    st = wl.device_stca(w.seed, B, R, k, D, "bf16")
+    args = [st[n] for n in ("Xs", "q", "Wq", "Wk", "Wv")]
+    out, lse = sa.stca_fwd(*args, h=h, want_lse=True)
+    g = sa.stca_bwd(*args, h=h, dout=st["dout"])
+    torch.cuda.synchronize()
+    users = [0, B - 1]
+    hargs = [np32(st["Xs"][users]), np32(st["q"][users])] + [np32(st[n]) for n in ("Wq", "Wk", "Wv")]
+    ro, rl = ostca.stca_fwd(*hargs, h=h)
+    ref = ostca.stca_bwd(*hargs, h=h, dout=np32(st["dout"][users]))
+    go, gl = out.cpu().numpy()[users], lse.cpu().numpy()[users]
+    assert np.all(rel(go, ro, (2,)) <= TOL), "out"
+    s_max = np.abs(rl).max() + np.log(k)
+    assert np.abs(gl - rl).max() <= 2.0 ** -7 * max(1.0, s_max), "lse"
+    assert np.all(rel(g["dXs"].cpu().numpy()[users], ref["dXs"], (1, 2)) <= TOL), "dXs"
+    assert np.all(rel(g["dq"].cpu().numpy()[users], ref["dq"], (2,)) <= TOL), "dq"
