@@ -439,6 +439,21 @@ sa_status run_fwd(const void* K, const void* V, const void* P, const int64_t* of
                   float* sketch, float* lse, uint8_t* ws, const FwdPlan& plan, hipStream_t stream,
                   bool p_user);
 
+// Batched product of the backward, C[z] (=, or += with accumulate) A[z] B[z'] with
+// z' = z % b_mod when b_mod > 0 (per-head weights shared by the users), in the
+// layout of launch_small_gemm (C dense [batch][M][N] fp32).  In bf16 mode its fp32
+// operands are rounded to bf16 and it runs on the matrix cores when the shapes
+// allow; otherwise (and always in fp32 mode) on the fp32 product.
+hipError_t grad_gemm(bool bf16_mode, const sa::MatView& a, const sa::MatView& b, float* c, int32_t batch,
+                     int32_t M, int32_t N, int32_t K, hipStream_t stream, int32_t b_mod = 0,
+                     bool accumulate = false) {
+    sa::GemmDesc g{a.p, a.bf16, a.s_h, a.s_0, a.s_1, b.p, b.bf16, b.s_h, b.s_0, b.s_1, c, false,
+                   (int64_t)M * N, N, M, N, K, batch, 1.0f, accumulate};
+    g.b_mod = b_mod > 0 ? b_mod : 0;
+    g.round_bf16 = bf16_mode;
+    return sa::launch_gemm(g, stream);
+}
+
 // Layer l's intermediates inside a saved region (layout s, L layers); its state
 // output is the next layer's state, or `last` for the last layer.  Xhat and Z
 // are scratch the caller sets.
@@ -999,6 +1014,8 @@ sa_status sa_layer_bwd(const void* X, const void* P, const void* Wq, const void*
     const bool bf = dtype == SA_BF16;
     const int64_t md = (int64_t)M * d, dd = (int64_t)d * d;
     sa::ProfScope ps("layer_proj_grads", stream);
+    // (fp32 products: with identity projections dP equals the sketching step's dP
+    // bit for bit)
     hipError_t e = sa::launch_small_gemm({dPp, false, md, 1, d}, {Q, false, md, d, 1}, dWk, false, H, d,
                                          d, M, stream);
     if (e == hipSuccess)
@@ -1175,33 +1192,33 @@ sa_status sa_block_bwd(const void* X, const void* P, const void* Wq, const void*
             // dW2 = sum over users of Z^T dY2, dZ = dY2 W2^T
             if (e == hipSuccess) e = sa::launch_swiglu_fwd(io.G, io.U, Zb, rows * d2, stream);
             if (e == hipSuccess)
-                e = sa::launch_small_gemm({Zb, false, M * d2, 1, d2}, {dY2, false, md, d, 1}, wpart, false,
-                                          (int32_t)BH, (int32_t)d2, d, M, stream);
+                e = grad_gemm(bf, {Zb, false, M * d2, 1, d2}, {dY2, false, md, d, 1}, wpart,
+                              (int32_t)BH, (int32_t)d2, d, M, stream);
             if (e == hipSuccess)
                 e = sa::launch_sum_users(wpart, B, H, d2 * d, dW2 + (size_t)l * H * d2 * d, stream);
             if (e == hipSuccess)
-                e = sa::launch_small_gemm({dY2, false, md, d, 1}, {w.w2(l), bf, d2 * d, 1, d}, Zb, false,
-                                          (int32_t)BH, M, (int32_t)d2, d, stream, H);
+                e = grad_gemm(bf, {dY2, false, md, d, 1}, {w.w2(l), bf, d2 * d, 1, d}, Zb,
+                              (int32_t)BH, M, (int32_t)d2, d, stream, H);
             // through the gate: dG (over dZ), dU
             if (e == hipSuccess) e = sa::launch_swiglu_bwd(Zb, io.G, io.U, dU, rows * d2, stream);
             // dW1 = sum Xbar^T dG, dW3 = sum Xbar^T dU
             if (e == hipSuccess)
-                e = sa::launch_small_gemm({io.Xbar, false, md, 1, d}, {Zb, false, M * d2, d2, 1}, wpart, false,
-                                          (int32_t)BH, d, (int32_t)d2, M, stream);
+                e = grad_gemm(bf, {io.Xbar, false, md, 1, d}, {Zb, false, M * d2, d2, 1}, wpart,
+                              (int32_t)BH, d, (int32_t)d2, M, stream);
             if (e == hipSuccess)
                 e = sa::launch_sum_users(wpart, B, H, d * d2, dW1 + (size_t)l * H * d * d2, stream);
             if (e == hipSuccess)
-                e = sa::launch_small_gemm({io.Xbar, false, md, 1, d}, {dU, false, M * d2, d2, 1}, wpart, false,
-                                          (int32_t)BH, d, (int32_t)d2, M, stream);
+                e = grad_gemm(bf, {io.Xbar, false, md, 1, d}, {dU, false, M * d2, d2, 1}, wpart,
+                              (int32_t)BH, d, (int32_t)d2, M, stream);
             if (e == hipSuccess)
                 e = sa::launch_sum_users(wpart, B, H, d * d2, dW3 + (size_t)l * H * d * d2, stream);
             // dXbar = dY2 + dG W1^T + dU W3^T (dY2 enters through the norm's second input)
             if (e == hipSuccess)
-                e = sa::launch_small_gemm({Zb, false, M * d2, d2, 1}, {w.w1(l), bf, d * d2, 1, d2}, dXbar, false,
-                                          (int32_t)BH, M, d, (int32_t)d2, stream, H);
+                e = grad_gemm(bf, {Zb, false, M * d2, d2, 1}, {w.w1(l), bf, d * d2, 1, d2}, dXbar,
+                              (int32_t)BH, M, d, (int32_t)d2, stream, H);
             if (e == hipSuccess)
-                e = sa::launch_small_gemm({dU, false, M * d2, d2, 1}, {w.w3(l), bf, d * d2, 1, d2}, dXbar, false,
-                                          (int32_t)BH, M, d, (int32_t)d2, stream, H, true);
+                e = grad_gemm(bf, {dU, false, M * d2, d2, 1}, {w.w3(l), bf, d * d2, 1, d2}, dXbar,
+                              (int32_t)BH, M, d, (int32_t)d2, stream, H, true);
             // LN1: dY1 = gradient of Xt + Xhat
             if (e == hipSuccess)
                 e = sa::launch_ln_bwd(dXbar, dY2, io.Y1, w.ln_(l, 0), bf, B, H, M, d, eps, dY1, stats, colpart,
@@ -1226,26 +1243,26 @@ sa_status sa_block_bwd(const void* X, const void* P, const void* Wq, const void*
         // and the state gradient dXt = dY1 + dQ W_Q^T
         float* dwk = dWk + (size_t)l * H * dd;
         float* dwq = dWq + (size_t)l * H * dd;
-        e = sa::launch_small_gemm({dPp, false, md, 1, d}, {io.Q, false, md, d, 1}, io.first ? dwk : wpart, false,
-                                  (int32_t)nq, d, d, M, stream);
+        e = grad_gemm(bf, {dPp, false, md, 1, d}, {io.Q, false, md, d, 1}, io.first ? dwk : wpart,
+                      (int32_t)nq, d, d, M, stream);
         if (e == hipSuccess && !io.first) e = sa::launch_sum_users(wpart, B, H, dd, dwk, stream);
         if (e == hipSuccess)
-            e = sa::launch_small_gemm({dPp, false, md, d, 1}, {w.wk(l), bf, dd, d, 1}, dQ, false, (int32_t)nq, M, d,
-                                      d, stream, H);
+            e = grad_gemm(bf, {dPp, false, md, d, 1}, {w.wk(l), bf, dd, d, 1}, dQ, (int32_t)nq, M, d,
+                          d, stream, H);
         if (e == hipSuccess)
-            e = sa::launch_small_gemm({io.xt, io.first && bf, md, 1, d}, {dQ, false, md, d, 1},
-                                      io.first ? dwq : wpart, false, (int32_t)nq, d, d, M, stream);
+            e = grad_gemm(bf, {io.xt, io.first && bf, md, 1, d}, {dQ, false, md, d, 1}, io.first ? dwq : wpart,
+                          (int32_t)nq, d, d, M, stream);
         if (e == hipSuccess && !io.first) e = sa::launch_sum_users(wpart, B, H, dd, dwq, stream);
         if (e == hipSuccess) {
             if (io.first) {
                 // the shared prototypes: dP = sum over users of dY1, plus dQ W_Q^T
                 e = sa::launch_sum_users(dY1, B, H, md, dP, stream);
                 if (e == hipSuccess)
-                    e = sa::launch_small_gemm({dQ, false, md, d, 1}, {w.wq(l), bf, dd, 1, d}, dP, false, H, M, d, d,
-                                              stream, H, true);
+                    e = grad_gemm(bf, {dQ, false, md, d, 1}, {w.wq(l), bf, dd, 1, d}, dP, H, M, d, d,
+                                  stream, H, true);
             } else {
-                e = sa::launch_small_gemm({dQ, false, md, d, 1}, {w.wq(l), bf, dd, 1, d}, dY1, false, (int32_t)BH,
-                                          M, d, d, stream, H, true);
+                e = grad_gemm(bf, {dQ, false, md, d, 1}, {w.wq(l), bf, dd, 1, d}, dY1, (int32_t)BH,
+                              M, d, d, stream, H, true);
             }
         }
         if (e != hipSuccess) return hip_fail(e, "block projection gradient launch");

@@ -16,9 +16,11 @@
 // as 4 k rows x 8 columns per thread, transposed in registers into 8 column
 // pieces of 4 k values (written so that each store instruction meets every
 // LDS bank twice, its minimum).  Tiles of one batch run on one XCD so that its operands share that
-// L2.  Products whose shapes or strides do not fit (k not a multiple of 64,
-// unaligned strides, fp32 operands) run on the register-tiled fp32 product of
-// layer.hip.
+// L2.  An fp32 operand (allowed when the caller accepts bf16 rounding of its
+// inputs) is loaded as the same pieces of fp32 values and rounded to bf16 when
+// its slab is staged.  Products whose shapes or strides do not fit (k not a
+// multiple of 64, unaligned strides, fp32 operands without that permission) run
+// on the register-tiled fp32 product of layer.hip.
 #include "sa_internal.h"
 #include "tile_ops.h"
 
@@ -31,10 +33,10 @@ using namespace tile;
 constexpr int GBM = 128, GBN = 128, GBK = 64;
 
 struct MgArgs {
-    const uint16_t* A;
+    const void* A;
     int64_t a_z, a_m, a_k;
-    const uint16_t* B;
-    int64_t b_z, b_k, b_n;
+    const void* B;
+    int64_t b_z, b_k, b_n, b_mod;
     void* C;
     int64_t c_z, c_m;
     int32_t M, N, K, tm, tn;
@@ -42,11 +44,26 @@ struct MgArgs {
     int32_t accumulate;
 };
 
-// One thread's share of a [128 rows][64 k] slab: four 16-byte pieces, named so
-// that they stay in registers.
+// One thread's share of a [128 rows][64 k] slab: four 16-byte pieces of 8 bf16,
+// named so that they stay in registers.
 struct Slab {
     uint4 p0, p1, p2, p3;
 };
+// The same share of an fp32 operand: each piece as two 16-byte halves.
+struct Slab32 {
+    uint4 p0a, p0b, p1a, p1b, p2a, p2b, p3a, p3b;
+};
+
+__device__ inline uint4 round8(const uint4& a, const uint4& b) {
+    return make_uint4(pack_bf16x2(__uint_as_float(a.x), __uint_as_float(a.y)),
+                      pack_bf16x2(__uint_as_float(a.z), __uint_as_float(a.w)),
+                      pack_bf16x2(__uint_as_float(b.x), __uint_as_float(b.y)),
+                      pack_bf16x2(__uint_as_float(b.z), __uint_as_float(b.w)));
+}
+__device__ inline Slab cook(const Slab& s) { return s; }
+__device__ inline Slab cook(const Slab32& s) {
+    return Slab{round8(s.p0a, s.p0b), round8(s.p1a, s.p1b), round8(s.p2a, s.p2b), round8(s.p3a, s.p3b)};
+}
 
 // Per-thread sources of the four pieces of an operand's slabs: element (row, k)
 // sits at base[row s_row + k s_k].  KC: s_k = 1 (rows are k runs), piece i is
@@ -54,17 +71,18 @@ struct Slab {
 // nrows - 1.  Otherwise s_row = 1: piece i is k row 4 (tid % 16) + i, columns
 // 8 (tid / 16) .. + 7 (nrows is a multiple of 8; columns past it read zeros).
 // Slab kt is the pieces at offset kt * step.
+template <typename T>
 struct Src {
-    const uint16_t *p0, *p1, *p2, *p3;
+    const T *p0, *p1, *p2, *p3;
     int64_t step;
     bool ok;
 };
 
-template <bool KC>
-__device__ inline Src make_src(const uint16_t* base, int64_t s_row, int64_t s_k, int row0, int nrows, int tid) {
-    Src s;
+template <bool KC, typename T>
+__device__ inline Src<T> make_src(const T* base, int64_t s_row, int64_t s_k, int row0, int nrows, int tid) {
+    Src<T> s;
     if constexpr (KC) {
-        const uint16_t* b = base + 8 * (tid & 7);
+        const T* b = base + 8 * (tid & 7);
         auto at = [&](int i) {
             const int row = row0 + ((tid + 256 * i) >> 3);
             return b + (int64_t)(row < nrows ? row : nrows - 1) * s_row;
@@ -87,7 +105,7 @@ __device__ inline Src make_src(const uint16_t* base, int64_t s_row, int64_t s_k,
     return s;
 }
 
-__device__ inline Slab load_slab(const Src& s, int kt) {
+__device__ inline Slab load_slab(const Src<uint16_t>& s, int kt) {
     const int64_t o = kt * s.step;
     Slab r;
     if (s.ok) {
@@ -97,6 +115,23 @@ __device__ inline Slab load_slab(const Src& s, int kt) {
         r.p3 = *reinterpret_cast<const uint4*>(s.p3 + o);
     } else {
         r.p0 = r.p1 = r.p2 = r.p3 = make_uint4(0, 0, 0, 0);
+    }
+    return r;
+}
+__device__ inline Slab32 load_slab(const Src<float>& s, int kt) {
+    const int64_t o = kt * s.step;
+    Slab32 r;
+    if (s.ok) {
+        r.p0a = *reinterpret_cast<const uint4*>(s.p0 + o);
+        r.p0b = *reinterpret_cast<const uint4*>(s.p0 + o + 4);
+        r.p1a = *reinterpret_cast<const uint4*>(s.p1 + o);
+        r.p1b = *reinterpret_cast<const uint4*>(s.p1 + o + 4);
+        r.p2a = *reinterpret_cast<const uint4*>(s.p2 + o);
+        r.p2b = *reinterpret_cast<const uint4*>(s.p2 + o + 4);
+        r.p3a = *reinterpret_cast<const uint4*>(s.p3 + o);
+        r.p3b = *reinterpret_cast<const uint4*>(s.p3 + o + 4);
+    } else {
+        r.p0a = r.p0b = r.p1a = r.p1b = r.p2a = r.p2b = r.p3a = r.p3b = make_uint4(0, 0, 0, 0);
     }
     return r;
 }
@@ -132,7 +167,7 @@ __device__ inline void store_slab(uint16_t* lds, const Slab& s, int tid) {
     }
 }
 
-template <bool A_KC, bool B_KC, bool C_BF16>
+template <bool A_KC, bool B_KC, bool C_BF16, typename TA, typename TB>
 __global__ __launch_bounds__(256, 2) void mfma_gemm_kernel(MgArgs g) {
     __shared__ __attribute__((aligned(16))) uint16_t As[2][GBM * GBK];
     __shared__ __attribute__((aligned(16))) uint16_t Bs[2][GBN * GBK];
@@ -142,11 +177,11 @@ __global__ __launch_bounds__(256, 2) void mfma_gemm_kernel(MgArgs g) {
     const int64_t z = id / tiles;
     const int tt = (int)(id % tiles);
     const int m0 = (tt / g.tn) * GBM, n0 = (tt % g.tn) * GBN;
-    const uint16_t* Ab = g.A + z * g.a_z;
-    const uint16_t* Bb = g.B + z * g.b_z;
+    const TA* Ab = reinterpret_cast<const TA*>(g.A) + z * g.a_z;
+    const TB* Bb = reinterpret_cast<const TB*>(g.B) + (g.b_mod > 0 ? z % g.b_mod : z) * g.b_z;
     const int nk = g.K / GBK;
-    const Src sa_ = make_src<A_KC>(Ab, g.a_m, g.a_k, m0, g.M, tid);
-    const Src sb_ = make_src<B_KC>(Bb, g.b_n, g.b_k, n0, g.N, tid);
+    const Src<TA> sa_ = make_src<A_KC>(Ab, g.a_m, g.a_k, m0, g.M, tid);
+    const Src<TB> sb_ = make_src<B_KC>(Bb, g.b_n, g.b_k, n0, g.N, tid);
     auto lda = [&](int kt) { return load_slab(sa_, kt); };
     auto ldb = [&](int kt) { return load_slab(sb_, kt); };
 
@@ -177,9 +212,10 @@ __global__ __launch_bounds__(256, 2) void mfma_gemm_kernel(MgArgs g) {
     // kt % 2 and slab kt + 2 is loaded: a load has two slabs of products to land.
     // The buffer a slab is stored into was last read before the previous barrier;
     // the barriers wait for LDS traffic only, so the loads stay in flight.
-    Slab an = lda(0), bn = ldb(0);
-    store_slab<A_KC>(As[0], an, tid);
-    store_slab<B_KC>(Bs[0], bn, tid);
+    auto an = lda(0);
+    auto bn = ldb(0);
+    store_slab<A_KC>(As[0], cook(an), tid);
+    store_slab<B_KC>(Bs[0], cook(bn), tid);
     if (nk > 1) {
         an = lda(1);
         bn = ldb(1);
@@ -187,15 +223,16 @@ __global__ __launch_bounds__(256, 2) void mfma_gemm_kernel(MgArgs g) {
     lds_barrier();
 #pragma unroll 2
     for (int kt = 0; kt < nk; ++kt) {
-        Slab af, bf;
+        decltype(an) af;
+        decltype(bn) bf;
         if (kt + 2 < nk) {
             af = lda(kt + 2);
             bf = ldb(kt + 2);
         }
         mul(kt & 1);
         if (kt + 1 < nk) {
-            store_slab<A_KC>(As[(kt + 1) & 1], an, tid);
-            store_slab<B_KC>(Bs[(kt + 1) & 1], bn, tid);
+            store_slab<A_KC>(As[(kt + 1) & 1], cook(an), tid);
+            store_slab<B_KC>(Bs[(kt + 1) & 1], cook(bn), tid);
         }
         lds_barrier();
         an = af;
@@ -228,14 +265,24 @@ __global__ __launch_bounds__(256, 2) void mfma_gemm_kernel(MgArgs g) {
         }
 }
 
-template <bool A_KC, bool B_KC>
-hipError_t mgemm_launch(const MgArgs& g, bool c_bf16, int64_t batch, hipStream_t stream) {
+template <bool A_KC, bool B_KC, typename TA, typename TB>
+hipError_t mgemm_launch_t(const MgArgs& g, bool c_bf16, int64_t batch, hipStream_t stream) {
     const int64_t blocks = (int64_t)g.tm * g.tn * batch;
     if (c_bf16)
-        hipLaunchKernelGGL((mfma_gemm_kernel<A_KC, B_KC, true>), dim3((unsigned)blocks), dim3(256), 0, stream, g);
+        hipLaunchKernelGGL((mfma_gemm_kernel<A_KC, B_KC, true, TA, TB>), dim3((unsigned)blocks), dim3(256), 0, stream,
+                           g);
     else
-        hipLaunchKernelGGL((mfma_gemm_kernel<A_KC, B_KC, false>), dim3((unsigned)blocks), dim3(256), 0, stream, g);
+        hipLaunchKernelGGL((mfma_gemm_kernel<A_KC, B_KC, false, TA, TB>), dim3((unsigned)blocks), dim3(256), 0,
+                           stream, g);
     return hipGetLastError();
+}
+
+template <bool A_KC, bool B_KC>
+hipError_t mgemm_launch(const MgArgs& g, bool a_bf16, bool b_bf16, bool c_bf16, int64_t batch, hipStream_t stream) {
+    if (a_bf16 && b_bf16) return mgemm_launch_t<A_KC, B_KC, uint16_t, uint16_t>(g, c_bf16, batch, stream);
+    if (a_bf16) return mgemm_launch_t<A_KC, B_KC, uint16_t, float>(g, c_bf16, batch, stream);
+    if (b_bf16) return mgemm_launch_t<A_KC, B_KC, float, uint16_t>(g, c_bf16, batch, stream);
+    return mgemm_launch_t<A_KC, B_KC, float, float>(g, c_bf16, batch, stream);
 }
 
 bool al8(int64_t v) { return v % 8 == 0; }
@@ -244,7 +291,8 @@ bool al16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15) == 0; }
 }  // namespace
 
 bool gemm_on_matrix_cores(const GemmDesc& d) {
-    if (!d.a_bf16 || !d.b_bf16 || d.K <= 0 || d.K % GBK != 0 || d.M <= 0 || d.N <= 0) return false;
+    if (!(d.a_bf16 || d.round_bf16) || !(d.b_bf16 || d.round_bf16)) return false;
+    if (d.K <= 0 || d.K % GBK != 0 || d.M <= 0 || d.N <= 0 || d.b_mod < 0) return false;
     const bool a_kc = d.a_k == 1, b_kc = d.b_k == 1;
     if (!a_kc && d.a_m != 1) return false;
     if (!b_kc && d.b_n != 1) return false;
@@ -261,10 +309,10 @@ hipError_t launch_gemm(const GemmDesc& d, hipStream_t stream) {
     if (d.batch <= 0 || d.M <= 0 || d.N <= 0) return hipSuccess;
     if (!gemm_on_matrix_cores(d)) return launch_small_gemm_general(d, stream);
     MgArgs g;
-    g.A = reinterpret_cast<const uint16_t*>(d.A);
+    g.A = d.A;
     g.a_z = d.a_z; g.a_m = d.a_m; g.a_k = d.a_k;
-    g.B = reinterpret_cast<const uint16_t*>(d.B);
-    g.b_z = d.b_z; g.b_k = d.b_k; g.b_n = d.b_n;
+    g.B = d.B;
+    g.b_z = d.b_z; g.b_k = d.b_k; g.b_n = d.b_n; g.b_mod = d.b_mod;
     g.C = d.C;
     g.c_z = d.c_z; g.c_m = d.c_m;
     g.M = d.M; g.N = d.N; g.K = d.K;
@@ -273,10 +321,10 @@ hipError_t launch_gemm(const GemmDesc& d, hipStream_t stream) {
     g.alpha = d.alpha;
     g.accumulate = d.accumulate ? 1 : 0;
     const bool a_kc = d.a_k == 1, b_kc = d.b_k == 1;
-    if (a_kc && b_kc) return mgemm_launch<true, true>(g, d.c_bf16, d.batch, stream);
-    if (a_kc) return mgemm_launch<true, false>(g, d.c_bf16, d.batch, stream);
-    if (b_kc) return mgemm_launch<false, true>(g, d.c_bf16, d.batch, stream);
-    return mgemm_launch<false, false>(g, d.c_bf16, d.batch, stream);
+    if (a_kc && b_kc) return mgemm_launch<true, true>(g, d.a_bf16, d.b_bf16, d.c_bf16, d.batch, stream);
+    if (a_kc) return mgemm_launch<true, false>(g, d.a_bf16, d.b_bf16, d.c_bf16, d.batch, stream);
+    if (b_kc) return mgemm_launch<false, true>(g, d.a_bf16, d.b_bf16, d.c_bf16, d.batch, stream);
+    return mgemm_launch<false, false>(g, d.a_bf16, d.b_bf16, d.c_bf16, d.batch, stream);
 }
 
 }  // namespace sa

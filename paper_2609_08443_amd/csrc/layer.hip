@@ -169,8 +169,8 @@ hipError_t launch_small_gemm(const MatView& a, const MatView& b, void* c, bool c
 
 hipError_t launch_small_gemm_general(const GemmDesc& d, hipStream_t stream) {
     return small_gemm_dispatch({d.A, d.a_bf16, d.a_z, d.a_m, d.a_k}, {d.B, d.b_bf16, d.b_z, d.b_k, d.b_n}, d.C,
-                               d.c_bf16, d.c_z, d.c_m, d.batch, d.M, d.N, d.K, d.batch, d.alpha, d.accumulate,
-                               stream);
+                               d.c_bf16, d.c_z, d.c_m, d.batch, d.M, d.N, d.K, d.b_mod > 0 ? (int32_t)d.b_mod : d.batch,
+                               d.alpha, d.accumulate, stream);
 }
 
 hipError_t launch_add(const float* a, const float* b, float* out, int64_t n, hipStream_t stream) {

@@ -161,6 +161,8 @@ struct GemmDesc {
     int32_t M, N, K, batch;
     float alpha;
     bool accumulate;
+    int64_t b_mod = 0;        // > 0: B's batch index is z % b_mod (weights shared across users)
+    bool round_bf16 = false;  // fp32 operands may be rounded to bf16 (matrix cores)
 };
 bool gemm_on_matrix_cores(const GemmDesc& d);
 hipError_t launch_gemm(const GemmDesc& d, hipStream_t stream);
