@@ -148,41 +148,71 @@ __global__ __launch_bounds__(256) void ln_bwd_kernel(const float* __restrict__ d
 
 // Column sums for gamma / beta of one layer norm: part[c][h][0][j] = sum over the
 // chunk c of head h's rows of (dy1 + dy2) * xh, part[c][h][1][j] of (dy1 + dy2).
-// Rows of head h: (b * H + h) * M + m; a chunk covers CH consecutive (b, m).
+// Rows of head h: (b * H + h) * M + m; a chunk covers CH consecutive (b, m).  The
+// 256 / D thread groups of a workgroup take every (256 / D)-th row of the chunk
+// in order, and their sums are added in group order (deterministic).
 template <int D>
 __global__ __launch_bounds__(256) void ln_colsum_kernel(const float* __restrict__ dy1, const float* __restrict__ dy2,
                                                         const float* __restrict__ y, const float2* __restrict__ stats,
                                                         int64_t B, int32_t H, int32_t M, int64_t CH,
                                                         float* __restrict__ part) {
-    const int j = blockIdx.y * 256 + threadIdx.x;
-    if (j >= D) return;
+    constexpr int G = 256 / D;
+    __shared__ float red[2][G][D];
+    const int j = threadIdx.x % D, g = threadIdx.x / D;
     const int64_t h = blockIdx.z, c = blockIdx.x;
-    const int64_t n = B * M;
+    const int64_t n = B * M;   // < 2^31 (checked by the host)
     const int64_t i0 = c * CH, i1 = i0 + CH < n ? i0 + CH : n;
     float sx = 0.f, s1 = 0.f;
-    for (int64_t i = i0; i < i1; ++i) {
-        const int64_t r = (i / M * H + h) * M + i % M;
+#pragma unroll 4
+    for (int64_t i = i0 + g; i < i1; i += G) {
+        const uint32_t b = (uint32_t)i / (uint32_t)M, m = (uint32_t)i - b * (uint32_t)M;
+        const int64_t r = ((int64_t)b * H + h) * M + m;
         float d = dy1[r * D + j];
         if (dy2) d += dy2[r * D + j];
         const float2 st = stats[r];
         sx = __builtin_fmaf(d, (y[r * D + j] - st.x) * st.y, sx);
         s1 += d;
     }
-    float* o = part + ((c * H + h) * 2) * D;
-    o[j] = sx;
-    o[D + j] = s1;
+    red[0][g][j] = sx;
+    red[1][g][j] = s1;
+    __syncthreads();
+    if (g == 0) {
+#pragma unroll
+        for (int q = 1; q < G; ++q) {
+            sx += red[0][q][j];
+            s1 += red[1][q][j];
+        }
+        float* o = part + ((c * H + h) * 2) * D;
+        o[j] = sx;
+        o[D + j] = s1;
+    }
 }
 
-// out[h][k][j] = sum over chunks, in order, of part[c][h][k][j]; out has a
-// stride of ostride floats between k = 0 (gamma) and k = 1 (beta)
+// out[h][k][j] = sum over chunks c of part[c][h][k][j]; out has a stride of
+// ostride floats between k = 0 (gamma) and k = 1 (beta).  A workgroup takes 32
+// columns of [h][k][j]; its eight thread groups each sum the chunks g, g + 8, ...
+// in order, and the eight group sums are added in group order (a fixed order,
+// so the result is deterministic).
 __global__ __launch_bounds__(256) void ln_chunk_sum_kernel(const float* __restrict__ part, int64_t nch, int32_t H,
                                                            int32_t D, float* __restrict__ out, int64_t ostride) {
-    const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
-    if (i >= (int64_t)H * 2 * D) return;
-    const int64_t h = i / (2 * D), k = (i / D) % 2, j = i % D;
+    __shared__ float red[8][32];
+    const int64_t m = (int64_t)H * 2 * D;
+    const int g = threadIdx.x >> 5, col = threadIdx.x & 31;
+    const int64_t i = (int64_t)blockIdx.x * 32 + col;
     float s = 0.f;
-    for (int64_t c = 0; c < nch; ++c) s += part[((c * H + h) * 2 + k) * D + j];
-    out[k * ostride + h * D + j] = s;
+    if (i < m) {
+#pragma unroll 8
+        for (int64_t c = g; c < nch; c += 8) s += part[c * m + i];
+    }
+    red[g][col] = s;
+    __syncthreads();
+    if (g == 0 && i < m) {
+        float t = red[0][col];
+#pragma unroll
+        for (int q = 1; q < 8; ++q) t += red[q][col];
+        const int64_t h = i / (2 * D), k = (i / D) % 2, j = i % D;
+        out[k * ostride + h * D + j] = t;
+    }
 }
 
 __global__ __launch_bounds__(256) void fill_kernel(float* __restrict__ p, int64_t n, float v) {
@@ -269,7 +299,7 @@ hipError_t launch_ln_bwd(const float* dy1, const float* dy2, const float* y, con
     e = hipGetLastError();
     if (e != hipSuccess) return e;
     const int64_t m = (int64_t)H * 2 * d;
-    hipLaunchKernelGGL(ln_chunk_sum_kernel, dim3((unsigned)((m + 255) / 256)), dim3(256), 0, stream, colpart, nch, H,
+    hipLaunchKernelGGL(ln_chunk_sum_kernel, dim3((unsigned)((m + 31) / 32)), dim3(256), 0, stream, colpart, nch, H,
                        d, dgamma_dbeta, ostride);
     return hipGetLastError();
 }
