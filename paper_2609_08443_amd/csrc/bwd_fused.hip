@@ -734,6 +734,7 @@ __global__ __launch_bounds__(256) void dp_sum_kernel(const int32_t* __restrict__
     s0 = s0 < 0 ? 0 : (s0 > max_items ? max_items : s0);
     s1 = s1 < s0 ? s0 : (s1 > max_items ? max_items : s1);
     float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll 8   // several segments' loads in flight; the sum keeps segment order
     for (int64_t k = s0; k < s1; ++k) {
         const float4 v = *reinterpret_cast<const float4*>(partials + k * MD + rest);
         acc.x += v.x;
@@ -759,6 +760,7 @@ __global__ __launch_bounds__(256) void dp_pair_sum_kernel(const int32_t* __restr
     s0 = s0 < 0 ? 0 : (s0 > max_items ? max_items : s0);
     s1 = s1 < s0 ? s0 : (s1 > max_items ? max_items : s1);
     float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll 8   // several segments' loads in flight; the sum keeps segment order
     for (int64_t k = s0; k < s1; ++k) {
         const float4 v = *reinterpret_cast<const float4*>(partials + k * MD + rest);
         acc.x += v.x;

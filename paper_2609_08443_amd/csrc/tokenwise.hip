@@ -329,9 +329,13 @@ __global__ __launch_bounds__(256) void tw_merge_kernel(const int32_t* __restrict
     const int lane = threadIdx.x & 63;
     const int64_t h = p / B, b = p % B;
     const int64_t MD = (int64_t)M * d;
+    // (unrolled so that the loads of several segments are in flight at once; the
+    // sums keep segment order)
     float mx = -INFINITY;
+#pragma unroll 8
     for (int64_t k = s0; k < s1; ++k) mx = fmaxf(mx, stats[(k * M + m) * 2]);
     float l = 0.f, v0 = 0.f, v1 = 0.f;
+#pragma unroll 4
     for (int64_t k = s0; k < s1; ++k) {
         const float f = exp2f(stats[(k * M + m) * 2] - mx);
         l += f * stats[(k * M + m) * 2 + 1];

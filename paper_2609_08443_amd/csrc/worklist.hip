@@ -112,6 +112,7 @@ __global__ __launch_bounds__(256) void merge_kernel(const int32_t* __restrict__ 
     if (idx >= MD) return;
     const int64_t h = p / B, b = p % B;
     float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll 8   // several segments' loads in flight; the sum keeps segment order
     for (int64_t k = s0; k < s1; ++k) {
         const float4 v = *reinterpret_cast<const float4*>(partials + k * MD + idx);
         acc.x += v.x;
