@@ -43,10 +43,10 @@ WORKLOADS = {"c1": 1, "c2": 2, "c3": 3, "c4": 4, "c5": 5}
 # Source: profiles/hbm_bytes_c5_ragged100k_fwd_bwd.md
 MEASURED_TRAFFIC = {
     "bwd_token": ("paper_2609_08443_amd/csrc/bwd_fused.hip",
-                  "746fb97a5a16b29b41d2969b1c8373afdfe3e682f0a88866c7885ff0bac5e119",
+                  "b66b549e4f06447911251d5c30d8ec6aa03ef5b43e6aaafcbd0b53868de97635",
                   2.190e9 + 2.250e9),
     "bwd_proto": ("paper_2609_08443_amd/csrc/bwd_fused.hip",
-                  "746fb97a5a16b29b41d2969b1c8373afdfe3e682f0a88866c7885ff0bac5e119",
+                  "b66b549e4f06447911251d5c30d8ec6aa03ef5b43e6aaafcbd0b53868de97635",
                   1.219e9 + 0.100e9),
     "fused_fwd": ("paper_2609_08443_amd/csrc/fwd_fused.hip",
                   "ca57c7c144f8a2e7ad85ff38e0947b73f812b4dd098b59210532c5c5a26b5c33",

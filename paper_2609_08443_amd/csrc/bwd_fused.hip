@@ -410,8 +410,9 @@ __global__ __launch_bounds__(NW * 64, 8 / NW) void bwd_token_kernel(TokArgs a) {
         // Pipelined form: iteration mb runs the elementwise work of block mb
         // beside the S^T MFMAs of block mb + 1, then the dK MFMAs of mb beside
         // the dA MFMAs of mb + 1 (two independent chains).  It holds 16 more
-        // registers than the plain form, which separate K and V operands at
-        // d = 128 do not leave.
+        // registers than the plain form; with separate K and V operands at
+        // d = 128 it fits only at the full 256 VGPRs and runs slower, so that
+        // instance keeps the plain form.
         constexpr bool kPipe2 = XV || D == 64;
         auto da_tile = [&](const uint16_t* Lb) {
             f32x16 da;
