@@ -156,7 +156,8 @@ struct Cfg {
     static constexpr int OFF_MAX = OFF_SUM + RED_BYTES;  // [NW][32] partial maxima (exact path)
     static constexpr int OFF_SUM2 = OFF_MAX + RED_BYTES; // [NW][32] partial sums (exact path)
     static constexpr int OFF_KN = OFF_SUM2 + RED_BYTES;  // [2][32] token norms
-    static constexpr int OFF_PN = OFF_KN + 2 * 32 * 4;   // [NW] prototype norm maxima
+    static constexpr int OFF_NB = OFF_KN + 2 * 32 * 4;   // [2][32] the tokens' shifts, -c_t log2(e)
+    static constexpr int OFF_PN = OFF_NB + 2 * 32 * 4;   // [NW] prototype norm maxima
     static constexpr int OFF_SH = OFF_PN + 16 * 4;       // [32] exact-path shifts
     static constexpr int LDS = OFF_SH + 32 * 4;
 };
@@ -172,6 +173,7 @@ __global__ __launch_bounds__(NW * 64, 1) void fwd_fused_kernel(FusedFwdArgs a) {
     float* red_max = reinterpret_cast<float*>(smem + C::OFF_MAX);
     float* red_sum2 = reinterpret_cast<float*>(smem + C::OFF_SUM2);
     float* knorm = reinterpret_cast<float*>(smem + C::OFF_KN);
+    float* kshift = reinterpret_cast<float*>(smem + C::OFF_NB);
     float* pnorm = reinterpret_cast<float*>(smem + C::OFF_PN);
     float* shift_s = reinterpret_cast<float*>(smem + C::OFF_SH);
 
@@ -264,7 +266,11 @@ __global__ __launch_bounds__(NW * 64, 1) void fwd_fused_kernel(FusedFwdArgs a) {
                     const int tok = idx / C::KCH, ch = idx % C::KCH;
                     *reinterpret_cast<uint4*>(Kd + swz<D>(tok, ch)) = kreg[i];
                     const float ss = group_sum<C::KCH>(sumsq8(kreg[i]));
-                    if (ch == 0) knorm[kb * 32 + tok] = __builtin_sqrtf(ss);
+                    if (ch == 0) {
+                        const float kn = __builtin_sqrtf(ss);
+                        knorm[kb * 32 + tok] = kn;
+                        kshift[kb * 32 + tok] = -cb * kLog2e * kn;
+                    }
                 }
             }
         };
@@ -306,7 +312,7 @@ __global__ __launch_bounds__(NW * 64, 1) void fwd_fused_kernel(FusedFwdArgs a) {
             // ---- per-row shift: -c_t * log2(e) for this lane's 16 rows, c_t = cb * |K_t|
             float nb[16];
 #pragma unroll
-            for (int r = 0; r < 16; ++r) nb[r] = -cb * kLog2e * knorm[kb * 32 + srow(r, hl)];
+            for (int r = 0; r < 16; ++r) nb[r] = kshift[kb * 32 + srow(r, hl)];
 
             // ---- S tiles, exponentiated as they complete
             bf16x8 kop[C::KS];
