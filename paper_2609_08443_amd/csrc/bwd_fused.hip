@@ -588,8 +588,9 @@ __global__ __launch_bounds__(NW * 64, 1) void bwd_proto_kernel(ProtoArgs a) {
                 vreg[c] = vv;
             }
             if (tid < 32) {
+                // raw values: arithmetic on them here would wait for the loads
                 const bool v = ts + tid < t1;
-                lse_r = v ? -a.lse[(int64_t)(ts + tid) * a.H + h] * kLog2e : 0.f;
+                lse_r = v ? a.lse[(int64_t)(ts + tid) * a.H + h] : 0.f;
                 d_r = v ? a.Dbuf[(int64_t)(ts + tid) * a.H + h] : 0.f;
             }
         };
@@ -606,7 +607,7 @@ __global__ __launch_bounds__(NW * 64, 1) void bwd_proto_kernel(ProtoArgs a) {
                 }
             }
             if (tid < 32) {
-                reinterpret_cast<float*>(smem + C::OFF_L)[buf * 32 + tid] = lse_r;
+                reinterpret_cast<float*>(smem + C::OFF_L)[buf * 32 + tid] = -lse_r * kLog2e;
                 reinterpret_cast<float*>(smem + C::OFF_D)[buf * 32 + tid] = d_r;
             }
         };
@@ -645,6 +646,14 @@ __global__ __launch_bounds__(NW * 64, 1) void bwd_proto_kernel(ProtoArgs a) {
             for (int jt = 0; jt < C::JT; ++jt)
 #pragma unroll
                 for (int r = 0; r < 16; ++r) acc[mt][jt][r] = 0.f;
+        if constexpr (kHold) {
+            // Wait here for the held operands.  Otherwise the compiler's
+            // load-counter waits for them inside the loop also wait for each
+            // iteration's prefetch of the next tile, issued after them, which
+            // then lands before the tile's chains are done.
+#pragma unroll
+            for (int kk = 0; kk < C::KS; ++kk) asm volatile("" ::"v"(pop[kk]), "v"(yop[kk]));
+        }
 
         int buf = 0;
         for (int ts = t0; ts < t1; ts += 32, buf ^= 1) {
