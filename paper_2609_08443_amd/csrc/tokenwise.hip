@@ -229,6 +229,12 @@ __global__ __launch_bounds__(NW * 64, 1) void tw_fused_kernel(TwArgs a) {
             for (int r = 0; r < 16; ++r) acc[jt][r] = 0.f;
         float mu = -INFINITY;   // running max of this lane's prototype, log2 units
         float lsum = 0.f;       // running sum over this lane's 16 token rows per tile
+        // Wait here for the held operands.  Otherwise the compiler's load-counter
+        // waits for them inside the loop also wait for each iteration's prefetch
+        // of the next tile, issued after them, which then lands before the
+        // tile's logits are done.
+#pragma unroll
+        for (int kk = 0; kk < KS; ++kk) asm volatile("" ::"v"(pop[kk]));
 
         int buf = 0;
         for (int ts = t0; ts < t1; ts += 32, buf ^= 1) {
