@@ -26,6 +26,8 @@
 //          accumulates in registers with K^T read by the transposing LDS load;
 //          one partial per work-list segment, summed per head in segment order
 //          (deterministic).
+#include <type_traits>
+
 #include "sa_internal.h"
 #include "tile_ops.h"
 
@@ -505,14 +507,18 @@ struct ProtoCfg {
     // P and dY slices stay in LDS.
     static constexpr bool HOLD = MT == 1;
     static constexpr int SLICE = HOLD ? 0 : MP * D * 2;
+    // Two waves per SIMD with one prototype tile each run phase-shifted (see the
+    // kernel); their token tiles rotate through three buffers, otherwise two.
+    static constexpr bool PING = NW == 8 && MT == 1;
+    static constexpr int NBUF = PING ? 3 : 2;
     static constexpr int TILE = 32 * D * 2;                // one [32][D] bf16 token tile
     static constexpr int OFF_P = 0;                        // [MP][D]
     static constexpr int OFF_Y = OFF_P + SLICE;            // [MP][D]
-    static constexpr int OFF_K = OFF_Y + SLICE;            // 2 x [32][D] token-major K tiles
-    static constexpr int OFF_V = OFF_K + 2 * TILE;         // 2 x [32][D] V tiles
-    static constexpr int OFF_L = OFF_V + 2 * TILE;         // 2 x [32] -lse*log2e
-    static constexpr int OFF_D = OFF_L + 2 * 32 * 4;       // 2 x [32] D_t
-    static constexpr int LDS = OFF_D + 2 * 32 * 4;
+    static constexpr int OFF_K = OFF_Y + SLICE;            // NBUF x [32][D] token-major K tiles
+    static constexpr int OFF_V = OFF_K + NBUF * TILE;      // NBUF x [32][D] V tiles
+    static constexpr int OFF_L = OFF_V + NBUF * TILE;      // NBUF x [32] -lse*log2e
+    static constexpr int OFF_D = OFF_L + NBUF * 32 * 4;    // NBUF x [32] D_t
+    static constexpr int LDS = OFF_D + NBUF * 32 * 4;
 };
 
 struct ProtoArgs {
@@ -655,6 +661,70 @@ __global__ __launch_bounds__(NW * 64, 1) void bwd_proto_kernel(ProtoArgs a) {
             for (int kk = 0; kk < C::KS; ++kk) asm volatile("" ::"v"(pop[kk]), "v"(yop[kk]));
         }
 
+        // Two waves per SIMD (waves w and w + 4 of the workgroup share a SIMD):
+        // waves 0-3 run each tile's phases in order (S and dA chains, elementwise
+        // dS, dP chain) while waves 4-7 run them one phase late (the elementwise
+        // and dP work of the previous tile, then the chains of this tile), so that
+        // between two barriers one wave of a SIMD feeds the matrix core while the
+        // other runs its VALU work.  A late wave reads tile i in intervals i and
+        // i + 1, so tiles rotate through three buffers; tile i + 1 is written at
+        // the end of interval i, into the buffer last read in interval i - 1.
+        if constexpr (C::PING) {
+            const bool late = __builtin_amdgcn_readfirstlane(w) >= 4;
+            const int n = (t1 - t0 + 31) / 32;
+            auto chains = [&](int bi, f32x16& s, f32x16& da) __attribute__((always_inline)) {
+                const uint16_t* Ks = reinterpret_cast<const uint16_t*>(smem + C::OFF_K + bi * C::TILE);
+                const uint16_t* Vs = XV ? Ks : reinterpret_cast<const uint16_t*>(smem + C::OFF_V + bi * C::TILE);
+#pragma unroll
+                for (int r = 0; r < 16; ++r) s[r] = da[r] = 0.f;
+#pragma unroll
+                for (int kk = 0; kk < C::KS; ++kk) {
+                    s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(lds_b128(Ks, swz<D>(l32, 2 * kk + hl)), pop[kk], s, 0, 0, 0);
+                    da = __builtin_amdgcn_mfma_f32_32x32x16_bf16(lds_b128(Vs, swz<D>(l32, 2 * kk + hl)), yop[kk], da, 0, 0, 0);
+                }
+            };
+            auto ds_dp = [&](int bi, const f32x16& s, const f32x16& da) __attribute__((always_inline)) {
+                const uint16_t* Ks = reinterpret_cast<const uint16_t*>(smem + C::OFF_K + bi * C::TILE);
+                const float* nls = reinterpret_cast<const float*>(smem + C::OFF_L) + bi * 32;
+                const float* Ds = reinterpret_cast<const float*>(smem + C::OFF_D) + bi * 32;
+                float e[16];
+#pragma unroll
+                for (int r = 0; r < 16; ++r) {
+                    const int t = srow(r, hl);
+                    const float A = __builtin_amdgcn_exp2f(__builtin_fmaf(s[r], ks2, nls[t]));
+                    e[r] = A * (da[r] - Ds[t]);
+                }
+                const bf16x8 d0 = pack8(e), d1 = pack8(e + 8);
+#pragma unroll
+                for (int jt = 0; jt < C::JT; ++jt) {
+                    const bf16x8 k0v = lds_tr_tokens<D>(Ks, lane, jt, 0);
+                    const bf16x8 k1v = lds_tr_tokens<D>(Ks, lane, jt, 1);
+                    acc[0][jt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(d0, k0v, acc[0][jt], 0, 0, 0);
+                    acc[0][jt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(d1, k1v, acc[0][jt], 0, 0, 0);
+                }
+            };
+            f32x16 s, da;   // a late wave carries its chains across the barrier
+            // interval i with buffer BI = i % 3 (a constant, so that every tile
+            // address is a fixed offset from the same lane registers)
+            auto interval = [&](int i, auto bic) __attribute__((always_inline)) {
+                constexpr int BI = decltype(bic)::value;
+                constexpr int BP = (BI + 2) % 3, BN = (BI + 1) % 3;
+                const bool more = i + 1 < n;
+                if (more) fetch(t0 + 32 * (i + 1));
+                if (!late && i < n) chains(BI, s, da);
+                if (late ? i > 0 : i < n) ds_dp(late ? BP : BI, s, da);
+                // the chains' operand reads are not hoisted into the dP work
+                __builtin_amdgcn_sched_barrier(0);
+                if (late && i < n) chains(BI, s, da);
+                if (more) store(BN);
+                __syncthreads();
+            };
+            for (int i = 0; i <= n; i += 3) {
+                interval(i, std::integral_constant<int, 0>{});
+                if (i + 1 <= n) interval(i + 1, std::integral_constant<int, 1>{});
+                if (i + 2 <= n) interval(i + 2, std::integral_constant<int, 2>{});
+            }
+        } else {
         int buf = 0;
         for (int ts = t0; ts < t1; ts += 32, buf ^= 1) {
             const bool more = ts + 32 < t1;
@@ -715,6 +785,7 @@ __global__ __launch_bounds__(NW * 64, 1) void bwd_proto_kernel(ProtoArgs a) {
             // tile) passed the barrier at the end of the previous iteration
             if (more) store(buf ^ 1);
             __syncthreads();
+        }
         }
         // partial of this segment for this part's prototype rows
         float* out = a.partials + k * MD + (int64_t)part * C::MP * D;
