@@ -43,13 +43,13 @@ WORKLOADS = {"c1": 1, "c2": 2, "c3": 3, "c4": 4, "c5": 5}
 # Source: profiles/hbm_bytes_c5_ragged100k_fwd_bwd.md
 MEASURED_TRAFFIC = {
     "bwd_token": ("paper_2609_08443_amd/csrc/bwd_fused.hip",
-                  "b66b549e4f06447911251d5c30d8ec6aa03ef5b43e6aaafcbd0b53868de97635",
-                  2.171e9 + 2.250e9),
+                  "3f6a20346815a088971fb5e9e62e4bfa3f9b5fbfb763d2cf7bfe344f7a6cdd34",
+                  2.172e9 + 2.250e9),
     "bwd_proto": ("paper_2609_08443_amd/csrc/bwd_fused.hip",
-                  "b66b549e4f06447911251d5c30d8ec6aa03ef5b43e6aaafcbd0b53868de97635",
+                  "3f6a20346815a088971fb5e9e62e4bfa3f9b5fbfb763d2cf7bfe344f7a6cdd34",
                   1.220e9 + 0.100e9),
     "fused_fwd": ("paper_2609_08443_amd/csrc/fwd_fused.hip",
-                  "bf5f02fa3cc5f92e022cd4c506ebc6da477cac3fefe1c6bfc82fa64759e75ae6",
+                  "1e239153960e2d13017c2e05fb257e572aba5fb49b2dd6a782bf5d5624754e29",
                   0.658e9 + 0.135e9),
 }
 
