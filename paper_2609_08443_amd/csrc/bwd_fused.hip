@@ -96,6 +96,8 @@ __global__ __launch_bounds__(256) void prep_kernel(const float* __restrict__ ds,
     if (!is_y && pair >= n_p) return;
     uint16_t* rowdst = is_y ? Ymj + pair * MD : nullptr;
     uint16_t* trdst = (is_y ? Yjm : Pjm) + pair * MD;
+    // (unrolled so that the loads of both chunks and several targets are in flight)
+#pragma unroll
     for (int i = tid; i < NCH; i += 256) {
         const int r = i / KCH, c = i % KCH;
         const int64_t off = (int64_t)(mb * 32 + r) * D + c * 8;
@@ -103,6 +105,7 @@ __global__ __launch_bounds__(256) void prep_kernel(const float* __restrict__ ds,
         if (is_y) {
             const int64_t b = pair / H, h = pair % H;
             float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+#pragma unroll 4
             for (int rr = 0; rr < R; ++rr) {
                 const float4* src = reinterpret_cast<const float4*>(ds + ((b * R + rr) * H + h) * MD + off);
                 const float4 x0 = src[0], x1 = src[1];
