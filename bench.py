@@ -11,10 +11,12 @@ device with fixed seeds, resident in HBM before timing starts.
 
 Prints one JSON line.  ``value`` is history tokens per second of the whole
 step; ``fwd_tokens_per_s`` is the forward alone.  ``roofline`` describes the
-kernel with the largest share of the step, with its algorithmic FLOPs (GEMM
-convention of Appendix G: 4 M d per (token, head) in the forward, 8 M d in the
-backward) over its live HIP-event time.  ``cpu_baseline`` times the CPU oracle
-on a bounded sample of the same batch.
+kernel with the largest share of the step against the roof that binds at its
+algorithmic FLOPs (GEMM convention of Appendix G: 4 M d per (token, head) in the
+forward, 8 M d in the backward) and algorithmic bytes: the one with the larger
+ideal time, so a kernel below the ridge point is measured in bytes per second
+over its live HIP-event time.  ``cpu_baseline`` times the CPU oracle on a
+bounded sample of the same batch.
 """
 from __future__ import annotations
 
@@ -244,6 +246,10 @@ def main(argv=None) -> int:
     if dom is not None:
         fl, fl_exec, by, bound = kernel_work(dom, w)
         avg_ms = kt[dom][1] / kt[dom][0]
+        if bound == "mfma" and by / (PEAK_HBM_GBS * 1e9) > fl / (PEAK_BF16_TFLOPS * 1e12):
+            # the matrix-core kernel's algorithmic intensity is below the ridge
+            # point: its roofline ceiling is the HBM roof
+            bound = "hbm"
         if bound == "mfma":
             ach, peak, unit = fl / (avg_ms * 1e-3) / 1e12, PEAK_BF16_TFLOPS, "TFLOP/s"
         elif bound == "hbm":
@@ -254,7 +260,9 @@ def main(argv=None) -> int:
                 "frac": ach / peak, "traffic": measured_traffic(dom, args.workload),
                 "avg_ms": avg_ms,
                 "algorithmic_flops_per_launch": fl, "algorithmic_bytes_per_launch": by,
-                "executed_mfma_tflops": fl_exec / (avg_ms * 1e-3) / 1e12 if fl_exec else None}
+                "executed_mfma_tflops": fl_exec / (avg_ms * 1e-3) / 1e12 if fl_exec else None,
+                "algorithmic_intensity_flop_per_byte": fl / by,
+                "mfma_frac": fl / (avg_ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS}
 
     def timed(fn):
         """ms per call of fn over the timed steps, and the library's per-kernel times."""
