@@ -295,3 +295,31 @@ def test_fwd_loose_bound_falls_back_to_exact_max(sa, M, d):
     assert np.all(np.isfinite(g)) and np.all(np.isfinite(lse.cpu().numpy()))
     assert normwise(g, ref, (2, 3)).max() <= 2e-2
     assert np.abs(lse.cpu().numpy() - ref_lse).max() <= 1e-3 * max(1.0, np.abs(ref_lse).max())
+
+
+# ------------------------------------------------------------------ offsets validation
+# With SA_DEBUG_VALIDATE=1 every entry point copies the offsets to the host and
+# rejects malformed ones with SA_ERR_BAD_OFFSETS before any launch; valid
+# offsets give the same results as without the check.
+def test_debug_validate_rejects_malformed_offsets(sa, monkeypatch):
+    w = wl.custom([40, 0, 70], 2, 128, 64, "bf16", seed=91, R=2, bwd=True)
+    host = wl.host_tensors(w)
+    dev = wl.to_device(host, "bf16")
+    sk0, lse0 = sa.sketch_fwd(dev["K"], dev["V"], dev["P"], dev["offsets"])
+    torch.cuda.synchronize()
+    monkeypatch.setenv("SA_DEBUG_VALIDATE", "1")
+    sk1, lse1 = sa.sketch_fwd(dev["K"], dev["V"], dev["P"], dev["offsets"])
+    sa.sketch_bwd(dev["K"], dev["V"], dev["P"], dev["offsets"], dev["dsketch"], lse1)
+    torch.cuda.synchronize()
+    assert torch.equal(sk0, sk1) and torch.equal(lse0, lse1)
+    T = w.T
+    bad = {"first not zero": [1, 40, 40, T], "decreasing": [0, 50, 40, T], "last not T": [0, 40, 40, T - 1]}
+    for name, o in bad.items():
+        off = torch.tensor(o, dtype=torch.int64, device="cuda")
+        print(f"malformed offsets case: {name}", flush=True)
+        for call in (lambda: sa.sketch_fwd(dev["K"], dev["V"], dev["P"], off),
+                     lambda: sa.sketch_bwd(dev["K"], dev["V"], dev["P"], off, dev["dsketch"], lse1),
+                     lambda: sa.sketch_fwd_tokenwise(dev["K"], dev["V"], dev["P"], off)):
+            with pytest.raises(sa.SAError) as ei:
+                call()
+            assert ei.value.status == 4, (name, ei.value)
