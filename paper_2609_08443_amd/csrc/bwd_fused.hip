@@ -193,16 +193,21 @@ __global__ __launch_bounds__(NW * 64, 8 / NW) void bwd_token_kernel(TokArgs a) {
     const int l32 = lane & 31, hl = lane >> 5;
     float* stg = reinterpret_cast<float*>(smem + C::OFF_STG) + w * C::STG_FLOATS;
 
-    const int64_t range = xcd_range(blockIdx.x, gridDim.x);
-    const int64_t k0 = a.wg_start[range], k1 = a.wg_start[range + 1];
+    // The workgroups of one XCD take the token blocks of that XCD's ranges in
+    // turn (workgroup i of the XCD: blocks i, i + nx, i + 2 nx, ...), so that at
+    // any time they work on neighbouring blocks, mostly of one (user, head),
+    // whose prototype-block stream then stays in that XCD's L2.
+    const int64_t nr = gridDim.x, xq = nr / 8, xrem = nr % 8, xcd = blockIdx.x % 8;
+    const int64_t lw = blockIdx.x / 8, nx = xq + (xcd < xrem ? 1 : 0);
+    const int64_t first_range = xcd * xq + (xcd < xrem ? xcd : xrem);
+    const int64_t k0 = a.wg_start[first_range], k1 = a.wg_start[first_range + nx];
     if (k0 < 0 || k1 < k0 || k1 > a.max_items) return;
     const float ks2 = a.scale * kLog2e;
     const int nblk = a.M / 32;   // >= 4
     const int64_t MD = (int64_t)a.M * D;
 
-    // Token blocks of the workgroup's segments, in order.  The first one is
-    // shortened by (range % 4) quarter blocks, so that workgroups reach their HBM
-    // phases (K/V loads, dV/dK stores) at staggered times.
+    // A token block: segment k of the work list (user b, head h, tokens up to
+    // t1) and its tokens [tb, te); blocks of a segment start at its first token.
     struct Blk {
         int64_t k;
         int b, h, t1, tb, te;
@@ -218,15 +223,22 @@ __global__ __launch_bounds__(NW * 64, 8 / NW) void bwd_token_kernel(TokArgs a) {
         }
         return false;
     };
-    auto next_of = [&](const Blk& c, Blk& o) -> bool {
-        if (c.te < c.t1) {
-            o = c;
-            o.tb = c.te;
-            o.te = c.te + C::TB < c.t1 ? c.te + C::TB : c.t1;
-            return true;
+    // the block `steps` blocks after c in the XCD's sequence (blocks start at
+    // their segment's first token)
+    auto advance = [&](Blk c, int64_t steps, Blk& o) -> bool {
+        while (true) {
+            const int64_t left = (c.t1 - c.tb + C::TB - 1) / C::TB;   // c and the blocks after it
+            if (steps < left) {
+                o = c;
+                o.tb = c.tb + (int)steps * C::TB;
+                o.te = o.tb + C::TB < c.t1 ? o.tb + C::TB : c.t1;
+                return true;
+            }
+            steps -= left;
+            if (!first_from(c.k + 1, 0, c)) return false;
         }
-        return first_from(c.k + 1, 0, o);
     };
+    auto next_of = [&](const Blk& c, Blk& o) -> bool { return advance(c, nx, o); };
 
     // K as B operands (lane (hl, t) holds 8 consecutive j of its token) and the
     // lane's -lse * log2(e), for block c
@@ -316,7 +328,7 @@ __global__ __launch_bounds__(NW * 64, 8 / NW) void bwd_token_kernel(TokArgs a) {
     };
 
     Blk cur;
-    if (!first_from(k0, (int)(range % 4) * (C::TB / 4), cur)) return;
+    if (!first_from(k0, 0, cur) || !advance(cur, lw, cur)) return;
     load_k(cur);
     fetch(cur, 0, 0, 0);
     fetch(cur, 1, 0, 1);
