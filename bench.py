@@ -45,10 +45,10 @@ WORKLOADS = {"c1": 1, "c2": 2, "c3": 3, "c4": 4, "c5": 5}
 # Source: profiles/hbm_bytes_c5_ragged100k_fwd_bwd.md
 MEASURED_TRAFFIC = {
     "bwd_token": ("paper_2609_08443_amd/csrc/bwd_fused.hip",
-                  "9389392504568208c78c45e37377a0288a1f6c12f83288417927605755358107",
-                  2.179e9 + 2.250e9),
+                  "57d0367bf7b2a9a5441602519ebfd053502bcd504f2584431bfee195eb7587c3",
+                  1.310e9 + 2.250e9),
     "bwd_proto": ("paper_2609_08443_amd/csrc/bwd_fused.hip",
-                  "9389392504568208c78c45e37377a0288a1f6c12f83288417927605755358107",
+                  "57d0367bf7b2a9a5441602519ebfd053502bcd504f2584431bfee195eb7587c3",
                   1.220e9 + 0.100e9),
     "fused_fwd": ("paper_2609_08443_amd/csrc/fwd_fused.hip",
                   "1e239153960e2d13017c2e05fb257e572aba5fb49b2dd6a782bf5d5624754e29",
