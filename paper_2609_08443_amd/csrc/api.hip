@@ -501,18 +501,18 @@ sa_status block_layer_fwd(const void* X, const int64_t* offsets, int64_t B, int6
                           w.ln_(l, 1), bf, rows, H, M, d, eps, io.Xbar, stream, io.Y1);
     // FFN(Xbar) = (silu(Xbar W1) * (Xbar W3)) W2, into the Xhat buffer
     if (e == hipSuccess)
-        e = sa::launch_small_gemm({io.Xbar, false, md, d, 1}, {w.w1(l), bf, d * d2, d2, 1}, io.G, false,
-                                  (int32_t)BH, M, (int32_t)d2, d, stream, H);
+        e = grad_gemm(bf, {io.Xbar, false, md, d, 1}, {w.w1(l), bf, d * d2, d2, 1}, io.G, (int32_t)BH, M,
+                      (int32_t)d2, d, stream, H);
     if (e == hipSuccess)
-        e = sa::launch_small_gemm({io.Xbar, false, md, d, 1}, {w.w3(l), bf, d * d2, d2, 1}, io.U, false,
-                                  (int32_t)BH, M, (int32_t)d2, d, stream, H);
+        e = grad_gemm(bf, {io.Xbar, false, md, d, 1}, {w.w3(l), bf, d * d2, d2, 1}, io.U, (int32_t)BH, M,
+                      (int32_t)d2, d, stream, H);
     float* Z = io.Z ? io.Z : io.G;
     if (e == hipSuccess)
         e = io.Z ? sa::launch_swiglu_fwd(io.G, io.U, io.Z, rows * d2, stream)
                  : sa::launch_swiglu_gate(io.G, io.U, rows * d2, stream);
     if (e == hipSuccess)
-        e = sa::launch_small_gemm({Z, false, M * d2, d2, 1}, {w.w2(l), bf, d2 * d, d, 1}, io.Xhat, false,
-                                  (int32_t)BH, M, d, (int32_t)d2, stream, H);
+        e = grad_gemm(bf, {Z, false, M * d2, d2, 1}, {w.w2(l), bf, d2 * d, d, 1}, io.Xhat, (int32_t)BH, M, d,
+                      (int32_t)d2, stream, H);
     // Xt' = LN2(Xbar + FFN)
     if (e == hipSuccess)
         e = sa::launch_add_ln(io.Xbar, false, rows, io.Xhat, w.ln_(l, 2), w.ln_(l, 3), bf, rows, H, M, d, eps,
