@@ -236,23 +236,28 @@ __global__ __launch_bounds__(NW * 64, 1) void fwd_fused_kernel(FusedFwdArgs a) {
                 for (int r = 0; r < 16; ++r) acc[mt][jt][r] = 0.f;
 
         // global tile loads into registers: 32-bit per-lane offsets, uniform tile base
-        uint4 kreg[C::NLD], vreg[C::NLD], vcur[C::NLD];
-        auto load_tile = [&](int ts) {
-            const int64_t tb = ((int64_t)ts * a.H + h) * D;
-            const uint16_t* Kb = a.K + tb;
-            const uint16_t* Vb = a.V + tb;
+        // K is loaded two tiles ahead of its use and V one tile ahead: both are
+        // issued at the end of a tile, so neither register set is copied
+        // between tiles.  Rows past the end of the range read its last token
+        // when every chunk slot is used (unpredicated loads; their V is zeroed
+        // at staging), else they are zero.
+        uint4 kreg[C::NLD], vreg[C::NLD];
+        auto load_rows = [&](const uint16_t* X, int ts, uint4 (&dst)[C::NLD]) {
+            const uint16_t* Xb = X + ((int64_t)ts * a.H + h) * D;
+            const int last = t1 - 1 - ts;
 #pragma unroll
             for (int i = 0; i < C::NLD; ++i) {
                 const int idx = tid + i * C::THREADS;
                 const int tok = idx / C::KCH, ch = idx % C::KCH;
-                uint4 kv = make_uint4(0, 0, 0, 0), vv = make_uint4(0, 0, 0, 0);
-                if (idx < C::LD_CHUNKS && ts + tok < t1) {
-                    const uint32_t off = (uint32_t)tok * row_stride + (uint32_t)(ch * 8);
-                    kv = *reinterpret_cast<const uint4*>(Kb + off);
-                    vv = *reinterpret_cast<const uint4*>(Vb + off);
+                if constexpr (C::LD_CHUNKS % C::THREADS == 0) {
+                    const uint32_t off = (uint32_t)min(tok, last) * row_stride + (uint32_t)(ch * 8);
+                    dst[i] = *reinterpret_cast<const uint4*>(Xb + off);
+                } else {
+                    uint4 x = make_uint4(0, 0, 0, 0);
+                    if (idx < C::LD_CHUNKS && tok <= last)
+                        x = *reinterpret_cast<const uint4*>(Xb + (uint32_t)tok * row_stride + (uint32_t)(ch * 8));
+                    dst[i] = x;
                 }
-                kreg[i] = kv;
-                vreg[i] = vv;
             }
         };
         // K tile (from kreg) into LDS buffer `buf`, with the token norms
@@ -280,12 +285,13 @@ __global__ __launch_bounds__(NW * 64, 1) void fwd_fused_kernel(FusedFwdArgs a) {
         // read it) while the accumulator stays in AGPRs; the compiler does not
         // model these instructions, so each waits 2 states after any VALU write
         // of its operands, and the tile is read 32 states after the last one.
-        auto s_tile = [&](const bf16x8* kop, int mt) {
-            f32x16 s;
+        auto read_bp = [&](bf16x8* bp, int mt) {
             const int prow = w * MW + mt * 32 + l32;
-            bf16x8 bp[C::KS];
 #pragma unroll
             for (int kk = 0; kk < C::KS; ++kk) bp[kk] = lds_b128(Ps, swz<D>(prow, 2 * kk + hl));
+        };
+        auto s_chain = [&](const bf16x8* kop, const bf16x8* bp) {
+            f32x16 s;
             __builtin_amdgcn_sched_barrier(0);
             asm("s_nop 1\n\tv_mfma_f32_32x32x16_bf16 %0, %1, %2, 0" : "=&v"(s) : "v"(kop[0]), "v"(bp[0]));
 #pragma unroll
@@ -294,14 +300,18 @@ __global__ __launch_bounds__(NW * 64, 1) void fwd_fused_kernel(FusedFwdArgs a) {
             asm volatile("s_nop 15\n\ts_nop 15" : "+v"(s));
             return s;
         };
+        auto s_tile = [&](const bf16x8* kop, int mt) {
+            bf16x8 bp[C::KS];
+            read_bp(bp, mt);
+            return s_chain(kop, bp);
+        };
 
         const int ntiles = (t1 - t0 + 31) / 32;
         // prologue: tile 0 staged, tile 1 in flight
-        load_tile(t0);
+        load_rows(a.K, t0, kreg);
+        load_rows(a.V, t0, vreg);
         stage_k(0);
-#pragma unroll
-        for (int i = 0; i < C::NLD; ++i) vcur[i] = vreg[i];
-        if (ntiles > 1) load_tile(t0 + 32);
+        if (ntiles > 1) load_rows(a.K, t0 + 32, kreg);
         __syncthreads();
 
         for (int ti = 0; ti < ntiles; ++ti) {
@@ -319,20 +329,26 @@ __global__ __launch_bounds__(NW * 64, 1) void fwd_fused_kernel(FusedFwdArgs a) {
 #pragma unroll
             for (int kk = 0; kk < C::KS; ++kk) kop[kk] = lds_b128(Ks, swz<D>(l32, 2 * kk + hl));
             float rsum[16];
-#pragma unroll
-            for (int r = 0; r < 16; ++r) rsum[r] = 0.f;
             bf16x8 eop[C::MT][2];
+            bf16x8 bp[C::KS];
+            read_bp(bp, 0);
 #pragma unroll
             for (int mt = 0; mt < C::MT; ++mt) {
-                const f32x16 s = s_tile(kop, mt);
+                const f32x16 s = s_chain(kop, bp);
+                // the chain has completed: the next prototype tile's operands load
+                // under this tile's exponentials
+                if (mt + 1 < C::MT) read_bp(bp, mt + 1);
                 float e[16];
 #pragma unroll
                 for (int r = 0; r < 16; ++r) {
                     e[r] = __builtin_amdgcn_exp2f(__builtin_fmaf(s[r], ks2, nb[r]));
-                    rsum[r] += e[r];
+                    rsum[r] = mt == 0 ? e[r] : rsum[r] + e[r];
                 }
                 eop[mt][0] = pack8(e);
                 eop[mt][1] = pack8(e + 8);
+                // packed here: left to the compiler, the packing sinks past the
+                // branch below and the fp32 exponentials stay live through it
+                asm volatile("" : "+v"(eop[mt][0]), "+v"(eop[mt][1]));
             }
             {
                 const float z = half_sum16(rsum, l32);
@@ -427,13 +443,13 @@ __global__ __launch_bounds__(NW * 64, 1) void fwd_fused_kernel(FusedFwdArgs a) {
                     float z = 0.f;
 #pragma unroll
                     for (int ww = 0; ww < NW; ++ww) z += zsrc[ww * 32 + tok];
-                    *reinterpret_cast<uint4*>(Vt + swz<D>(tok, ch)) = scale8(vcur[i], 1.0f / z);
+                    const float inv = ts + tok < t1 ? 1.0f / z : 0.0f;
+                    *reinterpret_cast<uint4*>(Vt + swz<D>(tok, ch)) = scale8(vreg[i], inv);
                 }
             }
-            // V of tile i+1 is in vreg; issue the loads of tile i+2
-#pragma unroll
-            for (int i = 0; i < C::NLD; ++i) vcur[i] = vreg[i];
-            if (ti + 2 < ntiles) load_tile(ts + 64);
+            // K of tile i+2 and V of tile i+1 (kreg was staged above, vreg just now)
+            if (ti + 2 < ntiles) load_rows(a.K, ts + 64, kreg);
+            if (ti + 1 < ntiles) load_rows(a.V, ts + 32, vreg);
             // B_v: V' staged, K(i+1) visible; the loads of tile i+2 stay in flight
             // (they have the aggregation of this tile and the logits of the next)
             lds_barrier();
