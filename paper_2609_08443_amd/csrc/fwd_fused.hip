@@ -79,6 +79,36 @@ constexpr int kRowMirror = 0x140;
 constexpr int kRowRor4 = 0x124;
 constexpr int kRowRor8 = 0x128;
 
+// One step of a logits chain overlapped with exponentials: one MFMA of the
+// chain that accumulates the next 32x32 logits tile into sn, then two rows of
+// the current tile, e = 2^(s * ks + n), added into their sums and packed to
+// bf16.  The VALU work is independent of the MFMA, so it issues while the
+// matrix core runs.  Each exponential's first use is one instruction after it
+// (the transcendental forwarding gap); sn must not be read for 32 states after
+// the last step of a chain.
+template <bool FIRST>
+__device__ inline void chain_exp_step(f32x16& sn, const bf16x8& k, const bf16x8& b, float s0, float s1,
+                                      float n0, float n1, float ks, float& z0, float& z1, uint32_t& ep) {
+    float t0, t1;
+    if constexpr (FIRST) {
+        asm("s_nop 1\n\tv_mfma_f32_32x32x16_bf16 %[sn], %[k], %[b], 0\n\t"
+            "v_fma_f32 %[t0], %[s0], %[ks], %[n0]\n\tv_fma_f32 %[t1], %[s1], %[ks], %[n1]\n\t"
+            "v_exp_f32 %[t0], %[t0]\n\tv_exp_f32 %[t1], %[t1]\n\t"
+            "v_add_f32 %[z0], %[z0], %[t0]\n\tv_add_f32 %[z1], %[z1], %[t1]\n\t"
+            "v_cvt_pk_bf16_f32 %[ep], %[t0], %[t1]"
+            : [sn] "=&v"(sn), [t0] "=&v"(t0), [t1] "=&v"(t1), [z0] "+v"(z0), [z1] "+v"(z1), [ep] "=&v"(ep)
+            : [k] "v"(k), [b] "v"(b), [s0] "v"(s0), [s1] "v"(s1), [n0] "v"(n0), [n1] "v"(n1), [ks] "v"(ks));
+    } else {
+        asm("s_nop 1\n\tv_mfma_f32_32x32x16_bf16 %[sn], %[k], %[b], %[sn]\n\t"
+            "v_fma_f32 %[t0], %[s0], %[ks], %[n0]\n\tv_fma_f32 %[t1], %[s1], %[ks], %[n1]\n\t"
+            "v_exp_f32 %[t0], %[t0]\n\tv_exp_f32 %[t1], %[t1]\n\t"
+            "v_add_f32 %[z0], %[z0], %[t0]\n\tv_add_f32 %[z1], %[z1], %[t1]\n\t"
+            "v_cvt_pk_bf16_f32 %[ep], %[t0], %[t1]"
+            : [sn] "+v"(sn), [t0] "=&v"(t0), [t1] "=&v"(t1), [z0] "+v"(z0), [z1] "+v"(z1), [ep] "=&v"(ep)
+            : [k] "v"(k), [b] "v"(b), [s0] "v"(s0), [s1] "v"(s1), [n0] "v"(n0), [n1] "v"(n1), [ks] "v"(ks));
+    }
+}
+
 // reduce across the 32 lanes of each half-wave; every lane gets the result
 __device__ inline float half_max(float v) {
     v = fmaxf(v, dpp<kQuadXor1>(v));
@@ -332,6 +362,43 @@ __global__ __launch_bounds__(NW * 64, 1) void fwd_fused_kernel(FusedFwdArgs a) {
             bf16x8 eop[C::MT][2];
             bf16x8 bp[C::KS];
             read_bp(bp, 0);
+            if constexpr (C::KS == 8 && C::MT > 1) {
+                // the chain of prototype tile mt+1 runs on the matrix cores while
+                // the exponentials of tile mt are taken, one MFMA per two rows
+#pragma unroll
+                for (int r = 0; r < 16; ++r) rsum[r] = 0.f;
+                f32x16 s = s_chain(kop, bp);
+#pragma unroll
+                for (int mt = 0; mt < C::MT; ++mt) {
+                    uint32_t ep[8];
+                    if (mt + 1 < C::MT) {
+                        read_bp(bp, mt + 1);
+                        // the eight operand reads are issued together, not each
+                        // just before its MFMA
+                        __builtin_amdgcn_sched_barrier(0);
+                        f32x16 sn;
+                        chain_exp_step<true>(sn, kop[0], bp[0], s[0], s[1], nb[0], nb[1], ks2, rsum[0], rsum[1], ep[0]);
+#pragma unroll
+                        for (int kk = 1; kk < 8; ++kk)
+                            chain_exp_step<false>(sn, kop[kk], bp[kk], s[2 * kk], s[2 * kk + 1], nb[2 * kk],
+                                                  nb[2 * kk + 1], ks2, rsum[2 * kk], rsum[2 * kk + 1], ep[kk]);
+                        asm volatile("s_nop 15\n\ts_nop 15" : "+v"(sn));
+                        s = sn;
+                    } else {
+#pragma unroll
+                        for (int kk = 0; kk < 8; ++kk) {
+                            const float e0 = __builtin_amdgcn_exp2f(__builtin_fmaf(s[2 * kk], ks2, nb[2 * kk]));
+                            const float e1 = __builtin_amdgcn_exp2f(__builtin_fmaf(s[2 * kk + 1], ks2, nb[2 * kk + 1]));
+                            rsum[2 * kk] += e0;
+                            rsum[2 * kk + 1] += e1;
+                            ep[kk] = pack_bf16x2(e0, e1);
+                        }
+                    }
+                    eop[mt][0] = __builtin_bit_cast(bf16x8, make_uint4(ep[0], ep[1], ep[2], ep[3]));
+                    eop[mt][1] = __builtin_bit_cast(bf16x8, make_uint4(ep[4], ep[5], ep[6], ep[7]));
+                    asm volatile("" : "+v"(eop[mt][0]), "+v"(eop[mt][1]));
+                }
+            } else
 #pragma unroll
             for (int mt = 0; mt < C::MT; ++mt) {
                 const f32x16 s = s_chain(kop, bp);
