@@ -51,7 +51,7 @@ MEASURED_TRAFFIC = {
                   "57d0367bf7b2a9a5441602519ebfd053502bcd504f2584431bfee195eb7587c3",
                   1.220e9 + 0.100e9),
     "fused_fwd": ("paper_2609_08443_amd/csrc/fwd_fused.hip",
-                  "1e239153960e2d13017c2e05fb257e572aba5fb49b2dd6a782bf5d5624754e29",
+                  "221f8a9cd9d47e29d8f3d3ad2c3d6abb3048e9c1b17f5877add84c3f71458562",
                   0.658e9 + 0.135e9),
 }
 
