@@ -1,6 +1,7 @@
 """Benchmark of the SA sketching step on one MI355X.
 
     python bench.py [--steps K] [--warmup W] [--workload c5] [--no-cpu-baseline]
+                    [--no-configs] [--no-variants]
 
 A step is one pass of the whole hot path over one batch: sa_sketch_fwd
 (work list, fused forward, split-L merge) then sa_sketch_bwd (MRLB target sum,
@@ -10,13 +11,20 @@ H = 4, d = 128, M = 512, bf16, R = 4).  Inputs are synthetic, drawn on the
 device with fixed seeds, resident in HBM before timing starts.
 
 Prints one JSON line.  ``value`` is history tokens per second of the whole
-step; ``fwd_tokens_per_s`` is the forward alone.  ``roofline`` describes the
-kernel with the largest share of the step against the roof that binds at its
-algorithmic FLOPs (GEMM convention of Appendix G: 4 M d per (token, head) in the
-forward, 8 M d in the backward) and algorithmic bytes: the one with the larger
-ideal time, so a kernel below the ridge point is measured in bytes per second
-over its live HIP-event time.  ``cpu_baseline`` times the CPU oracle on a
-bounded sample of the same batch.
+step, timed over K steps with nothing but the library's launches inside the
+timed region; ``fwd_tokens_per_s`` times the forward alone the same way.  The
+per-kernel figures come from a separate pass of K steps with the library's
+per-launch HIP events switched on.  ``roofline`` describes the kernel with the
+largest share of the step against the roof that binds at its algorithmic FLOPs
+(GEMM convention of Appendix G: 4 M d per (token, head) in the forward, 8 M d
+in the backward) and algorithmic bytes: the one with the larger ideal time, so
+a kernel below the ridge point is measured in bytes per second over its live
+HIP-event time; ``kernel_roofline`` does the same for every kernel of the
+step.  ``configs`` times the forward of the other paper-shaped batches (the
+single-user fp32 case, the uniform 16 x 10K batch with its inputs rotated
+through copies larger than the 256 MB Infinity Cache, and the 64 x 100K
+batch).  ``cpu_baseline`` times the CPU oracle on a bounded sample of the
+same batch.
 """
 from __future__ import annotations
 
@@ -39,21 +47,13 @@ METRIC = "history tokens sketched/sec (fwd+bwd step; fwd alone in fwd_tokens_per
 
 WORKLOADS = {"c1": 1, "c2": 2, "c3": 3, "c4": 4, "c5": 5}
 
-# HBM bytes per launch measured with rocprofv3 FETCH_SIZE / WRITE_SIZE (scaled by the
-# same counters on a plain 1 GiB copy) on the default workload, keyed by the sha256 of
-# the kernel's source file at the time: a changed kernel reports traffic = null.
-# Source: profiles/hbm_bytes_c5_ragged100k_fwd_bwd.md
-MEASURED_TRAFFIC = {
-    "bwd_token": ("paper_2609_08443_amd/csrc/bwd_fused.hip",
-                  "57d0367bf7b2a9a5441602519ebfd053502bcd504f2584431bfee195eb7587c3",
-                  1.310e9 + 2.250e9),
-    "bwd_proto": ("paper_2609_08443_amd/csrc/bwd_fused.hip",
-                  "57d0367bf7b2a9a5441602519ebfd053502bcd504f2584431bfee195eb7587c3",
-                  1.220e9 + 0.100e9),
-    "fused_fwd": ("paper_2609_08443_amd/csrc/fwd_fused.hip",
-                  "221f8a9cd9d47e29d8f3d3ad2c3d6abb3048e9c1b17f5877add84c3f71458562",
-                  0.658e9 + 0.135e9),
-}
+# HBM bytes per launch of the step's kernels on the default workload, from
+# rocprofv3's request counters (TCC_EA0_RDREQ_32B/64B/128B, TCC_EA0_WRREQ/_64B)
+# taken with --no-configs --no-variants so that only the step's launches are
+# averaged, keyed by the sha256 of the kernel's source file at the time: a
+# changed kernel reports traffic = null.  Empty until taken on the current
+# sources.
+MEASURED_TRAFFIC: dict = {}
 
 
 def measured_traffic(kernel: str, workload: str):
@@ -120,9 +120,21 @@ def kernel_work(name: str, w: wl.Workload):
 
 
 # ---------------------------------------------------------------- CPU baseline
+def cpu_model() -> str:
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
 def cpu_baseline(w: wl.Workload, dev: dict, budget_tokens: int) -> dict:
     """The fp64 oracle (fwd, plus bwd when the step has it) on the shortest users of the
-    batch whose total length reaches budget_tokens; reported in tokens/s."""
+    batch whose total length reaches budget_tokens, on every host thread; then on one
+    thread over the first 2000 tokens of the shortest user.  Reported in tokens/s."""
     import numpy as np
     import oracle
 
@@ -142,17 +154,34 @@ def cpu_baseline(w: wl.Workload, dev: dict, budget_tokens: int) -> dict:
     o = np.zeros(len(users) + 1, np.int64)
     np.cumsum(lens, out=o[1:])
     threads = oracle.max_threads()
-    t0 = time.perf_counter()
-    oracle.fwd(K, V, P, o, w.scale)
-    if w.bwd:
-        dS = dev["dsketch"][users].cpu().numpy()
-        oracle.bwd(K, V, P, o, dS, w.scale)
-    dt = time.perf_counter() - t0
+    dS = dev["dsketch"][users].cpu().numpy() if w.bwd else None
+
+    def run(K_, V_, o_, dS_, nthreads):
+        t0 = time.perf_counter()
+        oracle.fwd(K_, V_, P, o_, w.scale, nthreads=nthreads)
+        if w.bwd:
+            oracle.bwd(K_, V_, P, o_, dS_, w.scale, nthreads=nthreads)
+        return time.perf_counter() - t0
+
+    dt = run(K, V, o, dS, 0)
     ntok = int(lens.sum())
+    # one thread: the first n1 tokens of the shortest user (its upstream gradient as is)
+    b0 = int(order[0])
+    n1 = int(min(2000, w.lengths[b0]))
+    s0 = int(off[b0])
+    K1 = dev["K"][s0:s0 + n1].float().cpu().numpy()
+    V1 = dev["V"][s0:s0 + n1].float().cpu().numpy()
+    dS1 = dev["dsketch"][b0:b0 + 1].cpu().numpy() if w.bwd else None
+    dt1 = run(K1, V1, np.array([0, n1], np.int64), dS1, 1)
+    kind = "fwd+bwd" if w.bwd else "fwd"
     return {"value": ntok / dt, "unit": "tokens/s", "cores": min(threads, len(users) * w.H),
             "kind": "oracle",
-            "sample": f"{len(users)} shortest users ({ntok} tokens, all {w.H} heads, "
-                      f"{'fwd+bwd' if w.bwd else 'fwd'}) of the same batch, fp64, {dt:.1f} s"}
+            "sample": f"{len(users)} shortest users ({ntok} tokens, all {w.H} heads, {kind}) of the "
+                      f"same batch, fp64, {dt:.1f} s",
+            "cpu_model": cpu_model(), "host_threads": threads,
+            "single_thread": {"value": n1 / dt1, "unit": "tokens/s",
+                              "sample": f"first {n1} tokens of user {b0} (all {w.H} heads, {kind}), "
+                                        f"fp64, one thread, {dt1:.1f} s"}}
 
 
 # ---------------------------------------------------------------- main
@@ -164,7 +193,9 @@ def main(argv=None) -> int:
     ap.add_argument("--workload", default="c5", choices=sorted(WORKLOADS))
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-variants", action="store_true",
-                    help="skip the timings of the token-wise variant and of the SA layer")
+                    help="skip the timings of the token-wise variant, the SA layer, the block and STCA")
+    ap.add_argument("--no-configs", action="store_true",
+                    help="skip the forward timings of the other paper-shaped batches")
     ap.add_argument("--cpu-tokens", type=int, default=300000,
                     help="tokens of the CPU-baseline sample (shortest users first)")
     ap.add_argument("--copy-calibration", action="store_true",
@@ -216,36 +247,47 @@ def main(argv=None) -> int:
         step()
     torch.cuda.synchronize()
 
-    # timed region: outer events for the step, library events for each kernel
     stream = torch.cuda.current_stream()
-    e0 = torch.cuda.Event(enable_timing=True)
-    e1 = torch.cuda.Event(enable_timing=True)
+
+    def plain_loop(fn, reps):
+        """ms per call of fn over reps calls: two stream events around the calls,
+        nothing else inside the timed region."""
+        torch.cuda.synchronize()
+        t0 = torch.cuda.Event(enable_timing=True)
+        t1 = torch.cuda.Event(enable_timing=True)
+        t0.record(stream)
+        for _ in range(reps):
+            fn()
+        t1.record(stream)
+        torch.cuda.synchronize()
+        return t0.elapsed_time(t1) / reps
+
+    # headline: the step alone, no per-launch events
+    wall0 = time.perf_counter()
+    ms_step = plain_loop(step, args.steps)
+    wall = time.perf_counter() - wall0
+
+    # the forward alone, timed the same way
+    def fwd_only():
+        sa.sketch_fwd(dev["K"], dev["V"], dev["P"], dev["offsets"], w.scale, sketch=sketch, lse=lse,
+                      workspace=ws_f)
+    for _ in range(args.warmup):
+        fwd_only()
+    fwd_ms = plain_loop(fwd_only, args.steps)
+
+    # per-kernel times: a separate pass of the same steps with the library's
+    # per-launch events on the launch stream
     sa.kernel_times()  # clear
     sa.profile_enable(True)
-    torch.cuda.synchronize()
-    wall0 = time.perf_counter()
-    e0.record(stream)
-    for _ in range(args.steps):
-        step()
-    e1.record(stream)
-    torch.cuda.synchronize()
-    wall = time.perf_counter() - wall0
+    plain_loop(step, args.steps)
     sa.profile_enable(False)
     kt = sa.kernel_times()
-    ms_step = e0.elapsed_time(e1) / args.steps
-
-    # fwd-only rate from the per-kernel events of the forward's launches
-    fwd_names = ("worklist", "fused_fwd", "splitL_merge", "plain_fwd")
-    fwd_ms = sum(kt[n][1] for n in fwd_names if n in kt) / args.steps
     kernels = {n: {"launches": c, "avg_ms": tot / c} for n, (c, tot) in kt.items()}
 
     flops_step = fwd_algorithmic_flops(w) + (bwd_algorithmic_flops(w) if w.bwd else 0.0)
-    known = {n: v for n, v in kt.items() if kernel_work(n, w) is not None}
-    dom = max(known.items(), key=lambda kv: kv[1][1])[0] if known else None
-    roof = None
-    if dom is not None:
-        fl, fl_exec, by, bound = kernel_work(dom, w)
-        avg_ms = kt[dom][1] / kt[dom][0]
+
+    def kernel_roof(name, wk, avg_ms, workload_key):
+        fl, fl_exec, by, bound = kernel_work(name, wk)
         if bound == "mfma" and by / (PEAK_HBM_GBS * 1e9) > fl / (PEAK_BF16_TFLOPS * 1e12):
             # the matrix-core kernel's algorithmic intensity is below the ridge
             # point: its roofline ceiling is the HBM roof
@@ -256,30 +298,77 @@ def main(argv=None) -> int:
             ach, peak, unit = by / (avg_ms * 1e-3) / 1e9, PEAK_HBM_GBS, "GB/s"
         else:  # plain fp32 vector arithmetic: fp32 vector peak
             ach, peak, unit = fl / (avg_ms * 1e-3) / 1e12, 157.3, "TFLOP/s"
-        roof = {"kernel": dom, "bound": bound, "achieved": ach, "peak": peak, "unit": unit,
-                "frac": ach / peak, "traffic": measured_traffic(dom, args.workload),
+        return {"kernel": name, "bound": bound, "achieved": ach, "peak": peak, "unit": unit,
+                "frac": ach / peak, "traffic": measured_traffic(name, workload_key),
                 "avg_ms": avg_ms,
                 "algorithmic_flops_per_launch": fl, "algorithmic_bytes_per_launch": by,
                 "executed_mfma_tflops": fl_exec / (avg_ms * 1e-3) / 1e12 if fl_exec else None,
                 "algorithmic_intensity_flop_per_byte": fl / by,
                 "mfma_frac": fl / (avg_ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS}
 
+    known = {n: v for n, v in kt.items() if kernel_work(n, w) is not None}
+    kernel_roofline = {n: kernel_roof(n, w, tot / c, args.workload) for n, (c, tot) in known.items()}
+    dom = max(known.items(), key=lambda kv: kv[1][1])[0] if known else None
+    roof = kernel_roofline[dom] if dom is not None else None
+
+    # the forward of the other paper-shaped batches: the 2048-token fp32 case
+    # (time only), the 16 x 10K batch with its K and V rotated through copies that
+    # together exceed the 256 MB Infinity Cache (so every call reads HBM), and the
+    # 64 x 100K batch
+    configs = None
+    if not args.no_configs and args.workload == "c5":
+        configs = {}
+        for key in ("c1", "c2", "c4"):
+            wc = wl.config(WORKLOADS[key])
+            dc = wl.device_tensors(wc, "cuda")
+            cc = sa.SA_BF16 if wc.dtype == "bf16" else sa.SA_FP32
+            skc = torch.empty((wc.B, wc.H, wc.M, wc.d), dtype=torch.float32, device="cuda")
+            lsc = torch.empty((wc.T, wc.H), dtype=torch.float32, device="cuda")
+            wsc = torch.empty(max(sa.fwd_workspace_size(wc.B, wc.T, wc.H, wc.M, wc.d, cc), 1),
+                              dtype=torch.uint8, device="cuda")
+            kv_bytes = 2 * dc["K"].numel() * dc["K"].element_size()
+            n_copies = int(math.ceil(512e6 / kv_bytes)) + 1 if key == "c2" else 1
+            copies = [(dc["K"], dc["V"])] + [(dc["K"].clone(), dc["V"].clone()) for _ in range(n_copies - 1)]
+            it = [0]
+
+            def fc():
+                Kc, Vc = copies[it[0] % n_copies]
+                it[0] += 1
+                sa.sketch_fwd(Kc, Vc, dc["P"], dc["offsets"], wc.scale, sketch=skc, lse=lsc, workspace=wsc)
+            reps = 5 if key == "c4" else args.steps
+            for _ in range(max(args.warmup, n_copies)):
+                fc()
+            ms = plain_loop(fc, reps)
+            sa.kernel_times()
+            sa.profile_enable(True)
+            plain_loop(fc, reps)
+            sa.profile_enable(False)
+            kc = sa.kernel_times()
+            main_k = "fused_fwd" if "fused_fwd" in kc else "plain_fwd"
+            entry = {"workload": wc.name, "T": wc.T, "ms": ms, "tokens_per_s": wc.T / (ms * 1e-3),
+                     "reps": reps,
+                     "kernels": {n: {"launches": c, "avg_ms": tot / c} for n, (c, tot) in kc.items()}}
+            if key == "c2":
+                entry["input_copies"] = n_copies
+                entry["input_copy_bytes"] = kv_bytes
+            if key != "c1" and main_k in kc:
+                entry["roofline"] = kernel_roof(main_k, wc, kc[main_k][1] / kc[main_k][0], key)
+                entry["mfma_util"] = fwd_algorithmic_flops(wc) / (ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS
+            configs[key] = entry
+            del dc, copies, skc, lsc, wsc
+            torch.cuda.empty_cache()
+
     def timed(fn):
-        """ms per call of fn over the timed steps, and the library's per-kernel times."""
+        """ms per call of fn over the timed steps (no per-launch events), and the
+        library's per-kernel times from a second pass."""
         for _ in range(args.warmup):
             fn()
-        torch.cuda.synchronize()
+        ms = plain_loop(fn, args.steps)
         sa.kernel_times()
         sa.profile_enable(True)
-        t0 = torch.cuda.Event(enable_timing=True)
-        t1 = torch.cuda.Event(enable_timing=True)
-        t0.record(stream)
-        for _ in range(args.steps):
-            fn()
-        t1.record(stream)
-        torch.cuda.synchronize()
+        plain_loop(fn, args.steps)
         sa.profile_enable(False)
-        return t0.elapsed_time(t1) / args.steps, sa.kernel_times()
+        return ms, sa.kernel_times()
 
     def kernel_dict(kd):
         return {n: {"launches": c, "avg_ms": tot / c} for n, (c, tot) in kd.items()}
@@ -420,7 +509,10 @@ def main(argv=None) -> int:
                           if fwd_ms > 0 else None),
         "wall_s_timed": wall,
         "kernels": kernels,
+        "kernels_note": "per-launch HIP events, from a separate pass of the same steps",
         "roofline": roof,
+        "kernel_roofline": kernel_roofline,
+        "configs": configs,
         "tokenwise_fwd": tokenwise,
         "layer": layer,
         "block_fwd": block,

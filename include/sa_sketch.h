@@ -277,6 +277,26 @@ sa_status sa_block_fwd(const void* X, const void* P, const void* Wq, const void*
 size_t sa_block_saved_size(int64_t B, int64_t T, int32_t H, int32_t M, int32_t d, int32_t n_layers,
                            sa_dtype dtype);
 
+/* Intermediates that a training forward keeps in `saved`, for inspection by
+ * the caller (the backward reads them itself).  Layer l's block of `saved`
+ * holds, each at its own offset:
+ *   SA_SAVED_STATE  [B,H,M,d] fp32   the layer's query state Xt (l >= 1 only;
+ *                                    the first layer's state is P itself)
+ *   SA_SAVED_Q      [B,H,M,d] fp32   Q = Xt W_Q  ([H,M,d] used for l = 0)
+ *   SA_SAVED_PP     [B,H,M,d] dtype  P' = Q W_K^T as the sketch's prototypes
+ *                                    (bf16: rounded once from fp32; [H,M,d] used
+ *                                    for l = 0)
+ *   SA_SAVED_LSE    [T,H] fp32       the layer's per-token log-sum-exp
+ */
+typedef enum { SA_SAVED_STATE = 0, SA_SAVED_Q = 1, SA_SAVED_PP = 2, SA_SAVED_LSE = 3 } sa_saved_item;
+
+/* Byte offset of intermediate `item` of layer `layer` inside a `saved` buffer
+ * of this shape (sa_block_saved_size bytes for n_layers layers); (size_t)-1 for
+ * invalid sizes, a layer outside [0, n_layers), an unknown item, or the state of
+ * layer 0. */
+size_t sa_block_saved_offset(int64_t B, int64_t T, int32_t H, int32_t M, int32_t d, int32_t n_layers,
+                             sa_dtype dtype, int32_t layer, int32_t item);
+
 /* Bytes of workspace that sa_block_bwd needs for this shape; with_saved != 0
  * when it will be given a saved buffer (then the replay's region is left out). */
 size_t sa_block_bwd_workspace_size(int64_t B, int64_t T, int32_t H, int32_t M, int32_t d,

@@ -717,7 +717,7 @@ sa_status run_bwd(const void* K, const void* V, const void* P, const int64_t* of
         f.p_user = p_user;
         f.dx_add = dx_add;
         {
-            sa::ProfScope ps("worklist", stream);
+            sa::ProfScope ps("bwd_worklist", stream);
             e = sa::launch_worklist(offsets, B, T, H, plan.C, plan.n_ranges,
                                     const_cast<int32_t*>(f.items), plan.max_items,
                                     const_cast<int32_t*>(f.wg_start),
@@ -1038,6 +1038,22 @@ size_t sa_block_saved_size(int64_t B, int64_t T, int32_t H, int32_t M, int32_t d
                            sa_dtype dtype) {
     if (check_common(B, T, H, M, d, 1.0f, dtype) != SA_OK || n_layers < 1) return 0;
     return saved_layout(B, T, H, M, d, dtype).l_stride * (size_t)n_layers;
+}
+
+size_t sa_block_saved_offset(int64_t B, int64_t T, int32_t H, int32_t M, int32_t d, int32_t n_layers,
+                             sa_dtype dtype, int32_t layer, int32_t item) {
+    const size_t bad = ~(size_t)0;
+    if (check_common(B, T, H, M, d, 1.0f, dtype) != SA_OK || n_layers < 1 || layer < 0 || layer >= n_layers)
+        return bad;
+    const BlockSaved s = saved_layout(B, T, H, M, d, dtype);
+    const size_t base = s.l_stride * (size_t)layer;
+    switch (item) {
+        case SA_SAVED_STATE: return layer == 0 ? bad : base + s.l_state;
+        case SA_SAVED_Q: return base + s.l_q;
+        case SA_SAVED_PP: return base + s.l_pp;
+        case SA_SAVED_LSE: return base + s.l_lse;
+        default: return bad;
+    }
 }
 
 sa_status sa_block_fwd(const void* X, const void* P, const void* Wq, const void* Wk, const void* ln,

@@ -576,9 +576,8 @@ hipError_t occ_inst(int* blocks) {
 
 }  // namespace
 
-// Instances (d, prototypes per wave, waves): M = MW * NW.  Eight waves (two per
-// SIMD) hide the LDS latency of one wave behind the matrix work of the other
-// when the per-wave share of the accumulator allows it.
+// Instances (d, prototypes per wave, waves): M = MW * NW, four waves (one per
+// SIMD), each holding its MW x d share of the fp32 accumulator in registers.
 #define SA_FUSED_CASES(X)  \
     X(64, 32, 4)           \
     X(64, 64, 4)           \

@@ -25,7 +25,8 @@ EXPORTS = ("sa_sketch_fwd_workspace_size", "sa_sketch_fwd", "sa_sketch_bwd_works
            "sa_sketch_fwd_tokenwise_workspace_size", "sa_sketch_fwd_tokenwise",
            "sa_layer_fwd_workspace_size", "sa_layer_fwd", "sa_layer_bwd_workspace_size",
            "sa_layer_bwd", "sa_block_fwd_workspace_size", "sa_block_fwd",
-           "sa_block_saved_size", "sa_block_bwd_workspace_size", "sa_block_bwd", "sa_stca_fwd_workspace_size", "sa_stca_fwd",
+           "sa_block_saved_size", "sa_block_saved_offset", "sa_block_bwd_workspace_size", "sa_block_bwd",
+           "sa_stca_fwd_workspace_size", "sa_stca_fwd",
            "sa_stca_bwd_workspace_size", "sa_stca_bwd",
            "sa_profile_enable", "sa_kernel_times", "sa_status_string", "sa_last_error")
 
@@ -84,6 +85,8 @@ def lib() -> ctypes.CDLL:
     L.sa_block_fwd.restype = c.c_int
     L.sa_block_saved_size.argtypes = [i64, i64, i32, i32, i32, i32, c.c_int]
     L.sa_block_saved_size.restype = sz
+    L.sa_block_saved_offset.argtypes = [i64, i64, i32, i32, i32, i32, c.c_int, i32, i32]
+    L.sa_block_saved_offset.restype = sz
     L.sa_block_bwd_workspace_size.argtypes = [i64, i64, i32, i32, i32, i32, c.c_int, i32]
     L.sa_block_bwd_workspace_size.restype = sz
     L.sa_block_bwd.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp, vp, i64, i64, i32, i32, i32, i32, f32, f32,
@@ -349,6 +352,39 @@ def block_saved_buffer(X, P, Wq, offsets):
     T, H, d = X.shape
     n = block_saved_size(offsets.shape[0] - 1, T, H, P.shape[1], d, Wq.shape[0], _dtype_code(X))
     return torch.empty(max(n, 1), dtype=torch.uint8, device=X.device)
+
+
+SAVED_ITEMS = {"state": 0, "Q": 1, "Pp": 2, "lse": 3}
+
+
+def block_saved_views(saved, B, T, H, M, d, n_layers, dtype_code) -> list:
+    """Views of the intermediates that a training block_fwd kept in `saved`, one
+    dict per layer: "Q" and "Pp" [B,H,M,d] (fp32, and the input dtype for P'),
+    "lse" [T,H], and "state" [B,H,M,d] for layers after the first.  The first
+    layer's Q and P' are [H,M,d] (the shared prototypes' queries)."""
+    import torch
+    out = []
+    el_dt = torch.bfloat16 if dtype_code == SA_BF16 else torch.float32
+    for l in range(n_layers):
+        views = {}
+        for name, item in SAVED_ITEMS.items():
+            off = int(lib().sa_block_saved_offset(B, T, H, M, d, n_layers, dtype_code, l, item))
+            if off == (1 << 64) - 1:
+                continue
+            rows = (H * M if l == 0 else B * H * M) if name in ("Q", "Pp") else None
+            dt = el_dt if name == "Pp" else torch.float32
+            n = T * H if name == "lse" else (rows if rows is not None else B * H * M) * d
+            nbytes = n * (2 if dt == torch.bfloat16 else 4)
+            v = saved[off:off + nbytes].view(dt)
+            if name == "lse":
+                v = v.view(T, H)
+            elif l == 0:
+                v = v.view(H, M, d)
+            else:
+                v = v.view(B, H, M, d)
+            views[name] = v
+        out.append(views)
+    return out
 
 
 def _saved_arg(saved, nbytes):

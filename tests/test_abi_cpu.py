@@ -235,3 +235,28 @@ def test_stca_rejects_bad_arguments():
     assert bwd(B=0) == 1 and bwd(D=100, h=3) == 1
     assert bwd() == 3
     assert sa.stca_bwd_workspace_size(2, 4, 64, 128, 2, 0) > sa.stca_fwd_workspace_size(2, 4, 64, 128, 2, 0) > 0
+
+
+def test_block_saved_offsets():
+    """Offsets of the saved intermediates: inside the buffer, 256-byte aligned,
+    per layer at a fixed stride; invalid requests give (size_t)-1."""
+    L = sa.lib()
+    B, T, H, M, d, n = 3, 700, 2, 128, 64, 2
+    bad = (1 << 64) - 1
+    total = L.sa_block_saved_size(B, T, H, M, d, n, sa.SA_BF16)
+    offs = {}
+    for l in range(n):
+        for item in range(4):
+            o = L.sa_block_saved_offset(B, T, H, M, d, n, sa.SA_BF16, l, item)
+            if l == 0 and item == 0:
+                assert o == bad
+                continue
+            assert o % 256 == 0 and o < total
+            offs[l, item] = o
+    stride = total // n
+    for item in range(1, 4):
+        assert offs[1, item] - offs[0, item] == stride
+    assert offs[0, 2] - offs[0, 1] >= 4 * B * H * M * d       # Q (fp32) before P'
+    assert offs[0, 3] - offs[0, 2] >= 2 * B * H * M * d       # P' (bf16) before lse
+    for args in ((n, sa.SA_BF16, n, 1), (n, sa.SA_BF16, -1, 1), (n, sa.SA_BF16, 0, 4), (0, sa.SA_BF16, 0, 1)):
+        assert L.sa_block_saved_offset(B, T, H, M, d, *args) == bad

@@ -4,20 +4,24 @@ current state as queries, residual + LN, SwiGLU FFN + residual + LN; section
 
 Output tolerance: normwise max relative error per (user, head) slice <= 2e-2
 (bf16) / 1e-4 (fp32), as for the other paths.  The first layer's lse keeps the
-sketching step's absolute bounds (1e-3 bf16, 1e-5 fp32).  Later layers' logits
-come from per-user queries computed from the refined state and rounded to
-bf16 once (P' = state W_Q W_K^T, rows of unit-variance entries after the norm).
-A relative rounding of at most 2^-9 per entry of P' moves a logit
-scale * sum_j X_j P'_j by a sum of d independent terms, with standard deviation
-about 2^-9 / sqrt(3) * scale * sqrt(sum_j X_j^2 P'_j^2) ~ 1.1e-3 for unit-scale
-X and P'; the lse moves by a weighted mean of its logits' errors, so no more.
-The bound 1e-2 in bf16 is about nine of those standard deviations, which
-covers the largest of the ~10^6 token-head values of a full batch with the
-state's own error on top; 1e-4 in fp32.
+sketching step's absolute bounds (1e-3 bf16, 1e-5 fp32).
+
+A later layer's logits use per-user prototypes P' = state W_Q W_K^T computed on
+the device from the device's own state (and rounded once to bf16 in bf16
+mode), so its lse carries two errors, checked separately:
+* the sketching step itself: the kernel's lse against the fp64 oracle fed the
+  device's own P' (read back from the training forward's saved buffer) must
+  meet the first layer's bound;
+* the error of P' (the state's error from the earlier layers, plus the bf16
+  rounding of P'): changing the prototypes by dP'_m moves lse_t by
+  sum_m A_tm scale <X_t, dP'_m>, a weighted mean, so by at most
+  scale |X_t| max_m |dP'_m| (Cauchy-Schwarz).  The oracle fed the device's P'
+  and the oracle's own block must differ by no more than that, token by token.
 """
 import numpy as np
 import pytest
 
+from block_lse_check import later_layer_lse
 from oracle import block as oblock
 from paper_2609_08443_amd import workloads as wl
 
@@ -26,7 +30,6 @@ pytestmark = pytest.mark.gpu
 
 TOL = {"bf16": 2e-2, "fp32": 1e-4}
 LSE0 = {"bf16": 1e-3, "fp32": 1e-5}
-LSE1 = {"bf16": 1e-2, "fp32": 1e-4}
 
 
 @pytest.fixture(scope="module")
@@ -55,21 +58,26 @@ def run(sa, lengths, H, M, d, L, dtype, seed):
     del host["K"]
     dev = wl.to_device(host, dtype)
     print(f"block case lengths={lengths} H={H} M={M} d={d} L={L} {dtype}", flush=True)
+    saved = sa.block_saved_buffer(dev["X"], dev["P"], dev["Wq"], dev["offsets"])
     out, lse = sa.block_fwd(dev["X"], dev["P"], *[dev[k] for k in NAMES], dev["offsets"], w.scale,
-                            want_lse=True)
+                            want_lse=True, saved=saved)
     torch.cuda.synchronize()
+    code = sa.SA_BF16 if dtype == "bf16" else sa.SA_FP32
+    views = sa.block_saved_views(saved, w.B, w.T, H, M, d, L, code)
+    Pp = [None] + [views[l]["Pp"].float().cpu().numpy() for l in range(1, L)]
     ref, rlse = oblock.block_fwd(host["X"], host["P"], *[host[k] for k in NAMES], host["offsets"],
                                  scale=w.scale)
-    return w, out.cpu().numpy(), lse.cpu().numpy(), ref, rlse
+    return w, out.cpu().numpy(), lse.cpu().numpy(), ref, rlse, (host, Pp)
 
 
-def check(w, out, lse, ref, rlse, dtype):
+def check(w, out, lse, ref, rlse, extra, dtype):
     e = normwise(out, ref, (2, 3))
     assert np.all(e <= TOL[dtype]), ("out", e.max())
     if w.T:
         assert np.abs(lse[0] - rlse[0]).max() <= LSE0[dtype], ("lse0", np.abs(lse[0] - rlse[0]).max())
-        for l in range(1, lse.shape[0]):
-            assert np.abs(lse[l] - rlse[l]).max() <= LSE1[dtype], ("lse", l, np.abs(lse[l] - rlse[l]).max())
+        host, Pp = extra
+        later_layer_lse(w.scale, host["X"], host["P"], [host[k] for k in NAMES], host["offsets"], Pp, lse, rlse,
+                        LSE0[dtype], TOL[dtype])
 
 
 FUSED = [
@@ -99,10 +107,10 @@ def test_block_plain_matches_oracle(sa, lengths, H, M, d, L, dtype):
 
 def test_block_empty_users_and_determinism(sa):
     # users without tokens get the refinement of the prototypes alone: equal rows
-    w, out, lse, ref, rlse = run(sa, [0, 120, 0], 2, 128, 64, 2, "bf16", seed=31)
+    w, out, lse, ref, rlse, extra = run(sa, [0, 120, 0], 2, 128, 64, 2, "bf16", seed=31)
     np.testing.assert_array_equal(out[0], out[2])
-    check(w, out, lse, ref, rlse, "bf16")
-    _, out2, lse2, _, _ = run(sa, [0, 120, 0], 2, 128, 64, 2, "bf16", seed=31)
+    check(w, out, lse, ref, rlse, extra, "bf16")
+    _, out2, lse2, _, _, _ = run(sa, [0, 120, 0], 2, 128, 64, 2, "bf16", seed=31)
     np.testing.assert_array_equal(out, out2)
     np.testing.assert_array_equal(lse, lse2)
 

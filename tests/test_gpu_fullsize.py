@@ -10,6 +10,22 @@ seeded streams as the benchmark), the default fused path, one call per pass.
   tokens and P), and on every (user, head) the mass identity
   sum_m sketch[b,h,m,:] = sum_t V[t,h,:] (the weights of a token sum to one),
   which catches tokens lost, counted twice or leaked across users at full size.
+* config 4's batch trained (forward and backward, one target instance with a
+  seeded N(0,1) upstream gradient; 26 GB of fp32 dK and dV): dK and dV of the
+  first 3000 tokens of the first user and the last 3000 of the last user
+  against the oracle run on those tokens alone (a token's gradients depend
+  only on its own K, V, lse and its user's upstream gradient), and on dP, a
+  sum over all 51M token-heads, two identities that hold for any inputs:
+  sum_m dP[h,m,:] = 0 (the sketch does not change when a common vector is
+  added to every prototype) and <dK, K>_h = <dP, P>_h (the logits are bilinear
+  in K and P).  Both residuals come from the bf16 rounding of dS (relative
+  2^-9 per entry, independent from entry to entry).  sum_m dS_tm is then off
+  zero by about 2^-9/sqrt(3) sqrt(sum_m dS_tm^2), so the rms over j of
+  sum_m dP[h,m,j] is about 2^-9/sqrt(3) = 1.1e-3 of sqrt(M) rms(dP_h).  Each
+  token's q_t = <dK_t, K_t> carries a relative error of the same size, so
+  <dK,K>_h - <dP,P>_h is about 1.1e-3 sqrt(2 sum_t q_t^2) (a sum of independent
+  errors; <dK,K>_h itself, a sum of terms of either sign, can be far smaller
+  than that scale).  Both bounds are 2e-2 of those scales.
 * config 5 (config 3's ragged batch of 32 users with 1K-100K tokens, H=4,
   d=128, M=512, plus the backward with R=4): every sketch, lse, dK, dV and dP
   value against the oracle over the whole batch (about half a minute of host
@@ -101,6 +117,42 @@ def test_config4_sampled_users_and_mass(sa):
                                  dev["P"].float().cpu().numpy(), sub, w.scale)
     check_users(w, off, users, sk.cpu().numpy(), lse.cpu().numpy(), ref_sk,
                 [ref_lse[sub[i]:sub[i + 1]] for i in range(len(users))])
+
+
+def test_config4_backward_sampled_tokens_and_identities(sa):
+    w = wl.config(4)
+    w.R = 1
+    print(f"full-size case {w.name} fwd+bwd T={w.T}", flush=True)
+    dev = wl.device_tensors(w, "cuda", with_dsketch=True)
+    _, lse = sa.sketch_fwd(dev["K"], dev["V"], dev["P"], dev["offsets"], w.scale)
+    dK, dV, dP = sa.sketch_bwd(dev["K"], dev["V"], dev["P"], dev["offsets"], dev["dsketch"], lse, w.scale)
+    torch.cuda.synchronize()
+    off, n = w.offsets, 3000
+    P = dev["P"].float().cpu().numpy()
+    for b, (s, e) in ((0, (int(off[0]), int(off[0]) + n)), (w.B - 1, (int(off[-1]) - n, int(off[-1])))):
+        h = host_view(dev, ("K", "V"), s, e)
+        rK, rV, _ = oracle.bwd(h["K"], h["V"], P, np.array([0, n]), dev["dsketch"][b:b + 1].cpu().numpy(),
+                               w.scale)
+        for name, g, r in (("dK", dK, rK), ("dV", dV, rV)):
+            eb = rel(g[s:e].cpu().numpy(), r, (0, 2))
+            assert np.all(eb <= TOL), (name, b, eb.max())
+    gP = dP.double()
+    colsum = gP.sum(dim=1)                                        # [H, d]
+    rms = gP.pow(2).mean(dim=(1, 2)).sqrt()                       # [H]
+    r1 = (colsum.pow(2).mean(dim=1).sqrt() / (np.sqrt(w.M) * rms)).cpu().numpy()
+    print(f"sum_m dP residual {r1.max():.3g} of sqrt(M) rms(dP)", flush=True)
+    assert np.all(r1 <= 2e-2), ("sum_m dP", r1.max())
+    kk = torch.zeros(w.H, dtype=torch.float64, device="cuda")
+    kk2 = torch.zeros(w.H, dtype=torch.float64, device="cuda")
+    step = 1 << 20
+    for s in range(0, w.T, step):
+        q = (dK[s:s + step].double() * dev["K"][s:s + step].double()).sum(dim=2)   # [tokens, H]
+        kk += q.sum(dim=0)
+        kk2 += q.pow(2).sum(dim=0)
+    pp = (gP * dev["P"].double()).sum(dim=(1, 2))
+    r2 = ((kk - pp).abs() / kk2.sqrt()).cpu().numpy()
+    print(f"<dK,K> - <dP,P>: {r2.max():.3g} of sqrt(sum_t q_t^2)", flush=True)
+    assert np.all(r2 <= 2e-2), ("<dK,K> = <dP,P>", r2.max())
 
 
 def test_config5_full_forward_and_backward(sa):

@@ -64,6 +64,13 @@ FUSED_CASES = [
     ([29, 70, 0, 95], 2, 128, 128),
     ([260, 1], 1, 512, 128),
     ([96, 31, 200], 2, 384, 128),
+    # every other fused instance: d = 64 with 3, 5, 6, 7 prototype tiles per wave,
+    # d = 128 with 2
+    ([45, 0, 97, 3], 2, 384, 64),
+    ([70, 33, 1], 1, 640, 64),
+    ([130, 0, 64], 2, 768, 64),
+    ([99, 1, 40], 1, 896, 64),
+    ([61, 0, 140, 2], 2, 256, 128),
 ]
 
 
@@ -200,6 +207,11 @@ BWD_CASES = [
     ([260, 1], 1, 512, 128, "bf16", 4),
     ([40, 0, 77], 2, 64, 64, "fp32", 3),
     ([33, 64], 2, 64, 128, "bf16", 1),
+    # d = 64 with M a multiple of 512: the dP kernel with two prototype tiles per
+    # wave and its P / dY slices in LDS; an empty user, and users long enough to be
+    # cut into several segments, so dP sums partials of several ranges
+    ([300, 0, 1200, 7], 2, 512, 64, "bf16", 2),
+    ([700, 0, 45, 1500], 2, 1024, 64, "bf16", 4),
 ]
 
 
