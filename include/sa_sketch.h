@@ -113,6 +113,30 @@ sa_status sa_sketch_fwd(const void* K, const void* V, const void* P,
                         float* sketch, float* lse, void* workspace,
                         size_t workspace_bytes, void* stream);
 
+/*
+ * sa_sketch_fwd without a workspace argument and without any allocation, for
+ * callers that cannot allocate device memory: code under HIP graph capture,
+ * tight serving loops, harnesses that forbid hipMalloc.  Same operation,
+ * arguments, kernels, results (bit for bit) and errors as sa_sketch_fwd, with
+ * these differences:
+ *  * the work list, the per-range partial sketches and (plain path, lse = NULL)
+ *    the lse scratch live in a device array of SA_NOALLOC_SCRATCH_BYTES that the
+ *    library holds on every device it runs on until the process ends (looked up
+ *    once per device, on the first call with that device current);
+ *  * a shape whose scratch exceeds that size returns SA_ERR_WORKSPACE (the
+ *    ragged 100K batch at H = 4, d = 128, M = 512 needs about 100 MB and fits);
+ *  * every call on one device shares that device's array: calls that overlap
+ *    in time on one device (other streams, other host threads) race and give
+ *    wrong results.  Calls on one stream are ordered and safe.  Nothing in the
+ *    array needs to start at zero (every kernel writes what it later reads);
+ *  * it records no per-launch timing (sa_profile_enable) and ignores
+ *    SA_DEBUG_VALIDATE (which would synchronise the stream).
+ */
+#define SA_NOALLOC_SCRATCH_BYTES (128u << 20)
+sa_status sa_sketch_fwd_noalloc(const void* K, const void* V, const void* P, const int64_t* offsets,
+                                int64_t B, int64_t T, int32_t H, int32_t M, int32_t d, float scale,
+                                sa_dtype dtype, float* sketch, float* lse, void* stream);
+
 /* Bytes of workspace that sa_sketch_fwd_tokenwise needs for this shape. */
 size_t sa_sketch_fwd_tokenwise_workspace_size(int64_t B, int64_t T, int32_t H,
                                               int32_t M, int32_t d, sa_dtype dtype);

@@ -825,6 +825,71 @@ sa_status sa_sketch_fwd(const void* K, const void* V, const void* P, const int64
                    reinterpret_cast<uint8_t*>(workspace), plan, stream, false);
 }
 
+}  // extern "C"
+
+namespace {
+
+// Scratch space of sa_sketch_fwd_noalloc: one array per device, alive until the
+// process ends.  Host code never passes `scratch` itself to a kernel (on the
+// host the name stands for a host-side shadow, not a device address): each
+// device's address is looked up once, with that device current, and kept.
+__device__ __align__(256) uint8_t scratch[SA_NOALLOC_SCRATCH_BYTES];
+
+std::once_flag g_scratch_once[kMaxDevices];
+void* g_scratch_ptr[kMaxDevices];
+hipError_t g_scratch_err[kMaxDevices];
+
+// device address of this device's scratch array, or null (error in *err)
+uint8_t* device_scratch(hipError_t* err) {
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess || dev < 0 || dev >= kMaxDevices) {
+        *err = e != hipSuccess ? e : hipErrorInvalidDevice;
+        return nullptr;
+    }
+    std::call_once(g_scratch_once[dev], [dev] {
+        void* ptr = nullptr;
+        g_scratch_err[dev] = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+        g_scratch_ptr[dev] = g_scratch_err[dev] == hipSuccess ? ptr : nullptr;
+    });
+    *err = g_scratch_err[dev];
+    return reinterpret_cast<uint8_t*>(g_scratch_ptr[dev]);
+}
+
+}  // namespace
+
+extern "C" {
+
+sa_status sa_sketch_fwd_noalloc(const void* K, const void* V, const void* P, const int64_t* offsets,
+                                int64_t B, int64_t T, int32_t H, int32_t M, int32_t d, float scale,
+                                sa_dtype dtype, float* sketch, float* lse, void* stream_) {
+    g_last_error[0] = 0;
+    sa_status st = check_common(B, T, H, M, d, scale, dtype);
+    if (st != SA_OK) return st;
+    if (B == 0) return SA_OK;
+    if (!offsets || !sketch || !P || (T > 0 && (!K || !V)))
+        return fail(SA_ERR_INVALID_ARG, "null pointer argument");
+    if (!aligned16(K) || !aligned16(V) || !aligned16(P) || !aligned16(sketch) ||
+        !aligned16(lse))
+        return fail(SA_ERR_INVALID_ARG, "K, V, P, sketch and lse must be 16-byte aligned");
+    hipStream_t stream = reinterpret_cast<hipStream_t>(stream_);
+    const FwdPlan plan = plan_fwd(B, T, H, M, d, dtype, lse == nullptr);
+    if (plan.total > (size_t)SA_NOALLOC_SCRATCH_BYTES)
+        return fail(SA_ERR_WORKSPACE,
+                    "this shape needs %zu bytes of scratch; the no-allocation forward holds %zu "
+                    "(use sa_sketch_fwd with a workspace)",
+                    plan.total, (size_t)SA_NOALLOC_SCRATCH_BYTES);
+    hipError_t e = hipSuccess;
+    uint8_t* ws = device_scratch(&e);
+    if (!ws) return hip_fail(e, "looking up the device scratch array");
+    // no per-launch timing events here (creating them is an allocation)
+    const bool prof = g_prof_on;
+    g_prof_on = false;
+    st = run_fwd(K, V, P, offsets, B, T, H, M, d, scale, dtype, sketch, lse, ws, plan, stream, false);
+    g_prof_on = prof;
+    return st;
+}
+
 size_t sa_sketch_fwd_tokenwise_workspace_size(int64_t B, int64_t T, int32_t H, int32_t M,
                                               int32_t d, sa_dtype dtype) {
     if (check_common(B, T, H, M, d, 1.0f, dtype) != SA_OK) return 0;

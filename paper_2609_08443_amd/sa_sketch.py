@@ -20,7 +20,7 @@ _STATUS = {0: "SA_OK", 1: "SA_ERR_INVALID_ARG", 2: "SA_ERR_UNSUPPORTED", 3: "SA_
            4: "SA_ERR_BAD_OFFSETS", 5: "SA_ERR_HIP"}
 ITEM_WORDS = 8
 
-EXPORTS = ("sa_sketch_fwd_workspace_size", "sa_sketch_fwd", "sa_sketch_bwd_workspace_size",
+EXPORTS = ("sa_sketch_fwd_workspace_size", "sa_sketch_fwd", "sa_sketch_fwd_noalloc", "sa_sketch_bwd_workspace_size",
            "sa_sketch_bwd", "sa_build_worklist", "sa_sketch_fwd_chunk_tokens",
            "sa_sketch_fwd_tokenwise_workspace_size", "sa_sketch_fwd_tokenwise",
            "sa_layer_fwd_workspace_size", "sa_layer_fwd", "sa_layer_bwd_workspace_size",
@@ -63,6 +63,8 @@ def lib() -> ctypes.CDLL:
     L.sa_sketch_bwd.argtypes = [vp, vp, vp, vp, i64, i64, i32, i32, i32, f32, c.c_int, vp, i32,
                                 vp, vp, vp, vp, vp, sz, vp]
     L.sa_sketch_bwd.restype = c.c_int
+    L.sa_sketch_fwd_noalloc.argtypes = [vp, vp, vp, vp, i64, i64, i32, i32, i32, f32, c.c_int, vp, vp, vp]
+    L.sa_sketch_fwd_noalloc.restype = c.c_int
     L.sa_sketch_fwd_tokenwise_workspace_size.argtypes = [i64, i64, i32, i32, i32, c.c_int]
     L.sa_sketch_fwd_tokenwise_workspace_size.restype = sz
     L.sa_sketch_fwd_tokenwise.argtypes = [vp, vp, vp, vp, i64, i64, i32, i32, i32, f32, c.c_int,
@@ -199,6 +201,39 @@ def sketch_fwd(K, V, P, offsets, scale: Optional[float] = None, sketch=None, lse
     rc = lib().sa_sketch_fwd(_ptr(K), _ptr(V), _ptr(P), _ptr(offsets), B, T, H, M, d,
                              float(scale), code, _ptr(sketch), _ptr(lse), _ptr(ws), nbytes,
                              _stream_handle(stream))
+    _check(rc)
+    return sketch, lse
+
+
+NOALLOC_SCRATCH_BYTES = 128 << 20
+
+
+def sketch_fwd_noalloc(K, V, P, offsets, scale: Optional[float] = None, sketch=None, lse=None,
+                       want_lse: bool = True, stream=None):
+    """sa_sketch_fwd_noalloc on torch tensors: the library's own device scratch
+    array instead of a workspace.  The caller passes (or this allocates, before the
+    call) the outputs.  Returns (sketch, lse or None)."""
+    import torch
+    T, H, d = K.shape
+    M = P.shape[1]
+    B = offsets.shape[0] - 1
+    dev = K.device
+    code = _dtype_code(K)
+    _require(K, "K", (T, H, d), K.dtype, dev)
+    _require(V, "V", (T, H, d), K.dtype, dev)
+    _require(P, "P", (H, M, d), K.dtype, dev)
+    _require(offsets, "offsets", (B + 1,), torch.int64, dev)
+    if scale is None:
+        scale = 1.0 / math.sqrt(d)
+    if sketch is None:
+        sketch = torch.empty((B, H, M, d), dtype=torch.float32, device=dev)
+    _require(sketch, "sketch", (B, H, M, d), torch.float32, dev)
+    if lse is None and want_lse:
+        lse = torch.empty((T, H), dtype=torch.float32, device=dev)
+    if lse is not None:
+        _require(lse, "lse", (T, H), torch.float32, dev)
+    rc = lib().sa_sketch_fwd_noalloc(_ptr(K), _ptr(V), _ptr(P), _ptr(offsets), B, T, H, M, d,
+                                     float(scale), code, _ptr(sketch), _ptr(lse), _stream_handle(stream))
     _check(rc)
     return sketch, lse
 
