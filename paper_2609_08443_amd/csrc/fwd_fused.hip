@@ -21,25 +21,34 @@
 //
 // Workgroup = 4 waves (one per SIMD); wave w owns prototypes
 // [w*MW, (w+1)*MW) for both GEMMs, so the M x d fp32 accumulator is spread
-// over the four SIMDs' register files.  The per-token sums over the M
-// prototypes are reduced in registers (over the wave's 32x32 tiles), across
-// the 32 lanes of a row (DPP and permlane, no LDS), and across waves through
-// LDS.
+// over the four SIMDs' register files (accumulation registers).  The per-token
+// sums over the M prototypes are reduced in registers (over the wave's 32x32
+// tiles), across the 32 lanes of a row (DPP and permlane, no LDS), and across
+// waves through LDS.
 //
 // Layouts: see tile_ops.h.  S is computed with tokens as rows, so its C layout
 // (lane = prototype, register = token) is directly the A operand of the
 // aggregation acc[m, j] += sum_t E[t, m] V'[t, j], with the k slots in the perm16
 // token order; V' is staged row-major in LDS and read as the matching B operand
 // with the transposing LDS load.  1/z is folded into V' (d values per token
-// instead of M).
+// instead of M).  The shift enters the logits as the initial value of each
+// score chain's accumulator (-c_t / scale per token row), so an exponential
+// costs one multiply.
 //
-// Pipeline per tile i (two workgroup barriers on the common path):
-//   S/exp over the wave's prototype tiles  (K(i) in LDS buffer i%2)
-//   stage K(i+1) into buffer (i+1)%2; per-token partial sums to LDS
+// Software pipeline, iteration j (two workgroup barriers):
+//   prototype tile mt = 0 .. MT-1 of token tile j: its score chain, one matrix
+//     instruction per step, each step also issuing one aggregation instruction
+//     of token tile j-1 (prototype tile mt) and the exponentials of two (d=128)
+//     or four (d=64) rows of prototype tile mt-1 of token tile j, so that the
+//     matrix core and the VALU work side by side
+//   exponentials of the last prototype tile; per-token partial sums to LDS;
+//   stage K(j+1) into the other K buffer
 //   --- barrier ---
-//   z, lse; stage V(i)/z; issue the global loads of tile i+2
+//   z, lse of tile j; stage V(j)/z; issue the global loads of K(j+2), V(j+1)
 //   --- barrier ---
-//   aggregation MFMAs
+// Iteration 0 aggregates zero weights and the last iteration exponentiates a
+// tile of clamped rows past the range (finite, masked out), so every iteration
+// runs the same code.
 #include "sa_internal.h"
 #include "tile_ops.h"
 
@@ -79,33 +88,56 @@ constexpr int kRowMirror = 0x140;
 constexpr int kRowRor4 = 0x124;
 constexpr int kRowRor8 = 0x128;
 
-// One step of a logits chain overlapped with exponentials: one MFMA of the
-// chain that accumulates the next 32x32 logits tile into sn, then two rows of
-// the current tile, e = 2^(s * ks + n), added into their sums and packed to
-// bf16.  The VALU work is independent of the MFMA, so it issues while the
-// matrix core runs.  Each exponential's first use is one instruction after it
-// (the transcendental forwarding gap); sn must not be read for 32 states after
-// the last step of a chain.
-template <bool FIRST>
-__device__ inline void chain_exp_step(f32x16& sn, const bf16x8& k, const bf16x8& b, float s0, float s1,
-                                      float n0, float n1, float ks, float& z0, float& z1, uint32_t& ep) {
-    float t0, t1;
-    if constexpr (FIRST) {
-        asm("s_nop 1\n\tv_mfma_f32_32x32x16_bf16 %[sn], %[k], %[b], 0\n\t"
-            "v_fma_f32 %[t0], %[s0], %[ks], %[n0]\n\tv_fma_f32 %[t1], %[s1], %[ks], %[n1]\n\t"
+// One step of the pipelined tile loop: one matrix instruction of the score
+// chain that accumulates the next 32x32 logits tile into sn (VGPRs), one
+// aggregation instruction acc += e^T v of the previous token tile (accumulation
+// registers) and, with ROWS > 0, ROWS rows of the current logits tile
+// exponentiated, e = 2^(s * ks), added into their sums and packed to bf16.  The
+// VALU work is independent of both matrix instructions, so it issues while the
+// matrix core runs.  Each exponential's first use is at least one instruction
+// after it (the transcendental forwarding gap).  No wait states precede the
+// matrix instructions: their operands are written by LDS loads or by other
+// matrix instructions, and the weights e by the VALU a whole pipeline region
+// or more earlier.
+template <int ROWS>
+__device__ inline void pipe_step(f32x16& sn, const bf16x8& k, const bf16x8& b, f32x16& acc, const bf16x8& e,
+                                 const bf16x8& v, const float* s, float ks, float* z, uint32_t* ep) {
+    if constexpr (ROWS == 0) {
+        asm volatile(
+            "v_mfma_f32_32x32x16_bf16 %[sn], %[k], %[b], %[sn]\n\t"
+            "v_mfma_f32_32x32x16_bf16 %[acc], %[e], %[v], %[acc]"
+            : [sn] "+v"(sn), [acc] "+a"(acc)
+            : [k] "v"(k), [b] "v"(b), [e] "v"(e), [v] "v"(v));
+    } else if constexpr (ROWS == 2) {
+        float t0, t1;
+        asm volatile(
+            "v_mfma_f32_32x32x16_bf16 %[sn], %[k], %[b], %[sn]\n\t"
+            "v_mul_f32 %[t0], %[s0], %[ks]\n\tv_mul_f32 %[t1], %[s1], %[ks]\n\t"
             "v_exp_f32 %[t0], %[t0]\n\tv_exp_f32 %[t1], %[t1]\n\t"
+            "v_mfma_f32_32x32x16_bf16 %[acc], %[e], %[v], %[acc]\n\t"
             "v_add_f32 %[z0], %[z0], %[t0]\n\tv_add_f32 %[z1], %[z1], %[t1]\n\t"
             "v_cvt_pk_bf16_f32 %[ep], %[t0], %[t1]"
-            : [sn] "=&v"(sn), [t0] "=&v"(t0), [t1] "=&v"(t1), [z0] "+v"(z0), [z1] "+v"(z1), [ep] "=&v"(ep)
-            : [k] "v"(k), [b] "v"(b), [s0] "v"(s0), [s1] "v"(s1), [n0] "v"(n0), [n1] "v"(n1), [ks] "v"(ks));
+            : [sn] "+v"(sn), [acc] "+a"(acc), [t0] "=&v"(t0), [t1] "=&v"(t1), [z0] "+v"(z[0]),
+              [z1] "+v"(z[1]), [ep] "=&v"(ep[0])
+            : [k] "v"(k), [b] "v"(b), [e] "v"(e), [v] "v"(v), [s0] "v"(s[0]), [s1] "v"(s[1]), [ks] "v"(ks));
     } else {
-        asm("s_nop 1\n\tv_mfma_f32_32x32x16_bf16 %[sn], %[k], %[b], %[sn]\n\t"
-            "v_fma_f32 %[t0], %[s0], %[ks], %[n0]\n\tv_fma_f32 %[t1], %[s1], %[ks], %[n1]\n\t"
+        static_assert(ROWS == 4, "rows per step");
+        float t0, t1, t2, t3;
+        asm volatile(
+            "v_mfma_f32_32x32x16_bf16 %[sn], %[k], %[b], %[sn]\n\t"
+            "v_mul_f32 %[t0], %[s0], %[ks]\n\tv_mul_f32 %[t1], %[s1], %[ks]\n\t"
+            "v_mul_f32 %[t2], %[s2], %[ks]\n\tv_mul_f32 %[t3], %[s3], %[ks]\n\t"
             "v_exp_f32 %[t0], %[t0]\n\tv_exp_f32 %[t1], %[t1]\n\t"
+            "v_exp_f32 %[t2], %[t2]\n\tv_exp_f32 %[t3], %[t3]\n\t"
+            "v_mfma_f32_32x32x16_bf16 %[acc], %[e], %[v], %[acc]\n\t"
             "v_add_f32 %[z0], %[z0], %[t0]\n\tv_add_f32 %[z1], %[z1], %[t1]\n\t"
-            "v_cvt_pk_bf16_f32 %[ep], %[t0], %[t1]"
-            : [sn] "+v"(sn), [t0] "=&v"(t0), [t1] "=&v"(t1), [z0] "+v"(z0), [z1] "+v"(z1), [ep] "=&v"(ep)
-            : [k] "v"(k), [b] "v"(b), [s0] "v"(s0), [s1] "v"(s1), [n0] "v"(n0), [n1] "v"(n1), [ks] "v"(ks));
+            "v_add_f32 %[z2], %[z2], %[t2]\n\tv_add_f32 %[z3], %[z3], %[t3]\n\t"
+            "v_cvt_pk_bf16_f32 %[ep0], %[t0], %[t1]\n\tv_cvt_pk_bf16_f32 %[ep1], %[t2], %[t3]"
+            : [sn] "+v"(sn), [acc] "+a"(acc), [t0] "=&v"(t0), [t1] "=&v"(t1), [t2] "=&v"(t2), [t3] "=&v"(t3),
+              [z0] "+v"(z[0]), [z1] "+v"(z[1]), [z2] "+v"(z[2]), [z3] "+v"(z[3]), [ep0] "=&v"(ep[0]),
+              [ep1] "=&v"(ep[1])
+            : [k] "v"(k), [b] "v"(b), [e] "v"(e), [v] "v"(v), [s0] "v"(s[0]), [s1] "v"(s[1]), [s2] "v"(s[2]),
+              [s3] "v"(s[3]), [ks] "v"(ks));
     }
 }
 
@@ -186,7 +218,7 @@ struct Cfg {
     static constexpr int OFF_MAX = OFF_SUM + RED_BYTES;  // [NW][32] partial maxima (exact path)
     static constexpr int OFF_SUM2 = OFF_MAX + RED_BYTES; // [NW][32] partial sums (exact path)
     static constexpr int OFF_KN = OFF_SUM2 + RED_BYTES;  // [2][32] token norms
-    static constexpr int OFF_NB = OFF_KN + 2 * 32 * 4;   // [2][32] the tokens' shifts, -c_t log2(e)
+    static constexpr int OFF_NB = OFF_KN + 2 * 32 * 4;   // [2][32] score-chain inits, -c_t / scale
     static constexpr int OFF_PN = OFF_NB + 2 * 32 * 4;   // [NW] prototype norm maxima
     static constexpr int OFF_SH = OFF_PN + 16 * 4;       // [32] exact-path shifts
     static constexpr int LDS = OFF_SH + 32 * 4;
@@ -195,6 +227,9 @@ struct Cfg {
 template <int D, int MW, int NW>
 __global__ __launch_bounds__(NW * 64, 1) void fwd_fused_kernel(FusedFwdArgs a) {
     using C = Cfg<D, MW, NW>;
+    constexpr int MT = C::MT, KS = C::KS, JT = C::JT;
+    constexpr int ROWS = 16 / KS;   // rows of a logits tile exponentiated per pipeline step
+    static_assert(KS == 2 * JT, "one aggregation instruction per score-chain step");
     extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
     uint16_t* Ps = reinterpret_cast<uint16_t*>(smem);
     uint16_t* Kbuf = reinterpret_cast<uint16_t*>(smem + C::OFF_K);
@@ -203,7 +238,7 @@ __global__ __launch_bounds__(NW * 64, 1) void fwd_fused_kernel(FusedFwdArgs a) {
     float* red_max = reinterpret_cast<float*>(smem + C::OFF_MAX);
     float* red_sum2 = reinterpret_cast<float*>(smem + C::OFF_SUM2);
     float* knorm = reinterpret_cast<float*>(smem + C::OFF_KN);
-    float* kshift = reinterpret_cast<float*>(smem + C::OFF_NB);
+    float* kinit = reinterpret_cast<float*>(smem + C::OFF_NB);
     float* pnorm = reinterpret_cast<float*>(smem + C::OFF_PN);
     float* shift_s = reinterpret_cast<float*>(smem + C::OFF_SH);
 
@@ -231,7 +266,8 @@ __global__ __launch_bounds__(NW * 64, 1) void fwd_fused_kernel(FusedFwdArgs a) {
         const int t0 = it[IT_T0];
         const int t1 = it[IT_T1];
         const int split = it[IT_SPLIT];
-        if (b < 0 || b >= a.B || h < 0 || h >= a.H || t0 < 0 || t1 < t0 || t1 > a.T) continue;
+        // (segments of the work list are never empty)
+        if (b < 0 || b >= a.B || h < 0 || h >= a.H || t0 < 0 || t1 <= t0 || t1 > a.T) continue;
 
         // ---- prototypes of head h into LDS, with max_m |P_m|
         const int64_t pkey = a.p_user ? (int64_t)b * a.H + h : h;
@@ -254,193 +290,235 @@ __global__ __launch_bounds__(NW * 64, 1) void fwd_fused_kernel(FusedFwdArgs a) {
             pmax = __builtin_sqrtf(m2);
             cur_p = pkey;
         }
-        // shift bound of token t = cb * |K_t|
-        const float cb = a.scale * pmax * kBoundMargin;
+        // shift of token t: c_t = cb |K_t| >= max_m scale <K_t, P_m>; the score
+        // chains start from -c_t / scale = -pm |K_t|
+        const float pm = pmax * kBoundMargin;
+        const float cb = a.scale * pm;
 
-        f32x16 acc[C::MT][C::JT];
+        f32x16 acc[MT][JT];
 #pragma unroll
-        for (int mt = 0; mt < C::MT; ++mt)
+        for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
-            for (int jt = 0; jt < C::JT; ++jt)
+            for (int jt = 0; jt < JT; ++jt)
 #pragma unroll
                 for (int r = 0; r < 16; ++r) acc[mt][jt][r] = 0.f;
 
-        // global tile loads into registers: 32-bit per-lane offsets, uniform tile base
-        // K is loaded two tiles ahead of its use and V one tile ahead: both are
-        // issued at the end of a tile, so neither register set is copied
-        // between tiles.  Rows past the end of the range read its last token
-        // when every chunk slot is used (unpredicated loads; their V is zeroed
-        // at staging), else they are zero.
+        // global tile loads into registers: 32-bit per-lane offsets from the
+        // segment's first row.  Rows past the end of the range read its last token
+        // (their V is zeroed at staging), so every load is issued unconditionally,
+        // also for the tiles past the range, and the compiler's waits for one set
+        // of loads never include the next set.
         uint4 kreg[C::NLD], vreg[C::NLD];
+        static_assert(C::LD_CHUNKS % C::THREADS == 0, "every thread loads whole chunks");
+        const int64_t seg_row0 = ((int64_t)t0 * a.H + h) * D;
         auto load_rows = [&](const uint16_t* X, int ts, uint4 (&dst)[C::NLD]) {
-            const uint16_t* Xb = X + ((int64_t)ts * a.H + h) * D;
-            const int last = t1 - 1 - ts;
+            const uint16_t* Xb = X + seg_row0;
 #pragma unroll
             for (int i = 0; i < C::NLD; ++i) {
                 const int idx = tid + i * C::THREADS;
                 const int tok = idx / C::KCH, ch = idx % C::KCH;
-                if constexpr (C::LD_CHUNKS % C::THREADS == 0) {
-                    const uint32_t off = (uint32_t)min(tok, last) * row_stride + (uint32_t)(ch * 8);
-                    dst[i] = *reinterpret_cast<const uint4*>(Xb + off);
-                } else {
-                    uint4 x = make_uint4(0, 0, 0, 0);
-                    if (idx < C::LD_CHUNKS && tok <= last)
-                        x = *reinterpret_cast<const uint4*>(Xb + (uint32_t)tok * row_stride + (uint32_t)(ch * 8));
-                    dst[i] = x;
-                }
+                const int row = min(ts + tok, t1 - 1) - t0;
+                const uint32_t off = (uint32_t)row * row_stride + (uint32_t)(ch * 8);
+                dst[i] = *reinterpret_cast<const uint4*>(Xb + off);
             }
         };
-        // K tile (from kreg) into LDS buffer `buf`, with the token norms
+        // K tile (from kreg) into LDS buffer kb, with the token norms and chain
+        // inits.  Every lane of a row's KCH consecutive lanes computes the row's
+        // norm and stores it (the same value to the same word), so there is no
+        // branch; the chunks' squares are summed in independent pairs.
         auto stage_k = [&](int kb) {
             uint16_t* Kd = Kbuf + kb * (32 * D);
+            float ss[C::NLD];
 #pragma unroll
             for (int i = 0; i < C::NLD; ++i) {
                 int idx = tid + i * C::THREADS;
                 asm volatile("" : "+v"(idx));
-                if (idx < C::LD_CHUNKS) {
-                    const int tok = idx / C::KCH, ch = idx % C::KCH;
-                    *reinterpret_cast<uint4*>(Kd + swz<D>(tok, ch)) = kreg[i];
-                    const float ss = group_sum<C::KCH>(sumsq8(kreg[i]));
-                    if (ch == 0) {
-                        const float kn = __builtin_sqrtf(ss);
-                        knorm[kb * 32 + tok] = kn;
-                        kshift[kb * 32 + tok] = -cb * kLog2e * kn;
-                    }
-                }
+                const int tok = idx / C::KCH, ch = idx % C::KCH;
+                *reinterpret_cast<uint4*>(Kd + swz<D>(tok, ch)) = kreg[i];
+                const uint32_t q[4] = {kreg[i].x, kreg[i].y, kreg[i].z, kreg[i].w};
+                float p0 = bf16_lo(q[0]) * bf16_lo(q[0]), p1 = bf16_hi(q[0]) * bf16_hi(q[0]);
+                float p2 = bf16_lo(q[1]) * bf16_lo(q[1]), p3 = bf16_hi(q[1]) * bf16_hi(q[1]);
+                p0 = __builtin_fmaf(bf16_lo(q[2]), bf16_lo(q[2]), p0);
+                p1 = __builtin_fmaf(bf16_hi(q[2]), bf16_hi(q[2]), p1);
+                p2 = __builtin_fmaf(bf16_lo(q[3]), bf16_lo(q[3]), p2);
+                p3 = __builtin_fmaf(bf16_hi(q[3]), bf16_hi(q[3]), p3);
+                ss[i] = (p0 + p1) + (p2 + p3);
+            }
+#pragma unroll
+            for (int i = 0; i < C::NLD; ++i) ss[i] = group_sum<C::KCH>(ss[i]);
+#pragma unroll
+            for (int i = 0; i < C::NLD; ++i) {
+                const int tok = (tid + i * C::THREADS) / C::KCH;
+                const float kn = __builtin_sqrtf(ss[i]);
+                knorm[kb * 32 + tok] = kn;
+                kinit[kb * 32 + tok] = -pm * kn;
             }
         };
-        // one 32x32 tile of S for this wave's prototype tile mt
-        // one 32x32 tile of S for this wave's prototype tile mt.  The matrix-core
-        // chain is written out so that the tile lands in VGPRs (the exponentials
-        // read it) while the accumulator stays in AGPRs; the compiler does not
-        // model these instructions, so each waits 2 states after any VALU write
-        // of its operands, and the tile is read 32 states after the last one.
         auto read_bp = [&](bf16x8* bp, int mt) {
             const int prow = w * MW + mt * 32 + l32;
 #pragma unroll
-            for (int kk = 0; kk < C::KS; ++kk) bp[kk] = lds_b128(Ps, swz<D>(prow, 2 * kk + hl));
+            for (int kk = 0; kk < KS; ++kk) bp[kk] = lds_b128(Ps, swz<D>(prow, 2 * kk + hl));
         };
+        // one 32x32 logits tile (no shift), written out so that it lands in VGPRs
+        // (exact-maximum path only)
         auto s_chain = [&](const bf16x8* kop, const bf16x8* bp) {
             f32x16 s;
             __builtin_amdgcn_sched_barrier(0);
             asm("s_nop 1\n\tv_mfma_f32_32x32x16_bf16 %0, %1, %2, 0" : "=&v"(s) : "v"(kop[0]), "v"(bp[0]));
 #pragma unroll
-            for (int kk = 1; kk < C::KS; ++kk)
+            for (int kk = 1; kk < KS; ++kk)
                 asm("s_nop 1\n\tv_mfma_f32_32x32x16_bf16 %0, %1, %2, %0" : "+v"(s) : "v"(kop[kk]), "v"(bp[kk]));
             asm volatile("s_nop 15\n\ts_nop 15" : "+v"(s));
             return s;
         };
         auto s_tile = [&](const bf16x8* kop, int mt) {
-            bf16x8 bp[C::KS];
+            bf16x8 bp[KS];
             read_bp(bp, mt);
             return s_chain(kop, bp);
         };
+        // the chain init of a logits tile: -c_t / scale for this lane's 16 rows
+        auto chain_init = [&](int kb) {
+            f32x16 x;
+            const float* src = kinit + kb * 32 + 4 * hl;
+#pragma unroll
+            for (int g = 0; g < 4; ++g) {
+                const float4 q = *reinterpret_cast<const float4*>(src + 8 * g);
+                x[4 * g] = q.x;
+                x[4 * g + 1] = q.y;
+                x[4 * g + 2] = q.z;
+                x[4 * g + 3] = q.w;
+            }
+            return x;
+        };
 
         const int ntiles = (t1 - t0 + 31) / 32;
-        // prologue: tile 0 staged, tile 1 in flight
+        constexpr int NR = 4;   // P operands in flight (a ring, NR chain steps ahead)
+        auto p_op = [&](int q) {   // P operand of chain step q (prototype tile q / KS)
+            return lds_b128(Ps, swz<D>(w * MW + (q / KS) * 32 + l32, 2 * (q % KS) + hl));
+        };
+        // operands of a tile's first chain steps: K as A operands, the ring's
+        // first NR P operands, and the chain init
+        bf16x8 kop[KS], bp[NR];
+        f32x16 sn;
+        auto read_tile_ops = [&](int kb) {
+            const uint16_t* Ks = Kbuf + kb * (32 * D);
+#pragma unroll
+            for (int kk = 0; kk < KS; ++kk) {
+                kop[kk] = lds_b128(Ks, swz<D>(l32, 2 * kk + hl));
+                if (kk < NR) bp[kk] = p_op(kk);
+            }
+            sn = chain_init(kb);
+        };
+
+        // prologue: K(0) staged, K(1) and V(0) in flight, zero weights and V' for
+        // iteration 0's aggregation, tile 0's operands read
         load_rows(a.K, t0, kreg);
-        load_rows(a.V, t0, vreg);
         stage_k(0);
         if (ntiles > 1) load_rows(a.K, t0 + 32, kreg);
+        load_rows(a.V, t0, vreg);
+        bf16x8 eop[MT][2];
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt) eop[mt][0] = eop[mt][1] = __builtin_bit_cast(bf16x8, make_uint4(0, 0, 0, 0));
+#pragma unroll
+        for (int i = 0; i < C::NLD; ++i) {
+            const int idx = tid + i * C::THREADS;
+            *reinterpret_cast<uint4*>(Vt + swz<D>(idx / C::KCH, idx % C::KCH)) = make_uint4(0, 0, 0, 0);
+        }
         __syncthreads();
+        read_tile_ops(0);
 
-        for (int ti = 0; ti < ntiles; ++ti) {
-            const int ts = t0 + ti * 32;
-            const int kb = ti & 1;
-            const uint16_t* Ks = Kbuf + kb * (32 * D);
+        for (int j = 0; j <= ntiles; ++j) {
+            const int ts = t0 + j * 32;   // token tile j (past the range when j == ntiles)
+            const int kb = j & 1;
 
-            // ---- per-row shift: -c_t * log2(e) for this lane's 16 rows, c_t = cb * |K_t|
-            float nb[16];
+            // ---- V'(j-1) as the aggregation's B operands (K(j), the first P
+            // operands and the chain init were read before the last barrier)
+            bf16x8 vop[JT][2];
 #pragma unroll
-            for (int r = 0; r < 16; ++r) nb[r] = kshift[kb * 32 + srow(r, hl)];
-
-            // ---- S tiles, exponentiated as they complete
-            bf16x8 kop[C::KS];
-#pragma unroll
-            for (int kk = 0; kk < C::KS; ++kk) kop[kk] = lds_b128(Ks, swz<D>(l32, 2 * kk + hl));
+            for (int jt = 0; jt < JT; ++jt) {
+                vop[jt][0] = lds_tr_tokens<D>(Vt, lane, jt, 0);
+                vop[jt][1] = lds_tr_tokens<D>(Vt, lane, jt, 1);
+            }
+            f32x16 sp, snx;
             float rsum[16];
-            bf16x8 eop[C::MT][2];
-            bf16x8 bp[C::KS];
-            read_bp(bp, 0);
-            if constexpr (C::KS == 8 && C::MT > 1) {
-                // the chain of prototype tile mt+1 runs on the matrix cores while
-                // the exponentials of tile mt are taken, one MFMA per two rows
 #pragma unroll
-                for (int r = 0; r < 16; ++r) rsum[r] = 0.f;
-                f32x16 s = s_chain(kop, bp);
+            for (int r = 0; r < 16; ++r) rsum[r] = 0.f;
+
+            // ---- prototype tiles: score chain of mt (tile j) + aggregation of mt
+            // (tile j-1) + exponentials of mt-1 (tile j)
 #pragma unroll
-                for (int mt = 0; mt < C::MT; ++mt) {
-                    uint32_t ep[8];
-                    if (mt + 1 < C::MT) {
-                        read_bp(bp, mt + 1);
-                        // the eight operand reads are issued together, not each
-                        // just before its MFMA
-                        __builtin_amdgcn_sched_barrier(0);
-                        f32x16 sn;
-                        chain_exp_step<true>(sn, kop[0], bp[0], s[0], s[1], nb[0], nb[1], ks2, rsum[0], rsum[1], ep[0]);
-#pragma unroll
-                        for (int kk = 1; kk < 8; ++kk)
-                            chain_exp_step<false>(sn, kop[kk], bp[kk], s[2 * kk], s[2 * kk + 1], nb[2 * kk],
-                                                  nb[2 * kk + 1], ks2, rsum[2 * kk], rsum[2 * kk + 1], ep[kk]);
-                        asm volatile("s_nop 15\n\ts_nop 15" : "+v"(sn));
-                        s = sn;
-                    } else {
-#pragma unroll
-                        for (int kk = 0; kk < 8; ++kk) {
-                            const float e0 = __builtin_amdgcn_exp2f(__builtin_fmaf(s[2 * kk], ks2, nb[2 * kk]));
-                            const float e1 = __builtin_amdgcn_exp2f(__builtin_fmaf(s[2 * kk + 1], ks2, nb[2 * kk + 1]));
-                            rsum[2 * kk] += e0;
-                            rsum[2 * kk + 1] += e1;
-                            ep[kk] = pack_bf16x2(e0, e1);
-                        }
-                    }
-                    eop[mt][0] = __builtin_bit_cast(bf16x8, make_uint4(ep[0], ep[1], ep[2], ep[3]));
-                    eop[mt][1] = __builtin_bit_cast(bf16x8, make_uint4(ep[4], ep[5], ep[6], ep[7]));
-                    asm volatile("" : "+v"(eop[mt][0]), "+v"(eop[mt][1]));
+            for (int mt = 0; mt < MT; ++mt) {
+                uint32_t ep[8];
+                if (mt > 0) {
+                    sp = sn;
+                    sn = snx;
+                    // the previous chain's results are read from the first step on
+                    asm volatile("s_nop 4" : "+v"(sp));
                 }
-            } else
 #pragma unroll
-            for (int mt = 0; mt < C::MT; ++mt) {
-                const f32x16 s = s_chain(kop, bp);
-                // the chain has completed: the next prototype tile's operands load
-                // under this tile's exponentials
-                if (mt + 1 < C::MT) read_bp(bp, mt + 1);
+                for (int kk = 0; kk < KS; ++kk) {
+                    __builtin_amdgcn_sched_barrier(0);
+                    const bf16x8& ev = eop[mt][kk & 1];
+                    const bf16x8& vv = vop[kk >> 1][kk & 1];
+                    const int q = mt * KS + kk;
+                    bf16x8& pb = bp[q % NR];
+                    if (mt == 0) {
+                        pipe_step<0>(sn, kop[kk], pb, acc[mt][kk >> 1], ev, vv, nullptr, ks2, nullptr, nullptr);
+                    } else {
+                        float sr[ROWS];
+#pragma unroll
+                        for (int r = 0; r < ROWS; ++r) sr[r] = sp[ROWS * kk + r];
+                        pipe_step<ROWS>(sn, kop[kk], pb, acc[mt][kk >> 1], ev, vv, sr, ks2, rsum + ROWS * kk,
+                                        ep + (ROWS / 2) * kk);
+                    }
+                    if (q + NR < MT * KS) pb = p_op(q + NR);
+                    if (mt + 1 < MT && kk == KS - 3) snx = chain_init(kb);
+                }
+                __builtin_amdgcn_sched_barrier(0);
+                if (mt > 0) {
+                    eop[mt - 1][0] = __builtin_bit_cast(bf16x8, make_uint4(ep[0], ep[1], ep[2], ep[3]));
+                    eop[mt - 1][1] = __builtin_bit_cast(bf16x8, make_uint4(ep[4], ep[5], ep[6], ep[7]));
+                }
+            }
+            // ---- exponentials of the last prototype tile, the per-token partial
+            // sums, and K(j+1) into the other buffer (K(j-1)'s) with its norms: three
+            // independent chains the compiler interleaves
+            asm volatile("s_nop 7" : "+v"(sn));
+            {
                 float e[16];
 #pragma unroll
                 for (int r = 0; r < 16; ++r) {
-                    e[r] = __builtin_amdgcn_exp2f(__builtin_fmaf(s[r], ks2, nb[r]));
-                    rsum[r] = mt == 0 ? e[r] : rsum[r] + e[r];
+                    e[r] = __builtin_amdgcn_exp2f(sn[r] * ks2);
+                    rsum[r] += e[r];
                 }
-                eop[mt][0] = pack8(e);
-                eop[mt][1] = pack8(e + 8);
-                // packed here: left to the compiler, the packing sinks past the
-                // branch below and the fp32 exponentials stay live through it
-                asm volatile("" : "+v"(eop[mt][0]), "+v"(eop[mt][1]));
+                eop[MT - 1][0] = pack8(e);
+                eop[MT - 1][1] = pack8(e + 8);
             }
+            stage_k(kb ^ 1);
             {
                 const float z = half_sum16(rsum, l32);
                 if ((l32 & 1) == 0) red_sum[w * 32 + srow(l32 >> 1, hl)] = z;
             }
-            // ---- next K tile into the other buffer
-            if (ti + 1 < ntiles) stage_k(kb ^ 1);
             __syncthreads();  // B_z
+            // K of tile j+2 (kreg was staged above)
+            if (j + 2 < ntiles) load_rows(a.K, ts + 64, kreg);
 
-            // ---- tile-uniform check that the bound did not underflow any z_t
-            bool exact;
-            {
-                const int tt = lane & 31;
-                float z = 0.f;
+            // ---- per-token sums: lane t of each half holds token t's total
+            const int tt = l32;
+            float zt = 0.f;
 #pragma unroll
-                for (int ww = 0; ww < NW; ++ww) z += red_sum[ww * 32 + tt];
-                exact = __builtin_amdgcn_ballot_w64(z < kUnderflowZ && ts + tt < t1) != 0;
-            }
+            for (int ww = 0; ww < NW; ++ww) zt += red_sum[ww * 32 + tt];
+            const float kn_t = knorm[kb * 32 + tt];
+            // tile-uniform check that the bound did not underflow any z_t
+            const bool exact = __builtin_amdgcn_ballot_w64(zt < kUnderflowZ && ts + tt < t1) != 0;
+            float c_t = cb * kn_t;
             if (exact) {
                 // rare: exact per-token max over the prototypes, then the exponentials
-                // again (rsum holds the running max first; its sums are in LDS)
+                // again (rsum holds the running max first)
 #pragma unroll
                 for (int r = 0; r < 16; ++r) rsum[r] = -INFINITY;
 #pragma unroll
-                for (int mt = 0; mt < C::MT; ++mt) {
+                for (int mt = 0; mt < MT; ++mt) {
                     const f32x16 s = s_tile(kop, mt);
 #pragma unroll
                     for (int r = 0; r < 16; ++r) rsum[r] = fmaxf(rsum[r], s[r]);
@@ -459,13 +537,14 @@ __global__ __launch_bounds__(NW * 64, 1) void fwd_fused_kernel(FusedFwdArgs a) {
                     shift_s[tid] = -mu * ks2;
                 }
                 __syncthreads();
+                float nb[16];
 #pragma unroll
                 for (int r = 0; r < 16; ++r) {
                     nb[r] = shift_s[srow(r, hl)];
                     rsum[r] = 0.f;
                 }
 #pragma unroll
-                for (int mt = 0; mt < C::MT; ++mt) {
+                for (int mt = 0; mt < MT; ++mt) {
                     const f32x16 s = s_tile(kop, mt);
                     float e[16];
 #pragma unroll
@@ -483,55 +562,35 @@ __global__ __launch_bounds__(NW * 64, 1) void fwd_fused_kernel(FusedFwdArgs a) {
                     for (int r = 0; r < 16; ++r) red_sum2[w * 32 + srow(r, hl)] = rsum[r];
                 }
                 __syncthreads();
-            }
-            const float* zsrc = exact ? red_sum2 : red_sum;
-
-            // ---- lse of the tile's tokens: thread tt of wave 0 handles token tt
-            if (tid < 32 && a.lse && ts + tid < t1) {
-                float z = 0.f;
+                zt = 0.f;
 #pragma unroll
-                for (int ww = 0; ww < NW; ++ww) z += zsrc[ww * 32 + tid];
-                float c;
-                if (exact) {
-                    c = -shift_s[tid] / kLog2e;
-                } else {
-                    c = cb * knorm[kb * 32 + tid];
-                }
-                a.lse[(int64_t)(ts + tid) * a.H + h] = c + __logf(z);
+                for (int ww = 0; ww < NW; ++ww) zt += red_sum2[ww * 32 + tt];
+                c_t = -shift_s[tt] / kLog2e;
             }
+            // ---- the next tile's first operands (K(j+1) and its inits are visible)
+            read_tile_ops(kb ^ 1);
 
-            // ---- stage V / z (row-major; the aggregation reads it transposed)
+            // ---- lse: lanes 8w .. 8w+7 of wave w write tokens 8w .. 8w+7
+            static_assert(NW * 8 == 32, "four waves of eight tokens");
+            if ((lane >> 3) == w && a.lse && ts + tt < t1)
+                a.lse[(int64_t)(ts + tt) * a.H + h] = c_t + __logf(zt);
+
+            // ---- stage V / z (row-major; the aggregation reads it transposed).
+            // z >= 2^-64 here (the exact path's z >= 1): the hardware reciprocal
+            // (1 ulp) is as good as a division before the bf16 rounding of V / z.
+            const float inv_t = ts + tt < t1 ? __builtin_amdgcn_rcpf(zt) : 0.0f;
 #pragma unroll
             for (int i = 0; i < C::NLD; ++i) {
                 int idx = tid + i * C::THREADS;
                 asm volatile("" : "+v"(idx));  // addresses built here, not hoisted
-                if (idx < C::LD_CHUNKS) {
-                    const int tok = idx / C::KCH, ch = idx % C::KCH;
-                    float z = 0.f;
-#pragma unroll
-                    for (int ww = 0; ww < NW; ++ww) z += zsrc[ww * 32 + tok];
-                    const float inv = ts + tok < t1 ? 1.0f / z : 0.0f;
-                    *reinterpret_cast<uint4*>(Vt + swz<D>(tok, ch)) = scale8(vreg[i], inv);
-                }
+                const int tok = idx / C::KCH, ch = idx % C::KCH;
+                const float inv = __shfl(inv_t, tok);
+                *reinterpret_cast<uint4*>(Vt + swz<D>(tok, ch)) = scale8(vreg[i], inv);
             }
-            // K of tile i+2 and V of tile i+1 (kreg was staged above, vreg just now)
-            if (ti + 2 < ntiles) load_rows(a.K, ts + 64, kreg);
-            if (ti + 1 < ntiles) load_rows(a.V, ts + 32, vreg);
-            // B_v: V' staged, K(i+1) visible; the loads of tile i+2 stay in flight
-            // (they have the aggregation of this tile and the logits of the next)
+            // V of tile j+1
+            if (j + 1 < ntiles) load_rows(a.V, ts + 32, vreg);
+            // B_v: V' staged, the next tile's operands read; the loads stay in flight
             lds_barrier();
-
-            // ---- acc[m, j] += E^T . V'
-#pragma unroll
-            for (int jt = 0; jt < C::JT; ++jt) {
-                const bf16x8 v0 = lds_tr_tokens<D>(Vt, lane, jt, 0);
-                const bf16x8 v1 = lds_tr_tokens<D>(Vt, lane, jt, 1);
-#pragma unroll
-                for (int mt = 0; mt < C::MT; ++mt) {
-                    acc[mt][jt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(eop[mt][0], v0, acc[mt][jt], 0, 0, 0);
-                    acc[mt][jt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(eop[mt][1], v1, acc[mt][jt], 0, 0, 0);
-                }
-            }
         }
 
         // ---- flush: the whole sketch of the pair, or this segment's partial
@@ -541,9 +600,9 @@ __global__ __launch_bounds__(NW * 64, 1) void fwd_fused_kernel(FusedFwdArgs a) {
         // would stay live in registers through the whole tile loop)
         asm volatile("" : "+v"(lane_off));
 #pragma unroll
-        for (int mt = 0; mt < C::MT; ++mt)
+        for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
-            for (int jt = 0; jt < C::JT; ++jt)
+            for (int jt = 0; jt < JT; ++jt)
 #pragma unroll
                 for (int r = 0; r < 16; ++r) {
                     const uint32_t o = lane_off + (uint32_t)((mt * 32 + 8 * (r >> 2) + (r & 3)) * D + jt * 32);
