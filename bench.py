@@ -48,12 +48,23 @@ METRIC = "history tokens sketched/sec (fwd+bwd step; fwd alone in fwd_tokens_per
 WORKLOADS = {"c1": 1, "c2": 2, "c3": 3, "c4": 4, "c5": 5}
 
 # HBM bytes per launch of the step's kernels on the default workload, from
-# rocprofv3's request counters (TCC_EA0_RDREQ_32B/64B/128B, TCC_EA0_WRREQ/_64B)
+# rocprofv3's request counters (128 RDREQ_128B + 64 RDREQ_64B + 32 RDREQ_32B read,
+# 64 WRREQ_64B + 32 (WRREQ - WRREQ_64B) written; exact on a plain 1 GiB copy),
 # taken with --no-configs --no-variants so that only the step's launches are
 # averaged, keyed by the sha256 of the kernel's source file at the time: a
-# changed kernel reports traffic = null.  Empty until taken on the current
-# sources.
-MEASURED_TRAFFIC: dict = {}
+# changed kernel reports traffic = null.
+# Source: profiles/hbm_bytes_c5_ragged100k_fwd_bwd.md
+MEASURED_TRAFFIC = {
+    "fused_fwd": ("paper_2609_08443_amd/csrc/fwd_fused.hip",
+                  "1fd3bb6c2c0c4a006152acfb7c93a9ee6437cc66083fd46c1ac10f521f6e74db",
+                  1.115e9 + 0.143e9),
+    "bwd_token": ("paper_2609_08443_amd/csrc/bwd_fused.hip",
+                  "57d0367bf7b2a9a5441602519ebfd053502bcd504f2584431bfee195eb7587c3",
+                  1.311e9 + 2.250e9),
+    "bwd_proto": ("paper_2609_08443_amd/csrc/bwd_fused.hip",
+                  "57d0367bf7b2a9a5441602519ebfd053502bcd504f2584431bfee195eb7587c3",
+                  1.219e9 + 0.100e9),
+}
 
 
 def measured_traffic(kernel: str, workload: str):
