@@ -56,7 +56,7 @@ WORKLOADS = {"c1": 1, "c2": 2, "c3": 3, "c4": 4, "c5": 5}
 # Source: profiles/hbm_bytes_c5_ragged100k_fwd_bwd.md
 MEASURED_TRAFFIC = {
     "fused_fwd": ("paper_2609_08443_amd/csrc/fwd_fused.hip",
-                  "1fd3bb6c2c0c4a006152acfb7c93a9ee6437cc66083fd46c1ac10f521f6e74db",
+                  "64de729a0731a9ec24c6ecd9f1a1263cbbbb8b886e9dd98db9de8c9421d1097c",
                   1.115e9 + 0.143e9),
     "bwd_token": ("paper_2609_08443_amd/csrc/bwd_fused.hip",
                   "57d0367bf7b2a9a5441602519ebfd053502bcd504f2584431bfee195eb7587c3",

@@ -49,6 +49,7 @@
 // Iteration 0 aggregates zero weights and the last iteration exponentiates a
 // tile of clamped rows past the range (finite, masked out), so every iteration
 // runs the same code.
+#include "reduce_ops.h"
 #include "sa_internal.h"
 #include "tile_ops.h"
 
@@ -62,31 +63,6 @@ using namespace tile;
 constexpr float kUnderflowZ = 5.421010862427522e-20f;  // 2^-64
 // relative margin on the bound for the rounding of the fp32 norms and logits
 constexpr float kBoundMargin = 1.0f + 1.0f / 1024.0f;
-
-__device__ inline float sumsq8(uint4 v) {
-    const uint32_t w[4] = {v.x, v.y, v.z, v.w};
-    float s = 0.f;
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-        const float a = bf16_lo(w[i]), b = bf16_hi(w[i]);
-        s = __builtin_fmaf(a, a, s);
-        s = __builtin_fmaf(b, b, s);
-    }
-    return s;
-}
-
-// Cross-lane moves without LDS: DPP inside rows of 16 lanes, then
-// v_permlane16_swap between the two rows of each 32-lane half.
-template <int CTRL>
-__device__ inline float dpp(float v) {
-    return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), CTRL, 0xF, 0xF, true));
-}
-constexpr int kQuadXor1 = 0xB1;      // quad_perm [1,0,3,2]
-constexpr int kQuadXor2 = 0x4E;      // quad_perm [2,3,0,1]
-constexpr int kRowHalfMirror = 0x141;
-constexpr int kRowMirror = 0x140;
-constexpr int kRowRor4 = 0x124;
-constexpr int kRowRor8 = 0x128;
 
 // One step of the pipelined tile loop: one matrix instruction of the score
 // chain that accumulates the next 32x32 logits tile into sn (VGPRs), one
@@ -139,62 +115,6 @@ __device__ inline void pipe_step(f32x16& sn, const bf16x8& k, const bf16x8& b, f
             : [k] "v"(k), [b] "v"(b), [e] "v"(e), [v] "v"(v), [s0] "v"(s[0]), [s1] "v"(s[1]), [s2] "v"(s[2]),
               [s3] "v"(s[3]), [ks] "v"(ks));
     }
-}
-
-// reduce across the 32 lanes of each half-wave; every lane gets the result
-__device__ inline float half_max(float v) {
-    v = fmaxf(v, dpp<kQuadXor1>(v));
-    v = fmaxf(v, dpp<kQuadXor2>(v));
-    v = fmaxf(v, dpp<kRowRor4>(v));
-    v = fmaxf(v, dpp<kRowRor8>(v));
-    const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
-    return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
-}
-__device__ inline float half_sum(float v) {
-    v += dpp<kQuadXor1>(v);
-    v += dpp<kQuadXor2>(v);
-    v += dpp<kRowRor4>(v);
-    v += dpp<kRowRor8>(v);
-    const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
-    return __uint_as_float(r[0]) + __uint_as_float(r[1]);
-}
-// sum over aligned groups of G = 8 or 16 consecutive lanes; every lane gets it
-template <int G>
-__device__ inline float group_sum(float v) {
-    v += dpp<kQuadXor1>(v);
-    v += dpp<kQuadXor2>(v);
-    v += dpp<kRowHalfMirror>(v);
-    if constexpr (G == 16) v += dpp<kRowMirror>(v);
-    return v;
-}
-// Sums of 16 values across the 32 lanes of each half-wave, one value kept per
-// lane: the lanes exchange halves of their remaining values at each level
-// (partners l ^ 16, l ^ 8, l ^ 7, l ^ 2, l ^ 1), so 38 instructions do what 16
-// full reductions (96) would.  Afterwards lanes 2 t and 2 t + 1 of the half hold
-// the total of value t.  Every value is summed over the same tree of lanes (the
-// pairings are xor masks), whatever its index.
-__device__ inline float half_sum16(const float (&v)[16], int l32) {
-    float u[8], w[4], x[2];
-#pragma unroll
-    for (int i = 0; i < 8; ++i) {
-        // lanes 0-15 keep value i, lanes 16-31 value i + 8
-        const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(v[i]), __float_as_uint(v[i + 8]), false,
-                                                        false);
-        u[i] = __uint_as_float(r[0]) + __uint_as_float(r[1]);
-    }
-    const bool b3 = (l32 & 8) != 0, b2 = (l32 & 4) != 0, b1 = (l32 & 2) != 0;
-#pragma unroll
-    for (int j = 0; j < 4; ++j) w[j] = (b3 ? u[j + 4] : u[j]) + dpp<kRowRor8>(b3 ? u[j] : u[j + 4]);
-#pragma unroll
-    for (int k = 0; k < 2; ++k) x[k] = (b2 ? w[k + 2] : w[k]) + dpp<kRowHalfMirror>(b2 ? w[k] : w[k + 2]);
-    const float y = (b1 ? x[1] : x[0]) + dpp<kQuadXor2>(b1 ? x[0] : x[1]);
-    return y + dpp<kQuadXor1>(y);
-}
-
-__device__ inline float wave_max(float v) {
-    v = half_max(v);
-    const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
-    return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
 }
 
 template <int D, int MW, int NW>

@@ -112,6 +112,12 @@ __device__ inline void lds_barrier() {
     asm volatile("" ::: "memory");
 }
 
+// Lanes of one wave reading LDS words that other lanes of the same wave wrote
+// just before: the wave's LDS operations execute in program order, so only the
+// compiler has to be kept from moving the reads above the (lane-predicated)
+// writes or forwarding a lane's own stored values past them.
+__device__ inline void wave_lds_order() { asm volatile("" ::: "memory"); }
+
 __device__ inline bf16x8 lds_b128(const uint16_t* base, int off) {
     return __builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4*>(base + off));
 }

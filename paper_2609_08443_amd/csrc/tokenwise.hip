@@ -161,7 +161,7 @@ __global__ __launch_bounds__(NW * 64, 1) void tw_fused_kernel(TwArgs a) {
     // prototype) to the accumulator layout (register r = prototype srow(r, hl))
     auto to_rows = [&](float f, float (&out)[16]) __attribute__((always_inline)) {
         if (hl == 0) rowf[w * 32 + l32] = f;
-        __builtin_amdgcn_wave_barrier();
+        wave_lds_order();
 #pragma unroll
         for (int g = 0; g < 4; ++g) {
             const float4 v = *reinterpret_cast<const float4*>(rowf + w * 32 + 8 * g + 4 * hl);
@@ -170,7 +170,7 @@ __global__ __launch_bounds__(NW * 64, 1) void tw_fused_kernel(TwArgs a) {
             out[4 * g + 2] = v.z;
             out[4 * g + 3] = v.w;
         }
-        __builtin_amdgcn_wave_barrier();
+        wave_lds_order();
     };
 
     for (int64_t k = k0; k < k1; ++k) {

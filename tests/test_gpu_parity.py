@@ -101,9 +101,10 @@ def test_config1_fp32_single_user(sa):
     assert e.max() <= 1e-4
 
 
-def test_fused_split_users_across_ranges(sa):
+@pytest.mark.parametrize("M,d", [(256, 64), (512, 128)])
+def test_fused_split_users_across_ranges(sa, M, d):
     """Users longer than a workgroup range: the split-L merge sums partial sketches."""
-    w = wl.custom([5000, 12, 7000, 0, 2500], 2, 256, 64, "bf16", seed=5)
+    w = wl.custom([5000, 12, 7000, 0, 2500], 2, M, d, "bf16", seed=5)
     host, dev, sk, lse, e = run_case(sa, w)
     C = sa.fwd_chunk_tokens(w.B, w.T, w.H, w.M, w.d, 0)
     assert C < 5000 * 2, "the case must actually split users across ranges"
