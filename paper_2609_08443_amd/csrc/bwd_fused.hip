@@ -241,20 +241,19 @@ __global__ __launch_bounds__(NW * 64, 8 / NW) void bwd_token_kernel(TokArgs a) {
     auto next_of = [&](const Blk& c, Blk& o) -> bool { return advance(c, nx, o); };
 
     // K as B operands (lane (hl, t) holds 8 consecutive j of its token) and the
-    // lane's -lse * log2(e), for block c
+    // lane's lse, for block c.  Lanes past the block's end take its last token
+    // (finite weights in columns that are never stored), so the loads carry no
+    // predicate, and nothing is computed from them here: they stay in flight
+    // until their first use.
     bf16x8 kb[C::KS], vb[C::KS];
-    float nl = 0.f;
+    float lse_t = 0.f;
     auto load_k = [&](const Blk& c) __attribute__((always_inline)) {
-        const int tok = c.tb + 32 * w + l32;
-        const bool tv = tok < c.te;
-        const int64_t row = ((int64_t)(tv ? tok : c.tb) * a.H + c.h) * D;
+        const int tok = min(c.tb + 32 * w + l32, c.te - 1);
+        const int64_t row = ((int64_t)tok * a.H + c.h) * D;
 #pragma unroll
-        for (int kk = 0; kk < C::KS; ++kk) {
-            uint4 x = *reinterpret_cast<const uint4*>(a.K + row + 16 * kk + 8 * hl);
-            if (!tv) x = make_uint4(0, 0, 0, 0);
-            kb[kk] = __builtin_bit_cast(bf16x8, x);
-        }
-        nl = tv ? -a.lse[(int64_t)tok * a.H + c.h] * kLog2e : 0.f;
+        for (int kk = 0; kk < C::KS; ++kk)
+            kb[kk] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4*>(a.K + row + 16 * kk + 8 * hl));
+        lse_t = a.lse[(int64_t)tok * a.H + c.h];
     };
 
     // Prototype block mb of the matrices a sweep reads, straight into LDS buffer
@@ -336,12 +335,21 @@ __global__ __launch_bounds__(NW * 64, 8 / NW) void bwd_token_kernel(TokArgs a) {
     __syncthreads();
 
     // Per block: a stream of 2 nblk stages (sweep 1's prototype blocks, then sweep
-    // 2's) through three LDS buffers; at the block's entry its K and stages 0 and
-    // 1 are resident.
+    // 2's) through three LDS buffers, continued from block to block: the next
+    // block's first two stages are fetched during the last two stages of this one,
+    // so that at the block's entry its K and stages 0 and 1 (buffers ring and
+    // ring + 1) are resident.  The V rows (sweep 1's last stage) and the next
+    // block's K (sweep 2's last stage) are loaded beside a stage's compute too:
+    // each stage ends by waiting for every load it issued.
+    auto inc3 = [](int x) { return x == 2 ? 0 : x + 1; };
+    int ring = 0;
     while (true) {
         const int tb = cur.tb, te = cur.te, h = cur.h;
         const int tok = tb + 32 * w + l32;   // this lane's token (column of S^T)
         const bool tv = tok < te;
+        const float nl = -lse_t * kLog2e;
+        Blk nxt;
+        const bool more = next_of(cur, nxt);
 
         // ---------------- sweep 1: dV^T[j, t] = sum_m dY[m, j] A[t, m]
         // The S^T tile of block mb + 1 is issued before the exponentials of block
@@ -352,9 +360,9 @@ __global__ __launch_bounds__(NW * 64, 8 / NW) void bwd_token_kernel(TokArgs a) {
         for (int jt = 0; jt < C::JT; ++jt)
 #pragma unroll
             for (int r = 0; r < 16; ++r) dvt[jt][r] = 0.f;
-        f32x16 s_next = st_tile(lds);
-        for (int mb = 0, bc = 0; mb < nblk; ++mb, bc = bc == 2 ? 0 : bc + 1) {
-            const int bn = bc == 2 ? 0 : bc + 1, bnn = bn == 2 ? 0 : bn + 1;
+        f32x16 s_next = st_tile(lds + ring * C::BUF);
+        auto s1_stage = [&](int mb, int bc) __attribute__((always_inline)) {
+            const int bn = inc3(bc), bnn = inc3(bn);
             const uint16_t* L = lds + bc * C::BUF;
             if (mb + 2 < nblk) fetch(cur, mb + 2, 0, bnn);
             else fetch(cur, mb + 2 - nblk, 1, bnn);
@@ -376,17 +384,21 @@ __global__ __launch_bounds__(NW * 64, 8 / NW) void bwd_token_kernel(TokArgs a) {
             sched_mfma_ds_valu<2 * C::JT, 1, 0>();
             wait_vmem();   // stage mb + 2 has landed in LDS
             __syncthreads();
-        }
+        };
+        int bc1 = ring;
+        for (int mb = 0; mb + 1 < nblk; ++mb, bc1 = inc3(bc1)) s1_stage(mb, bc1);
+        if constexpr (!XV) {
+            // V of this wave's tokens (for D_t and sweep 2), in flight during the
+            // last stage
+            const int64_t row = ((int64_t)min(tok, te - 1) * a.H + h) * D;
 #pragma unroll
-        for (int kk = 0; kk < C::KS; ++kk) {
-            if constexpr (XV) {
-                vb[kk] = kb[kk];
-            } else {
-                const int64_t row = ((int64_t)(tv ? tok : tb) * a.H + h) * D;
-                uint4 y = *reinterpret_cast<const uint4*>(a.V + row + 16 * kk + 8 * hl);
-                if (!tv) y = make_uint4(0, 0, 0, 0);
-                vb[kk] = __builtin_bit_cast(bf16x8, y);
-            }
+            for (int kk = 0; kk < C::KS; ++kk)
+                vb[kk] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4*>(a.V + row + 16 * kk + 8 * hl));
+        }
+        s1_stage(nblk - 1, bc1);
+        if constexpr (XV) {
+#pragma unroll
+            for (int kk = 0; kk < C::KS; ++kk) vb[kk] = kb[kk];
         }
         // D_t = <V_t, dV_t>.  This lane holds dV[t, j] for j = 32 jt + 8 g + 4 hl + e
         // (e < 4) and V[t, j] for j = 16 kk + 8 hl + 0..7.  Swapping dwords 0-1
@@ -423,7 +435,12 @@ __global__ __launch_bounds__(NW * 64, 8 / NW) void bwd_token_kernel(TokArgs a) {
             for (int r = 0; r < 16; ++r) dkt[jt][r] = XV ? dvt[jt][r] : 0.f;
         const float nl2 = XV ? nl + __log2f(a.scale) : nl;
         // sweep 2's block mb is stage nblk + mb: blocks 0 and 1 are resident
-        const int b0 = nblk % 3;
+        const int b0 = (ring + nblk) % 3;
+        // stage mb + 2 of the stream: this sweep's, or the next block's first two
+        auto fetch2 = [&](int mb, int buf) __attribute__((always_inline)) {
+            if (mb + 2 < nblk) fetch(cur, mb + 2, 1, buf);
+            else if (more) fetch(nxt, mb + 2 - nblk, 0, buf);
+        };
         // Pipelined form: iteration mb runs the elementwise work of block mb
         // beside the S^T MFMAs of block mb + 1, then the dK MFMAs of mb beside
         // the dA MFMAs of mb + 1 (two independent chains).  It holds 16 more
@@ -459,11 +476,12 @@ __global__ __launch_bounds__(NW * 64, 8 / NW) void bwd_token_kernel(TokArgs a) {
         if constexpr (kPipe2) {
             s_next = st_tile(lds + b0 * C::BUF);
             f32x16 da_next = da_tile(lds + b0 * C::BUF);
-            for (int mb = 0, bc = b0; mb < nblk; ++mb, bc = bc == 2 ? 0 : bc + 1) {
-                const int bn = bc == 2 ? 0 : bc + 1, bnn = bn == 2 ? 0 : bn + 1;
+            int bc = b0;
+            for (int mb = 0; mb + 1 < nblk; ++mb, bc = inc3(bc)) {
+                const int bn = inc3(bc), bnn = inc3(bn);
                 const uint16_t* L = lds + bc * C::BUF;
-                if (mb + 2 < nblk) fetch(cur, mb + 2, 1, bnn);
-                const uint16_t* Ln = lds + (mb + 1 < nblk ? bn : bc) * C::BUF;   // last block: unused
+                fetch2(mb, bnn);
+                const uint16_t* Ln = lds + bn * C::BUF;
                 const f32x16 s = s_next, da = da_next;
                 s_next = st_tile(Ln);
                 dk_acc(L, s, da);
@@ -474,34 +492,36 @@ __global__ __launch_bounds__(NW * 64, 8 / NW) void bwd_token_kernel(TokArgs a) {
                 wait_vmem();
                 __syncthreads();
             }
+            // the last block: the next block's K goes out first (this block's S^T
+            // tiles are all done)
+            if (more) load_k(nxt);
+            fetch2(nblk - 1, inc3(inc3(bc)));
+            dk_acc(lds + bc * C::BUF, s_next, da_next);
+            wait_vmem();
+            __syncthreads();
         } else {
-            for (int mb = 0, bc = b0; mb < nblk; ++mb, bc = bc == 2 ? 0 : bc + 1) {
+            auto s2_stage = [&](int mb, int bc, bool last) __attribute__((always_inline)) {
                 const int bnn = bc == 0 ? 2 : bc - 1;   // (bc + 2) % 3
                 const uint16_t* L = lds + bc * C::BUF;
-                if (mb + 2 < nblk) fetch(cur, mb + 2, 1, bnn);
-                const f32x16 da = da_tile(L);
+                fetch2(mb, bnn);
                 const f32x16 s = st_tile(L);
+                // the last block: the next block's K right after its last S^T tile
+                if (last && more) load_k(nxt);
+                const f32x16 da = da_tile(L);
                 dk_acc(L, s, da);
                 wait_vmem();
                 __syncthreads();
-            }
+            };
+            int bc = b0;
+            for (int mb = 0; mb + 1 < nblk; ++mb, bc = inc3(bc)) s2_stage(mb, bc, false);
+            s2_stage(nblk - 1, bc, true);
         }
 
-        // The next block's K and its first two stages go out before this block's
-        // dK rows: the wait for them then includes no store, and the stores drain
-        // under the next block's first stage.
-        Blk nxt;
-        const bool more = next_of(cur, nxt);
-        if (more) {
-            load_k(nxt);
-            fetch(nxt, 0, 0, 0);
-            fetch(nxt, 1, 0, 1);
-            wait_vmem();
-            __syncthreads();
-        }
+        // The dK rows drain under the next block's first stage.
         store_rows(dkt, XV ? a.dX : a.dK, XV ? 1.0f : a.scale, tb, te, h, XV && a.dx_add);
         if (!more) break;
         cur = nxt;
+        ring = (ring + 2 * nblk) % 3;
     }
 }
 
