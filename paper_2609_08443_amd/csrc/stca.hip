@@ -3,7 +3,9 @@
 // its backward.  The products around them run on the batched matrix-core GEMM.
 //
 // Rows are [rows][k] fp32 logits already multiplied by the attention scale.  One
-// wave per row; lanes stride the row so that every access is coalesced.
+// wave per row.  With k a multiple of 4 and at most 1024, a row is read once into
+// registers (16 bytes per lane per 256 columns) and every pass runs on them;
+// otherwise lanes stride the row in each pass.
 #include "sa_internal.h"
 #include "tile_ops.h"
 
@@ -64,6 +66,86 @@ __global__ __launch_bounds__(256) void stca_softmax_bwd_kernel(const float* __re
     for (int j = lane; j < k; j += 64) put<BF16>(ds, row * k + j, scale * __expf(s[j] - l) * (da[j] - dot));
 }
 
+template <int NV>
+__device__ inline void load_row(const float* s, int k, int lane, float4 (&v)[NV]) {
+#pragma unroll
+    for (int i = 0; i < NV; ++i) {
+        const int c = 4 * (lane + 64 * i);
+        v[i] = c < k ? *reinterpret_cast<const float4*>(s + c) : make_float4(-INFINITY, -INFINITY, -INFINITY, -INFINITY);
+    }
+}
+template <bool BF16>
+__device__ inline void put4(void* p, int64_t i, float a, float b, float c, float d) {
+    if constexpr (BF16)
+        *reinterpret_cast<uint2*>(reinterpret_cast<uint16_t*>(p) + i) =
+            make_uint2(tile::pack_bf16x2(a, b), tile::pack_bf16x2(c, d));
+    else
+        *reinterpret_cast<float4*>(reinterpret_cast<float*>(p) + i) = make_float4(a, b, c, d);
+}
+
+// the register-resident forms of the two kernels above (NV 16-byte pieces per lane)
+template <bool BF16, int NV>
+__global__ __launch_bounds__(256) void stca_softmax_reg_kernel(const float* __restrict__ S, int64_t rows, int32_t k,
+                                                               void* __restrict__ alpha, float* __restrict__ lse) {
+    const int64_t row = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+    if (row >= rows) return;
+    const int lane = threadIdx.x & 63;
+    float4 v[NV];
+    load_row<NV>(S + row * k, k, lane, v);
+    float mx = -INFINITY;
+#pragma unroll
+    for (int i = 0; i < NV; ++i) mx = fmaxf(fmaxf(mx, fmaxf(v[i].x, v[i].y)), fmaxf(v[i].z, v[i].w));
+    mx = wave_max(mx);
+    float z = 0.f;
+#pragma unroll
+    for (int i = 0; i < NV; ++i)   // (padding columns hold -inf: exp gives 0)
+        z += (__expf(v[i].x - mx) + __expf(v[i].y - mx)) + (__expf(v[i].z - mx) + __expf(v[i].w - mx));
+    const float l = mx + __logf(wave_sum(z));
+#pragma unroll
+    for (int i = 0; i < NV; ++i) {
+        const int c = 4 * (lane + 64 * i);
+        if (c < k)
+            put4<BF16>(alpha, row * k + c, __expf(v[i].x - l), __expf(v[i].y - l), __expf(v[i].z - l),
+                       __expf(v[i].w - l));
+    }
+    if (lane == 0) lse[row] = l;
+}
+
+template <bool BF16, int NV>
+__global__ __launch_bounds__(256) void stca_softmax_bwd_reg_kernel(const float* __restrict__ S,
+                                                                   const float* __restrict__ lse,
+                                                                   const float* __restrict__ dA, int64_t rows,
+                                                                   int32_t k, float scale, void* __restrict__ ds) {
+    const int64_t row = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+    if (row >= rows) return;
+    const int lane = threadIdx.x & 63;
+    const float l = lse[row];
+    float4 v[NV], g[NV];
+    load_row<NV>(S + row * k, k, lane, v);
+#pragma unroll
+    for (int i = 0; i < NV; ++i) {
+        const int c = 4 * (lane + 64 * i);
+        g[i] = c < k ? *reinterpret_cast<const float4*>(dA + row * k + c) : make_float4(0.f, 0.f, 0.f, 0.f);
+        v[i] = make_float4(__expf(v[i].x - l), __expf(v[i].y - l), __expf(v[i].z - l), __expf(v[i].w - l));
+    }
+    float dot = 0.f;
+#pragma unroll
+    for (int i = 0; i < NV; ++i) {
+        dot = __builtin_fmaf(v[i].x, g[i].x, dot);
+        dot = __builtin_fmaf(v[i].y, g[i].y, dot);
+        dot = __builtin_fmaf(v[i].z, g[i].z, dot);
+        dot = __builtin_fmaf(v[i].w, g[i].w, dot);
+    }
+    dot = wave_sum(dot);
+#pragma unroll
+    for (int i = 0; i < NV; ++i) {
+        const int c = 4 * (lane + 64 * i);
+        if (c < k)
+            put4<BF16>(ds, row * k + c, scale * v[i].x * (g[i].x - dot), scale * v[i].y * (g[i].y - dot),
+                       scale * v[i].z * (g[i].z - dot), scale * v[i].w * (g[i].w - dot));
+    }
+}
+
 __global__ __launch_bounds__(256) void to_bf16_kernel(const float* __restrict__ x, uint16_t* __restrict__ y,
                                                       int64_t n) {
     const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
@@ -72,10 +154,32 @@ __global__ __launch_bounds__(256) void to_bf16_kernel(const float* __restrict__ 
 
 }  // namespace
 
+// pieces per lane of the register-resident kernels, 0 when k does not fit them
+int reg_pieces(int32_t k) {
+    if (k % 4 != 0) return 0;
+    if (k <= 256) return 1;
+    if (k <= 512) return 2;
+    if (k <= 1024) return 4;
+    return 0;
+}
+
 hipError_t launch_stca_softmax(const float* S, int64_t rows, int32_t k, bool bf16, void* alpha, float* lse,
                                hipStream_t stream) {
     if (rows <= 0) return hipSuccess;
     const dim3 grid((unsigned)((rows + 3) / 4));
+    const int nv = reg_pieces(k);
+#define SA_REG(NV)                                                                                              \
+    if (nv == NV) {                                                                                             \
+        if (bf16) hipLaunchKernelGGL((stca_softmax_reg_kernel<true, NV>), grid, dim3(256), 0, stream, S, rows, k, \
+                                     alpha, lse);                                                               \
+        else hipLaunchKernelGGL((stca_softmax_reg_kernel<false, NV>), grid, dim3(256), 0, stream, S, rows, k,     \
+                                alpha, lse);                                                                    \
+        return hipGetLastError();                                                                               \
+    }
+    SA_REG(1)
+    SA_REG(2)
+    SA_REG(4)
+#undef SA_REG
     if (bf16) hipLaunchKernelGGL(stca_softmax_kernel<true>, grid, dim3(256), 0, stream, S, rows, k, alpha, lse);
     else hipLaunchKernelGGL(stca_softmax_kernel<false>, grid, dim3(256), 0, stream, S, rows, k, alpha, lse);
     return hipGetLastError();
@@ -85,6 +189,19 @@ hipError_t launch_stca_softmax_bwd(const float* S, const float* lse, const float
                                    float scale, bool bf16, void* ds, hipStream_t stream) {
     if (rows <= 0) return hipSuccess;
     const dim3 grid((unsigned)((rows + 3) / 4));
+    const int nv = reg_pieces(k);
+#define SA_REG(NV)                                                                                                \
+    if (nv == NV) {                                                                                               \
+        if (bf16) hipLaunchKernelGGL((stca_softmax_bwd_reg_kernel<true, NV>), grid, dim3(256), 0, stream, S, lse, \
+                                     dA, rows, k, scale, ds);                                                     \
+        else hipLaunchKernelGGL((stca_softmax_bwd_reg_kernel<false, NV>), grid, dim3(256), 0, stream, S, lse, dA,  \
+                                rows, k, scale, ds);                                                              \
+        return hipGetLastError();                                                                                 \
+    }
+    SA_REG(1)
+    SA_REG(2)
+    SA_REG(4)
+#undef SA_REG
     if (bf16)
         hipLaunchKernelGGL(stca_softmax_bwd_kernel<true>, grid, dim3(256), 0, stream, S, lse, dA, rows, k, scale, ds);
     else

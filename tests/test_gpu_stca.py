@@ -82,6 +82,7 @@ CASES = [
     (3, 5, 128, 256, 4, "bf16"),     # weight gradients and dXs (k = 15, 20 rows) on the fallback
     (2, 16, 256, 512, 8, "bf16"),
     (2, 8, 100, 128, 2, "bf16"),     # k = 100: partial tiles, aggregation on the fallback
+    (1, 4, 600, 128, 2, "bf16"),     # k = 600: the widest register-resident softmax rows, partly filled
     (2, 3, 50, 64, 2, "fp32"),
     (1, 7, 33, 96, 3, "fp32"),
 ]
