@@ -18,8 +18,11 @@
 //          then dK (second sweep).  Works in the transposed orientation S^T (rows =
 //          prototypes, lanes = tokens) so that the reductions over prototypes are
 //          matrix-core contractions whose k slots are the register index of S^T.
-//          Prototype blocks of 32 are streamed through double-buffered LDS and
-//          shared by the eight waves (each wave owns 32 tokens).
+//          Prototype blocks of 32 are streamed through LDS and shared by the
+//          waves (each wave owns 32 tokens).  For M <= 512 the first sweep's
+//          weights are held in registers for the second (bwd_token_held_kernel,
+//          four waves); otherwise the second sweep recomputes them
+//          (bwd_token_kernel, eight waves).
 //   proto  dP for a slice of the prototypes, in the forward's orientation (lanes =
 //          prototypes): the prototype slice and the user's dY slice stay in LDS
 //          (or in registers with one 32-prototype tile per wave), dS^T . K
@@ -27,6 +30,7 @@
 //          one partial per work-list segment, summed per head in segment order
 //          (deterministic).
 #include <type_traits>
+#include <utility>
 
 #include "sa_internal.h"
 #include "tile_ops.h"
@@ -67,6 +71,168 @@ __device__ inline void sched_ds() {
 __device__ inline float xhalf_sum(float v) {
     const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
     return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+
+// f(integral_constant<int, I>) for I = 0 .. N-1, each I a compile-time constant
+// (so that arrays indexed by it stay in registers)
+template <typename F, int... I>
+__device__ __forceinline__ void static_for_seq(F&& f, std::integer_sequence<int, I...>) {
+    (f(std::integral_constant<int, I>{}), ...);
+}
+template <int N, typename F>
+__device__ __forceinline__ void static_for(F&& f) {
+    static_for_seq(f, std::make_integer_sequence<int, N>{});
+}
+
+// The value moved into accumulator registers: a held matrix-core operand stays
+// there (the matrix core reads either register file) and leaves the vector
+// registers to the working set; VALU uses copy it back when they need it.
+__device__ __forceinline__ bf16x8 to_agpr(bf16x8 v) {
+    u32x4 u = __builtin_bit_cast(u32x4, v), o;
+    asm volatile("" : "=a"(o) : "0"(u));
+    return __builtin_bit_cast(bf16x8, o);
+}
+
+// s_waitcnt for vector memory only: at most N of this wave's vector-memory
+// operations still outstanding (the other counters are not waited for)
+template <int N>
+__device__ __forceinline__ void wait_vm() {
+    static_assert(N >= 0 && N < 64, "vmcnt range");
+    __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | (15 << 8) | ((N >> 4) << 14));
+}
+
+// Token blocks of a token-side workgroup: segment k of the work list (user b,
+// head h, tokens up to t1) and its tokens [tb, te); the blocks of a segment
+// start at its first token.
+struct TokBlk {
+    int64_t k;
+    int b, h, t1, tb, te;
+};
+template <int TB>
+struct TokSeq {
+    const int32_t* items;
+    int64_t k1, T;
+    int B, H;
+    // the first block of the first valid segment at or after k
+    __device__ bool first_from(int64_t k, TokBlk& o) const {
+        // the item list is read through the constant address space, so that
+        // these wave-uniform reads are scalar loads (no vector-memory wait)
+        typedef const __attribute__((address_space(4))) int32_t cint;
+        for (; k < k1; ++k) {
+            cint* it = (cint*)items + k * IT_WORDS;
+            const int b = it[IT_B], h = it[IT_H], t0 = it[IT_T0], t1 = it[IT_T1];
+            if (b < 0 || b >= B || h < 0 || h >= H || t0 < 0 || t1 <= t0 || t1 > T) continue;
+            o.k = k; o.b = b; o.h = h; o.t1 = t1; o.tb = t0;
+            o.te = t0 + TB < t1 ? t0 + TB : t1;
+            return true;
+        }
+        return false;
+    }
+    // the block `steps` blocks after c
+    __device__ bool advance(TokBlk c, int64_t steps, TokBlk& o) const {
+        while (true) {
+            const int64_t left = (c.t1 - c.tb + TB - 1) / TB;   // c and the blocks after it
+            if (steps < left) {
+                o = c;
+                o.tb = c.tb + (int)steps * TB;
+                o.te = o.tb + TB < c.t1 ? o.tb + TB : c.t1;
+                return true;
+            }
+            steps -= left;
+            if (!first_from(c.k + 1, c)) return false;
+        }
+    }
+};
+
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+// A 16-byte LDS store written as inline assembly.  The compiler orders every
+// LDS access it knows of behind all outstanding direct global->LDS loads (it
+// cannot tell their target areas apart), which would drain the prototype-block
+// stream before each row-staging store; callers of this store keep it to an
+// area no direct load writes, and order its later reads with lgkmcnt.
+__device__ __forceinline__ void lds_store16_asm(float* p, f32x4 v) {
+    const uint32_t a = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) float*)p;
+    asm volatile("ds_write_b128 %0, %1" ::"v"(a), "v"(v) : "memory");
+}
+// Four 16-byte LDS loads at p + q * stride bytes (q < 4), in one inline-assembly
+// block that waits for them, for the same reason.
+__device__ __forceinline__ void lds_load16x4_asm(f32x4 (&o)[4], const float* p, int stride) {
+    const uint32_t a = (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) float*)p;
+    asm volatile(
+        "ds_read_b128 %0, %4\n"
+        "ds_read_b128 %1, %4 offset:%5\n"
+        "ds_read_b128 %2, %4 offset:%6\n"
+        "ds_read_b128 %3, %4 offset:%7\n"
+        "s_waitcnt lgkmcnt(0)"
+        : "=&v"(o[0]), "=&v"(o[1]), "=&v"(o[2]), "=&v"(o[3])
+        : "v"(a), "i"(stride), "i"(2 * stride), "i"(3 * stride)
+        : "memory");
+}
+
+// f * acc (a wave's 32 tokens tok0 + 0..31, lane = token, rows j = 32 jt +
+// srow(r, hl)) into the rows of out [T, H, D], only tokens below te.  The C
+// layout holds 16-byte pieces of 32 token rows per store; each 32-column slice
+// goes through the wave's LDS area stg ([32][ROWF] fp32) so that every store
+// instruction writes whole 128-byte lines of 8 tokens.
+template <int D, int ROWF>
+__device__ __forceinline__ void store_token_rows(const f32x16 (&acc)[D / 32], float* stg, float* out, float f,
+                                                 int tok0, int te, int H, int h, bool add, int lane) {
+    const int l32 = lane & 31, hl = lane >> 5;
+#pragma unroll
+    for (int jt = 0; jt < D / 32; ++jt) {
+#pragma unroll
+        for (int g = 0; g < 4; ++g)
+            lds_store16_asm(stg + l32 * ROWF + 8 * g + 4 * hl,
+                            (f32x4){f * acc[jt][4 * g], f * acc[jt][4 * g + 1], f * acc[jt][4 * g + 2],
+                                    f * acc[jt][4 * g + 3]});
+        asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");   // the wave's own area
+        f32x4 rows[4];
+        lds_load16x4_asm(rows, stg + (lane >> 3) * ROWF + 4 * (lane & 7), 8 * ROWF * 4);
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            const int t = 8 * q + (lane >> 3), cc = 4 * (lane & 7);
+            const float4 v = make_float4(rows[q][0], rows[q][1], rows[q][2], rows[q][3]);
+            const int tk = tok0 + t;
+            if (tk < te) {
+                float4* o = reinterpret_cast<float4*>(out + ((int64_t)tk * H + h) * D + jt * 32 + cc);
+                if (add) {
+                    const float4 u = *o;
+                    *o = make_float4(u.x + v.x, u.y + v.y, u.z + v.z, u.w + v.w);
+                } else {
+                    *o = v;
+                }
+            }
+        }
+        asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");   // reads done before the next slice
+    }
+}
+
+// D_t = <V_t, dV_t> for the lane's token.  The lane holds dV[t, j] for j = 32 jt +
+// 8 g + 4 hl + e (e < 4, C layout of dV^T) and V[t, j] for j = 16 kk + 8 hl +
+// 0..7 (B operand layout).  Swapping dwords 0-1 of the upper half with dwords
+// 2-3 of the lower half gives both halves V at j = 16 kk + 4 hl + 0..3 (dwords
+// 0-1) and 16 kk + 8 + 4 hl + 0..3 (dwords 2-3): with kk = 2 jt + g / 2, the
+// columns of dV registers 4 g .. 4 g + 3.  Each half holds half the sum.
+template <int D>
+__device__ __forceinline__ float dot_v_dv(const bf16x8 (&vb)[D / 16], const f32x16 (&dvt)[D / 32]) {
+    float Dt = 0.f;
+#pragma unroll
+    for (int kk = 0; kk < D / 16; ++kk) {
+        const u32x4 v = __builtin_bit_cast(u32x4, vb[kk]);
+        const auto p0 = __builtin_amdgcn_permlane32_swap(v[0], v[2], false, false);
+        const auto p1 = __builtin_amdgcn_permlane32_swap(v[1], v[3], false, false);
+        const uint32_t q[2][2] = {{p0[0], p1[0]}, {p0[1], p1[1]}};
+#pragma unroll
+        for (int sh = 0; sh < 2; ++sh) {
+            const int jt = kk >> 1, g = 2 * (kk & 1) + sh;
+            Dt = __builtin_fmaf(bf16_lo(q[sh][0]), dvt[jt][4 * g + 0], Dt);
+            Dt = __builtin_fmaf(bf16_hi(q[sh][0]), dvt[jt][4 * g + 1], Dt);
+            Dt = __builtin_fmaf(bf16_lo(q[sh][1]), dvt[jt][4 * g + 2], Dt);
+            Dt = __builtin_fmaf(bf16_hi(q[sh][1]), dvt[jt][4 * g + 3], Dt);
+        }
+    }
+    return Dt;
 }
 
 // ------------------------------------------------------------------ prep
@@ -206,39 +372,9 @@ __global__ __launch_bounds__(NW * 64, 8 / NW) void bwd_token_kernel(TokArgs a) {
     const int nblk = a.M / 32;   // >= 4
     const int64_t MD = (int64_t)a.M * D;
 
-    // A token block: segment k of the work list (user b, head h, tokens up to
-    // t1) and its tokens [tb, te); blocks of a segment start at its first token.
-    struct Blk {
-        int64_t k;
-        int b, h, t1, tb, te;
-    };
-    auto first_from = [&](int64_t k, int cut, Blk& o) -> bool {
-        for (; k < k1; ++k) {
-            const int32_t* it = a.items + k * IT_WORDS;
-            const int b = it[IT_B], h = it[IT_H], t0 = it[IT_T0], t1 = it[IT_T1];
-            if (b < 0 || b >= a.B || h < 0 || h >= a.H || t0 < 0 || t1 <= t0 || t1 > a.T) continue;
-            o.k = k; o.b = b; o.h = h; o.t1 = t1; o.tb = t0;
-            o.te = t0 + C::TB - cut < t1 ? t0 + C::TB - cut : t1;
-            return true;
-        }
-        return false;
-    };
-    // the block `steps` blocks after c in the XCD's sequence (blocks start at
-    // their segment's first token)
-    auto advance = [&](Blk c, int64_t steps, Blk& o) -> bool {
-        while (true) {
-            const int64_t left = (c.t1 - c.tb + C::TB - 1) / C::TB;   // c and the blocks after it
-            if (steps < left) {
-                o = c;
-                o.tb = c.tb + (int)steps * C::TB;
-                o.te = o.tb + C::TB < c.t1 ? o.tb + C::TB : c.t1;
-                return true;
-            }
-            steps -= left;
-            if (!first_from(c.k + 1, 0, c)) return false;
-        }
-    };
-    auto next_of = [&](const Blk& c, Blk& o) -> bool { return advance(c, nx, o); };
+    using Blk = TokBlk;
+    const TokSeq<C::TB> seq{a.items, k1, a.T, a.B, a.H};
+    auto next_of = [&](const Blk& c, Blk& o) -> bool { return seq.advance(c, nx, o); };
 
     // K as B operands (lane (hl, t) holds 8 consecutive j of its token) and the
     // lane's lse, for block c.  Lanes past the block's end take its last token
@@ -293,41 +429,13 @@ __global__ __launch_bounds__(NW * 64, 8 / NW) void bwd_token_kernel(TokArgs a) {
             s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(lds_b128(L, swz<D>(l32, 2 * kk + hl)), kb[kk], s, 0, 0, 0);
         return s;
     };
-    // f * acc (this wave's 32 tokens of the block, columns j = 32 jt + srow(r, hl))
-    // into the rows of `out`.  The C layout holds 16-byte pieces of 32 token rows
-    // per store; each 32-column slice goes through this wave's LDS area so that
-    // every store instruction writes whole 128-byte lines of 8 tokens.
     auto store_rows = [&](const f32x16 (&acc)[C::JT], float* out, float f, int tb, int te, int h, bool add)
         __attribute__((always_inline)) {
-#pragma unroll
-        for (int jt = 0; jt < C::JT; ++jt) {
-#pragma unroll
-            for (int g = 0; g < 4; ++g)
-                *reinterpret_cast<float4*>(stg + l32 * C::ROWF + 8 * g + 4 * hl) =
-                    make_float4(f * acc[jt][4 * g], f * acc[jt][4 * g + 1], f * acc[jt][4 * g + 2],
-                                f * acc[jt][4 * g + 3]);
-            asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");   // the wave's own area
-#pragma unroll
-            for (int q = 0; q < 4; ++q) {
-                const int t = 8 * q + (lane >> 3), cc = 4 * (lane & 7);
-                const float4 v = *reinterpret_cast<const float4*>(stg + t * C::ROWF + cc);
-                const int tk = tb + 32 * w + t;
-                if (tk < te) {
-                    float4* o = reinterpret_cast<float4*>(out + ((int64_t)tk * a.H + h) * D + jt * 32 + cc);
-                    if (add) {
-                        const float4 u = *o;
-                        *o = make_float4(u.x + v.x, u.y + v.y, u.z + v.z, u.w + v.w);
-                    } else {
-                        *o = v;
-                    }
-                }
-            }
-            asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");   // reads done before the next slice
-        }
+        store_token_rows<D, C::ROWF>(acc, stg, out, f, tb + 32 * w, te, a.H, h, add, lane);
     };
 
     Blk cur;
-    if (!first_from(k0, 0, cur) || !advance(cur, lw, cur)) return;
+    if (!seq.first_from(k0, cur) || !seq.advance(cur, lw, cur)) return;
     load_k(cur);
     fetch(cur, 0, 0, 0);
     fetch(cur, 1, 0, 1);
@@ -400,27 +508,8 @@ __global__ __launch_bounds__(NW * 64, 8 / NW) void bwd_token_kernel(TokArgs a) {
 #pragma unroll
             for (int kk = 0; kk < C::KS; ++kk) vb[kk] = kb[kk];
         }
-        // D_t = <V_t, dV_t>.  This lane holds dV[t, j] for j = 32 jt + 8 g + 4 hl + e
-        // (e < 4) and V[t, j] for j = 16 kk + 8 hl + 0..7.  Swapping dwords 0-1
-        // of the upper half with dwords 2-3 of the lower half gives both halves
-        // V at j = 16 kk + 4 hl + 0..3 (dwords 0-1) and 16 kk + 8 + 4 hl + 0..3
-        // (dwords 2-3): with kk = 2 jt + g / 2, the columns of dV registers 4 g..4 g + 3.
-        float Dt = 0.f;
-#pragma unroll
-        for (int kk = 0; kk < C::KS; ++kk) {
-            const u32x4 v = __builtin_bit_cast(u32x4, vb[kk]);
-            const auto p0 = __builtin_amdgcn_permlane32_swap(v[0], v[2], false, false);
-            const auto p1 = __builtin_amdgcn_permlane32_swap(v[1], v[3], false, false);
-            const uint32_t q[2][2] = {{p0[0], p1[0]}, {p0[1], p1[1]}};
-#pragma unroll
-            for (int sh = 0; sh < 2; ++sh) {
-                const int jt = kk >> 1, g = 2 * (kk & 1) + sh;
-                Dt = __builtin_fmaf(bf16_lo(q[sh][0]), dvt[jt][4 * g + 0], Dt);
-                Dt = __builtin_fmaf(bf16_hi(q[sh][0]), dvt[jt][4 * g + 1], Dt);
-                Dt = __builtin_fmaf(bf16_lo(q[sh][1]), dvt[jt][4 * g + 2], Dt);
-                Dt = __builtin_fmaf(bf16_hi(q[sh][1]), dvt[jt][4 * g + 3], Dt);
-            }
-        }
+        // D_t = <V_t, dV_t>
+        float Dt = dot_v_dv<D>(vb, dvt);
         Dt = tv ? xhalf_sum(Dt) : 0.f;
         if (tv && hl == 0) a.Dbuf[(int64_t)tok * a.H + h] = Dt;
         // dV rows now (frees their registers); they drain under sweep 2's first stage
@@ -522,6 +611,338 @@ __global__ __launch_bounds__(NW * 64, 8 / NW) void bwd_token_kernel(TokArgs a) {
         if (!more) break;
         cur = nxt;
         ring = (ring + 2 * nblk) % 3;
+    }
+}
+
+// ------------------------------------------------------------------ token side, weights held
+// For M <= 512 the first sweep's bf16 weights A^T of a wave's 32 tokens (M/32
+// tiles of 16 values per lane, at most 128 registers) stay in accumulator
+// registers until the second sweep, which then computes only dA and dK: 8
+// instead of 10 M d matrix FLOPs per (token, head) and one exponential per
+// (token, prototype) instead of two.  That takes one wave per SIMD (four per
+// workgroup, 128 tokens per block).  The second sweep uses the weights as
+// rounded to bf16 for the dV contraction (about 2^-9 relative).
+//
+// The prototype blocks stream through eight LDS buffers (stage s of a token
+// block's 2 M/32 stages in buffer s % 8, fetched six stages ahead), so a fetch
+// has four stages to land and every LDS address is a constant offset from a
+// lane register: the row-major matrices of the eight buffers fill the first
+// 64 KB (the reach of an instruction offset), the transposed ones the next.  A
+// stage ends by waiting for the fetch of stage s + 2 only (a vector-memory
+// count computed per stage), so that the row loads of K and V stay in flight
+// across five stages; the stages right after the row stores of dV and dK wait
+// for everything, since stores and loads do not complete in order.
+template <int D, int NBLK>
+struct HeldCfg {
+    static constexpr int NW = 4;
+    static constexpr int THREADS = NW * 64;
+    static constexpr int TB = 32 * NW;                 // tokens per block
+    static constexpr int KS = D / 16;
+    static constexpr int JT = D / 32;
+    static constexpr int KCH = D / 8;                  // 16-byte chunks per row
+    static constexpr int BLK = 32 * D;                 // bf16 elements of one 32-row block
+    static constexpr int NSTG = 2 * NBLK;              // stages per token block
+    static constexpr int NBUF = 8;
+    static constexpr int AHEAD = 6;
+    static constexpr int OFF_COL = NBUF * BLK * 2;     // bytes: the transposed matrices
+    static constexpr int ROWF = 36;
+    static constexpr int STG_FLOATS = 32 * ROWF;
+    static constexpr int OFF_STG = 2 * NBUF * BLK * 2;
+    static constexpr int LDS = OFF_STG + NW * STG_FLOATS * 4;
+    static constexpr int NQ = BLK / 8 / 64;            // wave-loads per matrix block
+    static constexpr int FL = 2 * NQ / NW;             // fetch loads per wave per stage
+    static_assert(NSTG % NBUF == 0 && NQ % NW == 0 && NSTG >= AHEAD + 2, "held-weights configuration");
+    static_assert(OFF_COL <= 65536 && LDS <= 160 * 1024, "LDS layout");
+
+    // vector-memory operations a wave issues in stage s after its fetch: the V
+    // rows in stage 1 (separate K and V), the next block's K rows and lse in
+    // stage NBLK + 1
+    template <bool XV>
+    static constexpr int extra(int s) {
+        return (!XV && s == 1) ? KS : (s == NBLK + 1 ? KS + 1 : 0);
+    }
+    // the count a wave waits down to at the end of stage s: the fetch of stage
+    // s + 2 (issued in stage s - 4) must have landed; everything issued after it
+    // may stay in flight (vector-memory loads complete in order).  Stages 0 and
+    // NBLK follow row stores and wait for all.
+    template <bool XV>
+    static constexpr int wait_count(int s) {
+        if (s == 0 || s == NBLK) return 0;
+        const int f = s < NBLK ? 0 : NBLK;   // the last full wait
+        const int first = s - (AHEAD - 2);   // the stage that issued that fetch
+        int n = 0;
+        if (first <= f) {
+            for (int x = f + 1; x <= s; ++x) n += FL + extra<XV>(x);
+        } else {
+            n = extra<XV>(first);
+            for (int x = first + 1; x <= s; ++x) n += FL + extra<XV>(x);
+        }
+        return n;
+    }
+};
+
+template <int D, int NBLK, bool XV>
+__global__ __launch_bounds__(256, 1) void bwd_token_held_kernel(TokArgs a) {
+    using C = HeldCfg<D, NBLK>;
+    constexpr int NW = C::NW, KS = C::KS, JT = C::JT, NSTG = C::NSTG, NBUF = C::NBUF;
+    // static LDS, so that buffer addresses are constants
+    __shared__ __attribute__((aligned(16))) uint8_t smem[C::LDS];
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int w = __builtin_amdgcn_readfirstlane(tid >> 6);   // wave-uniform: LDS bases in scalar registers
+    const int l32 = lane & 31, hl = lane >> 5;
+    float* stg = reinterpret_cast<float*>(smem + C::OFF_STG) + w * C::STG_FLOATS;
+
+    // block assignment as in bwd_token_kernel: the workgroups of an XCD take the
+    // token blocks of that XCD's ranges in turn
+    const int64_t nr = gridDim.x, xq = nr / 8, xrem = nr % 8, xcd = blockIdx.x % 8;
+    const int64_t lw = blockIdx.x / 8, nx = xq + (xcd < xrem ? 1 : 0);
+    const int64_t first_range = xcd * xq + (xcd < xrem ? xcd : xrem);
+    const int64_t k0 = a.wg_start[first_range], k1 = a.wg_start[first_range + nx];
+    if (k0 < 0 || k1 < k0 || k1 > a.max_items) return;
+    const TokSeq<C::TB> seq{a.items, k1, a.T, a.B, a.H};
+    const float ks2 = a.scale * kLog2e;
+    const int64_t MD = (int64_t)a.M * D;
+
+    // byte offsets inside a prototype block of the chunks this lane fetches (the
+    // same for every block), added to a wave-uniform block address
+    uint32_t rofs[C::NQ / NW], tofs[C::NQ / NW];
+#pragma unroll
+    for (int i = 0; i < C::NQ / NW; ++i) {
+        const int p = (w + NW * i) * 64 + lane;
+        const int r = p / C::KCH, cc = (p % C::KCH) ^ swz_x<D>(r);
+        rofs[i] = (uint32_t)((r * D + cc * 8) * 2);
+        const int j = p / 4, cj = (p % 4) ^ swz_x<32>(j);
+        tofs[i] = (uint32_t)((j * a.M + cj * 8) * 2);
+    }
+    // LDS byte offsets of this lane's operand reads: chunk 2 kk + hl of row l32 of
+    // a row-major block (plus buffer * BLK * 2), and the two k halves of row
+    // 32 jt + l32 of a transposed block (plus OFF_COL + buffer * BLK * 2 + jt * 2048)
+    uint32_t roff[KS], coff[2];
+#pragma unroll
+    for (int kk = 0; kk < KS; ++kk) roff[kk] = (uint32_t)swz<D>(l32, 2 * kk + hl) * 2;
+#pragma unroll
+    for (int c = 0; c < 2; ++c) {
+        coff[c] = (uint32_t)(C::OFF_COL + swz<32>(l32, 2 * c + hl) * 2);
+        asm volatile("" : "+v"(coff[c]));   // one base register, buffers as instruction offsets
+    }
+    auto rd = [&](uint32_t off) __attribute__((always_inline)) {
+        return __builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4*>(smem + off));
+    };
+
+    // Prototype block mb of the two matrices a sweep reads, straight into LDS
+    // buffer b (sweep 0: P rows [32][D] and dY^T [D][32]; sweep 1: dY rows and
+    // P^T).  Lane l of a wave fetches the global chunk that belongs at LDS chunk
+    // position p = 64 q + l of the swizzled layout (the XOR swizzle is its own
+    // inverse).  FL loads per wave.
+    auto fetch = [&](const TokBlk& c, int mb, int sweep, int b) __attribute__((always_inline)) {
+        const int64_t pkey = a.p_user ? (int64_t)c.b * a.H + c.h : c.h;
+        const int64_t ykey = (int64_t)c.b * a.H + c.h;
+        const char* Rg = reinterpret_cast<const char*>((sweep == 0 ? a.P + pkey * MD : a.Ymj + ykey * MD) + mb * 32 * D);
+        const char* Tg = reinterpret_cast<const char*>((sweep == 0 ? a.Yjm + ykey * MD : a.Pjm + pkey * MD) + mb * 32);
+#pragma unroll
+        for (int i = 0; i < C::NQ / NW; ++i) {
+            const int q = w + NW * i;
+            load_lds16(Rg + rofs[i], smem + b * C::BLK * 2 + q * 1024);
+            load_lds16(Tg + tofs[i], smem + C::OFF_COL + b * C::BLK * 2 + q * 1024);
+        }
+    };
+    // stage X of the stream: this block's, the next block's stage X - NSTG, or
+    // after the last block this block's stage X - NSTG again into a buffer that
+    // is not read any more (so that every stage issues the same loads)
+    auto fetch_stage = [&](auto xc, const TokBlk& cur, const TokBlk& nxt, bool more) __attribute__((always_inline)) {
+        constexpr int X = decltype(xc)::value;
+        constexpr int Y = X < NSTG ? X : X - NSTG;   // the stage within its block
+        static_assert(Y < NSTG, "fetch distance");
+        if constexpr (X < NSTG) fetch(cur, Y % NBLK, Y / NBLK, X % NBUF);
+        else fetch(more ? nxt : cur, Y % NBLK, Y / NBLK, X % NBUF);
+    };
+    // rows of this wave's tokens as B operands (lane (hl, t) holds 8 consecutive
+    // j of its token); lanes past the block's end take its last token, so the
+    // loads carry no predicate
+    auto load_rows = [&](const uint16_t* src, const TokBlk& c, bf16x8 (&dst)[KS]) __attribute__((always_inline)) {
+        const int t = min(32 * w + l32, c.te - 1 - c.tb);
+        const char* base = reinterpret_cast<const char*>(src + ((int64_t)c.tb * a.H + c.h) * D);
+        const uint32_t off = (uint32_t)(t * a.H * D + 8 * hl) * 2;
+#pragma unroll
+        for (int kk = 0; kk < KS; ++kk)
+            dst[kk] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4*>(base + off + 32 * kk));
+    };
+    auto load_lse = [&](const TokBlk& c) __attribute__((always_inline)) {
+        const int t = min(32 * w + l32, c.te - 1 - c.tb);
+        const char* base = reinterpret_cast<const char*>(a.lse + (int64_t)c.tb * a.H + c.h);
+        return *reinterpret_cast<const float*>(base + (uint32_t)(t * a.H) * 4);
+    };
+    // operands of a [32 prototypes] x [32 tokens] tile from the row-major block
+    // of buffer b (P, or dY in sweep 2), and of the contraction over the block's
+    // prototypes from its transposed block (dY^T, or P^T in sweep 2)
+    auto row_ops = [&](int b, bf16x8 (&op)[KS]) __attribute__((always_inline)) {
+#pragma unroll
+        for (int kk = 0; kk < KS; ++kk) op[kk] = rd(roff[kk] + b * C::BLK * 2);
+    };
+    auto col_ops = [&](int b, bf16x8 (&op)[2 * JT]) __attribute__((always_inline)) {
+#pragma unroll
+        for (int jt = 0; jt < JT; ++jt)
+#pragma unroll
+            for (int c = 0; c < 2; ++c) op[2 * jt + c] = rd(coff[c] + b * C::BLK * 2 + jt * 2048);
+    };
+    auto col_acc = [&](const bf16x8 (&op)[2 * JT], const bf16x8& w0, const bf16x8& w1, f32x16 (&acc)[JT])
+        __attribute__((always_inline)) {
+#pragma unroll
+        for (int jt = 0; jt < JT; ++jt) {
+            acc[jt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(op[2 * jt], w0, acc[jt], 0, 0, 0);
+            acc[jt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(op[2 * jt + 1], w1, acc[jt], 0, 0, 0);
+        }
+    };
+    auto row_tile = [&](const bf16x8 (&op)[KS], const bf16x8 (&b)[KS]) __attribute__((always_inline)) {
+        f32x16 s;
+#pragma unroll
+        for (int r = 0; r < 16; ++r) s[r] = 0.f;
+#pragma unroll
+        for (int kk = 0; kk < KS; ++kk) s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(op[kk], b[kk], s, 0, 0, 0);
+        return s;
+    };
+    auto stage_end = [&](auto sc) __attribute__((always_inline)) {
+        constexpr int S = decltype(sc)::value;
+        wait_vm<C::template wait_count<XV>(S)>();
+        lds_barrier();
+    };
+
+    TokBlk cur;
+    if (!seq.first_from(k0, cur) || !seq.advance(cur, lw, cur)) return;
+    // kb: K rows (the score chains of sweep 1); vb: V rows (D_t and the dA chains
+    // of sweep 2).  XV: kb holds X for both, and vb receives the next block's X.
+    bf16x8 kb[KS], vb[KS];
+    bf16x8 (&vop)[KS] = XV ? kb : vb;
+    load_rows(a.K, cur, kb);
+    float lse_n = load_lse(cur);
+    static_for<C::AHEAD>([&](auto xc) { fetch_stage(xc, cur, cur, false); });
+    wait_vmem();
+    __syncthreads();
+    f32x16 s_cur;
+    {
+        bf16x8 op[KS];
+        row_ops(0, op);
+        s_cur = row_tile(op, kb);
+    }
+    float nl = -lse_n * kLog2e;
+
+    while (true) {
+        const int tb = cur.tb, te = cur.te, h = cur.h;
+        const int tok = tb + 32 * w + l32;   // this lane's token (column of S^T)
+        const bool tv = tok < te;
+        TokBlk nxt;
+        const bool more = seq.advance(cur, nx, nxt);
+
+        // ---------------- sweep 1: A^T tiles (held), dV^T[j, t] = sum_m dY[m, j] A[t, m]
+        // Stage mb: the S^T chain of block mb + 1, one matrix instruction per two
+        // rows of block mb's exponentials, then block mb's dV contraction.
+        bf16x8 ah[NBLK][2];
+        f32x16 dvt[JT];
+#pragma unroll
+        for (int jt = 0; jt < JT; ++jt)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) dvt[jt][r] = 0.f;
+        static_for<NBLK>([&](auto mbc) {
+            constexpr int mb = decltype(mbc)::value, S = mb, B = S % NBUF;
+            constexpr bool nx_tile = mb + 1 < NBLK;
+            fetch_stage(std::integral_constant<int, S + C::AHEAD>{}, cur, nxt, more);
+            if constexpr (!XV && S == 1) load_rows(a.V, cur, vb);
+            bf16x8 pop[KS], yop[2 * JT];
+            if constexpr (nx_tile) row_ops((S + 1) % NBUF, pop);
+            col_ops(B, yop);
+            f32x16 s_nx;
+#pragma unroll
+            for (int r = 0; r < 16; ++r) s_nx[r] = 0.f;
+            float e[16];
+            constexpr int RPK = 16 / KS;   // exponential rows per chain step
+#pragma unroll
+            for (int kk = 0; kk < KS; ++kk) {
+                if constexpr (nx_tile) s_nx = __builtin_amdgcn_mfma_f32_32x32x16_bf16(pop[kk], kb[kk], s_nx, 0, 0, 0);
+#pragma unroll
+                for (int q = 0; q < RPK; ++q) {
+                    const int r = kk * RPK + q;
+                    e[r] = __builtin_amdgcn_exp2f(__builtin_fmaf(s_cur[r], ks2, nl));
+                }
+                __builtin_amdgcn_sched_barrier(0);
+            }
+            ah[mb][0] = to_agpr(pack8(e));
+            ah[mb][1] = to_agpr(pack8(e + 8));
+            col_acc(yop, ah[mb][0], ah[mb][1], dvt);
+            stage_end(std::integral_constant<int, S>{});
+            if constexpr (nx_tile) s_cur = s_nx;
+        });
+        // D_t = <V_t, dV_t>; the V rows are not touched before this point
+#pragma unroll
+        for (int kk = 0; kk < KS; ++kk) asm volatile("" : "+v"(vop[kk]));
+        float Dt = dot_v_dv<D>(vop, dvt);
+        Dt = tv ? xhalf_sum(Dt) : 0.f;
+        if (tv && hl == 0) a.Dbuf[(int64_t)tok * a.H + h] = Dt;
+        if constexpr (!XV) store_token_rows<D, C::ROWF>(dvt, stg, a.dV, 1.0f, tb + 32 * w, te, a.H, h, false, lane);
+
+        // ---------------- sweep 2: dK^T[j, t] = scale sum_m P[m, j] dS[t, m] with
+        // dS = A (dA - D_t) from the held A (XV: continues from dV^T, scale folded
+        // into dS).  Stage mb: the dA chain of block mb + 1, one matrix
+        // instruction per two rows of block mb's dS, then block mb's dK contraction.
+        f32x16 dkt[JT];
+#pragma unroll
+        for (int jt = 0; jt < JT; ++jt)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) dkt[jt][r] = XV ? dvt[jt][r] : 0.f;
+        f32x16 da_cur;
+        {
+            bf16x8 op[KS];
+            row_ops(NBLK % NBUF, op);
+            da_cur = row_tile(op, vop);
+        }
+        static_for<NBLK>([&](auto mbc) {
+            constexpr int mb = decltype(mbc)::value, S = NBLK + mb, B = S % NBUF;
+            constexpr bool nx_tile = mb + 1 < NBLK;
+            fetch_stage(std::integral_constant<int, S + C::AHEAD>{}, cur, nxt, more);
+            if constexpr (S == NBLK + 1) {
+                load_rows(a.K, more ? nxt : cur, XV ? vb : kb);
+                lse_n = load_lse(more ? nxt : cur);
+            }
+            bf16x8 yop[KS], pop[2 * JT];
+            if constexpr (nx_tile) row_ops((S + 1) % NBUF, yop);
+            col_ops(B, pop);
+            f32x16 da_nx;
+#pragma unroll
+            for (int r = 0; r < 16; ++r) da_nx[r] = 0.f;
+            float e[16];
+            constexpr int RPK = 16 / KS;
+#pragma unroll
+            for (int kk = 0; kk < KS; ++kk) {
+                if constexpr (nx_tile) da_nx = __builtin_amdgcn_mfma_f32_32x32x16_bf16(yop[kk], vop[kk], da_nx, 0, 0, 0);
+#pragma unroll
+                for (int q = 0; q < RPK; ++q) {
+                    const int r = kk * RPK + q;
+                    const float A = (float)ah[mb][r >> 3][r & 7];
+                    const float g = da_cur[r] - Dt;
+                    e[r] = XV ? A * (g * a.scale) : A * g;
+                }
+                __builtin_amdgcn_sched_barrier(0);
+            }
+            col_acc(pop, pack8(e), pack8(e + 8), dkt);
+            stage_end(std::integral_constant<int, S>{});
+            if constexpr (nx_tile) da_cur = da_nx;
+        });
+
+        // the next block's first S^T tile (its stage 0 has landed) before the row
+        // stores, whose completion the next stage's end waits for
+        if (more) {
+            if constexpr (XV) {
+#pragma unroll
+                for (int kk = 0; kk < KS; ++kk) kb[kk] = vb[kk];
+            }
+            bf16x8 op[KS];
+            row_ops(0, op);
+            s_cur = row_tile(op, kb);
+            nl = -lse_n * kLog2e;
+        }
+        store_token_rows<D, C::ROWF>(dkt, stg, XV ? a.dX : a.dK, XV ? 1.0f : a.scale, tb + 32 * w, te, a.H, h,
+                                     XV && a.dx_add, lane);
+        if (!more) break;
+        cur = nxt;
     }
 }
 
@@ -919,10 +1340,28 @@ hipError_t launch_proto(const ProtoArgs& a, bool xv, int64_t n_ranges, hipStream
               : launch_proto_t<D, MW, NW, false>(a, n_ranges, stream);
 }
 
+template <int D, int NBLK, bool XV>
+hipError_t launch_token_held(const TokArgs& a, int64_t n_ranges, hipStream_t stream) {
+    using C = HeldCfg<D, NBLK>;
+    auto kern = bwd_token_held_kernel<D, NBLK, XV>;
+    hipLaunchKernelGGL(kern, dim3((unsigned)n_ranges), dim3(C::THREADS), 0, stream, a);
+    return hipGetLastError();
+}
+
+template <int D, bool XV>
+hipError_t launch_token_xv(const TokArgs& a, int64_t n_ranges, hipStream_t stream) {
+    switch (a.M) {
+        case 128: return launch_token_held<D, 4, XV>(a, n_ranges, stream);
+        case 256: return launch_token_held<D, 8, XV>(a, n_ranges, stream);
+        case 384: return launch_token_held<D, 12, XV>(a, n_ranges, stream);
+        case 512: return launch_token_held<D, 16, XV>(a, n_ranges, stream);
+        default: return launch_token<D, kTokWaves, XV>(a, n_ranges, stream);
+    }
+}
+
 template <int D>
 hipError_t launch_token_d(const TokArgs& a, bool xv, int64_t n_ranges, hipStream_t stream) {
-    return xv ? launch_token<D, kTokWaves, true>(a, n_ranges, stream)
-              : launch_token<D, kTokWaves, false>(a, n_ranges, stream);
+    return xv ? launch_token_xv<D, true>(a, n_ranges, stream) : launch_token_xv<D, false>(a, n_ranges, stream);
 }
 
 }  // namespace
