@@ -84,21 +84,25 @@ __device__ __forceinline__ void static_for(F&& f) {
     static_for_seq(f, std::make_integer_sequence<int, N>{});
 }
 
-// The value moved into accumulator registers: a held matrix-core operand stays
-// there (the matrix core reads either register file) and leaves the vector
-// registers to the working set; VALU uses copy it back when they need it.
-__device__ __forceinline__ bf16x8 to_agpr(bf16x8 v) {
-    u32x4 u = __builtin_bit_cast(u32x4, v), o;
-    asm volatile("" : "=a"(o) : "0"(u));
-    return __builtin_bit_cast(bf16x8, o);
-}
-
 // s_waitcnt for vector memory only: at most N of this wave's vector-memory
 // operations still outstanding (the other counters are not waited for)
 template <int N>
 __device__ __forceinline__ void wait_vm() {
     static_assert(N >= 0 && N < 64, "vmcnt range");
     __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | (15 << 8) | ((N >> 4) << 14));
+}
+// A workgroup barrier after at most N outstanding vector-memory operations and
+// none of LDS.  The wait is the compiler's own instruction, so it knows that
+// every earlier LDS read has landed (an inline-assembly wait would leave it
+// waiting again, after the barrier, behind newer reads); the scheduling fences
+// keep each side's instructions on its side.
+template <int N>
+__device__ __forceinline__ void stage_barrier() {
+    static_assert(N >= 0 && N < 64, "vmcnt range");
+    __builtin_amdgcn_sched_barrier(0);
+    __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | (0 << 8) | ((N >> 4) << 14));
+    __builtin_amdgcn_s_barrier();
+    __builtin_amdgcn_sched_barrier(0);
 }
 
 // Token blocks of a token-side workgroup: segment k of the work list (user b,
@@ -175,7 +179,12 @@ __device__ __forceinline__ void lds_load16x4_asm(f32x4 (&o)[4], const float* p, 
 // layout holds 16-byte pieces of 32 token rows per store; each 32-column slice
 // goes through the wave's LDS area stg ([32][ROWF] fp32) so that every store
 // instruction writes whole 128-byte lines of 8 tokens.
-template <int D, int ROWF>
+//
+// CLAMP: lanes past te store to row te - 1 instead of being masked off, so that
+// every wave issues the same number of store instructions; only for callers
+// whose lanes past the end computed exactly the last token's values (their
+// inputs are copies of its rows), and never with add.
+template <int D, int ROWF, bool CLAMP = false>
 __device__ __forceinline__ void store_token_rows(const f32x16 (&acc)[D / 32], float* stg, float* out, float f,
                                                  int tok0, int te, int H, int h, bool add, int lane) {
     const int l32 = lane & 31, hl = lane >> 5;
@@ -193,10 +202,10 @@ __device__ __forceinline__ void store_token_rows(const f32x16 (&acc)[D / 32], fl
         for (int q = 0; q < 4; ++q) {
             const int t = 8 * q + (lane >> 3), cc = 4 * (lane & 7);
             const float4 v = make_float4(rows[q][0], rows[q][1], rows[q][2], rows[q][3]);
-            const int tk = tok0 + t;
-            if (tk < te) {
+            const int tk = CLAMP ? min(tok0 + t, te - 1) : tok0 + t;
+            if (CLAMP || tk < te) {
                 float4* o = reinterpret_cast<float4*>(out + ((int64_t)tk * H + h) * D + jt * 32 + cc);
-                if (add) {
+                if (!CLAMP && add) {
                     const float4 u = *o;
                     *o = make_float4(u.x + v.x, u.y + v.y, u.z + v.z, u.w + v.w);
                 } else {
@@ -616,8 +625,8 @@ __global__ __launch_bounds__(NW * 64, 8 / NW) void bwd_token_kernel(TokArgs a) {
 
 // ------------------------------------------------------------------ token side, weights held
 // For M <= 512 the first sweep's bf16 weights A^T of a wave's 32 tokens (M/32
-// tiles of 16 values per lane, at most 128 registers) stay in accumulator
-// registers until the second sweep, which then computes only dA and dK: 8
+// tiles of 16 values per lane, at most 128 registers) stay in registers until
+// the second sweep, which then computes only dA and dK: 8
 // instead of 10 M d matrix FLOPs per (token, head) and one exponential per
 // (token, prototype) instead of two.  That takes one wave per SIMD (four per
 // workgroup, 128 tokens per block).  The second sweep uses the weights as
@@ -629,9 +638,15 @@ __global__ __launch_bounds__(NW * 64, 8 / NW) void bwd_token_kernel(TokArgs a) {
 // lane register: the row-major matrices of the eight buffers fill the first
 // 64 KB (the reach of an instruction offset), the transposed ones the next.  A
 // stage ends by waiting for the fetch of stage s + 2 only (a vector-memory
-// count computed per stage), so that the row loads of K and V stay in flight
-// across five stages; the stages right after the row stores of dV and dK wait
-// for everything, since stores and loads do not complete in order.
+// count computed per stage: the fetches, row loads and row stores each wave
+// issues are fixed in number and complete in issue order), so that the row
+// loads of K and V stay in flight across five stages and no stage waits for
+// the row stores.
+//
+// The stages are pipelined by one prototype block: stage mb contracts block
+// mb - 1 (its weights and operands prepared in the previous stage) beside the
+// exponentials (or dS) of block mb, then runs the S^T (or dA) chain of block
+// mb + 1, reading block mb's contraction operands between the chain's steps.
 template <int D, int NBLK>
 struct HeldCfg {
     static constexpr int NW = 4;
@@ -661,24 +676,31 @@ struct HeldCfg {
     static constexpr int extra(int s) {
         return (!XV && s == 1) ? KS : (s == NBLK + 1 ? KS + 1 : 0);
     }
-    // the count a wave waits down to at the end of stage s: the fetch of stage
-    // s + 2 (issued in stage s - 4) must have landed; everything issued after it
-    // may stay in flight (vector-memory loads complete in order).  Stages 0 and
-    // NBLK follow row stores and wait for all.
+    // ... and between stage s - 1's barrier and stage s's fetch: D_t and the dV
+    // rows before stage NBLK, the dK (or dX) rows of the previous block before
+    // stage 0
+    template <bool XV>
+    static constexpr int bnd(int s) {
+        return s == NBLK ? 1 + (XV ? 0 : 4 * JT) : (s == 0 ? 4 * JT : 0);
+    }
+    // The count a wave waits down to at the end of stage s: the fetch of stage
+    // s + 2, issued in stage s - 4 (of the previous block if negative), must have
+    // landed; everything issued after it may stay in flight.  Vector-memory
+    // operations complete in issue order (loads and stores alike), so this
+    // count is exact.  (The first block's early fetches precede a full wait.)
     template <bool XV>
     static constexpr int wait_count(int s) {
-        if (s == 0 || s == NBLK) return 0;
-        const int f = s < NBLK ? 0 : NBLK;   // the last full wait
-        const int first = s - (AHEAD - 2);   // the stage that issued that fetch
-        int n = 0;
-        if (first <= f) {
-            for (int x = f + 1; x <= s; ++x) n += FL + extra<XV>(x);
-        } else {
-            n = extra<XV>(first);
-            for (int x = first + 1; x <= s; ++x) n += FL + extra<XV>(x);
+        const int first = s - (AHEAD - 2);
+        int n = extra<XV>((first % NSTG + NSTG) % NSTG);
+        for (int x = first + 1; x <= s; ++x) {
+            const int y = (x % NSTG + NSTG) % NSTG;
+            n += bnd<XV>(y) + FL + extra<XV>(y);
         }
         return n;
     }
+    // the stages whose window holds the previous block's row stores (their
+    // count is data dependent when the rows are added to dX: full waits then)
+    static constexpr bool after_rows(int s) { return s < AHEAD - 2; }
 };
 
 template <int D, int NBLK, bool XV>
@@ -801,10 +823,29 @@ __global__ __launch_bounds__(256, 1) void bwd_token_held_kernel(TokArgs a) {
         for (int kk = 0; kk < KS; ++kk) s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(op[kk], b[kk], s, 0, 0, 0);
         return s;
     };
+    const bool add = XV && a.dx_add;   // dX rows read and added: masked, so counted by a full wait
+    // the score (or dA) chain of the next block, one read of this block's
+    // contraction operands (for the next stage) issued after each of its steps,
+    // so that the reads land while the dependent chain runs
+    auto chain_and_reads = [&](const bf16x8 (&op)[KS], const bf16x8 (&b)[KS], f32x16& s, int bufc,
+                               bf16x8 (&cnext)[2 * JT]) __attribute__((always_inline)) {
+        static_assert(2 * JT <= KS, "one read per chain step");
+#pragma unroll
+        for (int r = 0; r < 16; ++r) s[r] = 0.f;
+#pragma unroll
+        for (int kk = 0; kk < KS; ++kk) {
+            s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(op[kk], b[kk], s, 0, 0, 0);
+            if (kk < 2 * JT) {
+                const int jt = kk >> 1, c = kk & 1;
+                cnext[kk] = rd(coff[c] + bufc * C::BLK * 2 + jt * 2048);
+            }
+            __builtin_amdgcn_sched_barrier(0);
+        }
+    };
     auto stage_end = [&](auto sc) __attribute__((always_inline)) {
         constexpr int S = decltype(sc)::value;
-        wait_vm<C::template wait_count<XV>(S)>();
-        lds_barrier();
+        if (C::after_rows(S) && add) stage_barrier<0>();
+        else stage_barrier<C::template wait_count<XV>(S)>();
     };
 
     TokBlk cur;
@@ -826,109 +867,120 @@ __global__ __launch_bounds__(256, 1) void bwd_token_held_kernel(TokArgs a) {
     }
     float nl = -lse_n * kLog2e;
 
+    // The stages are software-pipelined by one prototype block: stage mb runs the
+    // contraction of block mb - 1 (its weights packed and its operands read in
+    // the previous stage) beside the elementwise work of block mb (whose score
+    // or dA tile the previous stage computed), then the score or dA chain of
+    // block mb + 1 (its operands read at the top of the stage), and reads the
+    // operands of block mb's contraction for the next stage.  So every matrix
+    // instruction's operands were requested a phase earlier, and the VALU work
+    // runs beside independent matrix instructions.
+    constexpr int RPS = 16 / (2 * JT);   // elementwise rows per contraction instruction
     while (true) {
         const int tb = cur.tb, te = cur.te, h = cur.h;
         const int tok = tb + 32 * w + l32;   // this lane's token (column of S^T)
-        const bool tv = tok < te;
         TokBlk nxt;
         const bool more = seq.advance(cur, nx, nxt);
 
         // ---------------- sweep 1: A^T tiles (held), dV^T[j, t] = sum_m dY[m, j] A[t, m]
-        // Stage mb: the S^T chain of block mb + 1, one matrix instruction per two
-        // rows of block mb's exponentials, then block mb's dV contraction.
         bf16x8 ah[NBLK][2];
         f32x16 dvt[JT];
 #pragma unroll
         for (int jt = 0; jt < JT; ++jt)
 #pragma unroll
             for (int r = 0; r < 16; ++r) dvt[jt][r] = 0.f;
+        bf16x8 cop[2 * JT];   // contraction operands of the previous block
         static_for<NBLK>([&](auto mbc) {
             constexpr int mb = decltype(mbc)::value, S = mb, B = S % NBUF;
-            constexpr bool nx_tile = mb + 1 < NBLK;
             fetch_stage(std::integral_constant<int, S + C::AHEAD>{}, cur, nxt, more);
             if constexpr (!XV && S == 1) load_rows(a.V, cur, vb);
-            bf16x8 pop[KS], yop[2 * JT];
-            if constexpr (nx_tile) row_ops((S + 1) % NBUF, pop);
-            col_ops(B, yop);
-            f32x16 s_nx;
-#pragma unroll
-            for (int r = 0; r < 16; ++r) s_nx[r] = 0.f;
+            bf16x8 pop[KS];
+            if constexpr (mb + 1 < NBLK) row_ops((S + 1) % NBUF, pop);
+            // dV(mb - 1) beside the exponentials of block mb
             float e[16];
-            constexpr int RPK = 16 / KS;   // exponential rows per chain step
 #pragma unroll
-            for (int kk = 0; kk < KS; ++kk) {
-                if constexpr (nx_tile) s_nx = __builtin_amdgcn_mfma_f32_32x32x16_bf16(pop[kk], kb[kk], s_nx, 0, 0, 0);
+            for (int q = 0; q < 2 * JT; ++q) {
+                if constexpr (mb > 0) {
+                    const int jt = q >> 1, c = q & 1;
+                    dvt[jt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(cop[q], ah[mb - 1][c], dvt[jt], 0, 0, 0);
+                }
 #pragma unroll
-                for (int q = 0; q < RPK; ++q) {
-                    const int r = kk * RPK + q;
+                for (int u = 0; u < RPS; ++u) {
+                    const int r = q * RPS + u;
                     e[r] = __builtin_amdgcn_exp2f(__builtin_fmaf(s_cur[r], ks2, nl));
                 }
                 __builtin_amdgcn_sched_barrier(0);
             }
-            ah[mb][0] = to_agpr(pack8(e));
-            ah[mb][1] = to_agpr(pack8(e + 8));
-            col_acc(yop, ah[mb][0], ah[mb][1], dvt);
+            ah[mb][0] = pack8(e);
+            ah[mb][1] = pack8(e + 8);
+            // S^T chain of block mb + 1, and block mb's dV operands for the next stage
+            if constexpr (mb + 1 < NBLK) chain_and_reads(pop, kb, s_cur, B, cop);
+            else col_ops(B, cop);
             stage_end(std::integral_constant<int, S>{});
-            if constexpr (nx_tile) s_cur = s_nx;
         });
+        // sweep 2's first dA tile beside the last dV contraction
+        f32x16 da_cur;
+        {
+            bf16x8 op[KS];
+            row_ops(NBLK % NBUF, op);
+            col_acc(cop, ah[NBLK - 1][0], ah[NBLK - 1][1], dvt);
+            da_cur = row_tile(op, vop);
+        }
         // D_t = <V_t, dV_t>; the V rows are not touched before this point
 #pragma unroll
         for (int kk = 0; kk < KS; ++kk) asm volatile("" : "+v"(vop[kk]));
-        float Dt = dot_v_dv<D>(vop, dvt);
-        Dt = tv ? xhalf_sum(Dt) : 0.f;
-        if (tv && hl == 0) a.Dbuf[(int64_t)tok * a.H + h] = Dt;
-        if constexpr (!XV) store_token_rows<D, C::ROWF>(dvt, stg, a.dV, 1.0f, tb + 32 * w, te, a.H, h, false, lane);
+        // (lanes past the block's end hold the last token's values, stored to its row)
+        const float Dt = xhalf_sum(dot_v_dv<D>(vop, dvt));
+        if (hl == 0) a.Dbuf[(int64_t)min(tok, te - 1) * a.H + h] = Dt;
+        if constexpr (!XV)
+            store_token_rows<D, C::ROWF, true>(dvt, stg, a.dV, 1.0f, tb + 32 * w, te, a.H, h, false, lane);
 
         // ---------------- sweep 2: dK^T[j, t] = scale sum_m P[m, j] dS[t, m] with
         // dS = A (dA - D_t) from the held A (XV: continues from dV^T, scale folded
-        // into dS).  Stage mb: the dA chain of block mb + 1, one matrix
-        // instruction per two rows of block mb's dS, then block mb's dK contraction.
+        // into dS)
         f32x16 dkt[JT];
 #pragma unroll
         for (int jt = 0; jt < JT; ++jt)
 #pragma unroll
             for (int r = 0; r < 16; ++r) dkt[jt][r] = XV ? dvt[jt][r] : 0.f;
-        f32x16 da_cur;
-        {
-            bf16x8 op[KS];
-            row_ops(NBLK % NBUF, op);
-            da_cur = row_tile(op, vop);
-        }
+        bf16x8 dsp[2];   // dS of the previous block, packed
         static_for<NBLK>([&](auto mbc) {
             constexpr int mb = decltype(mbc)::value, S = NBLK + mb, B = S % NBUF;
-            constexpr bool nx_tile = mb + 1 < NBLK;
             fetch_stage(std::integral_constant<int, S + C::AHEAD>{}, cur, nxt, more);
             if constexpr (S == NBLK + 1) {
                 load_rows(a.K, more ? nxt : cur, XV ? vb : kb);
                 lse_n = load_lse(more ? nxt : cur);
             }
-            bf16x8 yop[KS], pop[2 * JT];
-            if constexpr (nx_tile) row_ops((S + 1) % NBUF, yop);
-            col_ops(B, pop);
-            f32x16 da_nx;
-#pragma unroll
-            for (int r = 0; r < 16; ++r) da_nx[r] = 0.f;
+            bf16x8 yop[KS];
+            if constexpr (mb + 1 < NBLK) row_ops((S + 1) % NBUF, yop);
+            // dK(mb - 1) beside dS of block mb
             float e[16];
-            constexpr int RPK = 16 / KS;
 #pragma unroll
-            for (int kk = 0; kk < KS; ++kk) {
-                if constexpr (nx_tile) da_nx = __builtin_amdgcn_mfma_f32_32x32x16_bf16(yop[kk], vop[kk], da_nx, 0, 0, 0);
+            for (int q = 0; q < 2 * JT; ++q) {
+                if constexpr (mb > 0) {
+                    const int jt = q >> 1, c = q & 1;
+                    dkt[jt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(cop[q], dsp[c], dkt[jt], 0, 0, 0);
+                }
 #pragma unroll
-                for (int q = 0; q < RPK; ++q) {
-                    const int r = kk * RPK + q;
+                for (int u = 0; u < RPS; ++u) {
+                    const int r = q * RPS + u;
                     const float A = (float)ah[mb][r >> 3][r & 7];
                     const float g = da_cur[r] - Dt;
                     e[r] = XV ? A * (g * a.scale) : A * g;
                 }
                 __builtin_amdgcn_sched_barrier(0);
             }
-            col_acc(pop, pack8(e), pack8(e + 8), dkt);
+            dsp[0] = pack8(e);
+            dsp[1] = pack8(e + 8);
+            // dA chain of block mb + 1, and block mb's dK operands for the next stage
+            if constexpr (mb + 1 < NBLK) chain_and_reads(yop, vop, da_cur, B, cop);
+            else col_ops(B, cop);
             stage_end(std::integral_constant<int, S>{});
-            if constexpr (nx_tile) da_cur = da_nx;
         });
 
-        // the next block's first S^T tile (its stage 0 has landed) before the row
-        // stores, whose completion the next stage's end waits for
+        // the next block's first S^T tile (its stage 0 has landed) beside the last
+        // dK contraction, before the row stores, whose completion the next stage's
+        // end waits for
         if (more) {
             if constexpr (XV) {
 #pragma unroll
@@ -936,11 +988,17 @@ __global__ __launch_bounds__(256, 1) void bwd_token_held_kernel(TokArgs a) {
             }
             bf16x8 op[KS];
             row_ops(0, op);
+            col_acc(cop, dsp[0], dsp[1], dkt);
             s_cur = row_tile(op, kb);
             nl = -lse_n * kLog2e;
+        } else {
+            col_acc(cop, dsp[0], dsp[1], dkt);
         }
-        store_token_rows<D, C::ROWF>(dkt, stg, XV ? a.dX : a.dK, XV ? 1.0f : a.scale, tb + 32 * w, te, a.H, h,
-                                     XV && a.dx_add, lane);
+        if (add)
+            store_token_rows<D, C::ROWF>(dkt, stg, a.dX, 1.0f, tb + 32 * w, te, a.H, h, true, lane);
+        else
+            store_token_rows<D, C::ROWF, true>(dkt, stg, XV ? a.dX : a.dK, XV ? 1.0f : a.scale, tb + 32 * w, te,
+                                               a.H, h, false, lane);
         if (!more) break;
         cur = nxt;
     }
