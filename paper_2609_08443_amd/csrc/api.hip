@@ -141,19 +141,27 @@ FwdPlan plan_fwd(int64_t B, int64_t T, int32_t H, int32_t M, int32_t d, sa_dtype
         off = align_up(off + bytes, 256);
         return o;
     };
+    // both paths cut the head-major token space into equal ranges (a work list
+    // of (user, head) segments, split pairs merged in segment order): the fused
+    // kernel runs one range per workgroup slot, the plain aggregation one range
+    // per 64 prototypes and about four workgroups per CU
+    const int64_t HT = (int64_t)H * T;
     if (p.fused) {
-        const int64_t HT = (int64_t)H * T;
         p.C = fused_chunk_tokens(T, H, M, d);
-        p.n_ranges = (HT + p.C - 1) / p.C;
-        p.max_items = p.n_ranges + (int64_t)H * B;
-        p.off_nitems = carve(sizeof(int64_t));
-        p.off_wgstart = carve(sizeof(int32_t) * (p.n_ranges + 1));
-        p.off_pairstart = carve(sizeof(int32_t) * ((int64_t)H * B + 1));
-        p.off_items = carve(sizeof(int32_t) * sa::IT_WORDS * p.max_items);
-        p.off_partials = carve(sizeof(float) * (size_t)p.max_items * M * d);
-    } else if (need_lse_scratch) {
-        p.off_lse = carve(sizeof(float) * (size_t)T * H);
+    } else {
+        const int64_t target = 4 * (int64_t)device_cus();
+        int64_t C = (HT + target - 1) / target;
+        C = (C + sa::kTileTokens - 1) / sa::kTileTokens * sa::kTileTokens;
+        p.C = C < sa::kTileTokens ? sa::kTileTokens : C;
     }
+    p.n_ranges = (HT + p.C - 1) / p.C;
+    p.max_items = p.n_ranges + (int64_t)H * B;
+    p.off_nitems = carve(sizeof(int64_t));
+    p.off_wgstart = carve(sizeof(int32_t) * (p.n_ranges + 1));
+    p.off_pairstart = carve(sizeof(int32_t) * ((int64_t)H * B + 1));
+    p.off_items = carve(sizeof(int32_t) * sa::IT_WORDS * p.max_items);
+    p.off_partials = carve(sizeof(float) * (size_t)p.max_items * M * d);
+    if (!p.fused && need_lse_scratch) p.off_lse = carve(sizeof(float) * (size_t)T * H);
     p.total = off;
     return p;
 }
@@ -619,18 +627,18 @@ sa_status run_fwd(const void* K, const void* V, const void* P, const int64_t* of
                   float* sketch, float* lse, uint8_t* ws, const FwdPlan& plan, hipStream_t stream,
                   bool p_user) {
     hipError_t e;
+    int32_t* items = reinterpret_cast<int32_t*>(ws + plan.off_items);
+    int32_t* wg_start = reinterpret_cast<int32_t*>(ws + plan.off_wgstart);
+    int32_t* pair_start = reinterpret_cast<int32_t*>(ws + plan.off_pairstart);
+    int64_t* n_items = reinterpret_cast<int64_t*>(ws + plan.off_nitems);
+    float* partials = reinterpret_cast<float*>(ws + plan.off_partials);
+    {
+        sa::ProfScope ps("worklist", stream);
+        e = sa::launch_worklist(offsets, B, T, H, plan.C, plan.n_ranges, items, plan.max_items, wg_start,
+                                pair_start, n_items, stream);
+    }
+    if (e != hipSuccess) return hip_fail(e, "work list launch");
     if (plan.fused) {
-        int32_t* items = reinterpret_cast<int32_t*>(ws + plan.off_items);
-        int32_t* wg_start = reinterpret_cast<int32_t*>(ws + plan.off_wgstart);
-        int32_t* pair_start = reinterpret_cast<int32_t*>(ws + plan.off_pairstart);
-        int64_t* n_items = reinterpret_cast<int64_t*>(ws + plan.off_nitems);
-        float* partials = reinterpret_cast<float*>(ws + plan.off_partials);
-        {
-            sa::ProfScope ps("worklist", stream);
-            e = sa::launch_worklist(offsets, B, T, H, plan.C, plan.n_ranges, items,
-                                    plan.max_items, wg_start, pair_start, n_items, stream);
-        }
-        if (e != hipSuccess) return hip_fail(e, "work list launch");
         sa::FusedFwdArgs a;
         a.K = reinterpret_cast<const uint16_t*>(K);
         a.V = reinterpret_cast<const uint16_t*>(V);
@@ -665,10 +673,21 @@ sa_status run_fwd(const void* K, const void* V, const void* P, const int64_t* of
     float* lse_out = lse ? lse : reinterpret_cast<float*>(ws + plan.off_lse);
     {
         sa::ProfScope ps("plain_fwd", stream);
-        e = sa::launch_generic_fwd(K, V, P, offsets, B, T, H, M, d, scale, dtype == SA_BF16,
-                                   sketch, lse_out, stream, p_user);
+        sa::GenericFwdItems wi;
+        wi.items = items;
+        wi.wg_start = wg_start;
+        wi.n_ranges = plan.n_ranges;
+        wi.max_items = plan.max_items;
+        wi.partials = partials;
+        e = sa::launch_generic_fwd(K, V, P, offsets, B, T, H, M, d, scale, dtype == SA_BF16, sketch, lse_out, wi,
+                                   stream, p_user);
     }
     if (e != hipSuccess) return hip_fail(e, "fp32 forward launch");
+    {
+        sa::ProfScope ps("splitL_merge", stream);
+        e = sa::launch_merge(pair_start, B, H, plan.max_items, partials, (int64_t)M * d, sketch, stream);
+    }
+    if (e != hipSuccess) return hip_fail(e, "split-L merge launch");
     return SA_OK;
 }
 

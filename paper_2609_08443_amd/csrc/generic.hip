@@ -3,9 +3,13 @@
 // instance for.  Same ABI and results as the fused path up to rounding.
 //
 // Forward (section 3.1): a first kernel computes each token's log-sum-exp of
-// its scaled logits over the M prototypes; a second computes, for a block of
-// 64 prototypes of one (user, head), A[t,m] = exp(s[t,m] - lse[t]) and
-// accumulates A[t,m] V[t,:] over the user's tokens.
+// its scaled logits over the M prototypes (one wave per token and head, lanes
+// over the prototypes); a second computes, for a block of 64 prototypes and
+// one work-list segment (a user's tokens inside one token range, the ranges
+// cutting the head-major token space into equal parts), A[t,m] = exp(s[t,m] -
+// lse[t]) and accumulates A[t,m] V[t,:] over the segment.  A (user, head) held
+// by one segment writes its sketch directly; split ones write partials that
+// the work list's merge adds in segment order.
 //
 // Backward (chain rule of the forward; the MRLB sum over R target instances of
 // section 4.2 is done first): per token, D_t = sum_m A g, dV_t = sum_m A dY_m,
@@ -50,16 +54,16 @@ __device__ inline float wave_sum(float v) {
 }
 
 // ---------------------------------------------------------------- forward
-// one thread per (t, h): lse = log sum_m exp(scale * <K_t, P_m>).  With per-user
-// prototypes (p_user) P is [B, H, M, d] and the token's user selects its block.
+// one wave per (t, h): lane l takes prototypes l, l + 64, ...; each lane keeps
+// a running maximum and a sum rescaled to it, and the wave combines them
+// (maximum first, then the rescaled sums)
 template <bool BF16, int D>
-__global__ __launch_bounds__(256) void lse_kernel(const void* __restrict__ K,
-                                                  const void* __restrict__ P,
-                                                  const int64_t* __restrict__ off, int64_t B,
-                                                  int64_t T, int32_t H, int32_t M, float scale,
-                                                  bool p_user, float* __restrict__ lse) {
-    constexpr int d = D;
-    const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+__global__ __launch_bounds__(256) void lse_wave_kernel(const void* __restrict__ K, const void* __restrict__ P,
+                                                       const int64_t* __restrict__ off, int64_t B, int64_t T,
+                                                       int32_t H, int32_t M, float scale, bool p_user,
+                                                       float* __restrict__ lse) {
+    const int lane = threadIdx.x & 63;
+    const int64_t i = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
     if (i >= T * H) return;
     const int64_t t = i / H;
     const int32_t h = (int32_t)(i % H);
@@ -71,13 +75,13 @@ __global__ __launch_bounds__(256) void lse_kernel(const void* __restrict__ K,
     }
     float kr[D];
 #pragma unroll
-    for (int j = 0; j < d; ++j) kr[j] = ld<BF16>(K, (t * H + h) * d + j);
+    for (int j = 0; j < D; ++j) kr[j] = ld<BF16>(K, (t * H + h) * D + j);
     float mu = -INFINITY, z = 0.f;
-    for (int m = 0; m < M; ++m) {
+    for (int m = lane; m < M; m += 64) {
         float s = 0.f;
-        const int64_t pb = (pi * M + m) * d;
+        const int64_t pb = (pi * M + m) * D;
 #pragma unroll
-        for (int j = 0; j < d; ++j) s = __builtin_fmaf(kr[j], ld<BF16>(P, pb + j), s);
+        for (int j = 0; j < D; ++j) s = __builtin_fmaf(kr[j], ld<BF16>(P, pb + j), s);
         s *= scale;
         if (s > mu) {
             z = z * expf(mu - s) + 1.0f;
@@ -86,45 +90,58 @@ __global__ __launch_bounds__(256) void lse_kernel(const void* __restrict__ K,
             z += expf(s - mu);
         }
     }
-    lse[i] = mu + logf(z);
+    float mw = mu;
+#pragma unroll
+    for (int k = 1; k < 64; k <<= 1) mw = fmaxf(mw, __shfl_xor(mw, k, 64));
+    const float zw = wave_sum(mu == -INFINITY ? 0.f : z * expf(mu - mw));
+    if (lane == 0) lse[i] = mw + logf(zw);
 }
 
-// block = 256 threads: 64 prototypes x 4 column quarters; grid = (B*H, ceil(M/64))
+// block = 256 threads: 64 prototypes x 4 column quarters; grid = (ranges,
+// ceil(M/64)); the block takes the segments of its range in order
 template <bool BF16, int D>
-__global__ __launch_bounds__(256) void agg_kernel(const void* __restrict__ K,
-                                                  const void* __restrict__ V,
-                                                  const void* __restrict__ P,
-                                                  const int64_t* __restrict__ off, int64_t B,
-                                                  int64_t T, int32_t H, int32_t M,
-                                                  float scale, bool p_user, const float* __restrict__ lse,
-                                                  float* __restrict__ sketch) {
-    constexpr int d = D;
-    const int64_t pair = blockIdx.x;  // b*H + h
-    const int64_t b = pair / H;
-    const int32_t h = (int32_t)(pair % H);
+__global__ __launch_bounds__(256) void agg_items_kernel(const void* __restrict__ K, const void* __restrict__ V,
+                                                        const void* __restrict__ P,
+                                                        const int32_t* __restrict__ items,
+                                                        const int32_t* __restrict__ wg_start, int64_t max_items,
+                                                        int64_t B, int64_t T, int32_t H, int32_t M, float scale,
+                                                        bool p_user, const float* __restrict__ lse,
+                                                        float* __restrict__ sketch, float* __restrict__ partials) {
+    constexpr int dq = D / 4;
     const int mi = threadIdx.x >> 2, jq = threadIdx.x & 3;
     const int m = blockIdx.y * 64 + mi;
-    constexpr int dq = D / 4;
     const int jb = jq * dq;
     const bool mv = m < M;
-    float pr[dq], acc[dq];
-    for (int c = 0; c < dq; ++c) {
-        pr[c] = mv ? ld<BF16>(P, ((p_user ? pair : (int64_t)h) * M + m) * d + jb + c) : 0.f;
-        acc[c] = 0.f;
-    }
-    const int64_t t0 = clampT(off[b], T), t1 = clampT(off[b + 1], T);
-    for (int64_t t = t0; t < t1; ++t) {
-        const int64_t base = (t * H + h) * d + jb;
-        float ps = 0.f;
-        for (int c = 0; c < dq; ++c) ps = __builtin_fmaf(ld<BF16>(K, base + c), pr[c], ps);
-        ps += __shfl_xor(ps, 1, 64);
-        ps += __shfl_xor(ps, 2, 64);
-        const float aw = expf(ps * scale - lse[t * H + h]);
-        for (int c = 0; c < dq; ++c) acc[c] = __builtin_fmaf(aw, ld<BF16>(V, base + c), acc[c]);
-    }
-    if (mv) {
-        float* out = sketch + (pair * M + m) * (int64_t)d + jb;
-        for (int c = 0; c < dq; ++c) out[c] = acc[c];
+    const int64_t k0 = wg_start[blockIdx.x], k1 = wg_start[blockIdx.x + 1];
+    if (k0 < 0 || k1 < k0 || k1 > max_items) return;
+    for (int64_t k = k0; k < k1; ++k) {
+        const int32_t* it = items + k * IT_WORDS;
+        const int b = it[IT_B], h = it[IT_H], t0 = it[IT_T0], t1 = it[IT_T1];
+        if (b < 0 || b >= B || h < 0 || h >= H || t0 < 0 || t1 < t0 || t1 > T) continue;
+        const int64_t pair = (int64_t)b * H + h;
+        float pr[dq], acc[dq];
+#pragma unroll
+        for (int c = 0; c < dq; ++c) {
+            pr[c] = mv ? ld<BF16>(P, ((p_user ? pair : (int64_t)h) * M + m) * D + jb + c) : 0.f;
+            acc[c] = 0.f;
+        }
+        for (int64_t t = t0; t < t1; ++t) {
+            const int64_t base = (t * H + h) * D + jb;
+            float ps = 0.f;
+#pragma unroll
+            for (int c = 0; c < dq; ++c) ps = __builtin_fmaf(ld<BF16>(K, base + c), pr[c], ps);
+            ps += __shfl_xor(ps, 1, 64);
+            ps += __shfl_xor(ps, 2, 64);
+            const float aw = expf(ps * scale - lse[t * H + h]);
+#pragma unroll
+            for (int c = 0; c < dq; ++c) acc[c] = __builtin_fmaf(aw, ld<BF16>(V, base + c), acc[c]);
+        }
+        if (mv) {
+            float* out = (it[IT_SPLIT] ? partials + k * (int64_t)M * D : sketch + pair * (int64_t)M * D) +
+                         (int64_t)m * D + jb;
+#pragma unroll
+            for (int c = 0; c < dq; ++c) out[c] = acc[c];
+        }
     }
 }
 
@@ -291,17 +308,18 @@ __global__ __launch_bounds__(256) void dp_reduce_kernel(const float* __restrict_
 
 template <bool BF16, int D>
 hipError_t fwd_impl(const void* K, const void* V, const void* P, const int64_t* off, int64_t B,
-                    int64_t T, int32_t H, int32_t M, int32_t d, float scale, bool p_user, float* sketch,
-                    float* lse, hipStream_t stream) {
+                    int64_t T, int32_t H, int32_t M, float scale, bool p_user, float* sketch,
+                    float* lse, const GenericFwdItems& w, hipStream_t stream) {
     if (T * H > 0) {
-        hipLaunchKernelGGL((lse_kernel<BF16, D>), dim3((unsigned)((T * H + 255) / 256)), dim3(256), 0,
+        hipLaunchKernelGGL((lse_wave_kernel<BF16, D>), dim3((unsigned)((T * H + 3) / 4)), dim3(256), 0,
                            stream, K, P, off, B, T, H, M, scale, p_user, lse);
         hipError_t e = hipGetLastError();
         if (e != hipSuccess) return e;
     }
-    if (B * H > 0) {
-        hipLaunchKernelGGL((agg_kernel<BF16, D>), dim3((unsigned)(B * H), (unsigned)((M + 63) / 64)),
-                           dim3(256), 0, stream, K, V, P, off, B, T, H, M, scale, p_user, lse, sketch);
+    if (w.n_ranges > 0) {
+        hipLaunchKernelGGL((agg_items_kernel<BF16, D>), dim3((unsigned)w.n_ranges, (unsigned)((M + 63) / 64)),
+                           dim3(256), 0, stream, K, V, P, w.items, w.wg_start, w.max_items, B, T, H, M, scale,
+                           p_user, lse, sketch, w.partials);
         return hipGetLastError();
     }
     return hipSuccess;
@@ -347,8 +365,9 @@ hipError_t bwd_impl(const void* K, const void* V, const void* P, const int64_t* 
 
 hipError_t launch_generic_fwd(const void* K, const void* V, const void* P, const int64_t* off,
                               int64_t B, int64_t T, int32_t H, int32_t M, int32_t d, float scale,
-                              bool bf16, float* sketch, float* lse_out, hipStream_t stream, bool p_user) {
-#define SA_FWD(BF, DD) fwd_impl<BF, DD>(K, V, P, off, B, T, H, M, d, scale, p_user, sketch, lse_out, stream)
+                              bool bf16, float* sketch, float* lse_out, const GenericFwdItems& w,
+                              hipStream_t stream, bool p_user) {
+#define SA_FWD(BF, DD) fwd_impl<BF, DD>(K, V, P, off, B, T, H, M, scale, p_user, sketch, lse_out, w, stream)
     if (d == 64) return bf16 ? SA_FWD(true, 64) : SA_FWD(false, 64);
     if (d == 128) return bf16 ? SA_FWD(true, 128) : SA_FWD(false, 128);
 #undef SA_FWD

@@ -210,10 +210,18 @@ hipError_t launch_sum_users(const float* part, int64_t B, int32_t H, int64_t n, 
 hipError_t launch_add(const float* a, const float* b, float* out, int64_t n, hipStream_t stream);
 
 // Plain fp32-arithmetic path (fp32 or bf16 inputs).
-hipError_t launch_generic_fwd(const void* K, const void* V, const void* P,
-                              const int64_t* offsets, int64_t B, int64_t T, int32_t H,
-                              int32_t M, int32_t d, float scale, bool bf16, float* sketch,
-                              float* lse_out, hipStream_t stream, bool p_user = false);
+// Work list of the plain forward's aggregation (the fused forward's format:
+// items and per-range starts from launch_worklist) and the partial sketches of
+// (user, head) pairs split across ranges, merged by launch_merge.
+struct GenericFwdItems {
+    const int32_t* items = nullptr;
+    const int32_t* wg_start = nullptr;
+    int64_t n_ranges = 0, max_items = 0;
+    float* partials = nullptr;
+};
+hipError_t launch_generic_fwd(const void* K, const void* V, const void* P, const int64_t* off, int64_t B,
+                              int64_t T, int32_t H, int32_t M, int32_t d, float scale, bool bf16, float* sketch,
+                              float* lse_out, const GenericFwdItems& w, hipStream_t stream, bool p_user);
 
 // dY[b,h] = sum_r dsketch[b,r,h]  (fp32, [B,H,M,d])
 hipError_t launch_dy_reduce(const float* dsketch, int64_t B, int32_t R, int32_t H, int64_t MD,
