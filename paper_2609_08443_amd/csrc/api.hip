@@ -33,23 +33,8 @@ inline size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 
-// per-device constant: number of compute units (read once per device)
+using sa::device_cus;
 constexpr int kMaxDevices = 64;
-std::once_flag g_cu_once[kMaxDevices];
-int g_cu_count[kMaxDevices];
-
-int device_cus() {
-    int dev = 0;
-    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return 256;
-    std::call_once(g_cu_once[dev], [dev] {
-        int n = 0;
-        if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
-            n <= 0)
-            n = 256;
-        g_cu_count[dev] = n;
-    });
-    return g_cu_count[dev];
-}
 
 // ---------------------------------------------------------------- kernel timing
 struct ProfRec {
@@ -772,6 +757,24 @@ sa_status run_bwd(const void* K, const void* V, const void* P, const int64_t* of
 }  // namespace
 
 namespace sa {
+
+// per-device constant: number of compute units (read once per device)
+static constexpr int kMaxCuDevices = 64;
+static std::once_flag g_cu_once[kMaxCuDevices];
+static int g_cu_count[kMaxCuDevices];
+
+int device_cus() {
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxCuDevices) return 256;
+    std::call_once(g_cu_once[dev], [dev] {
+        int n = 0;
+        if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+            n <= 0)
+            n = 256;
+        g_cu_count[dev] = n;
+    });
+    return g_cu_count[dev];
+}
 
 ProfScope::ProfScope(const char* name, hipStream_t stream) : stream_(stream) {
     if (!g_prof_on) return;

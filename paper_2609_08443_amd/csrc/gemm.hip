@@ -42,6 +42,7 @@ struct MgArgs {
     int32_t M, N, K, tm, tn;
     float alpha;
     int32_t accumulate;
+    int32_t c_rows16;   // N, c_m, c_z multiples of 8 and C 16-byte aligned
 };
 
 // One thread's share of a [128 rows][64 k] slab: four 16-byte pieces of 8 bf16,
@@ -265,6 +266,367 @@ __global__ __launch_bounds__(256, 2) void mfma_gemm_kernel(MgArgs g) {
         }
 }
 
+// ---------------------------------------------------------------------------
+// Large tiles for bf16 operands: BM x BN = (32 FM PM) x (32 FN PN) per workgroup of
+// four waves in a PM x PN grid, each wave FM x FN v_mfma_f32_32x32x16_bf16 tiles,
+// one workgroup per CU.  Three LDS stages of one 64-deep k slab each, loaded two
+// slabs ahead.  A k-contiguous operand goes straight from global memory into its
+// swizzled LDS layout (global_load_lds, lane l of a load writing the 16-byte
+// chunk that belongs at LDS position l), so it takes neither registers nor LDS
+// store instructions; an m- (n-) contiguous operand is loaded into one of two
+// register sets and transposed into LDS by the stores of store_slab, one slab
+// after it was loaded.  Every slab issues the same number of loads per thread
+// ((BM + BN) / 32: rows and columns past the matrix read its last ones), so the
+// wait for slab kt + 1 at the end of slab kt is a fixed count: the loads of slab
+// kt + 2 stay in flight across the barrier.
+template <int FM, int FN, int PM, int PN>
+struct LtCfg {
+    static constexpr int BM = 32 * FM * PM, BN = 32 * FN * PN;
+    static constexpr int A_BYTES = BM * GBK * 2, B_BYTES = BN * GBK * 2;
+    static constexpr int STAGE = A_BYTES + B_BYTES, NS = 3, LDS = NS * STAGE;
+    static constexpr int LOADS = (BM + BN) / 32;
+    // workgroups per CU that the LDS allows (registers are sized for it)
+    static constexpr int OCC = LDS <= 80 * 1024 ? 2 : 1;
+    static_assert(PM * PN == 4, "four waves");
+    static_assert(LDS <= 160 * 1024, "LDS");
+    static_assert(LOADS < 64, "vmcnt range");
+};
+
+// Direct global -> LDS copy of 16 bytes per lane (global_load_lds_dwordx4) from
+// base + off (base wave-uniform) to LDS bytes [lds + 16 lane, + 16), written as
+// inline assembly: the compiler cannot tell which LDS bytes such a load writes,
+// so for the builtin it makes the transposing LDS reads wait for every load in
+// flight, the next slabs' included.  Completion is awaited by the explicit
+// vmcnt waits of lt_barrier (and the vmcnt(0) before the epilogue).
+__device__ __forceinline__ void lt_dma16(const char* base, uint32_t off, const uint8_t* lds) {
+    const uint32_t l = (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) uint8_t*)lds;
+    asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, %1" ::"v"(off), "s"(base), "s"(l)
+                 : "memory", "m0");
+}
+
+template <int N>
+__device__ __forceinline__ void lt_barrier() {
+    static_assert(N >= 0 && N < 64, "vmcnt range");
+    __builtin_amdgcn_sched_barrier(0);
+    __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | (0 << 8) | ((N >> 4) << 14));
+    __builtin_amdgcn_s_barrier();
+    __builtin_amdgcn_sched_barrier(0);
+}
+
+template <int R, bool KC>
+struct LtOperand;
+
+// k-contiguous operand, R rows: load q = w + 4 i (i < R / 32) of a slab fills LDS
+// rows 8 q .. 8 q + 7; lane l takes row 8 q + l / 8 and the chunk whose swizzled
+// position is l % 8.  Offsets are 32-bit byte offsets from the batch's base.
+template <int R>
+struct LtOperand<R, true> {
+    static constexpr int Q = R / 32;
+    const char* base;
+    int64_t step;   // bytes from one slab to the next
+    uint32_t off[Q];
+    __device__ __forceinline__ void init(const uint16_t* b, int64_t s_row, int64_t /*s_k*/, int row0, int nrows,
+                                         int w, int lane) {
+        base = reinterpret_cast<const char*>(b);
+        step = GBK * 2;
+#pragma unroll
+        for (int i = 0; i < Q; ++i) {
+            const int row = 8 * (w + 4 * i) + (lane >> 3);
+            const int c = (lane & 7) ^ swz_x<64>(row);
+            const int gr = min(row0 + row, nrows - 1);
+            off[i] = (uint32_t)(((int64_t)gr * s_row + 8 * c) * 2);
+        }
+    }
+    __device__ __forceinline__ void issue(int kt, uint8_t* lds, int w) {
+        const char* p = base + kt * step;
+#pragma unroll
+        for (int i = 0; i < Q; ++i) lt_dma16(p, off[i], lds + (w + 4 * i) * 1024);
+    }
+};
+
+// m- (n-) contiguous operand: the slab is kept as it lies in memory, [64 k][R]
+// (rows of R bf16, unswizzled), two rows per load of a wave: lane l of load
+// q = w + 4 i takes row 2 q + l / 32, columns 8 (l % 32) .. + 7 (columns past the
+// matrix read its last eight).  Its fragments are read with the transposing
+// ds_read_b64_tr_b16 (frag).
+template <int R>
+struct LtOperand<R, false> {
+    static_assert(R % 64 == 0 && R <= 512, "transposed operand tile");
+    static constexpr int Q = R / 32, LPR = R / 8;   // loads per thread, lanes per row
+    static_assert(64 % LPR == 0, "whole rows per load");
+    static constexpr int RPL = 64 / LPR;            // rows per load
+    const char* base;
+    int64_t step;
+    uint32_t off[Q];
+    __device__ __forceinline__ void init(const uint16_t* b, int64_t /*s_row*/, int64_t s_k, int row0, int nrows,
+                                         int w, int lane) {
+        base = reinterpret_cast<const char*>(b);
+        step = GBK * s_k * 2;
+#pragma unroll
+        for (int i = 0; i < Q; ++i) {
+            const int idx = (w + 4 * i) * 64 + lane;        // chunk index in the slab
+            const int k = idx / LPR, col = min(row0 + 8 * (idx % LPR), nrows - 8);
+            off[i] = (uint32_t)(((int64_t)k * s_k + col) * 2);
+        }
+    }
+    __device__ __forceinline__ void issue(int kt, uint8_t* lds, int w) {
+        const char* p = base + kt * step;
+#pragma unroll
+        for (int i = 0; i < Q; ++i) lt_dma16(p, off[i], lds + (w + 4 * i) * 1024);
+    }
+};
+
+// fragment (32 rows or columns from `first`, k step ks) of an operand slab in LDS:
+// k-contiguous: ds_read_b128 of the swizzled rows; otherwise two transposing
+// reads: inside each 16-lane group, lane i receives element i % 4 of the 8-byte
+// pieces addressed by lanes 4 e + i / 4 (e < 4), so lane 4 e + j addresses k row
+// e (then e + 4) and columns 4 j .. 4 j + 3 of its group's 16 columns.
+template <int R, bool KC>
+__device__ __forceinline__ bf16x8 lt_frag(const uint8_t* lds, int first, int ks, int lane) {
+    const int l32 = lane & 31, hl = lane >> 5;
+    if constexpr (KC) {
+        return lds_b128(reinterpret_cast<const uint16_t*>(lds), swz<64>(first + l32, 2 * ks + hl));
+    } else {
+        typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
+        const int s = lane & 15, g = (lane >> 4) & 1;
+        const int k = 16 * ks + 8 * hl + (s >> 2), col = first + 16 * g + 4 * (s & 3);
+        typedef __attribute__((address_space(3))) short lds_short;
+        lds_short* p = (lds_short*)(const_cast<uint8_t*>(lds)) + k * R + col;
+        const s16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)p);
+        const s16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(p + 4 * R));
+        return __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
+    }
+}
+
+template <int FM, int FN, int PM, int PN, bool A_KC, bool B_KC, bool C_BF16>
+__global__ __launch_bounds__(256, (LtCfg<FM, FN, PM, PN>::OCC)) void mfma_gemm_lt_kernel(MgArgs g) {
+    using C = LtCfg<FM, FN, PM, PN>;
+    __shared__ __attribute__((aligned(16))) uint8_t smem[C::LDS];
+    const int tid = threadIdx.x, lane = tid & 63, l32 = lane & 31, hl = lane >> 5;
+    const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int64_t tiles = (int64_t)g.tm * g.tn;
+    const int64_t id = xcd_range(blockIdx.x, gridDim.x);
+    const int64_t z = id / tiles;
+    const int tt = (int)(id % tiles);
+    const int m0 = (tt / g.tn) * C::BM, n0 = (tt % g.tn) * C::BN;
+    const uint16_t* Ab = reinterpret_cast<const uint16_t*>(g.A) + z * g.a_z;
+    const uint16_t* Bb = reinterpret_cast<const uint16_t*>(g.B) + (g.b_mod > 0 ? z % g.b_mod : z) * g.b_z;
+    const int nk = g.K / GBK;
+    LtOperand<C::BM, A_KC> opa;
+    LtOperand<C::BN, B_KC> opb;
+    opa.init(Ab, g.a_m, g.a_k, m0, g.M, w, lane);
+    opb.init(Bb, g.b_n, g.b_k, n0, g.N, w, lane);
+    auto stage = [&](int s) { return smem + (s % 3) * C::STAGE; };
+    // slab kt into the stage of slab position pos
+    auto issue = [&](int kt, int pos) __attribute__((always_inline)) {
+        uint8_t* st = stage(pos);
+        opa.issue(kt, st, w);
+        opb.issue(kt, st + C::A_BYTES, w);
+    };
+
+    f32x16 acc[FM][FN];
+#pragma unroll
+    for (int i = 0; i < FM; ++i)
+#pragma unroll
+        for (int j = 0; j < FN; ++j)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
+    const int wm = w % PM, wn = w / PM;
+    // operand reads of step ks + 1 are issued before the products of step ks
+    auto mul = [&](int kt) __attribute__((always_inline)) {
+        const uint8_t* As = stage(kt);
+        const uint8_t* Bs = stage(kt) + C::A_BYTES;
+        bf16x8 a[2][FM], b[2][FN];
+        auto rd = [&](int ks, bf16x8 (&ao)[FM], bf16x8 (&bo)[FN]) __attribute__((always_inline)) {
+#pragma unroll
+            for (int i = 0; i < FM; ++i) ao[i] = lt_frag<C::BM, A_KC>(As, 32 * (FM * wm + i), ks, lane);
+#pragma unroll
+            for (int j = 0; j < FN; ++j) bo[j] = lt_frag<C::BN, B_KC>(Bs, 32 * (FN * wn + j), ks, lane);
+        };
+        rd(0, a[0], b[0]);
+#pragma unroll
+        for (int ks = 0; ks < GBK / 16; ++ks) {
+            if (ks + 1 < GBK / 16) rd(ks + 1, a[(ks + 1) & 1], b[(ks + 1) & 1]);
+            __builtin_amdgcn_sched_barrier(0);   // keep the reads ahead of the products
+#pragma unroll
+            for (int i = 0; i < FM; ++i)
+#pragma unroll
+                for (int j = 0; j < FN; ++j)
+                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[ks & 1][i], b[ks & 1][j], acc[i][j], 0, 0, 0);
+            __builtin_amdgcn_sched_barrier(0);
+        }
+    };
+    // slab kt: slab kt + 2 is loaded, slab kt is multiplied, slab kt + 1's loads are
+    // awaited (the loads of slab kt + 2, if any, stay in flight)
+    issue(0, 0);
+    if (nk > 1) issue(1, 1);
+    if (nk > 1) lt_barrier<C::LOADS>();
+    else lt_barrier<0>();
+    for (int kt = 0; kt < nk; ++kt) {
+        const bool ahead = kt + 2 < nk;
+        if (ahead) issue(kt + 2, kt + 2);
+        mul(kt);
+        if (ahead) lt_barrier<C::LOADS>();
+        else if (kt + 1 < nk) lt_barrier<0>();
+    }
+
+    // Epilogue.  With 16-byte aligned rows of C, each wave passes its results
+    // through its own LDS area ([32 rows][32 FN + 8] fp32, one row of tiles at a
+    // time) so that a lane stores 8 consecutive outputs; otherwise one element per
+    // lane and register.
+    const bool rows16 = g.c_rows16 != 0;
+    __syncthreads();   // every wave is done with the operand stages
+    constexpr int P = 32 * FN + 8, LPR = 4 * FN, RPP = 64 / LPR;
+    float* stg = reinterpret_cast<float*>(smem) + w * 32 * P;
+#pragma unroll
+    for (int i = 0; i < FM; ++i) {
+        const int mt = m0 + 32 * (FM * wm + i);
+        if (rows16) {
+#pragma unroll
+            for (int j = 0; j < FN; ++j)
+#pragma unroll
+                for (int r = 0; r < 16; ++r) stg[srow(r, hl) * P + 32 * j + l32] = g.alpha * acc[i][j][r];
+            wave_lds_order();
+#pragma unroll
+            for (int ps = 0; ps < 32 / RPP; ++ps) {
+                const int rr = ps * RPP + lane / LPR, cc = 8 * (lane % LPR);
+                const float4 v0 = *reinterpret_cast<const float4*>(stg + rr * P + cc);
+                const float4 v1 = *reinterpret_cast<const float4*>(stg + rr * P + cc + 4);
+                const int m = mt + rr, n = n0 + 32 * FN * wn + cc;
+                if (m < g.M && n < g.N) {
+                    const int64_t o = z * g.c_z + (int64_t)m * g.c_m + n;
+                    float v[8] = {v0.x, v0.y, v0.z, v0.w, v1.x, v1.y, v1.z, v1.w};
+                    if constexpr (C_BF16) {
+                        uint4* Cp = reinterpret_cast<uint4*>(reinterpret_cast<uint16_t*>(g.C) + o);
+                        if (g.accumulate) {
+                            const uint4 c = *Cp;
+                            const uint32_t cw[4] = {c.x, c.y, c.z, c.w};
+#pragma unroll
+                            for (int e = 0; e < 8; ++e)
+                                v[e] += __uint_as_float((e & 1) ? (cw[e >> 1] & 0xffff0000u) : (cw[e >> 1] << 16));
+                        }
+                        *Cp = make_uint4(pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3]), pack_bf16x2(v[4], v[5]),
+                                         pack_bf16x2(v[6], v[7]));
+                    } else {
+                        float4* Cp = reinterpret_cast<float4*>(reinterpret_cast<float*>(g.C) + o);
+                        if (g.accumulate) {
+                            const float4 c0 = Cp[0], c1 = Cp[1];
+                            v[0] += c0.x; v[1] += c0.y; v[2] += c0.z; v[3] += c0.w;
+                            v[4] += c1.x; v[5] += c1.y; v[6] += c1.z; v[7] += c1.w;
+                        }
+                        Cp[0] = make_float4(v[0], v[1], v[2], v[3]);
+                        Cp[1] = make_float4(v[4], v[5], v[6], v[7]);
+                    }
+                }
+            }
+            wave_lds_order();
+        } else {
+#pragma unroll
+            for (int j = 0; j < FN; ++j) {
+                const int n = n0 + 32 * (FN * wn + j) + l32;
+                if (n >= g.N) continue;
+#pragma unroll
+                for (int r = 0; r < 16; ++r) {
+                    const int m = mt + srow(r, hl);
+                    if (m >= g.M) continue;
+                    const int64_t o = z * g.c_z + (int64_t)m * g.c_m + n;
+                    float v = g.alpha * acc[i][j][r];
+                    if constexpr (C_BF16) {
+                        uint16_t* Cp = reinterpret_cast<uint16_t*>(g.C);
+                        if (g.accumulate) v += __uint_as_float((uint32_t)Cp[o] << 16);
+                        Cp[o] = to_bf16(v);
+                    } else {
+                        float* Cp = reinterpret_cast<float*>(g.C);
+                        if (g.accumulate) v += Cp[o];
+                        Cp[o] = v;
+                    }
+                }
+            }
+        }
+    }
+}
+
+template <int FM, int FN, int PM, int PN, bool A_KC, bool B_KC>
+hipError_t lt_launch(MgArgs g, bool c_bf16, int64_t batch, hipStream_t stream) {
+    using C = LtCfg<FM, FN, PM, PN>;
+    g.tm = (g.M + C::BM - 1) / C::BM;
+    g.tn = (g.N + C::BN - 1) / C::BN;
+    const int64_t blocks = (int64_t)g.tm * g.tn * batch;
+    if (c_bf16)
+        hipLaunchKernelGGL((mfma_gemm_lt_kernel<FM, FN, PM, PN, A_KC, B_KC, true>), dim3((unsigned)blocks), dim3(256),
+                           0, stream, g);
+    else
+        hipLaunchKernelGGL((mfma_gemm_lt_kernel<FM, FN, PM, PN, A_KC, B_KC, false>), dim3((unsigned)blocks),
+                           dim3(256), 0, stream, g);
+    return hipGetLastError();
+}
+
+template <int FM, int FN, int PM, int PN>
+hipError_t lt_dispatch(const MgArgs& g, bool a_kc, bool b_kc, bool c_bf16, int64_t batch, hipStream_t stream) {
+    if (a_kc && b_kc) return lt_launch<FM, FN, PM, PN, true, true>(g, c_bf16, batch, stream);
+    if (a_kc) return lt_launch<FM, FN, PM, PN, true, false>(g, c_bf16, batch, stream);
+    if constexpr (LtCfg<FM, FN, PM, PN>::BM % 64 == 0) {
+        if (b_kc) return lt_launch<FM, FN, PM, PN, false, true>(g, c_bf16, batch, stream);
+        return lt_launch<FM, FN, PM, PN, false, false>(g, c_bf16, batch, stream);
+    }
+    return hipErrorInvalidValue;
+}
+
+// Tile shapes: rows, columns, relative speed per tile element (fewer LDS and L2
+// bytes per product for bigger tiles), workgroups per CU, and whether the A
+// operand may be m-contiguous (160 rows do not split into whole loads of rows).
+struct LtShape {
+    int bm, bn;
+    double eff;
+    int occ;
+    bool a_mc_ok;
+};
+constexpr LtShape kLtShapes[] = {{160, 256, 1.0, 1, false}, {128, 256, 0.85, 1, true}, {256, 128, 0.85, 1, true},
+                                 {128, 128, 0.7, 1, true},   {64, 128, 0.55, 2, true},  {128, 64, 0.6, 2, true},
+                                 {64, 64, 0.5, 2, true}};
+
+// The shape with the least estimated time: rounds of `occ` tiles per compute unit,
+// each round the tile's work over its speed times the tiles that share a CU (two
+// resident workgroups split its matrix cores); small tiles win where big ones
+// leave compute units idle.  -1 if none applies (byte offsets of a k-contiguous
+// operand beyond 32 bits).
+int choose_lt(const GemmDesc& d, bool a_kc, bool b_kc) {
+    auto fits = [&](bool kc, int64_t rows, int64_t s_row) {
+        return !kc || ((rows - 1) * s_row + d.K) * 2 < (int64_t(1) << 32);
+    };
+    if (!fits(a_kc, d.M, d.a_m) || !fits(b_kc, d.N, d.b_n)) return -1;
+    const int64_t cus = device_cus();
+    int best = -1;
+    double best_cost = 0;
+    for (int i = 0; i < (int)(sizeof(kLtShapes) / sizeof(kLtShapes[0])); ++i) {
+        const LtShape& t = kLtShapes[i];
+        if (!a_kc && !t.a_mc_ok) continue;
+        const int64_t tiles = (int64_t)((d.M + t.bm - 1) / t.bm) * ((d.N + t.bn - 1) / t.bn) * d.batch;
+        if (tiles >= (int64_t(1) << 31)) continue;
+        const int64_t rounds = (tiles + cus * t.occ - 1) / (cus * t.occ);
+        const int64_t share = std::min<int64_t>(t.occ, (tiles + cus - 1) / cus);
+        const double cost = (double)rounds * share * t.bm * t.bn / t.eff;
+        if (best < 0 || cost < best_cost) {
+            best = i;
+            best_cost = cost;
+        }
+    }
+    return best;
+}
+
+hipError_t lt_run(int shape, const MgArgs& g, bool a_kc, bool b_kc, bool c_bf16, int64_t batch,
+                  hipStream_t stream) {
+    switch (shape) {
+        case 0: return lt_dispatch<5, 2, 1, 4>(g, a_kc, b_kc, c_bf16, batch, stream);
+        case 1: return lt_dispatch<4, 2, 1, 4>(g, a_kc, b_kc, c_bf16, batch, stream);
+        case 2: return lt_dispatch<4, 2, 2, 2>(g, a_kc, b_kc, c_bf16, batch, stream);
+        case 3: return lt_dispatch<2, 2, 2, 2>(g, a_kc, b_kc, c_bf16, batch, stream);
+        case 4: return lt_dispatch<1, 2, 2, 2>(g, a_kc, b_kc, c_bf16, batch, stream);
+        case 5: return lt_dispatch<2, 1, 2, 2>(g, a_kc, b_kc, c_bf16, batch, stream);
+        default: return lt_dispatch<1, 1, 2, 2>(g, a_kc, b_kc, c_bf16, batch, stream);
+    }
+}
+
 template <bool A_KC, bool B_KC, typename TA, typename TB>
 hipError_t mgemm_launch_t(const MgArgs& g, bool c_bf16, int64_t batch, hipStream_t stream) {
     const int64_t blocks = (int64_t)g.tm * g.tn * batch;
@@ -320,7 +682,12 @@ hipError_t launch_gemm(const GemmDesc& d, hipStream_t stream) {
     g.tn = (d.N + GBN - 1) / GBN;
     g.alpha = d.alpha;
     g.accumulate = d.accumulate ? 1 : 0;
+    g.c_rows16 = (d.N % 8 == 0 && d.c_m % 8 == 0 && d.c_z % 8 == 0 && al16(d.C)) ? 1 : 0;
     const bool a_kc = d.a_k == 1, b_kc = d.b_k == 1;
+    if (d.a_bf16 && d.b_bf16) {
+        const int shape = choose_lt(d, a_kc, b_kc);
+        if (shape >= 0) return lt_run(shape, g, a_kc, b_kc, d.c_bf16, d.batch, stream);
+    }
     if (a_kc && b_kc) return mgemm_launch<true, true>(g, d.a_bf16, d.b_bf16, d.c_bf16, d.batch, stream);
     if (a_kc) return mgemm_launch<true, false>(g, d.a_bf16, d.b_bf16, d.c_bf16, d.batch, stream);
     if (b_kc) return mgemm_launch<false, true>(g, d.a_bf16, d.b_bf16, d.c_bf16, d.batch, stream);

@@ -165,6 +165,8 @@ struct GemmDesc {
     bool round_bf16 = false;  // fp32 operands may be rounded to bf16 (matrix cores)
 };
 bool gemm_on_matrix_cores(const GemmDesc& d);
+// number of compute units of the current device (read once per device)
+int device_cus();
 hipError_t launch_gemm(const GemmDesc& d, hipStream_t stream);
 hipError_t launch_small_gemm_general(const GemmDesc& d, hipStream_t stream);
 
