@@ -112,15 +112,16 @@ def bwd_algorithmic_bytes(w: wl.Workload) -> float:
 
 # kernel name -> (algorithmic flops, executed matrix flops, algorithmic bytes, bound) of one
 # launch.  Algorithmic = the GEMMs of the method (Appendix G convention); executed also
-# counts the recomputation of S (and of dA) that the backward kernels do instead of storing.
+# counts the recomputation of S (and of dA) that the backward kernels do instead of storing:
+# the token side computes S once when its first sweep's weights fit in registers (M <= 512).
 def kernel_work(name: str, w: wl.Workload):
     th = float(w.T) * w.H
     md = float(w.M) * w.d
     el = 2 if w.dtype == "bf16" else 4
     if name == "fused_fwd":
         return 4 * md * th, 4 * md * th, fwd_algorithmic_bytes(w), "mfma"
-    if name == "bwd_token":   # dA, dV, dK (+ S twice)
-        return 6 * md * th, 10 * md * th, th * w.d * (2 * el + 8) + 4 * th, "mfma"
+    if name == "bwd_token":   # dA, dV, dK (+ S; for M > 512 S again in the second sweep)
+        return 6 * md * th, (8 if w.M <= 512 else 10) * md * th, th * w.d * (2 * el + 8) + 4 * th, "mfma"
     if name == "bwd_proto":   # dP (+ S and dA)
         return 2 * md * th, 6 * md * th, th * w.d * 2 * el + 8 * th, "mfma"
     if name == "plain_fwd":
