@@ -59,10 +59,10 @@ MEASURED_TRAFFIC = {
                   "64de729a0731a9ec24c6ecd9f1a1263cbbbb8b886e9dd98db9de8c9421d1097c",
                   1.115e9 + 0.143e9),
     "bwd_token": ("paper_2609_08443_amd/csrc/bwd_fused.hip",
-                  "57d0367bf7b2a9a5441602519ebfd053502bcd504f2584431bfee195eb7587c3",
-                  1.311e9 + 2.250e9),
+                  "04c2f979ec2709a93a48939f23c469eddc2e712161f692aa703e9002acbfd291",
+                  1.361e9 + 2.250e9),
     "bwd_proto": ("paper_2609_08443_amd/csrc/bwd_fused.hip",
-                  "57d0367bf7b2a9a5441602519ebfd053502bcd504f2584431bfee195eb7587c3",
+                  "04c2f979ec2709a93a48939f23c469eddc2e712161f692aa703e9002acbfd291",
                   1.219e9 + 0.100e9),
 }
 
