@@ -298,10 +298,20 @@ struct LtCfg {
 // so for the builtin it makes the transposing LDS reads wait for every load in
 // flight, the next slabs' included.  Completion is awaited by the explicit
 // vmcnt waits of lt_barrier (and the vmcnt(0) before the epilogue).
+// M0 (which holds the load's LDS address) is a reserved register, so the block
+// saves and restores it instead of declaring it clobbered.
 __device__ __forceinline__ void lt_dma16(const char* base, uint32_t off, const uint8_t* lds) {
     const uint32_t l = (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) uint8_t*)lds;
-    asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, %1" ::"v"(off), "s"(base), "s"(l)
-                 : "memory", "m0");
+    uint32_t saved;
+    asm volatile(
+        "s_mov_b32 %0, m0\n\t"
+        "s_mov_b32 m0, %3\n\t"
+        "s_nop 0\n\t"
+        "global_load_lds_dwordx4 %1, %2\n\t"
+        "s_mov_b32 m0, %0"
+        : "=&s"(saved)
+        : "v"(off), "s"(base), "s"(l)
+        : "memory");
 }
 
 template <int N>
