@@ -451,6 +451,30 @@ int64_t sa_sketch_fwd_chunk_tokens(int64_t B, int64_t T, int32_t H, int32_t M,
                                    int32_t d, sa_dtype dtype);
 
 /*
+ * The library's batched product on the matrix cores, for tests of each of its
+ * tile shapes (the STCA step and the layer and block gradients run on it):
+ *
+ *   C[z](m, n) = alpha sum_k A[z](m, k) B[z](k, n)  (+ C[z](m, n) when accumulate)
+ *
+ * with A[z](m, k) = A[z a_z + m a_m + k a_k] and B[z](k, n) = B[(z mod b_mod, or
+ * z when b_mod = 0) b_z + k b_k + n b_n] bf16 (device pointers, strides in
+ * elements), C[z](m, n) = C[z c_z + m c_m + n] fp32 (c_bf16 = 0) or bf16, fp32
+ * accumulation.  A is contiguous along k (a_k = 1) or along m (a_m = 1), B along k
+ * (b_k = 1) or along n (b_n = 1).  tile_shape < 0 lets the library pick the
+ * shape (as it does for its own products, including the register-tiled fp32
+ * product when the matrix cores cannot take it); 0 .. sa_gemm_tile_shapes() - 1
+ * forces one shape and returns SA_ERR_UNSUPPORTED where that shape cannot take
+ * the product (K not a multiple of 64, strides or bases not on 16 bytes, an
+ * m-contiguous A on the 160-row shape, byte offsets beyond 32 bits).  Operands
+ * and result are the caller's; asynchronous on `stream`.
+ */
+int32_t sa_gemm_tile_shapes(void);
+sa_status sa_gemm_bf16(const void* A, int64_t a_z, int64_t a_m, int64_t a_k, const void* B, int64_t b_z,
+                       int64_t b_k, int64_t b_n, int64_t b_mod, void* C, int32_t c_bf16, int64_t c_z, int64_t c_m,
+                       int32_t M, int32_t N, int32_t K, int32_t batch, float alpha, int32_t accumulate,
+                       int32_t tile_shape, void* stream);
+
+/*
  * Kernel timing for benchmarks.  While enabled (on = 1) on the calling thread,
  * every kernel the library launches from that thread is bracketed by two HIP
  * events recorded on the launch stream.  sa_kernel_times() waits for those

@@ -1550,4 +1550,27 @@ sa_status sa_build_worklist(const int64_t* offsets, int64_t B, int64_t T, int32_
     return SA_OK;
 }
 
+int32_t sa_gemm_tile_shapes(void) { return sa::gemm_tile_shapes(); }
+
+sa_status sa_gemm_bf16(const void* A, int64_t a_z, int64_t a_m, int64_t a_k, const void* B, int64_t b_z,
+                       int64_t b_k, int64_t b_n, int64_t b_mod, void* C, int32_t c_bf16, int64_t c_z, int64_t c_m,
+                       int32_t M, int32_t N, int32_t K, int32_t batch, float alpha, int32_t accumulate,
+                       int32_t tile_shape, void* stream_) {
+    g_last_error[0] = 0;
+    if (M < 0 || N < 0 || K < 1 || batch < 0 || b_mod < 0 || tile_shape >= sa::gemm_tile_shapes())
+        return fail(SA_ERR_INVALID_ARG, "bad sizes or tile shape");
+    if (M == 0 || N == 0 || batch == 0) return SA_OK;
+    if (!A || !B || !C) return fail(SA_ERR_INVALID_ARG, "null pointer argument");
+    if (!std::isfinite(alpha)) return fail(SA_ERR_INVALID_ARG, "alpha must be finite");
+    sa::GemmDesc d{A, true, a_z, a_m, a_k, B, true, b_z, b_k, b_n, C, c_bf16 != 0, c_z, c_m,
+                   M, N, K, batch, alpha, accumulate != 0, b_mod, false};
+    if (tile_shape >= 0 && !sa::gemm_on_matrix_cores(d))
+        return fail(SA_ERR_UNSUPPORTED, "this product does not run on the matrix cores (layout, alignment or K)");
+    hipStream_t stream = reinterpret_cast<hipStream_t>(stream_);
+    const hipError_t e = sa::launch_gemm_tile_shape(d, tile_shape, stream);
+    if (e == hipErrorInvalidValue) return fail(SA_ERR_UNSUPPORTED, "tile shape %d cannot take this product", tile_shape);
+    if (e != hipSuccess) return hip_fail(e, "product launch");
+    return SA_OK;
+}
+
 }  // extern "C"

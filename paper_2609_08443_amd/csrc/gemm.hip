@@ -677,9 +677,9 @@ bool gemm_on_matrix_cores(const GemmDesc& d) {
     return blocks < (int64_t(1) << 31);
 }
 
-hipError_t launch_gemm(const GemmDesc& d, hipStream_t stream) {
-    if (d.batch <= 0 || d.M <= 0 || d.N <= 0) return hipSuccess;
-    if (!gemm_on_matrix_cores(d)) return launch_small_gemm_general(d, stream);
+namespace {
+
+MgArgs make_args(const GemmDesc& d) {
     MgArgs g;
     g.A = d.A;
     g.a_z = d.a_z; g.a_m = d.a_m; g.a_k = d.a_k;
@@ -693,6 +693,15 @@ hipError_t launch_gemm(const GemmDesc& d, hipStream_t stream) {
     g.alpha = d.alpha;
     g.accumulate = d.accumulate ? 1 : 0;
     g.c_rows16 = (d.N % 8 == 0 && d.c_m % 8 == 0 && d.c_z % 8 == 0 && al16(d.C)) ? 1 : 0;
+    return g;
+}
+
+}  // namespace
+
+hipError_t launch_gemm(const GemmDesc& d, hipStream_t stream) {
+    if (d.batch <= 0 || d.M <= 0 || d.N <= 0) return hipSuccess;
+    if (!gemm_on_matrix_cores(d)) return launch_small_gemm_general(d, stream);
+    const MgArgs g = make_args(d);
     const bool a_kc = d.a_k == 1, b_kc = d.b_k == 1;
     if (d.a_bf16 && d.b_bf16) {
         const int shape = choose_lt(d, a_kc, b_kc);
@@ -702,6 +711,24 @@ hipError_t launch_gemm(const GemmDesc& d, hipStream_t stream) {
     if (a_kc) return mgemm_launch<true, false>(g, d.a_bf16, d.b_bf16, d.c_bf16, d.batch, stream);
     if (b_kc) return mgemm_launch<false, true>(g, d.a_bf16, d.b_bf16, d.c_bf16, d.batch, stream);
     return mgemm_launch<false, false>(g, d.a_bf16, d.b_bf16, d.c_bf16, d.batch, stream);
+}
+
+int gemm_tile_shapes() { return (int)(sizeof(kLtShapes) / sizeof(kLtShapes[0])); }
+
+hipError_t launch_gemm_tile_shape(const GemmDesc& d, int shape, hipStream_t stream) {
+    if (shape < 0) return launch_gemm(d, stream);
+    if (shape >= gemm_tile_shapes() || !d.a_bf16 || !d.b_bf16 || !gemm_on_matrix_cores(d))
+        return hipErrorInvalidValue;
+    const bool a_kc = d.a_k == 1, b_kc = d.b_k == 1;
+    const LtShape& t = kLtShapes[shape];
+    auto fits = [&](bool kc, int64_t rows, int64_t s_row) {
+        return !kc || ((rows - 1) * s_row + d.K) * 2 < (int64_t(1) << 32);
+    };
+    if ((!a_kc && !t.a_mc_ok) || !fits(a_kc, d.M, d.a_m) || !fits(b_kc, d.N, d.b_n)) return hipErrorInvalidValue;
+    if ((int64_t)((d.M + t.bm - 1) / t.bm) * ((d.N + t.bn - 1) / t.bn) * d.batch >= (int64_t(1) << 31))
+        return hipErrorInvalidValue;
+    if (d.batch <= 0 || d.M <= 0 || d.N <= 0) return hipSuccess;
+    return lt_run(shape, make_args(d), a_kc, b_kc, d.c_bf16, d.batch, stream);
 }
 
 }  // namespace sa

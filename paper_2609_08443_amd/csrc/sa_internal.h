@@ -167,6 +167,11 @@ struct GemmDesc {
 bool gemm_on_matrix_cores(const GemmDesc& d);
 // number of compute units of the current device (read once per device)
 int device_cus();
+// The bf16-operand product on one given tile shape (0 .. gemm_tile_shapes() - 1,
+// the largest first) instead of the one launch_gemm picks (shape < 0: as
+// launch_gemm); hipErrorInvalidValue where that shape cannot take the product.
+int gemm_tile_shapes();
+hipError_t launch_gemm_tile_shape(const GemmDesc& d, int shape, hipStream_t stream);
 hipError_t launch_gemm(const GemmDesc& d, hipStream_t stream);
 hipError_t launch_small_gemm_general(const GemmDesc& d, hipStream_t stream);
 

@@ -27,7 +27,7 @@ EXPORTS = ("sa_sketch_fwd_workspace_size", "sa_sketch_fwd", "sa_sketch_fwd_noall
            "sa_layer_bwd", "sa_block_fwd_workspace_size", "sa_block_fwd",
            "sa_block_saved_size", "sa_block_saved_offset", "sa_block_bwd_workspace_size", "sa_block_bwd",
            "sa_stca_fwd_workspace_size", "sa_stca_fwd",
-           "sa_stca_bwd_workspace_size", "sa_stca_bwd",
+           "sa_stca_bwd_workspace_size", "sa_stca_bwd", "sa_gemm_tile_shapes", "sa_gemm_bf16",
            "sa_profile_enable", "sa_kernel_times", "sa_status_string", "sa_last_error")
 
 
@@ -63,6 +63,11 @@ def lib() -> ctypes.CDLL:
     L.sa_sketch_bwd.argtypes = [vp, vp, vp, vp, i64, i64, i32, i32, i32, f32, c.c_int, vp, i32,
                                 vp, vp, vp, vp, vp, sz, vp]
     L.sa_sketch_bwd.restype = c.c_int
+    L.sa_gemm_tile_shapes.argtypes = []
+    L.sa_gemm_tile_shapes.restype = i32
+    L.sa_gemm_bf16.argtypes = [vp, i64, i64, i64, vp, i64, i64, i64, i64, vp, i32, i64, i64, i32, i32, i32, i32,
+                               f32, i32, i32, vp]
+    L.sa_gemm_bf16.restype = c.c_int
     L.sa_sketch_fwd_noalloc.argtypes = [vp, vp, vp, vp, i64, i64, i32, i32, i32, f32, c.c_int, vp, vp, vp]
     L.sa_sketch_fwd_noalloc.restype = c.c_int
     L.sa_sketch_fwd_tokenwise_workspace_size.argtypes = [i64, i64, i32, i32, i32, c.c_int]
@@ -568,6 +573,28 @@ def stca_bwd(Xs, q, Wq, Wk, Wv, h: int, dout, scale: Optional[float] = None, wor
                            _ptr(g["dWv"]), _ptr(ws), nbytes, _stream_handle(stream))
     _check(rc)
     return g
+
+
+def gemm_tile_shapes() -> int:
+    return int(lib().sa_gemm_tile_shapes())
+
+
+def gemm_bf16(A, a_strides, B, b_strides, C, c_strides, M, N, K, batch, alpha=1.0, accumulate=False, b_mod=0,
+              tile_shape=-1, stream=None):
+    """sa_gemm_bf16 on torch tensors: A, B bf16 and C (fp32 or bf16) device
+    tensors addressed by (z, row, col) element strides a_strides = (a_z, a_m, a_k),
+    b_strides = (b_z, b_k, b_n), c_strides = (c_z, c_m).  Returns C."""
+    import torch
+    for name, t in (("A", A), ("B", B)):
+        if t.dtype != torch.bfloat16 or not t.is_cuda:
+            raise SAError(1, f"{name} must be a bf16 device tensor")
+    if C.dtype not in (torch.float32, torch.bfloat16) or not C.is_cuda:
+        raise SAError(1, "C must be a fp32 or bf16 device tensor")
+    rc = lib().sa_gemm_bf16(_ptr(A), *a_strides, _ptr(B), *b_strides, b_mod, _ptr(C),
+                            1 if C.dtype == torch.bfloat16 else 0, *c_strides, M, N, K, batch, float(alpha),
+                            1 if accumulate else 0, tile_shape, _stream_handle(stream))
+    _check(rc)
+    return C
 
 
 def profile_enable(on: bool = True) -> None:
