@@ -595,16 +595,24 @@ constexpr LtShape kLtShapes[] = {{160, 256, 1.0, 1, false}, {128, 256, 0.85, 1, 
                                  {128, 128, 0.7, 1, true},   {64, 128, 0.55, 2, true},  {128, 64, 0.6, 2, true},
                                  {64, 64, 0.5, 2, true}};
 
+// The per-lane load offsets of an operand are 32-bit byte offsets from the slab's
+// base: a k-contiguous operand's reach over its rows and K, an m- (n-)
+// contiguous one's over one slab's 64 k rows and its columns.
+bool lt_offsets_fit(const GemmDesc& d, bool a_kc, bool b_kc) {
+    auto fits = [&](bool kc, int64_t rows, int64_t s_row, int64_t s_k) {
+        const int64_t reach = kc ? (rows - 1) * s_row + d.K : (GBK - 1) * s_k + rows;
+        return reach * 2 < (int64_t(1) << 32);
+    };
+    return fits(a_kc, d.M, d.a_m, d.a_k) && fits(b_kc, d.N, d.b_n, d.b_k);
+}
+
 // The shape with the least estimated time: rounds of `occ` tiles per compute unit,
 // each round the tile's work over its speed times the tiles that share a CU (two
 // resident workgroups split its matrix cores); small tiles win where big ones
 // leave compute units idle.  -1 if none applies (byte offsets of a k-contiguous
 // operand beyond 32 bits).
 int choose_lt(const GemmDesc& d, bool a_kc, bool b_kc) {
-    auto fits = [&](bool kc, int64_t rows, int64_t s_row) {
-        return !kc || ((rows - 1) * s_row + d.K) * 2 < (int64_t(1) << 32);
-    };
-    if (!fits(a_kc, d.M, d.a_m) || !fits(b_kc, d.N, d.b_n)) return -1;
+    if (!lt_offsets_fit(d, a_kc, b_kc)) return -1;
     const int64_t cus = device_cus();
     int best = -1;
     double best_cost = 0;
@@ -721,10 +729,7 @@ hipError_t launch_gemm_tile_shape(const GemmDesc& d, int shape, hipStream_t stre
         return hipErrorInvalidValue;
     const bool a_kc = d.a_k == 1, b_kc = d.b_k == 1;
     const LtShape& t = kLtShapes[shape];
-    auto fits = [&](bool kc, int64_t rows, int64_t s_row) {
-        return !kc || ((rows - 1) * s_row + d.K) * 2 < (int64_t(1) << 32);
-    };
-    if ((!a_kc && !t.a_mc_ok) || !fits(a_kc, d.M, d.a_m) || !fits(b_kc, d.N, d.b_n)) return hipErrorInvalidValue;
+    if ((!a_kc && !t.a_mc_ok) || !lt_offsets_fit(d, a_kc, b_kc)) return hipErrorInvalidValue;
     if ((int64_t)((d.M + t.bm - 1) / t.bm) * ((d.N + t.bn - 1) / t.bn) * d.batch >= (int64_t(1) << 31))
         return hipErrorInvalidValue;
     if (d.batch <= 0 || d.M <= 0 || d.N <= 0) return hipSuccess;
