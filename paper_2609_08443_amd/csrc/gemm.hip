@@ -279,14 +279,22 @@ __global__ __launch_bounds__(256, 2) void mfma_gemm_kernel(MgArgs g) {
 // ((BM + BN) / 32: rows and columns past the matrix read its last ones), so the
 // wait for slab kt + 1 at the end of slab kt is a fixed count: the loads of slab
 // kt + 2 stay in flight across the barrier.
-template <int FM, int FN, int PM, int PN>
+template <int FM, int FN, int PM, int PN, int NS_ = 3>
 struct LtCfg {
     static constexpr int BM = 32 * FM * PM, BN = 32 * FN * PN;
     static constexpr int A_BYTES = BM * GBK * 2, B_BYTES = BN * GBK * 2;
-    static constexpr int STAGE = A_BYTES + B_BYTES, NS = 3, LDS = NS * STAGE;
+    // NS = 3: three stages, loaded two slabs ahead; NS = 1: one slab (K = 64), so
+    // that several workgroups share a CU and one's loads overlap another's stores
+    static constexpr int NS = NS_, STAGE = A_BYTES + B_BYTES;
+    static constexpr int STAGING = 4 * 32 * (32 * FN + 8) * 4;   // the epilogue's areas
+    static constexpr int LDS = NS * STAGE > STAGING ? NS * STAGE : STAGING;
     static constexpr int LOADS = (BM + BN) / 32;
-    // workgroups per CU that the LDS allows (registers are sized for it)
-    static constexpr int OCC = LDS <= 80 * 1024 ? 2 : 1;
+    // workgroups per CU that the LDS and (estimated) registers allow
+    static constexpr int REGS = 16 * FM * FN + 8 * (FM + FN) + 32;
+    static constexpr int OCC_LDS = (160 * 1024) / LDS, OCC_REG = 512 / REGS;
+    static constexpr int OCC1 = OCC_LDS < OCC_REG ? OCC_LDS : OCC_REG;
+    static constexpr int OCC = NS == 1 ? (OCC1 > 4 ? 4 : OCC1) : (LDS <= 80 * 1024 ? 2 : 1);
+    static_assert(NS == 1 || NS == 3, "stages");
     static_assert(PM * PN == 4, "four waves");
     static_assert(LDS <= 160 * 1024, "LDS");
     static_assert(LOADS < 64, "vmcnt range");
@@ -408,9 +416,9 @@ __device__ __forceinline__ bf16x8 lt_frag(const uint8_t* lds, int first, int ks,
     }
 }
 
-template <int FM, int FN, int PM, int PN, bool A_KC, bool B_KC, bool C_BF16>
-__global__ __launch_bounds__(256, (LtCfg<FM, FN, PM, PN>::OCC)) void mfma_gemm_lt_kernel(MgArgs g) {
-    using C = LtCfg<FM, FN, PM, PN>;
+template <int FM, int FN, int PM, int PN, bool A_KC, bool B_KC, bool C_BF16, int NS>
+__global__ __launch_bounds__(256, (LtCfg<FM, FN, PM, PN, NS>::OCC)) void mfma_gemm_lt_kernel(MgArgs g) {
+    using C = LtCfg<FM, FN, PM, PN, NS>;
     __shared__ __attribute__((aligned(16))) uint8_t smem[C::LDS];
     const int tid = threadIdx.x, lane = tid & 63, l32 = lane & 31, hl = lane >> 5;
     const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -426,7 +434,7 @@ __global__ __launch_bounds__(256, (LtCfg<FM, FN, PM, PN>::OCC)) void mfma_gemm_l
     LtOperand<C::BN, B_KC> opb;
     opa.init(Ab, g.a_m, g.a_k, m0, g.M, w, lane);
     opb.init(Bb, g.b_n, g.b_k, n0, g.N, w, lane);
-    auto stage = [&](int s) { return smem + (s % 3) * C::STAGE; };
+    auto stage = [&](int s) { return smem + (s % C::NS) * C::STAGE; };
     // slab kt into the stage of slab position pos
     auto issue = [&](int kt, int pos) __attribute__((always_inline)) {
         uint8_t* st = stage(pos);
@@ -468,16 +476,22 @@ __global__ __launch_bounds__(256, (LtCfg<FM, FN, PM, PN>::OCC)) void mfma_gemm_l
     };
     // slab kt: slab kt + 2 is loaded, slab kt is multiplied, slab kt + 1's loads are
     // awaited (the loads of slab kt + 2, if any, stay in flight)
-    issue(0, 0);
-    if (nk > 1) issue(1, 1);
-    if (nk > 1) lt_barrier<C::LOADS>();
-    else lt_barrier<0>();
-    for (int kt = 0; kt < nk; ++kt) {
-        const bool ahead = kt + 2 < nk;
-        if (ahead) issue(kt + 2, kt + 2);
-        mul(kt);
-        if (ahead) lt_barrier<C::LOADS>();
-        else if (kt + 1 < nk) lt_barrier<0>();
+    if constexpr (C::NS == 1) {   // the host launches it for K = 64 only
+        issue(0, 0);
+        lt_barrier<0>();
+        mul(0);
+    } else {
+        issue(0, 0);
+        if (nk > 1) issue(1, 1);
+        if (nk > 1) lt_barrier<C::LOADS>();
+        else lt_barrier<0>();
+        for (int kt = 0; kt < nk; ++kt) {
+            const bool ahead = kt + 2 < nk;
+            if (ahead) issue(kt + 2, kt + 2);
+            mul(kt);
+            if (ahead) lt_barrier<C::LOADS>();
+            else if (kt + 1 < nk) lt_barrier<0>();
+        }
     }
 
     // Epilogue.  With 16-byte aligned rows of C, each wave passes its results
@@ -556,44 +570,48 @@ __global__ __launch_bounds__(256, (LtCfg<FM, FN, PM, PN>::OCC)) void mfma_gemm_l
     }
 }
 
-template <int FM, int FN, int PM, int PN, bool A_KC, bool B_KC>
+template <int FM, int FN, int PM, int PN, int NS, bool A_KC, bool B_KC>
 hipError_t lt_launch(MgArgs g, bool c_bf16, int64_t batch, hipStream_t stream) {
-    using C = LtCfg<FM, FN, PM, PN>;
+    using C = LtCfg<FM, FN, PM, PN, NS>;
     g.tm = (g.M + C::BM - 1) / C::BM;
     g.tn = (g.N + C::BN - 1) / C::BN;
     const int64_t blocks = (int64_t)g.tm * g.tn * batch;
     if (c_bf16)
-        hipLaunchKernelGGL((mfma_gemm_lt_kernel<FM, FN, PM, PN, A_KC, B_KC, true>), dim3((unsigned)blocks), dim3(256),
-                           0, stream, g);
+        hipLaunchKernelGGL((mfma_gemm_lt_kernel<FM, FN, PM, PN, A_KC, B_KC, true, NS>), dim3((unsigned)blocks),
+                           dim3(256), 0, stream, g);
     else
-        hipLaunchKernelGGL((mfma_gemm_lt_kernel<FM, FN, PM, PN, A_KC, B_KC, false>), dim3((unsigned)blocks),
+        hipLaunchKernelGGL((mfma_gemm_lt_kernel<FM, FN, PM, PN, A_KC, B_KC, false, NS>), dim3((unsigned)blocks),
                            dim3(256), 0, stream, g);
     return hipGetLastError();
 }
 
-template <int FM, int FN, int PM, int PN>
+template <int FM, int FN, int PM, int PN, int NS>
 hipError_t lt_dispatch(const MgArgs& g, bool a_kc, bool b_kc, bool c_bf16, int64_t batch, hipStream_t stream) {
-    if (a_kc && b_kc) return lt_launch<FM, FN, PM, PN, true, true>(g, c_bf16, batch, stream);
-    if (a_kc) return lt_launch<FM, FN, PM, PN, true, false>(g, c_bf16, batch, stream);
-    if constexpr (LtCfg<FM, FN, PM, PN>::BM % 64 == 0) {
-        if (b_kc) return lt_launch<FM, FN, PM, PN, false, true>(g, c_bf16, batch, stream);
-        return lt_launch<FM, FN, PM, PN, false, false>(g, c_bf16, batch, stream);
+    if (a_kc && b_kc) return lt_launch<FM, FN, PM, PN, NS, true, true>(g, c_bf16, batch, stream);
+    if (a_kc) return lt_launch<FM, FN, PM, PN, NS, true, false>(g, c_bf16, batch, stream);
+    if constexpr (LtCfg<FM, FN, PM, PN, NS>::BM % 64 == 0) {
+        if (b_kc) return lt_launch<FM, FN, PM, PN, NS, false, true>(g, c_bf16, batch, stream);
+        return lt_launch<FM, FN, PM, PN, NS, false, false>(g, c_bf16, batch, stream);
     }
     return hipErrorInvalidValue;
 }
 
 // Tile shapes: rows, columns, relative speed per tile element (fewer LDS and L2
-// bytes per product for bigger tiles), workgroups per CU, and whether the A
-// operand may be m-contiguous (160 rows do not split into whole loads of rows).
+// bytes per product for bigger tiles), workgroups per CU, whether the A operand
+// may be m-contiguous (160 rows do not split into whole loads of rows), and
+// whether the shape is a one-slab (K = 64) variant.
 struct LtShape {
     int bm, bn;
     double eff;
     int occ;
     bool a_mc_ok;
+    bool one_slab;   // K = 64 only
 };
-constexpr LtShape kLtShapes[] = {{160, 256, 1.0, 1, false}, {128, 256, 0.85, 1, true}, {256, 128, 0.85, 1, true},
-                                 {128, 128, 0.7, 1, true},   {64, 128, 0.55, 2, true},  {128, 64, 0.6, 2, true},
-                                 {64, 64, 0.5, 2, true}};
+constexpr LtShape kLtShapes[] = {
+    {160, 256, 1.0, 1, false, false}, {128, 256, 0.85, 1, true, false}, {256, 128, 0.85, 1, true, false},
+    {128, 128, 0.7, 1, true, false},  {64, 128, 0.55, 2, true, false},  {128, 64, 0.6, 2, true, false},
+    {64, 64, 0.5, 2, true, false},    {160, 256, 1.0, 2, false, true},  {128, 128, 0.7, 4, true, true},
+    {128, 64, 0.6, 4, true, true},    {64, 64, 0.5, 4, true, true}};
 
 // The per-lane load offsets of an operand are 32-bit byte offsets from the slab's
 // base: a k-contiguous operand's reach over its rows and K, an m- (n-)
@@ -618,7 +636,8 @@ int choose_lt(const GemmDesc& d, bool a_kc, bool b_kc) {
     double best_cost = 0;
     for (int i = 0; i < (int)(sizeof(kLtShapes) / sizeof(kLtShapes[0])); ++i) {
         const LtShape& t = kLtShapes[i];
-        if (!a_kc && !t.a_mc_ok) continue;
+        // one-slab products take the one-slab shapes (same tiles, more of them per CU)
+        if ((!a_kc && !t.a_mc_ok) || t.one_slab != (d.K == GBK)) continue;
         const int64_t tiles = (int64_t)((d.M + t.bm - 1) / t.bm) * ((d.N + t.bn - 1) / t.bn) * d.batch;
         if (tiles >= (int64_t(1) << 31)) continue;
         const int64_t rounds = (tiles + cus * t.occ - 1) / (cus * t.occ);
@@ -635,13 +654,17 @@ int choose_lt(const GemmDesc& d, bool a_kc, bool b_kc) {
 hipError_t lt_run(int shape, const MgArgs& g, bool a_kc, bool b_kc, bool c_bf16, int64_t batch,
                   hipStream_t stream) {
     switch (shape) {
-        case 0: return lt_dispatch<5, 2, 1, 4>(g, a_kc, b_kc, c_bf16, batch, stream);
-        case 1: return lt_dispatch<4, 2, 1, 4>(g, a_kc, b_kc, c_bf16, batch, stream);
-        case 2: return lt_dispatch<4, 2, 2, 2>(g, a_kc, b_kc, c_bf16, batch, stream);
-        case 3: return lt_dispatch<2, 2, 2, 2>(g, a_kc, b_kc, c_bf16, batch, stream);
-        case 4: return lt_dispatch<1, 2, 2, 2>(g, a_kc, b_kc, c_bf16, batch, stream);
-        case 5: return lt_dispatch<2, 1, 2, 2>(g, a_kc, b_kc, c_bf16, batch, stream);
-        default: return lt_dispatch<1, 1, 2, 2>(g, a_kc, b_kc, c_bf16, batch, stream);
+        case 0: return lt_dispatch<5, 2, 1, 4, 3>(g, a_kc, b_kc, c_bf16, batch, stream);
+        case 1: return lt_dispatch<4, 2, 1, 4, 3>(g, a_kc, b_kc, c_bf16, batch, stream);
+        case 2: return lt_dispatch<4, 2, 2, 2, 3>(g, a_kc, b_kc, c_bf16, batch, stream);
+        case 3: return lt_dispatch<2, 2, 2, 2, 3>(g, a_kc, b_kc, c_bf16, batch, stream);
+        case 4: return lt_dispatch<1, 2, 2, 2, 3>(g, a_kc, b_kc, c_bf16, batch, stream);
+        case 5: return lt_dispatch<2, 1, 2, 2, 3>(g, a_kc, b_kc, c_bf16, batch, stream);
+        case 6: return lt_dispatch<1, 1, 2, 2, 3>(g, a_kc, b_kc, c_bf16, batch, stream);
+        case 7: return lt_dispatch<5, 2, 1, 4, 1>(g, a_kc, b_kc, c_bf16, batch, stream);
+        case 8: return lt_dispatch<2, 2, 2, 2, 1>(g, a_kc, b_kc, c_bf16, batch, stream);
+        case 9: return lt_dispatch<2, 1, 2, 2, 1>(g, a_kc, b_kc, c_bf16, batch, stream);
+        default: return lt_dispatch<1, 1, 2, 2, 1>(g, a_kc, b_kc, c_bf16, batch, stream);
     }
 }
 
@@ -729,7 +752,8 @@ hipError_t launch_gemm_tile_shape(const GemmDesc& d, int shape, hipStream_t stre
         return hipErrorInvalidValue;
     const bool a_kc = d.a_k == 1, b_kc = d.b_k == 1;
     const LtShape& t = kLtShapes[shape];
-    if ((!a_kc && !t.a_mc_ok) || !lt_offsets_fit(d, a_kc, b_kc)) return hipErrorInvalidValue;
+    if ((!a_kc && !t.a_mc_ok) || (t.one_slab && d.K != GBK) || !lt_offsets_fit(d, a_kc, b_kc))
+        return hipErrorInvalidValue;
     if ((int64_t)((d.M + t.bm - 1) / t.bm) * ((d.N + t.bn - 1) / t.bn) * d.batch >= (int64_t(1) << 31))
         return hipErrorInvalidValue;
     if (d.batch <= 0 || d.M <= 0 || d.N <= 0) return hipSuccess;

@@ -4,8 +4,8 @@ shape and operand layout, against a float64 numpy product of the same bf16
 operands.
 
 Each case is ragged (M and N one partial tile past a whole one) with a batch of
-two.  fp32 results: max |C - ref| <= 2e-5 max |ref| (fp32 accumulation of exact
-bf16 x bf16 products over K = 192).  bf16 results: |C - ref| <= 2^-8 |ref| +
+two, K = 192 (three slabs; 64 for the one-slab shapes).  fp32 results: max
+|C - ref| <= 2e-5 max |ref| (fp32 accumulation of exact bf16 x bf16 products).  bf16 results: |C - ref| <= 2^-8 |ref| +
 2e-5 max |ref| per element (one rounding to bf16)."""
 import numpy as np
 import pytest
@@ -13,7 +13,9 @@ import pytest
 torch = pytest.importorskip("torch")
 pytestmark = pytest.mark.gpu
 
-SHAPES = [(160, 256), (128, 256), (256, 128), (128, 128), (64, 128), (128, 64), (64, 64)]
+# (rows, columns, one 64-deep slab only): the library's tile shapes in order
+SHAPES = [(160, 256, False), (128, 256, False), (256, 128, False), (128, 128, False), (64, 128, False),
+          (128, 64, False), (64, 64, False), (160, 256, True), (128, 128, True), (128, 64, True), (64, 64, True)]
 
 
 @pytest.fixture(scope="module")
@@ -63,12 +65,12 @@ def check(c, ref, c_bf16):
 @pytest.mark.parametrize("c_bf16", [False, True])
 def test_tile_shape_matches_numpy(sa, shape, a_kc, b_kc, c_bf16):
     assert sa.gemm_tile_shapes() == len(SHAPES)
-    bm, bn = SHAPES[shape]
-    M, N, K, batch = bm + 24, bn + 40, 192, 2
+    bm, bn, one = SHAPES[shape]
+    M, N, K, batch = bm + 24, bn + 40, 64 if one else 192, 2
     print(f"gemm shape {shape} ({bm}x{bn}) a_kc={a_kc} b_kc={b_kc} c_bf16={c_bf16}", flush=True)
     a, b, a_dev, a_str, b_dev, b_str = operands(100 + shape, M, N, K, batch, a_kc, b_kc, 0)
     c = torch.zeros((batch, M, N), dtype=torch.bfloat16 if c_bf16 else torch.float32, device="cuda")
-    if shape == 0 and not a_kc:
+    if bm == 160 and not a_kc:
         # 160 rows do not split into whole loads of an m-contiguous operand
         with pytest.raises(sa.SAError):
             sa.gemm_bf16(a_dev, a_str, b_dev, b_str, c, (M * N, N), M, N, K, batch, tile_shape=shape)
@@ -81,7 +83,7 @@ def test_tile_shape_matches_numpy(sa, shape, a_kc, b_kc, c_bf16):
 @pytest.mark.parametrize("shape", range(len(SHAPES)))
 def test_accumulate_shared_weights_single_slab(sa, shape):
     """C += alpha A B with B shared by the batch (b_mod = 1) and one 64-deep slab."""
-    bm, bn = SHAPES[shape]
+    bm, bn, _ = SHAPES[shape]
     M, N, K, batch = 2 * bm - 8, bn + 8, 64, 3
     print(f"gemm accumulate shape {shape} M={M} N={N} K={K}", flush=True)
     a, b, a_dev, a_str, b_dev, b_str = operands(200 + shape, M, N, K, batch, True, shape % 2 == 0, 1)
@@ -97,7 +99,7 @@ def test_accumulate_shared_weights_single_slab(sa, shape):
 def test_automatic_choice_and_fallback(sa):
     """tile_shape = -1: the library's own choice, on a product that fills the chip
     and on one whose contraction length (100) the matrix cores do not take."""
-    for (M, N, K, batch) in ((640, 512, 256, 8), (72, 40, 100, 2)):
+    for (M, N, K, batch) in ((640, 512, 256, 8), (640, 1024, 64, 4), (72, 40, 100, 2)):
         print(f"gemm automatic M={M} N={N} K={K} batch={batch}", flush=True)
         a, b, a_dev, a_str, b_dev, b_str = operands(7 + K, M, N, K, batch, True, False, 0)
         c = torch.zeros((batch, M, N), dtype=torch.float32, device="cuda")
