@@ -293,7 +293,7 @@ struct LtCfg {
     static constexpr int REGS = 16 * FM * FN + 8 * (FM + FN) + 32;
     static constexpr int OCC_LDS = (160 * 1024) / LDS, OCC_REG = 512 / REGS;
     static constexpr int OCC1 = OCC_LDS < OCC_REG ? OCC_LDS : OCC_REG;
-    static constexpr int OCC = NS == 1 ? (OCC1 > 4 ? 4 : OCC1) : (LDS <= 80 * 1024 ? 2 : 1);
+    static constexpr int OCC = OCC1 > 4 ? 4 : (OCC1 < 1 ? 1 : OCC1);
     static_assert(NS == 1 || NS == 3, "stages");
     static_assert(PM * PN == 4, "four waves");
     static_assert(LDS <= 160 * 1024, "LDS");
@@ -610,7 +610,7 @@ struct LtShape {
 constexpr LtShape kLtShapes[] = {
     {160, 256, 1.0, 1, false, false}, {128, 256, 0.85, 1, true, false}, {256, 128, 0.85, 1, true, false},
     {128, 128, 0.7, 1, true, false},  {64, 128, 0.55, 2, true, false},  {128, 64, 0.6, 2, true, false},
-    {64, 64, 0.5, 2, true, false},    {160, 256, 1.0, 2, false, true},  {128, 128, 0.7, 4, true, true},
+    {64, 64, 0.62, 3, true, false},   {160, 256, 1.0, 2, false, true},  {128, 128, 0.7, 4, true, true},
     {128, 64, 0.6, 4, true, true},    {64, 64, 0.5, 4, true, true}};
 
 // The per-lane load offsets of an operand are 32-bit byte offsets from the slab's
