@@ -96,19 +96,21 @@ __global__ __launch_bounds__(256) void stca_softmax_reg_kernel(const float* __re
 #pragma unroll
     for (int i = 0; i < NV; ++i) mx = fmaxf(fmaxf(mx, fmaxf(v[i].x, v[i].y)), fmaxf(v[i].z, v[i].w));
     mx = wave_max(mx);
+    // each exponential once: alpha = exp(s - max) / z
     float z = 0.f;
 #pragma unroll
-    for (int i = 0; i < NV; ++i)   // (padding columns hold -inf: exp gives 0)
-        z += (__expf(v[i].x - mx) + __expf(v[i].y - mx)) + (__expf(v[i].z - mx) + __expf(v[i].w - mx));
-    const float l = mx + __logf(wave_sum(z));
+    for (int i = 0; i < NV; ++i) {   // (padding columns hold -inf: exp gives 0)
+        v[i] = make_float4(__expf(v[i].x - mx), __expf(v[i].y - mx), __expf(v[i].z - mx), __expf(v[i].w - mx));
+        z += (v[i].x + v[i].y) + (v[i].z + v[i].w);
+    }
+    z = wave_sum(z);
+    const float inv = 1.f / z;
 #pragma unroll
     for (int i = 0; i < NV; ++i) {
         const int c = 4 * (lane + 64 * i);
-        if (c < k)
-            put4<BF16>(alpha, row * k + c, __expf(v[i].x - l), __expf(v[i].y - l), __expf(v[i].z - l),
-                       __expf(v[i].w - l));
+        if (c < k) put4<BF16>(alpha, row * k + c, v[i].x * inv, v[i].y * inv, v[i].z * inv, v[i].w * inv);
     }
-    if (lane == 0) lse[row] = l;
+    if (lane == 0) lse[row] = mx + __logf(z);
 }
 
 template <bool BF16, int NV>
