@@ -7,20 +7,21 @@
 // (a_k = 1, b_k = 1) or along its other index (a_m = 1, b_n = 1), so transposed
 // operands cost nothing at the call site.
 //
-// Tile 128 x 128 x 64 per workgroup of four waves, each wave a 64 x 64 block of
-// 2 x 2 v_mfma_f32_32x32x16_bf16 tiles.  Both operands are staged in LDS as
-// [row][64 k] bf16 (16-byte chunks XOR-swizzled so that operand reads of 32
-// rows are conflict free) in two buffers; global loads run two k slabs ahead
-// through two register sets, so a load has two slabs of products to land.  A
-// k-contiguous tile is loaded as 16-byte row pieces; an m- (n-) contiguous tile
-// as 4 k rows x 8 columns per thread, transposed in registers into 8 column
-// pieces of 4 k values (written so that each store instruction meets every
-// LDS bank twice, its minimum).  Tiles of one batch run on one XCD so that its operands share that
-// L2.  An fp32 operand (allowed when the caller accepts bf16 rounding of its
-// inputs) is loaded as the same pieces of fp32 values and rounded to bf16 when
-// its slab is staged.  Products whose shapes or strides do not fit (k not a
-// multiple of 64, unaligned strides, fp32 operands without that permission) run
-// on the register-tiled fp32 product of layer.hip.
+// Two kernels.  Products with bf16 operands run mfma_gemm_lt_kernel (tile shape
+// chosen per product, operands loaded straight into LDS; see below).  Products
+// with an fp32 operand the caller allows rounding to bf16 run mfma_gemm_kernel:
+// tile 128 x 128 x 64 per workgroup of four waves, each wave a 64 x 64 block of
+// 2 x 2 v_mfma_f32_32x32x16_bf16 tiles; both operands staged in LDS as [row][64 k]
+// bf16 (16-byte chunks XOR-swizzled so that operand reads of 32 rows are conflict
+// free) in two buffers, global loads running two k slabs ahead through two
+// register sets; a k-contiguous tile loaded as 16-byte row pieces, an m- (n-)
+// contiguous tile as 4 k rows x 8 columns per thread transposed in registers into
+// 8 column pieces of 4 k values (written so that each store instruction meets
+// every LDS bank twice, its minimum); fp32 pieces rounded to bf16 as the slab is
+// staged.  In both, the tiles of one batch run on one XCD so that its operands
+// share that L2.  Products whose shapes or strides do not fit (k not a multiple of
+// 64, unaligned strides, fp32 operands without that permission) run on the
+// register-tiled fp32 product of layer.hip.
 #include "sa_internal.h"
 #include "tile_ops.h"
 
@@ -267,18 +268,20 @@ __global__ __launch_bounds__(256, 2) void mfma_gemm_kernel(MgArgs g) {
 }
 
 // ---------------------------------------------------------------------------
-// Large tiles for bf16 operands: BM x BN = (32 FM PM) x (32 FN PN) per workgroup of
-// four waves in a PM x PN grid, each wave FM x FN v_mfma_f32_32x32x16_bf16 tiles,
-// one workgroup per CU.  Three LDS stages of one 64-deep k slab each, loaded two
-// slabs ahead.  A k-contiguous operand goes straight from global memory into its
-// swizzled LDS layout (global_load_lds, lane l of a load writing the 16-byte
-// chunk that belongs at LDS position l), so it takes neither registers nor LDS
-// store instructions; an m- (n-) contiguous operand is loaded into one of two
-// register sets and transposed into LDS by the stores of store_slab, one slab
-// after it was loaded.  Every slab issues the same number of loads per thread
-// ((BM + BN) / 32: rows and columns past the matrix read its last ones), so the
-// wait for slab kt + 1 at the end of slab kt is a fixed count: the loads of slab
-// kt + 2 stay in flight across the barrier.
+// Tiles for bf16 operands: BM x BN = (32 FM PM) x (32 FN PN) per workgroup of four
+// waves in a PM x PN grid, each wave FM x FN v_mfma_f32_32x32x16_bf16 tiles; as many
+// workgroups per CU as the shape's LDS and registers allow.  Three LDS stages of
+// one 64-deep k slab each, loaded two slabs ahead (one stage for one-slab
+// products).  Both operands go straight from global memory into LDS by direct
+// loads (global_load_lds, lane l of a load writing the 16-byte chunk that belongs
+// at LDS position l), so they take neither registers nor LDS store instructions:
+// a k-contiguous operand into a swizzled [rows][64 k] layout read with
+// ds_read_b128, an m- (n-) contiguous one as it lies in memory, [64 k][R], read
+// with the transposing ds_read_b64_tr_b16.  Every slab issues the same number of
+// loads per thread ((BM + BN) / 32: rows and columns past the matrix read its
+// last ones), so the wait for slab kt + 1 at the end of slab kt is a fixed count
+// and the loads of slab kt + 2 stay in flight across the barrier.  Results pass
+// through a wave-private LDS area so that a lane stores 8 consecutive outputs.
 template <int FM, int FN, int PM, int PN, int NS_ = 3>
 struct LtCfg {
     static constexpr int BM = 32 * FM * PM, BN = 32 * FN * PN;
