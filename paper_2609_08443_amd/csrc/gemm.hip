@@ -372,11 +372,12 @@ struct LtOperand<R, true> {
 // 8% less time on a product with both operands transposed, 2% on one.
 __device__ __forceinline__ int tr_swizzle(int k, int lpr) { return ((k & 3) << 2) & (lpr - 1); }
 
-// m- (n-) contiguous operand: the slab is kept as it lies in memory, [64 k][R]
-// (rows of R bf16, chunks swizzled by tr_swizzle), two rows per load of a wave: lane l of load
-// q = w + 4 i takes row 2 q + l / 32, columns 8 (l % 32) .. + 7 (columns past the
-// matrix read its last eight).  Its fragments are read with the transposing
-// ds_read_b64_tr_b16 (frag).
+// m- (n-) contiguous operand: the slab is kept as it lies in memory, [64 k][R] (rows
+// of R bf16), its 16-byte chunks permuted within each row by tr_swizzle.  Lane l of
+// load q = w + 4 i fills LDS chunk p = 64 q + l, at row k = p / LPR and position
+// p mod LPR, with the global chunk at that position XOR tr_swizzle(k) (columns
+// past the matrix read its last eight).  Its fragments are read with the
+// transposing ds_read_b64_tr_b16 (lt_frag).
 template <int R>
 struct LtOperand<R, false> {
     static_assert(R % 64 == 0 && R <= 512, "transposed operand tile");
