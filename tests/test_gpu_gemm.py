@@ -81,19 +81,22 @@ def test_tile_shape_matches_numpy(sa, shape, a_kc, b_kc, c_bf16):
 
 
 @pytest.mark.parametrize("shape", range(len(SHAPES)))
-def test_accumulate_shared_weights_single_slab(sa, shape):
+@pytest.mark.parametrize("c_bf16", [False, True])
+def test_accumulate_shared_weights_single_slab(sa, shape, c_bf16):
     """C += alpha A B with B shared by the batch (b_mod = 1) and one 64-deep slab."""
     bm, bn, _ = SHAPES[shape]
     M, N, K, batch = 2 * bm - 8, bn + 8, 64, 3
-    print(f"gemm accumulate shape {shape} M={M} N={N} K={K}", flush=True)
+    print(f"gemm accumulate shape {shape} M={M} N={N} K={K} c_bf16={c_bf16}", flush=True)
     a, b, a_dev, a_str, b_dev, b_str = operands(200 + shape, M, N, K, batch, True, shape % 2 == 0, 1)
     g = torch.Generator().manual_seed(300 + shape)
     c0 = torch.randn((batch, M, N), generator=g)
+    if c_bf16:
+        c0 = c0.to(torch.bfloat16)
     c = c0.cuda()
     sa.gemm_bf16(a_dev, a_str, b_dev, b_str, c, (M * N, N), M, N, K, batch, alpha=-1.5, accumulate=True,
                  b_mod=1, tile_shape=shape)
     torch.cuda.synchronize()
-    check(c, reference(a, b, batch, 1, -1.5, c0.double().numpy()), False)
+    check(c, reference(a, b, batch, 1, -1.5, c0.double().numpy()), c_bf16)
 
 
 def test_automatic_choice_and_fallback(sa):
