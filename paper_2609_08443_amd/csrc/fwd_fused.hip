@@ -44,7 +44,9 @@
 //   exponentials of the last prototype tile; per-token partial sums to LDS;
 //   stage K(j+1) into the other K buffer
 //   --- barrier ---
-//   z, lse of tile j; stage V(j)/z; issue the global loads of K(j+2), V(j+1)
+//   z of tile j (one LDS round trip also gives each thread the sums of the
+//   tokens whose V chunks it stages); the next tile's first operands; lse;
+//   stage V(j)/z; issue the global loads of K(j+2), V(j+1)
 //   --- barrier ---
 // Iteration 0 aggregates zero weights and the last iteration exponentiates a
 // tile of clamped rows past the range (finite, masked out), so every iteration
@@ -59,6 +61,7 @@ namespace {
 
 using namespace tile;
 
+constexpr float kLn2 = 0.6931471805599453f;
 // z below this means the shift was too far above the largest logit
 constexpr float kUnderflowZ = 5.421010862427522e-20f;  // 2^-64
 // relative margin on the bound for the rounding of the fp32 norms and logits
@@ -117,6 +120,17 @@ __device__ inline void pipe_step(f32x16& sn, const bf16x8& k, const bf16x8& b, f
     }
 }
 
+// sum of the squares of eight bf16 values, two per packed dot product
+// (exact products, fp32 sums), in two independent chains
+__device__ inline float sumsq8_dot(uint4 v) {
+    using b2 = __bf16 __attribute__((ext_vector_type(2)));
+    const b2 x = __builtin_bit_cast(b2, v.x), y = __builtin_bit_cast(b2, v.y);
+    const b2 z = __builtin_bit_cast(b2, v.z), u = __builtin_bit_cast(b2, v.w);
+    const float s0 = __builtin_amdgcn_fdot2_f32_bf16(z, z, __builtin_amdgcn_fdot2_f32_bf16(x, x, 0.f, false), false);
+    const float s1 = __builtin_amdgcn_fdot2_f32_bf16(u, u, __builtin_amdgcn_fdot2_f32_bf16(y, y, 0.f, false), false);
+    return s0 + s1;
+}
+
 template <int D, int MW, int NW>
 struct Cfg {
     static constexpr int M = MW * NW;
@@ -134,9 +148,9 @@ struct Cfg {
     static constexpr int RED_BYTES = NW * 32 * 4;
     static constexpr int OFF_K = P_BYTES;
     static constexpr int OFF_V = OFF_K + 2 * K_BYTES;
-    static constexpr int OFF_SUM = OFF_V + V_BYTES;      // [NW][32] partial sums (bound path)
+    static constexpr int OFF_SUM = OFF_V + V_BYTES;      // [32][NW] partial sums (bound path)
     static constexpr int OFF_MAX = OFF_SUM + RED_BYTES;  // [NW][32] partial maxima (exact path)
-    static constexpr int OFF_SUM2 = OFF_MAX + RED_BYTES; // [NW][32] partial sums (exact path)
+    static constexpr int OFF_SUM2 = OFF_MAX + RED_BYTES; // [32][NW] partial sums (exact path)
     static constexpr int OFF_KN = OFF_SUM2 + RED_BYTES;  // [2][32] token norms
     static constexpr int OFF_NB = OFF_KN + 2 * 32 * 4;   // [2][32] score-chain inits, -c_t / scale
     static constexpr int OFF_PN = OFF_NB + 2 * 32 * 4;   // [NW] prototype norm maxima
@@ -255,14 +269,7 @@ __global__ __launch_bounds__(NW * 64, 1) void fwd_fused_kernel(FusedFwdArgs a) {
                 asm volatile("" : "+v"(idx));
                 const int tok = idx / C::KCH, ch = idx % C::KCH;
                 *reinterpret_cast<uint4*>(Kd + swz<D>(tok, ch)) = kreg[i];
-                const uint32_t q[4] = {kreg[i].x, kreg[i].y, kreg[i].z, kreg[i].w};
-                float p0 = bf16_lo(q[0]) * bf16_lo(q[0]), p1 = bf16_hi(q[0]) * bf16_hi(q[0]);
-                float p2 = bf16_lo(q[1]) * bf16_lo(q[1]), p3 = bf16_hi(q[1]) * bf16_hi(q[1]);
-                p0 = __builtin_fmaf(bf16_lo(q[2]), bf16_lo(q[2]), p0);
-                p1 = __builtin_fmaf(bf16_hi(q[2]), bf16_hi(q[2]), p1);
-                p2 = __builtin_fmaf(bf16_lo(q[3]), bf16_lo(q[3]), p2);
-                p3 = __builtin_fmaf(bf16_hi(q[3]), bf16_hi(q[3]), p3);
-                ss[i] = (p0 + p1) + (p2 + p3);
+                ss[i] = sumsq8_dot(kreg[i]);
             }
 #pragma unroll
             for (int i = 0; i < C::NLD; ++i) ss[i] = group_sum<C::KCH>(ss[i]);
@@ -417,24 +424,41 @@ __global__ __launch_bounds__(NW * 64, 1) void fwd_fused_kernel(FusedFwdArgs a) {
             stage_k(kb ^ 1);
             {
                 const float z = half_sum16(rsum, l32);
-                if ((l32 & 1) == 0) red_sum[w * 32 + srow(l32 >> 1, hl)] = z;
+                // the store address is rebuilt here from the lane id rather than
+                // kept live through the tile loop (it would be spilled)
+                int ln = tid;
+                asm volatile("" : "+v"(ln));
+                if ((ln & 1) == 0)
+                    reinterpret_cast<float*>(smem + C::OFF_SUM)[srow((ln & 31) >> 1, (ln >> 5) & 1) * NW + (ln >> 6)] = z;
             }
             __syncthreads();  // B_z
             // K of tile j+2 (kreg was staged above)
             if (j + 2 < ntiles) load_rows(a.K, ts + 64, kreg);
 
-            // ---- per-token sums: lane t of each half holds token t's total
+            // ---- per-token sums, in one LDS round trip: lane t of each half gets
+            // token t's total, and each thread the totals of the tokens of its V
+            // chunks; the next tile's operands are read meanwhile
+            static_assert(NW == 4, "one 16-byte read per token");
+            auto tok_z = [&](const float* part, int tok) {
+                const float4 q = *reinterpret_cast<const float4*>(part + tok * NW);
+                return (q.x + q.y) + (q.z + q.w);
+            };
             const int tt = l32;
-            float zt = 0.f;
+            float zt = tok_z(red_sum, tt);
+            float zv[C::NLD];
 #pragma unroll
-            for (int ww = 0; ww < NW; ++ww) zt += red_sum[ww * 32 + tt];
+            for (int i = 0; i < C::NLD; ++i) zv[i] = tok_z(red_sum, (tid + i * C::THREADS) / C::KCH);
             const float kn_t = knorm[kb * 32 + tt];
+            read_tile_ops(kb ^ 1);
             // tile-uniform check that the bound did not underflow any z_t
             const bool exact = __builtin_amdgcn_ballot_w64(zt < kUnderflowZ && ts + tt < t1) != 0;
             float c_t = cb * kn_t;
             if (exact) {
                 // rare: exact per-token max over the prototypes, then the exponentials
-                // again (rsum holds the running max first)
+                // again (rsum holds the running max first); the K operands of tile j
+                // are read again (those of tile j+1 are back afterwards)
+#pragma unroll
+                for (int kk = 0; kk < KS; ++kk) kop[kk] = lds_b128(Kbuf + kb * (32 * D), swz<D>(l32, 2 * kk + hl));
 #pragma unroll
                 for (int r = 0; r < 16; ++r) rsum[r] = -INFINITY;
 #pragma unroll
@@ -479,32 +503,31 @@ __global__ __launch_bounds__(NW * 64, 1) void fwd_fused_kernel(FusedFwdArgs a) {
                 for (int r = 0; r < 16; ++r) rsum[r] = half_sum(rsum[r]);
                 if (l32 == 0) {
 #pragma unroll
-                    for (int r = 0; r < 16; ++r) red_sum2[w * 32 + srow(r, hl)] = rsum[r];
+                    for (int r = 0; r < 16; ++r) red_sum2[srow(r, hl) * NW + w] = rsum[r];
                 }
                 __syncthreads();
-                zt = 0.f;
+                zt = tok_z(red_sum2, tt);
 #pragma unroll
-                for (int ww = 0; ww < NW; ++ww) zt += red_sum2[ww * 32 + tt];
+                for (int i = 0; i < C::NLD; ++i) zv[i] = tok_z(red_sum2, (tid + i * C::THREADS) / C::KCH);
                 c_t = -shift_s[tt] / kLog2e;
+                read_tile_ops(kb ^ 1);
             }
-            // ---- the next tile's first operands (K(j+1) and its inits are visible)
-            read_tile_ops(kb ^ 1);
 
-            // ---- lse: lanes 8w .. 8w+7 of wave w write tokens 8w .. 8w+7
+            // ---- lse: lanes 8w .. 8w+7 of wave w write tokens 8w .. 8w+7 (z is a
+            // normal number here, so the hardware log2 is good to about an ulp)
             static_assert(NW * 8 == 32, "four waves of eight tokens");
             if ((lane >> 3) == w && a.lse && ts + tt < t1)
-                a.lse[(int64_t)(ts + tt) * a.H + h] = c_t + __logf(zt);
+                a.lse[(int64_t)(ts + tt) * a.H + h] = c_t + __builtin_amdgcn_logf(zt) * kLn2;
 
             // ---- stage V / z (row-major; the aggregation reads it transposed).
             // z >= 2^-64 here (the exact path's z >= 1): the hardware reciprocal
             // (1 ulp) is as good as a division before the bf16 rounding of V / z.
-            const float inv_t = ts + tt < t1 ? __builtin_amdgcn_rcpf(zt) : 0.0f;
 #pragma unroll
             for (int i = 0; i < C::NLD; ++i) {
                 int idx = tid + i * C::THREADS;
                 asm volatile("" : "+v"(idx));  // addresses built here, not hoisted
                 const int tok = idx / C::KCH, ch = idx % C::KCH;
-                const float inv = __shfl(inv_t, tok);
+                const float inv = ts + tok < t1 ? __builtin_amdgcn_rcpf(zv[i]) : 0.0f;
                 *reinterpret_cast<uint4*>(Vt + swz<D>(tok, ch)) = scale8(vreg[i], inv);
             }
             // V of tile j+1
