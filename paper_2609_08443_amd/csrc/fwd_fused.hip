@@ -45,8 +45,9 @@
 //   stage K(j+1) into the other K buffer
 //   --- barrier ---
 //   z of tile j (one LDS round trip also gives each thread the sums of the
-//   tokens whose V chunks it stages); the next tile's first operands; lse;
-//   stage V(j)/z; issue the global loads of K(j+2), V(j+1)
+//   tokens whose V chunks it stages); the next tile's first operands; stage
+//   V(j)/z; then the lse stores and the global loads of K(j+2), V(j+1), so
+//   that the staging's wait for V(j) covers none of them
 //   --- barrier ---
 // Iteration 0 aggregates zero weights and the last iteration exponentiates a
 // tile of clamped rows past the range (finite, masked out), so every iteration
@@ -163,6 +164,11 @@ __global__ __launch_bounds__(NW * 64, 1) void fwd_fused_kernel(FusedFwdArgs a) {
     using C = Cfg<D, MW, NW>;
     constexpr int MT = C::MT, KS = C::KS, JT = C::JT;
     constexpr int ROWS = 16 / KS;   // rows of a logits tile exponentiated per pipeline step
+    // The next tile's first operands are read right after the per-token sums'
+    // LDS round trip with four or more prototype tiles per wave, after the
+    // bound check (and the rare exact path) with fewer: measured, the early
+    // reads pay with the longer tile loops and cost with the short ones.
+    constexpr bool EARLY_OPS = MT >= 4;
     static_assert(KS == 2 * JT, "one aggregation instruction per score-chain step");
     extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
     uint16_t* Ps = reinterpret_cast<uint16_t*>(smem);
@@ -432,8 +438,6 @@ __global__ __launch_bounds__(NW * 64, 1) void fwd_fused_kernel(FusedFwdArgs a) {
                     reinterpret_cast<float*>(smem + C::OFF_SUM)[srow((ln & 31) >> 1, (ln >> 5) & 1) * NW + (ln >> 6)] = z;
             }
             __syncthreads();  // B_z
-            // K of tile j+2 (kreg was staged above)
-            if (j + 2 < ntiles) load_rows(a.K, ts + 64, kreg);
 
             // ---- per-token sums, in one LDS round trip: lane t of each half gets
             // token t's total, and each thread the totals of the tokens of its V
@@ -449,16 +453,20 @@ __global__ __launch_bounds__(NW * 64, 1) void fwd_fused_kernel(FusedFwdArgs a) {
 #pragma unroll
             for (int i = 0; i < C::NLD; ++i) zv[i] = tok_z(red_sum, (tid + i * C::THREADS) / C::KCH);
             const float kn_t = knorm[kb * 32 + tt];
-            read_tile_ops(kb ^ 1);
+            if constexpr (EARLY_OPS) read_tile_ops(kb ^ 1);
             // tile-uniform check that the bound did not underflow any z_t
             const bool exact = __builtin_amdgcn_ballot_w64(zt < kUnderflowZ && ts + tt < t1) != 0;
             float c_t = cb * kn_t;
             if (exact) {
                 // rare: exact per-token max over the prototypes, then the exponentials
-                // again (rsum holds the running max first); the K operands of tile j
-                // are read again (those of tile j+1 are back afterwards)
+                // again (rsum holds the running max first); with the next tile's
+                // operands already read, the K operands of tile j are read again
+                // (those of tile j+1 are back afterwards)
+                if constexpr (EARLY_OPS) {
 #pragma unroll
-                for (int kk = 0; kk < KS; ++kk) kop[kk] = lds_b128(Kbuf + kb * (32 * D), swz<D>(l32, 2 * kk + hl));
+                    for (int kk = 0; kk < KS; ++kk)
+                        kop[kk] = lds_b128(Kbuf + kb * (32 * D), swz<D>(l32, 2 * kk + hl));
+                }
 #pragma unroll
                 for (int r = 0; r < 16; ++r) rsum[r] = -INFINITY;
 #pragma unroll
@@ -510,14 +518,9 @@ __global__ __launch_bounds__(NW * 64, 1) void fwd_fused_kernel(FusedFwdArgs a) {
 #pragma unroll
                 for (int i = 0; i < C::NLD; ++i) zv[i] = tok_z(red_sum2, (tid + i * C::THREADS) / C::KCH);
                 c_t = -shift_s[tt] / kLog2e;
-                read_tile_ops(kb ^ 1);
+                if constexpr (EARLY_OPS) read_tile_ops(kb ^ 1);
             }
-
-            // ---- lse: lanes 8w .. 8w+7 of wave w write tokens 8w .. 8w+7 (z is a
-            // normal number here, so the hardware log2 is good to about an ulp)
-            static_assert(NW * 8 == 32, "four waves of eight tokens");
-            if ((lane >> 3) == w && a.lse && ts + tt < t1)
-                a.lse[(int64_t)(ts + tt) * a.H + h] = c_t + __builtin_amdgcn_logf(zt) * kLn2;
+            if constexpr (!EARLY_OPS) read_tile_ops(kb ^ 1);
 
             // ---- stage V / z (row-major; the aggregation reads it transposed).
             // z >= 2^-64 here (the exact path's z >= 1): the hardware reciprocal
@@ -530,7 +533,13 @@ __global__ __launch_bounds__(NW * 64, 1) void fwd_fused_kernel(FusedFwdArgs a) {
                 const float inv = ts + tok < t1 ? __builtin_amdgcn_rcpf(zv[i]) : 0.0f;
                 *reinterpret_cast<uint4*>(Vt + swz<D>(tok, ch)) = scale8(vreg[i], inv);
             }
-            // V of tile j+1
+            // ---- then the lse, the K of tile j+2 (kreg was staged before B_z) and the
+            // V of tile j+1: issued after the staging, so that its wait for V(j)
+            // includes none of them
+            static_assert(NW * 8 == 32, "four waves of eight tokens");
+            if ((lane >> 3) == w && a.lse && ts + tt < t1)   // lanes 8w .. 8w+7 write tokens 8w .. 8w+7
+                a.lse[(int64_t)(ts + tt) * a.H + h] = c_t + __builtin_amdgcn_logf(zt) * kLn2;
+            if (j + 2 < ntiles) load_rows(a.K, ts + 64, kreg);
             if (j + 1 < ntiles) load_rows(a.V, ts + 32, vreg);
             // B_v: V' staged, the next tile's operands read; the loads stay in flight
             lds_barrier();
