@@ -347,7 +347,7 @@ __global__ __launch_bounds__(NW * 64, 1) void fwd_fused_kernel(FusedFwdArgs a) {
         // iteration 0's aggregation, tile 0's operands read
         load_rows(a.K, t0, kreg);
         stage_k(0);
-        if (ntiles > 1) load_rows(a.K, t0 + 32, kreg);
+        load_rows(a.K, t0 + 32, kreg);
         load_rows(a.V, t0, vreg);
         bf16x8 eop[MT][2];
 #pragma unroll
@@ -535,12 +535,13 @@ __global__ __launch_bounds__(NW * 64, 1) void fwd_fused_kernel(FusedFwdArgs a) {
             }
             // ---- then the lse, the K of tile j+2 (kreg was staged before B_z) and the
             // V of tile j+1: issued after the staging, so that its wait for V(j)
-            // includes none of them
+            // includes none of them.  The loads are issued in every iteration (rows
+            // past the range are clamped), so each wait for them is an exact count.
             static_assert(NW * 8 == 32, "four waves of eight tokens");
             if ((lane >> 3) == w && a.lse && ts + tt < t1)   // lanes 8w .. 8w+7 write tokens 8w .. 8w+7
                 a.lse[(int64_t)(ts + tt) * a.H + h] = c_t + __builtin_amdgcn_logf(zt) * kLn2;
-            if (j + 2 < ntiles) load_rows(a.K, ts + 64, kreg);
-            if (j + 1 < ntiles) load_rows(a.V, ts + 32, vreg);
+            load_rows(a.K, ts + 64, kreg);
+            load_rows(a.V, ts + 32, vreg);
             // B_v: V' staged, the next tile's operands read; the loads stay in flight
             lds_barrier();
         }
