@@ -187,24 +187,28 @@ __global__ __launch_bounds__(NW * 64, 1) void tw_fused_kernel(TwArgs a) {
             for (int kk = 0; kk < KS; ++kk)
                 pop[kk] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(Pg + 16 * kk + 8 * hl));
         }
-        u32x4 kreg[C::NCH], vreg[C::NCH];
-        auto fetch = [&](int ts) __attribute__((always_inline)) {
-            const int64_t tb = ((int64_t)ts * a.H + h) * D;
+        // Token tiles go global -> registers two tiles ahead (two register sets,
+        // used alternately) -> LDS buffer.  Every fetch issues the same loads (rows
+        // past the range read its last token, threads past the tile's chunks
+        // reload a chunk they do not store), so the wait before a store counts
+        // exactly the newer set's loads.  Rows past the range need no zeros: their
+        // logits are masked to -inf, so their weights are 0 and their V is unused.
+        struct Regs { u32x4 k[C::NCH], v[C::NCH]; };
+        Regs ra, rb;
+        auto fetch = [&](int ts, Regs& r) __attribute__((always_inline)) {
+            const char* Kb = reinterpret_cast<const char*>(a.K + ((int64_t)t0 * a.H + h) * D);
+            const char* Vb = reinterpret_cast<const char*>(a.V + ((int64_t)t0 * a.H + h) * D);
 #pragma unroll
             for (int c = 0; c < C::NCH; ++c) {
-                const int idx = tid + c * C::THREADS;
+                const int idx = (tid + c * C::THREADS) % C::LD_CHUNKS;
                 const int tok = idx / C::KCH, ch = idx % C::KCH;
-                u32x4 kv = (u32x4){0u, 0u, 0u, 0u}, vv = kv;
-                if (idx < C::LD_CHUNKS && ts + tok < t1) {
-                    const uint32_t off = (uint32_t)tok * row_stride + (uint32_t)(ch * 8);
-                    kv = *reinterpret_cast<const u32x4*>(a.K + tb + off);
-                    vv = *reinterpret_cast<const u32x4*>(a.V + tb + off);
-                }
-                kreg[c] = kv;
-                vreg[c] = vv;
+                const int row = min(ts + tok, t1 - 1) - t0;
+                const uint32_t off = ((uint32_t)row * row_stride + (uint32_t)(ch * 8)) * 2;
+                r.k[c] = *reinterpret_cast<const u32x4*>(Kb + off);
+                r.v[c] = *reinterpret_cast<const u32x4*>(Vb + off);
             }
         };
-        auto store = [&](int buf) __attribute__((always_inline)) {
+        auto store = [&](int buf, const Regs& r) __attribute__((always_inline)) {
             uint16_t* Kd = reinterpret_cast<uint16_t*>(smem + C::OFF_K + buf * C::TILE);
             uint16_t* Vd = reinterpret_cast<uint16_t*>(smem + C::OFF_V + buf * C::TILE);
 #pragma unroll
@@ -212,14 +216,18 @@ __global__ __launch_bounds__(NW * 64, 1) void tw_fused_kernel(TwArgs a) {
                 const int idx = tid + c * C::THREADS;
                 if (idx < C::LD_CHUNKS) {
                     const int tok = idx / C::KCH, ch = idx % C::KCH;
-                    *reinterpret_cast<u32x4*>(Kd + swz<D>(tok, ch)) = kreg[c];
-                    *reinterpret_cast<u32x4*>(Vd + swz<D>(tok, ch)) = vreg[c];
+                    *reinterpret_cast<u32x4*>(Kd + swz<D>(tok, ch)) = r.k[c];
+                    *reinterpret_cast<u32x4*>(Vd + swz<D>(tok, ch)) = r.v[c];
                 }
             }
         };
-        fetch(t0);
+        const bool any = t1 > t0;   // (an empty segment still writes its zero output)
+        if (any) {
+            fetch(t0, ra);
+            fetch(t0 + 32, rb);
+        }
         __syncthreads();  // the previous segment is done with every LDS buffer
-        store(0);
+        if (any) store(0, ra);
         __syncthreads();
 
         f32x16 acc[JT];
@@ -236,10 +244,11 @@ __global__ __launch_bounds__(NW * 64, 1) void tw_fused_kernel(TwArgs a) {
 #pragma unroll
         for (int kk = 0; kk < KS; ++kk) asm volatile("" ::"v"(pop[kk]));
 
-        int buf = 0;
-        for (int ts = t0; ts < t1; ts += 32, buf ^= 1) {
+        // tile at ts in LDS buffer buf; the next tile is in `nxt` (stored at the end
+        // of this step into the other buffer), the one after it fetched into `far`
+        auto step = [&](int ts, int buf, Regs& far, const Regs& nxt) __attribute__((always_inline)) {
             const bool more = ts + 32 < t1;
-            if (more) fetch(ts + 32);
+            fetch(ts + 64, far);
             const uint16_t* Ks = reinterpret_cast<const uint16_t*>(smem + C::OFF_K + buf * C::TILE);
             const uint16_t* Vs = reinterpret_cast<const uint16_t*>(smem + C::OFF_V + buf * C::TILE);
             // S[t, m]: lane = prototype, register r = token srow(r, hl)
@@ -285,8 +294,19 @@ __global__ __launch_bounds__(NW * 64, 1) void tw_fused_kernel(TwArgs a) {
                 acc[jt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(e0, lds_tr_tokens<D>(Vs, lane, jt, 0), acc[jt], 0, 0, 0);
                 acc[jt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(e1, lds_tr_tokens<D>(Vs, lane, jt, 1), acc[jt], 0, 0, 0);
             }
-            if (more) store(buf ^ 1);
+            if (more) store(buf ^ 1, nxt);
             __syncthreads();
+        };
+        // two tiles per trip; the exits sit after each step, so that the path back
+        // to the top always comes from the second step (whose pending loads fill
+        // the other register set)
+        if (any) {
+            for (int ts = t0;; ts += 64) {
+                step(ts, 0, ra, rb);
+                if (ts + 32 >= t1) break;
+                step(ts + 32, 1, rb, ra);
+                if (ts + 64 >= t1) break;
+            }
         }
         const float ltot = xhalf_add(lsum);   // both halves hold the same prototype
         // rows of this wave: prototypes part*MP + w*32 + srow(r, hl), columns jt*32 + l32
