@@ -515,7 +515,7 @@ sa_status block_layer_fwd(const void* X, const int64_t* offsets, int64_t B, int6
 }
 
 // ---------------------------------------------------------------- STCA over the sketch
-// [Qp | U | S (fp32) | alpha | C | lse (fp32) | (bwd) dout in the operand dtype | dC |
+// [Qp | U | S | alpha | C | lse (fp32) | (bwd) dout in the operand dtype | dC |
 //  dalpha (fp32) | ds | dU | dQp]; operand buffers in the input dtype.  Per user b,
 // target r and head i: Qp = q W_Q [B,R,D]; U = per-head (Qp W_K^T) [B,R,h,D]; S =
 // scale U Xs^T [B,R h,k]; alpha = softmax rows; C = alpha Xs [B,R,h,D].
@@ -536,7 +536,7 @@ StcaPlan plan_stca(int64_t B, int32_t R, int32_t k, int32_t D, int32_t h, sa_dty
     const size_t BR = (size_t)B * R, rows = BR * h;
     p.off_qp = carve(el * BR * D);
     p.off_u = carve(el * rows * D);
-    p.off_s = carve(4 * rows * k);
+    p.off_s = carve(el * rows * k);
     p.off_al = carve(el * rows * k);
     p.off_c = carve(el * rows * D);
     p.off_lse = carve(4 * rows);
@@ -571,7 +571,7 @@ sa_status stca_forward(const void* Xs, const void* q, const void* Wq, const void
     const int64_t kD = (int64_t)k * D, RhD = (int64_t)Rh * D, Rhk = (int64_t)Rh * k;
     void* Qp = ws + p.off_qp;
     void* U = ws + p.off_u;
-    float* S = reinterpret_cast<float*>(ws + p.off_s);
+    void* S = ws + p.off_s;   // logits, in the operand dtype
     void* Al = ws + p.off_al;
     void* Cc = ws + p.off_c;
     hipError_t e;
@@ -585,12 +585,12 @@ sa_status stca_forward(const void* Xs, const void* q, const void* Wq, const void
     }
     if (e == hipSuccess) {
         sa::ProfScope ps("stca_logits", stream);   // S = scale U Xs^T per user
-        e = sa::launch_gemm({U, bf, RhD, D, 1, Xs, bf, kD, 1, D, S, false, Rhk, k, Rh, k, D, (int32_t)B, scale, false},
+        e = sa::launch_gemm({U, bf, RhD, D, 1, Xs, bf, kD, 1, D, S, bf, Rhk, k, Rh, k, D, (int32_t)B, scale, false},
                             stream);
     }
     if (e == hipSuccess) {
         sa::ProfScope ps("stca_softmax", stream);
-        e = sa::launch_stca_softmax(S, (int64_t)BR * h, k, bf, Al, lse, stream);
+        e = sa::launch_stca_softmax(S, bf, (int64_t)BR * h, k, bf, Al, lse, stream);
     }
     if (e == hipSuccess) {
         sa::ProfScope ps("stca_aggregate", stream);   // C = alpha Xs per user
@@ -1433,7 +1433,7 @@ sa_status sa_stca_bwd(const void* Xs, const void* q, const void* Wq, const void*
     const int64_t kD = (int64_t)k * D, RhD = (int64_t)Rh * D, Rhk = (int64_t)Rh * k, hD = (int64_t)h * D;
     void* Qp = ws + p.off_qp;
     void* U = ws + p.off_u;
-    float* S = reinterpret_cast<float*>(ws + p.off_s);
+    const void* S = ws + p.off_s;
     void* Al = ws + p.off_al;
     void* Cc = ws + p.off_c;
     void* dC = ws + p.off_dc;
@@ -1462,7 +1462,7 @@ sa_status sa_stca_bwd(const void* Xs, const void* q, const void* Wq, const void*
     }
     if (e == hipSuccess) {
         sa::ProfScope ps("stca_softmax_bwd", stream);
-        e = sa::launch_stca_softmax_bwd(S, lse, dA, (int64_t)BR * h, k, scale, bf, ds, stream);
+        e = sa::launch_stca_softmax_bwd(S, bf, lse, dA, (int64_t)BR * h, k, scale, bf, ds, stream);
     }
     if (e == hipSuccess) {
         sa::ProfScope ps("stca_sketch_grads", stream);

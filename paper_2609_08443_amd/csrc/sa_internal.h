@@ -178,10 +178,10 @@ hipError_t launch_small_gemm_general(const GemmDesc& d, hipStream_t stream);
 // Reordered single-query STCA rows (stca.hip), over [rows][k] fp32 logits already
 // scaled: lse and alpha = exp(s - lse) in bf16 or fp32; the backward writes
 // ds = scale alpha (da - <alpha, da>).
-hipError_t launch_stca_softmax(const float* S, int64_t rows, int32_t k, bool bf16, void* alpha, float* lse,
-                               hipStream_t stream);
-hipError_t launch_stca_softmax_bwd(const float* S, const float* lse, const float* dA, int64_t rows, int32_t k,
-                                   float scale, bool bf16, void* ds, hipStream_t stream);
+hipError_t launch_stca_softmax(const void* S, bool s_bf16, int64_t rows, int32_t k, bool bf16, void* alpha,
+                               float* lse, hipStream_t stream);
+hipError_t launch_stca_softmax_bwd(const void* S, bool s_bf16, const float* lse, const float* dA, int64_t rows,
+                                   int32_t k, float scale, bool bf16, void* ds, hipStream_t stream);
 hipError_t launch_to_bf16(const float* x, uint16_t* y, int64_t n, hipStream_t stream);
 
 // Stacked-SA refinement (block.hip).  add_ln: one row of d features per

@@ -4,8 +4,9 @@ sa_stca_bwd, Appendix G.2) against the fp64 numpy oracle, through the C ABI.
 Tolerances: normwise max relative error <= 2e-2 (bf16) / 1e-4 (fp32) per
 (user, target) row block for the output and dq, per user for dXs, per head's
 column block for dW_Q, dW_K, dW_V.  lse absolute error: fp32 1e-4; bf16 mode
-rounds q W_Q and u = (q W_Q) W_K^T to bf16 once each, so a logit of magnitude
-|s| moves by up to about 2 * 2^-9 |s|; the bound is 2^-7 max(1, max |s|).
+rounds q W_Q, u = (q W_Q) W_K^T and the logits themselves to bf16 once each, so a
+logit of magnitude |s| moves by up to about 3 * 2^-9 |s|; the bound is
+2^-7 max(1, max |s|).
 The cases mix products that run on the matrix cores (every contraction length
 a multiple of 64) with ones that do not (the register-tiled fallback).
 """
