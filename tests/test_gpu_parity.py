@@ -277,7 +277,9 @@ def test_bwd_is_deterministic(sa):
         assert torch.equal(a_, b_)
 
 
-@pytest.mark.parametrize("M,d", [(256, 64), (512, 128)])
+# (M, d) = (256, 64) reads the next tile's operands after the bound check, the
+# other two before it (four or more prototype tiles per wave)
+@pytest.mark.parametrize("M,d", [(256, 64), (512, 128), (1024, 64)])
 def test_fwd_loose_bound_falls_back_to_exact_max(sa, M, d):
     """Keys of huge norm nearly orthogonal to every prototype: the logits sit far below
     the Cauchy-Schwarz shift, so exp(logit - shift) would underflow; the tile is
